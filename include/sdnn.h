@@ -1,0 +1,134 @@
+/*
+ * sdnn.h -- C ABI of the MI355X (gfx950) sparse-weight x dense-activation product.
+ *
+ * The operator is the core of SparseDNN (Wang, arXiv 2101.07948): a sparse matrix
+ * (pruned weights) times a dense matrix (activations), Sec. 2.2 and Sec. 3.2.2, with
+ * a fused bias + element-wise activation epilogue (layer fusion, Sec. 3.1):
+ *
+ *     C[i][n] = act( sum_p W[i][c_p] * B[c_p][n] + bias[i] )
+ *
+ * It follows the paper's two-stage engine (Sec. 2.1, Sec. 3): a one-time preparation
+ * stage (sdnn_plan_create: CSR validation, the greedy weight-row permutation of
+ * Sec. 3.1.2 / Algorithm 1, and repacking of W into a per-matrix traversal-ordered
+ * stream, Sec. 3.2.2) and a per-request execution stage (sdnn_spmm).
+ *
+ * Conventions shared by every entry point:
+ *   - Every call returns an sdnn_status; no C++ exception crosses this boundary.
+ *   - Host pointers are read during the call only and never retained.
+ *   - Device pointers are raw HIP device addresses; "stream" is a hipStream_t passed
+ *     as void* (NULL = the default stream).
+ *   - Dense matrices are row-major with no padding: B is K x N (ld = N), C is M x N
+ *     (ld = N).  Lanes of the GPU kernel run along N, so a PyTorch activation of
+ *     shape (tokens, hidden) is B transposed.
+ *   - CSR input: row_ptr[M+1] with row_ptr[0] = 0, non-decreasing, row_ptr[M] = nnz;
+ *     col_idx[nnz] in [0, K), strictly increasing within each row (no duplicates);
+ *     values[nnz] fp32.  Explicitly stored zeros count as nonzeros.
+ *   - Inputs must be finite; results for NaN/Inf inputs are unspecified.
+ */
+#ifndef SDNN_H_
+#define SDNN_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Opaque plan; immutable after creation. */
+typedef struct sdnn_plan_s* sdnn_plan;
+
+typedef enum {
+  SDNN_OK = 0,
+  SDNN_ERR_NULL = 1,   /* a required pointer is NULL */
+  SDNN_ERR_DIM = 2,    /* negative or too-large size, or overlapping B/C/bias ranges */
+  SDNN_ERR_CSR = 3,    /* malformed CSR: row_ptr, column range, unsorted/duplicate cols */
+  SDNN_ERR_ALLOC = 4,  /* host or device allocation failed */
+  SDNN_ERR_HIP = 5,    /* a HIP runtime call or kernel launch failed */
+  SDNN_ERR_DEVICE = 6  /* plan used on a device other than the one it was created on */
+} sdnn_status;
+
+/* Fused epilogue applied after the bias add (Sec. 3.1 layer fusion; GELU is the exact
+ * erf form x * Phi(x), named in Sec. 5). */
+typedef enum {
+  SDNN_EPI_NONE = 0,
+  SDNN_EPI_RELU = 1, /* max(x, 0) */
+  SDNN_EPI_GELU = 2  /* 0.5 * x * (1 + erf(x / sqrt(2))) */
+} sdnn_epilogue;
+
+/* Options for sdnn_plan_create; pass NULL for the defaults {0, 1}.
+ *   panel_rows: rows per register panel (0 = library default; otherwise 4, 8 or 16).
+ *   permute:    1 = apply Algorithm 1 (default), 0 = identity order (ablation). */
+typedef struct {
+  int32_t panel_rows;
+  int32_t permute;
+} sdnn_plan_opts;
+
+/* Plan statistics.
+ *   panels:       number of row panels (ceil(M / panel_rows)).
+ *   packed_bytes: device bytes of the packed weight stream and its indexes.
+ *   rho:          nnz / sum over panels of |union of the panel rows' column sets|,
+ *                 the reuse an ideal panel kernel gets per staged B row (>= 1).
+ *   fill:         nnz / stored stream entries (1.0 = no padding). */
+typedef struct {
+  int32_t M, K;
+  int64_t nnz, panels, packed_bytes;
+  double rho, fill;
+  int32_t panel_rows, k_chunk;
+} sdnn_plan_info_t;
+
+/* Greedy weight-row permutation (Sec. 3.1.2, Algorithm 1), host only, no GPU needed.
+ * perm_out[i] is the original row placed at position i (gather convention:
+ * W_perm[i] = W[perm_out[i]]).  First pick: most nonzeros (ties: lower index); each
+ * next pick: the remaining row with the largest |cols(prev) ∩ cols(x)| (ties: more
+ * nonzeros, then lower index).  perm_out has M entries, caller-owned.
+ * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM, SDNN_ERR_CSR, SDNN_ERR_ALLOC. */
+sdnn_status sdnn_reorder_rows(const int32_t* row_ptr, const int32_t* col_idx, int32_t M,
+                              int32_t K, int32_t* perm_out);
+
+/* Preparation stage (Sec. 2.1, Sec. 3.1.2, Sec. 3.2.2).  Validates the host CSR,
+ * computes the row permutation, packs W into the kernel's traversal-ordered stream
+ * and uploads it to the current HIP device.  The caller keeps ownership of the CSR
+ * arrays (they are copied).  The plan owns its device memory and is bound to the
+ * device current at creation.  values may be NULL only when nnz = 0.
+ * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM, SDNN_ERR_CSR, SDNN_ERR_ALLOC, SDNN_ERR_HIP. */
+sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx,
+                             const float* values, int32_t M, int32_t K,
+                             const sdnn_plan_opts* opts, sdnn_plan* out);
+
+/* Copies the plan's permutation (M int32, host memory) to perm_out. */
+sdnn_status sdnn_plan_get_perm(sdnn_plan p, int32_t* perm_out);
+
+/* Fills *out with the plan's statistics. */
+sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out);
+
+/* Execution stage (Sec. 3.2.2): C = act(W * B + bias), enqueued on `stream`.
+ *   B:    device, K x N row-major fp32, read only.
+ *   C:    device, M x N row-major fp32, written once, in the ORIGINAL row order.
+ *   N:    columns of B and C, any N >= 0 (N = 0 or M = 0 is a no-op).
+ *   bias: device, M fp32 in original row order, or NULL (treated as zeros).
+ * Asynchronous: no allocation, no synchronisation, no pointer retained.  A plan may
+ * be used from several streams at once.  B must not overlap C or bias; the bias may
+ * not overlap C (SDNN_ERR_DIM).  Device faults surface at the caller's next sync.
+ * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM, SDNN_ERR_DEVICE, SDNN_ERR_HIP. */
+sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
+                      sdnn_epilogue epi, void* stream);
+
+/* Frees the plan and its device memory.  NULL is a no-op. */
+void sdnn_plan_destroy(sdnn_plan p);
+
+/* Static, human-readable name of a status code. */
+const char* sdnn_status_str(sdnn_status s);
+
+/* Dense comparison kernel (the dense GEMM the paper measures its sparse kernels
+ * against, Sec. 3.2.1 / Sec. 4.1): C = act(W * B + bias) with W dense M x K row-major
+ * fp32 on the device, same layouts, epilogue and stream semantics as sdnn_spmm.
+ * It is a measurement aid, not part of the sparse method.
+ * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM, SDNN_ERR_HIP. */
+sdnn_status sdnn_dense_gemm(const float* W, const float* B, float* C, int32_t M, int32_t K,
+                            int32_t N, const float* bias, sdnn_epilogue epi, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SDNN_H_ */

@@ -1,0 +1,211 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+Each check takes an oracle library handle (``lib=None`` means the real oracle) and
+returns a list of failure messages (empty = pass), so the same checks both gate the
+real oracle and are shown to reject planted mistakes (tests/test_oracle_mutants.py).
+None of them re-uses the oracle's own code or formula: they compare against NumPy
+float64 dense products, closed forms, tabulated normal-CDF values, invariants and
+exhaustive/brute-force searches.
+"""
+
+import numpy as np
+from scipy.special import ndtr
+
+import oracle
+from conftest import (dense_to_csr, load_normal_cdf, load_reorder_examples, pattern_to_csr,
+                      random_csr)
+
+
+def _act_np(x, epi):
+    if epi == "relu":
+        return np.maximum(x, 0.0)
+    if epi == "gelu":
+        return x * ndtr(x)  # Phi from scipy's normal CDF: a library routine, not erf
+    return x
+
+
+def check_bruteforce(lib=None):
+    """Sparse product vs NumPy float64 dense W @ B on tiny non-square shapes."""
+    fails = []
+    rng = np.random.default_rng(1234)
+    for trial in range(60):
+        M, K, N = (int(x) for x in rng.integers(1, 17, size=3))
+        d = [0.1, 0.5, 0.9][trial % 3]
+        epi = ["none", "relu", "gelu"][(trial // 3) % 3]
+        row_ptr, col_idx, vals, W = random_csr(rng, M, K, d)
+        B = rng.standard_normal((K, N)).astype(np.float32)
+        bias = rng.standard_normal(M).astype(np.float32) if trial % 2 else None
+        C, bound = oracle.spmm_f64(row_ptr, col_idx, vals, K, B, bias, epi, lib=lib)
+        ref = W.astype(np.float64) @ B.astype(np.float64)
+        if bias is not None:
+            ref = ref + bias.astype(np.float64)[:, None]
+        ref = _act_np(ref, epi)
+        ref_bound = np.abs(W.astype(np.float64)) @ np.abs(B.astype(np.float64))
+        scale = ref_bound + np.abs(ref) + 1.0
+        if not np.all(np.abs(C - ref) <= 1e-12 * scale):
+            fails.append(f"bruteforce value mismatch M={M} K={K} N={N} d={d} epi={epi}")
+        if not np.all(np.abs(bound - ref_bound) <= 1e-12 * (ref_bound + 1.0)):
+            fails.append(f"bruteforce bound mismatch M={M} K={K} N={N}")
+    return fails
+
+
+def check_special_cases(lib=None):
+    """Density 0 -> act(bias); identity W -> act(B + bias); one 1.0 per row -> gather;
+    density 1 -> dense product."""
+    fails = []
+    rng = np.random.default_rng(99)
+    M, K, N = 7, 9, 5
+    B = rng.standard_normal((K, N)).astype(np.float32)
+    bias = rng.standard_normal(M).astype(np.float32)
+    for epi in ("none", "relu", "gelu"):
+        # density 0
+        row_ptr = np.zeros(M + 1, np.int32)
+        C, bound = oracle.spmm_f64(row_ptr, np.zeros(0, np.int32), np.zeros(0, np.float32), K, B,
+                                   bias, epi, lib=lib)
+        want = _act_np(np.repeat(bias.astype(np.float64)[:, None], N, axis=1), epi)
+        if not np.allclose(C, want, rtol=1e-15, atol=1e-15 if epi == "gelu" else 0.0) \
+                or np.any(bound != 0):
+            fails.append(f"density 0 != act(bias) ({epi})")
+        # identity (M = K)
+        I = np.eye(K, dtype=np.float32)
+        rp, ci, v = dense_to_csr(I)
+        biasK = rng.standard_normal(K).astype(np.float32)
+        C, _ = oracle.spmm_f64(rp, ci, v, K, B, biasK, epi, lib=lib)
+        want = _act_np(B.astype(np.float64) + biasK.astype(np.float64)[:, None], epi)
+        # erf's form of Phi cancels for negative x: allow 1e-15 absolute there
+        if not np.allclose(C, want, rtol=1e-15, atol=1e-15 if epi == "gelu" else 0.0):
+            fails.append(f"identity W != act(B + bias) ({epi})")
+    # gather: row i has a single 1.0 at column sigma(i)
+    sigma = rng.integers(0, K, size=M)
+    G = np.zeros((M, K), np.float32)
+    G[np.arange(M), sigma] = 1.0
+    rp, ci, v = dense_to_csr(G)
+    C, _ = oracle.spmm_f64(rp, ci, v, K, B, None, "none", lib=lib)
+    if not np.array_equal(C, B[sigma].astype(np.float64)):
+        fails.append("single-one rows do not gather B rows")
+    # density 1
+    Wd = rng.standard_normal((M, K)).astype(np.float32)
+    Wd[Wd == 0] = 1.0
+    rp, ci, v = dense_to_csr(Wd)
+    C, _ = oracle.spmm_f64(rp, ci, v, K, B, bias, "none", lib=lib)
+    ref = Wd.astype(np.float64) @ B.astype(np.float64) + bias.astype(np.float64)[:, None]
+    if not np.allclose(C, ref, rtol=1e-13, atol=1e-13):
+        fails.append("density 1 != dense product")
+    return fails
+
+
+def check_gelu_table(lib=None):
+    """GELU epilogue equals x * Phi(x) at tabulated normal-CDF points; ReLU = max(x, 0)."""
+    fails = []
+    xs, phis = load_normal_cdf()
+    rp, ci, v = dense_to_csr(np.ones((1, 1), np.float32))
+    for x, phi in zip(xs, phis):
+        B = np.array([[x]], np.float32)
+        C, _ = oracle.spmm_f64(rp, ci, v, 1, B, None, "gelu", lib=lib)
+        if abs(C[0, 0] - x * phi) > 2e-10 * max(1.0, abs(x)):
+            fails.append(f"gelu({x}) = {C[0, 0]!r}, table gives {x * phi!r}")
+        C, _ = oracle.spmm_f64(rp, ci, v, 1, B, None, "relu", lib=lib)
+        if C[0, 0] != max(x, 0.0):
+            fails.append(f"relu({x}) = {C[0, 0]!r}")
+    return fails
+
+
+def check_invariants(lib=None):
+    """Row-permutation equivariance (bit-exact) and exact linearity under scaling by 2."""
+    fails = []
+    rng = np.random.default_rng(7)
+    for trial in range(10):
+        M, K, N = 23, 31, 13
+        row_ptr, col_idx, vals, W = random_csr(rng, M, K, 0.2)
+        B = rng.standard_normal((K, N)).astype(np.float32)
+        bias = rng.standard_normal(M).astype(np.float32)
+        epi = ["none", "relu", "gelu"][trial % 3]
+        C, _ = oracle.spmm_f64(row_ptr, col_idx, vals, K, B, bias, epi, lib=lib)
+        pi = rng.permutation(M)
+        rp, ci, v = dense_to_csr(W[pi])
+        Cp, _ = oracle.spmm_f64(rp, ci, v, K, B, bias[pi], epi, lib=lib)
+        if not np.array_equal(Cp, C[pi]):
+            fails.append("row permutation is not bit-exactly equivariant")
+        C1, _ = oracle.spmm_f64(row_ptr, col_idx, vals, K, B, None, "none", lib=lib)
+        C2, _ = oracle.spmm_f64(row_ptr, col_idx, vals, K, 2 * B, None, "none", lib=lib)
+        if not np.array_equal(C2, 2 * C1):
+            fails.append("scaling B by 2 does not scale C by 2 exactly")
+    return fails
+
+
+def _reorder_properties(row_ptr, col_idx, K, perm):
+    """Tie-break-free properties of Algorithm 1: bijection, first = a densest row,
+    every later pick attains the maximum overlap with its predecessor."""
+    M = len(row_ptr) - 1
+    sets = [set(col_idx[row_ptr[i]:row_ptr[i + 1]].tolist()) for i in range(M)]
+    if sorted(perm.tolist()) != list(range(M)):
+        return "not a bijection"
+    if M and len(sets[perm[0]]) != max(len(s) for s in sets):
+        return "first row is not a densest row"
+    remaining = set(range(M)) - {int(perm[0])}
+    for i in range(1, M):
+        prev = sets[perm[i - 1]]
+        best = max(len(prev & sets[x]) for x in remaining)
+        if len(prev & sets[perm[i]]) != best:
+            return f"pick {i} does not maximise overlap"
+        remaining.discard(int(perm[i]))
+    return None
+
+
+def check_reorder(lib=None):
+    """Worked examples (exact permutation, pins the tie-break), and the tie-break-free
+    properties exhaustively over all 3x3 and random 5x6 binary patterns."""
+    fails = []
+    for name, K, rows, want in load_reorder_examples():
+        rp, ci, _ = pattern_to_csr(rows, K)
+        got = oracle.reorder(rp, ci, K, lib=lib).tolist()
+        if got != want:
+            fails.append(f"reorder {name}: got {got}, want {want}")
+    for bits in range(512):
+        rows = [[c for c in range(3) if bits >> (3 * r + c) & 1] for r in range(3)]
+        rp, ci, _ = pattern_to_csr(rows, 3)
+        msg = _reorder_properties(rp, ci, 3, oracle.reorder(rp, ci, 3, lib=lib))
+        if msg:
+            fails.append(f"reorder 3x3 pattern {bits}: {msg}")
+            break
+    rng = np.random.default_rng(5)
+    for _ in range(300):
+        M, K = 5, 6
+        mask = rng.random((M, K)) < rng.choice([0.2, 0.4, 0.6])
+        rows = [list(np.nonzero(mask[i])[0]) for i in range(M)]
+        rp, ci, _ = pattern_to_csr(rows, K)
+        perm = oracle.reorder(rp, ci, K, lib=lib)
+        msg = _reorder_properties(rp, ci, K, perm)
+        if msg:
+            fails.append(f"reorder random 5x6: {msg}")
+            break
+        # full tie-break check by brute force over the key (overlap, nnz, -index)
+        sets = [set(r) for r in rows]
+        want = [max(range(M), key=lambda x: (len(sets[x]), -x))]
+        rem = set(range(M)) - {want[0]}
+        while rem:
+            prev = sets[want[-1]]
+            nxt = max(rem, key=lambda x: (len(prev & sets[x]), len(sets[x]), -x))
+            want.append(nxt)
+            rem.discard(nxt)
+        if perm.tolist() != want:
+            fails.append(f"reorder random 5x6 tie-break: got {perm.tolist()}, want {want}")
+            break
+    # identity cases: diagonal, empty, full
+    for W in (np.eye(6), np.zeros((6, 6)), np.ones((6, 6))):
+        rows = [list(np.nonzero(W[i])[0]) for i in range(6)]
+        rp, ci, _ = pattern_to_csr(rows, 6)
+        if oracle.reorder(rp, ci, 6, lib=lib).tolist() != list(range(6)):
+            fails.append("reorder of a diagonal/empty/full pattern is not the identity")
+    return fails
+
+
+ALL_CHECKS = [check_bruteforce, check_special_cases, check_gelu_table, check_invariants,
+              check_reorder]
+
+
+def run_all(lib=None):
+    fails = []
+    for chk in ALL_CHECKS:
+        fails.extend(chk(lib))
+    return fails

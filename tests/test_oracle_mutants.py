@@ -1,0 +1,59 @@
+"""Plants plausible mistakes in a copy of the oracle (on the CPU) and checks that the
+pins reject every one of them.  The real oracle source is never modified."""
+import os
+import shutil
+import subprocess
+import tempfile
+
+import pytest
+
+import _pins
+import oracle
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
+
+# (name, text in oracle.c, replacement): each is a mistake a careful reader might make
+MUTANTS = [
+    ("drop_last_term", "p < row_ptr[i + 1]; ++p) {\n      const double w",
+     "p < row_ptr[i + 1] - 1; ++p) {\n      const double w"),
+    ("wrong_sign", "acc[n] += t;", "acc[n] -= t;"),
+    ("wrong_B_row", "const float* brow = B + (size_t)col_idx[p] * N;\n      for (int32_t n = 0; n < N; ++n) {\n        const double t",
+     "const float* brow = B + (size_t)col_idx[row_ptr[i]] * N;\n      for (int32_t n = 0; n < N; ++n) {\n        const double t"),
+    ("bias_dropped", "acc[n] = act_f64(acc[n] + bi, epi);", "acc[n] = act_f64(acc[n], epi);"),
+    ("bias_wrong_row", "const double bi = bias ? (double)bias[i] : 0.0;",
+     "const double bi = bias ? (double)bias[0] : 0.0;"),
+    ("gelu_tanh_approx", "return 0.5 * x * (1.0 + erf(x / sqrt(2.0)));",
+     "return 0.5 * x * (1.0 + tanh(0.7978845608028654 * (x + 0.044715 * x * x * x)));"),
+    ("gelu_no_sqrt2", "return 0.5 * x * (1.0 + erf(x / sqrt(2.0)));",
+     "return 0.5 * x * (1.0 + erf(x));"),
+    ("relu_identity", "if (epi == 1) return x > 0.0 ? x : 0.0;", "if (epi == 1) return x;"),
+    ("bound_signed", "bnd[n] += fabs(t);", "bnd[n] += t;"),
+    ("reorder_first_sparsest", "if (nx > nf) first = x;", "if (nx < nf) first = x;"),
+    ("reorder_against_first_row", "const int32_t prev = perm_out[i - 1];",
+     "const int32_t prev = perm_out[0];"),
+    ("reorder_index_only_ties", "(ov == best_ov && xn > best_nnz)", "(0)"),
+    ("reorder_last_index_ties", "(ov == best_ov && xn > best_nnz)", "(ov == best_ov && xn >= best_nnz)"),
+    ("reorder_merge_wrong_advance", "} else if (a[i] < b[j]) {", "} else if (a[i] > b[j]) {"),
+    ("reorder_fewest_overlap", "if (ov > best_ov ||", "if (best_ov < 0 || ov < best_ov ||"),
+]
+
+
+@pytest.fixture(scope="module")
+def workdir():
+    d = tempfile.mkdtemp(prefix="oracle_mut_")
+    yield d
+    shutil.rmtree(d, ignore_errors=True)
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_reject_mutant(workdir, name, old, new):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique"
+    path = os.path.join(workdir, f"{name}.c")
+    open(path, "w").write(src.replace(old, new))
+    so = os.path.join(workdir, f"lib{name}.so")
+    subprocess.run(["gcc", "-O1", "-fopenmp", "-fPIC", "-shared", "-o", so, path, "-lm"],
+                   check=True)
+    lib = oracle.load(so)
+    fails = _pins.run_all(lib)
+    assert fails, f"no pin rejects the planted mistake {name}"
