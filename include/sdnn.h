@@ -44,7 +44,8 @@ typedef enum {
   SDNN_ERR_CSR = 3,    /* malformed CSR: row_ptr, column range, unsorted/duplicate cols */
   SDNN_ERR_ALLOC = 4,  /* host or device allocation failed */
   SDNN_ERR_HIP = 5,    /* a HIP runtime call or kernel launch failed */
-  SDNN_ERR_DEVICE = 6  /* plan used on a device other than the one it was created on */
+  SDNN_ERR_DEVICE = 6, /* plan used on a device other than the one it was created on */
+  SDNN_ERR_INTERNAL = 7 /* the packed stream failed its own consistency check */
 } sdnn_status;
 
 /* Fused epilogue applied after the bias add (Sec. 3.1 layer fusion; GELU is the exact
@@ -94,6 +95,16 @@ sdnn_status sdnn_reorder_rows(const int32_t* row_ptr, const int32_t* col_idx, in
 sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx,
                              const float* values, int32_t M, int32_t K,
                              const sdnn_plan_opts* opts, sdnn_plan* out);
+
+/* Host-only self-check of the preparation stage (no GPU needed): validates the CSR,
+ * computes the permutation and packs the stream exactly as sdnn_plan_create does,
+ * then re-walks the stream and checks that every stored entry appears exactly once,
+ * in its row's panel and K-chunk, in ascending column order, with unchanged weight
+ * bits and a column offset inside its chunk.  On success fills *info if non-NULL.
+ * Errors: as sdnn_plan_create, plus SDNN_ERR_INTERNAL if the stream is inconsistent. */
+sdnn_status sdnn_plan_check_host(const int32_t* row_ptr, const int32_t* col_idx,
+                                 const float* values, int32_t M, int32_t K,
+                                 const sdnn_plan_opts* opts, sdnn_plan_info_t* info);
 
 /* Copies the plan's permutation (M int32, host memory) to perm_out. */
 sdnn_status sdnn_plan_get_perm(sdnn_plan p, int32_t* perm_out);

@@ -1,0 +1,229 @@
+"""MI355X (gfx950) sparse-weight x dense-activation product of SparseDNN (arXiv 2101.07948).
+
+Thin ctypes binding over ``libsdnn.so`` (C ABI in ``include/sdnn.h``).  Every step of
+the operator runs in the library: this module only checks shapes and dtypes, passes
+raw pointers and the current HIP stream, and turns status codes into exceptions.
+PyTorch supplies device memory and streams.  There is no fallback path: if the
+library is missing, every call raises.
+
+    plan = Plan(row_ptr, col_idx, values, M, K)    # preparation (Sec. 2.1, 3.1.2, 3.2.2)
+    plan.spmm(B, C, bias, "gelu")                   # execution: C = gelu(W @ B + bias)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsdnn.so")
+
+EPI = {"none": 0, "relu": 1, "gelu": 2}
+STATUS = {0: "SDNN_OK", 1: "SDNN_ERR_NULL", 2: "SDNN_ERR_DIM", 3: "SDNN_ERR_CSR",
+          4: "SDNN_ERR_ALLOC", 5: "SDNN_ERR_HIP", 6: "SDNN_ERR_DEVICE", 7: "SDNN_ERR_INTERNAL"}
+
+
+class SdnnError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {STATUS.get(code, code)}")
+
+
+class PlanOpts(ctypes.Structure):
+    _fields_ = [("panel_rows", ctypes.c_int32), ("permute", ctypes.c_int32)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int32), ("K", ctypes.c_int32), ("nnz", ctypes.c_int64),
+                ("panels", ctypes.c_int64), ("packed_bytes", ctypes.c_int64),
+                ("rho", ctypes.c_double), ("fill", ctypes.c_double),
+                ("panel_rows", ctypes.c_int32), ("k_chunk", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+_lib_handle = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libsdnn.so; raises if it has not been built."""
+    global _lib_handle
+    if _lib_handle is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2101_07948_amd.build` (no fallback path exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        p, i32 = ctypes.c_void_p, ctypes.c_int32
+        L.sdnn_status_str.argtypes = [ctypes.c_int]
+        L.sdnn_status_str.restype = ctypes.c_char_p
+        L.sdnn_reorder_rows.argtypes = [p, p, i32, i32, p]
+        L.sdnn_plan_check_host.argtypes = [p, p, p, i32, i32, ctypes.POINTER(PlanOpts),
+                                           ctypes.POINTER(PlanInfo)]
+        L.sdnn_plan_create.argtypes = [p, p, p, i32, i32, ctypes.POINTER(PlanOpts),
+                                       ctypes.POINTER(p)]
+        L.sdnn_plan_get_perm.argtypes = [p, p]
+        L.sdnn_plan_info.argtypes = [p, ctypes.POINTER(PlanInfo)]
+        L.sdnn_spmm.argtypes = [p, p, p, i32, p, ctypes.c_int, p]
+        L.sdnn_plan_destroy.argtypes = [p]
+        L.sdnn_plan_destroy.restype = None
+        L.sdnn_dense_gemm.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
+        for fn in ("sdnn_reorder_rows", "sdnn_plan_check_host", "sdnn_plan_create",
+                   "sdnn_plan_get_perm", "sdnn_plan_info", "sdnn_spmm", "sdnn_dense_gemm"):
+            getattr(L, fn).restype = ctypes.c_int
+        _lib_handle = L
+    return _lib_handle
+
+
+def _check(code: int, where: str):
+    if code != 0:
+        raise SdnnError(code, where)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _np_ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _opts(panel_rows: int, permute: bool) -> PlanOpts:
+    return PlanOpts(int(panel_rows), 1 if permute else 0)
+
+
+def reorder_rows(row_ptr, col_idx, K: int) -> np.ndarray:
+    """Algorithm 1 (Sec. 3.1.2) computed by the library on the host."""
+    row_ptr, col_idx = _i32(row_ptr), _i32(col_idx)
+    M = row_ptr.shape[0] - 1
+    perm = np.empty(M, dtype=np.int32)
+    _check(lib().sdnn_reorder_rows(_np_ptr(row_ptr), _np_ptr(col_idx), M, K, _np_ptr(perm)),
+           "sdnn_reorder_rows")
+    return perm
+
+
+def plan_check_host(row_ptr, col_idx, values, M: int, K: int, panel_rows: int = 0,
+                    permute: bool = True) -> dict:
+    """Host-only self-check of the preparation stage; returns the plan statistics."""
+    row_ptr, col_idx, values = _i32(row_ptr), _i32(col_idx), _f32(values)
+    info = PlanInfo()
+    o = _opts(panel_rows, permute)
+    _check(lib().sdnn_plan_check_host(_np_ptr(row_ptr), _np_ptr(col_idx), _np_ptr(values), M, K,
+                                      ctypes.byref(o), ctypes.byref(info)),
+           "sdnn_plan_check_host")
+    return info.as_dict()
+
+
+def _stream_handle(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev_ptr(t, name: str, shape, allow_none=False):
+    import torch
+    if t is None:
+        if allow_none:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError(f"{name} must be a CUDA/HIP torch tensor")
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous (row-major)")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class Plan:
+    """Preparation-stage result for one sparse weight matrix W (M x K, CSR on the host).
+
+    The plan owns device memory on the device that is current when it is created.
+    """
+
+    def __init__(self, row_ptr, col_idx, values, M: int, K: int, panel_rows: int = 0,
+                 permute: bool = True):
+        row_ptr, col_idx, values = _i32(row_ptr), _i32(col_idx), _f32(values)
+        self.M, self.K = int(M), int(K)
+        h = ctypes.c_void_p()
+        o = _opts(panel_rows, permute)
+        self._lib = lib()
+        _check(self._lib.sdnn_plan_create(_np_ptr(row_ptr), _np_ptr(col_idx), _np_ptr(values),
+                                          self.M, self.K, ctypes.byref(o), ctypes.byref(h)),
+               "sdnn_plan_create")
+        self._h = h
+
+    @classmethod
+    def from_csr(cls, W, **kw):
+        return cls(W.row_ptr, W.col_idx, W.values, W.M, W.K, **kw)
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise RuntimeError("plan is closed")
+        return self._h
+
+    @property
+    def perm(self) -> np.ndarray:
+        out = np.empty(self.M, dtype=np.int32)
+        _check(self._lib.sdnn_plan_get_perm(self.handle, _np_ptr(out)), "sdnn_plan_get_perm")
+        return out
+
+    @property
+    def info(self) -> dict:
+        info = PlanInfo()
+        _check(self._lib.sdnn_plan_info(self.handle, ctypes.byref(info)), "sdnn_plan_info")
+        return info.as_dict()
+
+    def spmm(self, B, C, bias=None, epi: str = "none", stream=None):
+        """C = act(W @ B + bias) on the GPU, enqueued on `stream` (default: current)."""
+        N = int(B.shape[1]) if B is not None and B.dim() == 2 else int(C.shape[1])
+        pb = _dev_ptr(B, "B", (self.K, N))
+        pc = _dev_ptr(C, "C", (self.M, N))
+        pbias = _dev_ptr(bias, "bias", (self.M,), allow_none=True)
+        _check(self._lib.sdnn_spmm(self.handle, pb, pc, N, pbias, EPI[epi],
+                                   _stream_handle(stream)), "sdnn_spmm")
+        return C
+
+    def close(self):
+        if getattr(self, "_h", None) is not None:
+            self._lib.sdnn_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+
+def dense_gemm(W, B, C, bias=None, epi: str = "none", stream=None):
+    """Dense FP32 comparison GEMM: C = act(W @ B + bias) (a measurement aid)."""
+    M, K = int(W.shape[0]), int(W.shape[1])
+    N = int(B.shape[1])
+    pw = _dev_ptr(W, "W", (M, K))
+    pb = _dev_ptr(B, "B", (K, N))
+    pc = _dev_ptr(C, "C", (M, N))
+    pbias = _dev_ptr(bias, "bias", (M,), allow_none=True)
+    _check(lib().sdnn_dense_gemm(pw, pb, pc, M, K, N, pbias, EPI[epi], _stream_handle(stream)),
+           "sdnn_dense_gemm")
+    return C
+
+
+def status_str(code: int) -> str:
+    return lib().sdnn_status_str(code).decode()

@@ -1,0 +1,462 @@
+// Host side of the C ABI: CSR validation, the greedy weight-row permutation
+// (Sec. 3.1.2, Algorithm 1) on column bitsets, packing of W into the kernel's
+// traversal-ordered stream (Sec. 3.2.2), plan lifetime and argument checks.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+#include <vector>
+
+#include "sdnn_internal.h"
+
+namespace sdnn {
+
+sdnn_status validate_csr(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K) {
+  if (M < 0 || K < 0) return SDNN_ERR_DIM;
+  if (!row_ptr) return SDNN_ERR_NULL;
+  if (row_ptr[0] != 0) return SDNN_ERR_CSR;
+  for (int32_t i = 0; i < M; ++i)
+    if (row_ptr[i + 1] < row_ptr[i]) return SDNN_ERR_CSR;
+  const int32_t nnz = row_ptr[M];
+  if (nnz > 0 && !col_idx) return SDNN_ERR_NULL;
+  for (int32_t i = 0; i < M; ++i) {
+    for (int32_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p) {
+      const int32_t c = col_idx[p];
+      if (c < 0 || c >= K) return SDNN_ERR_CSR;
+      if (p > row_ptr[i] && c <= col_idx[p - 1]) return SDNN_ERR_CSR;  // unsorted or duplicate
+    }
+  }
+  return SDNN_OK;
+}
+
+// Algorithm 1 with each row's column set held as ceil(K/64) 64-bit words; the overlap
+// |cols(prev) ∩ cols(x)| is a popcount of the AND.  Picks: first the densest row;
+// then, repeatedly, the remaining row with the largest overlap with the row placed
+// last.  Ties: more nonzeros first, then the lower original index.
+sdnn_status reorder_bitset(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K,
+                           int32_t* perm_out) {
+  if (M == 0) return SDNN_OK;
+  const int64_t words = (K + 63) / 64;
+  std::vector<uint64_t> bits;
+  std::vector<int32_t> remaining;
+  try {
+    bits.assign((size_t)M * (size_t)std::max<int64_t>(words, 1), 0);
+    remaining.resize(M);
+  } catch (const std::bad_alloc&) {
+    return SDNN_ERR_ALLOC;
+  }
+  for (int32_t i = 0; i < M; ++i) {
+    uint64_t* row = bits.data() + (size_t)i * words;
+    for (int32_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p)
+      row[col_idx[p] >> 6] |= 1ull << (col_idx[p] & 63);
+  }
+  auto nnz = [&](int32_t x) { return row_ptr[x + 1] - row_ptr[x]; };
+
+  int32_t first = 0;
+  for (int32_t x = 1; x < M; ++x)
+    if (nnz(x) > nnz(first)) first = x;
+  perm_out[0] = first;
+
+  // remaining rows, kept in ascending index order so equal keys resolve to the lower index
+  int32_t nrem = 0;
+  for (int32_t x = 0; x < M; ++x)
+    if (x != first) remaining[nrem++] = x;
+
+  for (int32_t i = 1; i < M; ++i) {
+    const uint64_t* prev = bits.data() + (size_t)perm_out[i - 1] * words;
+    int32_t best_pos = 0, best_ov = -1, best_nnz = -1;
+    for (int32_t j = 0; j < nrem; ++j) {
+      const int32_t x = remaining[j];
+      const uint64_t* row = bits.data() + (size_t)x * words;
+      int32_t ov = 0;
+      for (int64_t w = 0; w < words; ++w) ov += __builtin_popcountll(prev[w] & row[w]);
+      const int32_t nx = nnz(x);
+      if (ov > best_ov || (ov == best_ov && nx > best_nnz)) {
+        best_pos = j;
+        best_ov = ov;
+        best_nnz = nx;
+      }
+    }
+    perm_out[i] = remaining[best_pos];
+    // erase while keeping ascending order
+    memmove(remaining.data() + best_pos, remaining.data() + best_pos + 1,
+            sizeof(int32_t) * (size_t)(nrem - best_pos - 1));
+    --nrem;
+  }
+  return SDNN_OK;
+}
+
+sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* values, int32_t M,
+                 int32_t K, int32_t RW, const int32_t* perm, Packed* out) {
+  try {
+    Packed& P = *out;
+    P.M = M;
+    P.K = K;
+    P.RW = RW;
+    P.nnz = M ? row_ptr[M] : 0;
+    P.nchunks = (K + kChunk - 1) / kChunk;
+    P.npanels = (M + RW - 1) / RW;
+    P.perm.assign(perm, perm + M);
+    P.panel_rows.assign((size_t)P.npanels * RW, -1);
+    for (int32_t i = 0; i < M; ++i) P.panel_rows[i] = perm[i];
+    const size_t nseg = (size_t)P.npanels * P.nchunks;
+    P.seg_start.assign(nseg, 0);
+    P.counts.assign(nseg * RW, 0);
+    P.entries.resize((size_t)P.nnz * 2);
+
+    std::vector<int32_t> cursor(RW);
+    std::vector<int32_t> mark((size_t)std::max(K, 1), -1);
+    int64_t pos = 0, union_total = 0;
+    for (int32_t p = 0; p < P.npanels; ++p) {
+      for (int32_t r = 0; r < RW; ++r) {
+        const int32_t orig = P.panel_rows[(size_t)p * RW + r];
+        cursor[r] = orig >= 0 ? row_ptr[orig] : 0;
+        if (orig >= 0)
+          for (int32_t q = row_ptr[orig]; q < row_ptr[orig + 1]; ++q)
+            if (mark[col_idx[q]] != p) {
+              mark[col_idx[q]] = p;
+              ++union_total;
+            }
+      }
+      for (int32_t k = 0; k < P.nchunks; ++k) {
+        const int32_t hi = (k + 1) * kChunk;
+        P.seg_start[(size_t)p * P.nchunks + k] = (int32_t)pos;
+        for (int32_t r = 0; r < RW; ++r) {
+          const int32_t orig = P.panel_rows[(size_t)p * RW + r];
+          if (orig < 0) continue;
+          int32_t q = cursor[r];
+          const int32_t end = row_ptr[orig + 1];
+          int32_t c = 0;
+          while (q < end && col_idx[q] < hi) {
+            uint32_t wbits;
+            memcpy(&wbits, &values[q], 4);
+            P.entries[2 * pos] = wbits;
+            P.entries[2 * pos + 1] = (uint32_t)(col_idx[q] - k * kChunk);
+            ++pos;
+            ++q;
+            ++c;
+          }
+          cursor[r] = q;
+          P.counts[((size_t)p * P.nchunks + k) * RW + r] = (uint16_t)c;
+        }
+      }
+    }
+    P.rho = union_total ? (double)P.nnz / (double)union_total : 1.0;
+  } catch (const std::bad_alloc&) {
+    return SDNN_ERR_ALLOC;
+  }
+  return SDNN_OK;
+}
+
+// Independent re-walk of a packed stream: every CSR entry must appear exactly once, in
+// its row's panel and chunk, ascending, weight bits unchanged, offsets inside the chunk.
+static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const float* values,
+                         const Packed& P) {
+  std::vector<char> seen((size_t)P.nnz, 0);
+  std::vector<int32_t> pos_of_row((size_t)std::max(P.M, 1), 0);
+  for (int32_t i = 0; i < P.M; ++i) pos_of_row[i] = row_ptr[i];
+  for (int32_t p = 0; p < P.npanels; ++p) {
+    for (int32_t k = 0; k < P.nchunks; ++k) {
+      int64_t e = P.seg_start[(size_t)p * P.nchunks + k];
+      for (int32_t r = 0; r < P.RW; ++r) {
+        const int32_t orig = P.panel_rows[(size_t)p * P.RW + r];
+        const int32_t c = P.counts[((size_t)p * P.nchunks + k) * P.RW + r];
+        if (orig < 0) {
+          if (c != 0) return false;
+          continue;
+        }
+        for (int32_t j = 0; j < c; ++j, ++e) {
+          if (e < 0 || e >= P.nnz) return false;
+          const uint32_t off = P.entries[2 * e + 1];
+          if (off >= (uint32_t)kChunk) return false;
+          const int32_t col = k * kChunk + (int32_t)off;
+          const int32_t q = pos_of_row[orig]++;
+          if (q >= row_ptr[orig + 1] || col_idx[q] != col || seen[q]) return false;
+          uint32_t wbits;
+          memcpy(&wbits, &values[q], 4);
+          if (wbits != P.entries[2 * e]) return false;
+          seen[q] = 1;
+        }
+      }
+      const int64_t next = (k + 1 < P.nchunks) ? P.seg_start[(size_t)p * P.nchunks + k + 1]
+                           : (p + 1 < P.npanels) ? P.seg_start[(size_t)(p + 1) * P.nchunks]
+                                                 : P.nnz;
+      if (e != next) return false;
+    }
+  }
+  for (int64_t q = 0; q < P.nnz; ++q)
+    if (!seen[q]) return false;
+  std::vector<char> used((size_t)std::max(P.M, 1), 0);
+  for (int32_t i = 0; i < P.M; ++i) {
+    const int32_t x = P.perm[i];
+    if (x < 0 || x >= P.M || used[x]) return false;
+    used[x] = 1;
+  }
+  return true;
+}
+
+static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t* RW, int32_t* permute) {
+  *RW = 8;
+  *permute = 1;
+  if (opts) {
+    if (opts->panel_rows != 0) {
+      if (opts->panel_rows != 4 && opts->panel_rows != 8 && opts->panel_rows != 16)
+        return SDNN_ERR_DIM;
+      *RW = opts->panel_rows;
+    }
+    if (opts->permute != 0 && opts->permute != 1) return SDNN_ERR_DIM;
+    *permute = opts->permute;
+  }
+  return SDNN_OK;
+}
+
+static sdnn_status prepare(const int32_t* row_ptr, const int32_t* col_idx, const float* values,
+                           int32_t M, int32_t K, const sdnn_plan_opts* opts, Packed* P) {
+  int32_t RW, permute;
+  sdnn_status st = resolve_opts(opts, &RW, &permute);
+  if (st != SDNN_OK) return st;
+  st = validate_csr(row_ptr, col_idx, M, K);
+  if (st != SDNN_OK) return st;
+  if (M > 0 && row_ptr[M] > 0 && !values) return SDNN_ERR_NULL;
+  std::vector<int32_t> perm;
+  try {
+    perm.resize(M);
+  } catch (const std::bad_alloc&) {
+    return SDNN_ERR_ALLOC;
+  }
+  if (permute) {
+    st = reorder_bitset(row_ptr, col_idx, M, K, perm.data());
+    if (st != SDNN_OK) return st;
+  } else {
+    for (int32_t i = 0; i < M; ++i) perm[i] = i;
+  }
+  return pack(row_ptr, col_idx, values, M, K, RW, perm.data(), P);
+}
+
+static void fill_info(const Packed& P, int64_t packed_bytes, sdnn_plan_info_t* out) {
+  out->M = P.M;
+  out->K = P.K;
+  out->nnz = P.nnz;
+  out->panels = P.npanels;
+  out->packed_bytes = packed_bytes;
+  out->rho = P.rho;
+  out->fill = 1.0;
+  out->panel_rows = P.RW;
+  out->k_chunk = kChunk;
+}
+
+static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
+
+}  // namespace sdnn
+
+using namespace sdnn;
+
+extern "C" {
+
+const char* sdnn_status_str(sdnn_status s) {
+  switch (s) {
+    case SDNN_OK: return "SDNN_OK";
+    case SDNN_ERR_NULL: return "SDNN_ERR_NULL: required pointer is NULL";
+    case SDNN_ERR_DIM: return "SDNN_ERR_DIM: invalid size, option or overlapping buffers";
+    case SDNN_ERR_CSR: return "SDNN_ERR_CSR: malformed CSR input";
+    case SDNN_ERR_ALLOC: return "SDNN_ERR_ALLOC: allocation failed";
+    case SDNN_ERR_HIP: return "SDNN_ERR_HIP: HIP runtime or launch error";
+    case SDNN_ERR_DEVICE: return "SDNN_ERR_DEVICE: plan used on another device";
+    case SDNN_ERR_INTERNAL: return "SDNN_ERR_INTERNAL: packed stream failed its self-check";
+  }
+  return "SDNN_ERR_UNKNOWN";
+}
+
+sdnn_status sdnn_reorder_rows(const int32_t* row_ptr, const int32_t* col_idx, int32_t M,
+                              int32_t K, int32_t* perm_out) {
+  if (M < 0 || K < 0) return SDNN_ERR_DIM;
+  if (M > 0 && !perm_out) return SDNN_ERR_NULL;
+  sdnn_status st = validate_csr(row_ptr, col_idx, M, K);
+  if (st != SDNN_OK) return st;
+  try {
+    return reorder_bitset(row_ptr, col_idx, M, K, perm_out);
+  } catch (...) {
+    return SDNN_ERR_ALLOC;
+  }
+}
+
+sdnn_status sdnn_plan_check_host(const int32_t* row_ptr, const int32_t* col_idx,
+                                 const float* values, int32_t M, int32_t K,
+                                 const sdnn_plan_opts* opts, sdnn_plan_info_t* info) {
+  try {
+    Packed P;
+    sdnn_status st = prepare(row_ptr, col_idx, values, M, K, opts, &P);
+    if (st != SDNN_OK) return st;
+    if (!check_packed(row_ptr, col_idx, values, P)) return SDNN_ERR_INTERNAL;
+    if (info) {
+      const int64_t bytes = align256((int64_t)P.entries.size() * 4) +
+                            align256((int64_t)P.seg_start.size() * 4) +
+                            align256((int64_t)P.counts.size() * 2) +
+                            align256((int64_t)P.panel_rows.size() * 4);
+      fill_info(P, bytes, info);
+    }
+    return SDNN_OK;
+  } catch (...) {
+    return SDNN_ERR_ALLOC;
+  }
+}
+
+sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, const float* values,
+                             int32_t M, int32_t K, const sdnn_plan_opts* opts, sdnn_plan* out) {
+  if (!out) return SDNN_ERR_NULL;
+  *out = nullptr;
+  sdnn_plan_s* plan = nullptr;
+  try {
+    Packed P;
+    sdnn_status st = prepare(row_ptr, col_idx, values, M, K, opts, &P);
+    if (st != SDNN_OK) return st;
+
+    plan = new sdnn_plan_s();
+    if (hipGetDevice(&plan->device) != hipSuccess) {
+      delete plan;
+      return SDNN_ERR_HIP;
+    }
+    if (hipDeviceGetAttribute(&plan->num_cus, hipDeviceAttributeMultiprocessorCount,
+                              plan->device) != hipSuccess) {
+      delete plan;
+      return SDNN_ERR_HIP;
+    }
+    plan->M = P.M;
+    plan->K = P.K;
+    plan->RW = P.RW;
+    plan->nchunks = P.nchunks;
+    plan->npanels = P.npanels;
+    plan->nnz = P.nnz;
+    plan->rho = P.rho;
+    plan->fill = 1.0;
+    plan->perm = P.perm;
+
+    const int64_t b_ent = align256((int64_t)P.entries.size() * 4);
+    const int64_t b_seg = align256((int64_t)P.seg_start.size() * 4);
+    const int64_t b_cnt = align256((int64_t)P.counts.size() * 2);
+    const int64_t b_rows = align256((int64_t)P.panel_rows.size() * 4);
+    const int64_t total = b_ent + b_seg + b_cnt + b_rows;
+    plan->packed_bytes = total;
+    if (total > 0) {
+      if (hipMalloc(&plan->d_mem, (size_t)total) != hipSuccess) {
+        (void)hipGetLastError();
+        delete plan;
+        return SDNN_ERR_ALLOC;
+      }
+      char* base = (char*)plan->d_mem;
+      plan->d_entries = (const uint2*)base;
+      plan->d_seg = (const int32_t*)(base + b_ent);
+      plan->d_counts = (const uint16_t*)(base + b_ent + b_seg);
+      plan->d_panel_rows = (const int32_t*)(base + b_ent + b_seg + b_cnt);
+      std::vector<char> host((size_t)total, 0);
+      if (!P.entries.empty()) memcpy(host.data(), P.entries.data(), P.entries.size() * 4);
+      if (!P.seg_start.empty())
+        memcpy(host.data() + b_ent, P.seg_start.data(), P.seg_start.size() * 4);
+      if (!P.counts.empty())
+        memcpy(host.data() + b_ent + b_seg, P.counts.data(), P.counts.size() * 2);
+      if (!P.panel_rows.empty())
+        memcpy(host.data() + b_ent + b_seg + b_cnt, P.panel_rows.data(), P.panel_rows.size() * 4);
+      if (hipMemcpy(plan->d_mem, host.data(), (size_t)total, hipMemcpyHostToDevice) !=
+          hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipFree(plan->d_mem);
+        delete plan;
+        return SDNN_ERR_HIP;
+      }
+    }
+    *out = plan;
+    return SDNN_OK;
+  } catch (...) {
+    if (plan) {
+      if (plan->d_mem) (void)hipFree(plan->d_mem);
+      delete plan;
+    }
+    return SDNN_ERR_ALLOC;
+  }
+}
+
+sdnn_status sdnn_plan_get_perm(sdnn_plan p, int32_t* perm_out) {
+  if (!p) return SDNN_ERR_NULL;
+  if (p->M > 0 && !perm_out) return SDNN_ERR_NULL;
+  if (p->M > 0) memcpy(perm_out, p->perm.data(), sizeof(int32_t) * (size_t)p->M);
+  return SDNN_OK;
+}
+
+sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out) {
+  if (!p || !out) return SDNN_ERR_NULL;
+  out->M = p->M;
+  out->K = p->K;
+  out->nnz = p->nnz;
+  out->panels = p->npanels;
+  out->packed_bytes = p->packed_bytes;
+  out->rho = p->rho;
+  out->fill = p->fill;
+  out->panel_rows = p->RW;
+  out->k_chunk = kChunk;
+  return SDNN_OK;
+}
+
+void sdnn_plan_destroy(sdnn_plan p) {
+  if (!p) return;
+  if (p->d_mem) {
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    if (cur != p->device) (void)hipSetDevice(p->device);
+    (void)hipFree(p->d_mem);
+    if (cur != p->device && cur >= 0) (void)hipSetDevice(cur);
+  }
+  delete p;
+}
+
+static bool ranges_overlap(const void* a, int64_t abytes, const void* b, int64_t bbytes) {
+  if (!a || !b || abytes <= 0 || bbytes <= 0) return false;
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + (uintptr_t)bbytes && b0 < a0 + (uintptr_t)abytes;
+}
+
+sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
+                      sdnn_epilogue epi, void* stream) {
+  if (!p) return SDNN_ERR_NULL;
+  if (N < 0) return SDNN_ERR_DIM;
+  if (epi != SDNN_EPI_NONE && epi != SDNN_EPI_RELU && epi != SDNN_EPI_GELU) return SDNN_ERR_DIM;
+  if (p->M == 0 || N == 0) return SDNN_OK;
+  if (!C) return SDNN_ERR_NULL;
+  if (p->K > 0 && !B) return SDNN_ERR_NULL;
+  const int64_t bbytes = (int64_t)p->K * N * 4, cbytes = (int64_t)p->M * N * 4;
+  if (ranges_overlap(B, bbytes, C, cbytes)) return SDNN_ERR_DIM;
+  if (ranges_overlap(bias, (int64_t)p->M * 4, C, cbytes)) return SDNN_ERR_DIM;
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return SDNN_ERR_HIP;
+  if (cur != p->device) return SDNN_ERR_DEVICE;
+  try {
+    hipError_t e = launch_spmm(p, B, C, N, bias, (int)epi, (hipStream_t)stream);
+    return e == hipSuccess ? SDNN_OK : SDNN_ERR_HIP;
+  } catch (...) {
+    return SDNN_ERR_HIP;
+  }
+}
+
+sdnn_status sdnn_dense_gemm(const float* W, const float* B, float* C, int32_t M, int32_t K,
+                            int32_t N, const float* bias, sdnn_epilogue epi, void* stream) {
+  if (M < 0 || K < 0 || N < 0) return SDNN_ERR_DIM;
+  if (epi != SDNN_EPI_NONE && epi != SDNN_EPI_RELU && epi != SDNN_EPI_GELU) return SDNN_ERR_DIM;
+  if (M == 0 || N == 0) return SDNN_OK;
+  if (!C) return SDNN_ERR_NULL;
+  if (K > 0 && (!W || !B)) return SDNN_ERR_NULL;
+  const int64_t cbytes = (int64_t)M * N * 4;
+  if (ranges_overlap(B, (int64_t)K * N * 4, C, cbytes) ||
+      ranges_overlap(W, (int64_t)M * K * 4, C, cbytes) ||
+      ranges_overlap(bias, (int64_t)M * 4, C, cbytes))
+    return SDNN_ERR_DIM;
+  try {
+    hipError_t e = launch_dense(W, B, C, M, K, N, bias, (int)epi, (hipStream_t)stream);
+    return e == hipSuccess ? SDNN_OK : SDNN_ERR_HIP;
+  } catch (...) {
+    return SDNN_ERR_HIP;
+  }
+}
+
+}  // extern "C"

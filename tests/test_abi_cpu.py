@@ -1,0 +1,157 @@
+"""CPU-only tests of the C ABI library: exports, host-side preparation stage (CSR
+validation, Algorithm 1 on bitsets, packing) and error codes.  No GPU is touched:
+only host-only entry points are called, plus plan_create on inputs it must reject
+before any device work."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2101_07948_amd as sd
+from conftest import ROOT, pattern_to_csr, load_reorder_examples
+from paper_2101_07948_amd import inputs
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "sdnn.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sdnn_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_header_symbol():
+    L = sd.lib()
+    names = header_functions()
+    assert "sdnn_spmm" in names and "sdnn_plan_create" in names
+    for n in names:
+        assert hasattr(L, n), f"libsdnn.so does not export {n}"
+
+
+def test_status_strings():
+    for code, name in sd.STATUS.items():
+        assert sd.status_str(code).startswith(name)
+
+
+def test_destroy_null_is_noop():
+    sd.lib().sdnn_plan_destroy(None)
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c4", "w0", "c3"])
+def test_library_reorder_matches_oracle_on_workloads(name):
+    for L in inputs.workload(name, N=4).layers:
+        got = sd.reorder_rows(L.W.row_ptr, L.W.col_idx, L.W.K)
+        want = oracle.reorder(L.W.row_ptr, L.W.col_idx, L.W.K)
+        assert np.array_equal(got, want)
+
+
+def test_library_reorder_matches_oracle_grouped():
+    W = inputs.pattern_grouped8(768, 768, 0.03, inputs.CFG_C5, 0, 0.1)
+    assert np.array_equal(sd.reorder_rows(W.row_ptr, W.col_idx, W.K),
+                          oracle.reorder(W.row_ptr, W.col_idx, W.K))
+
+
+def test_library_reorder_worked_examples_and_random():
+    for name, K, rows, want in load_reorder_examples():
+        rp, ci, _ = pattern_to_csr(rows, K)
+        assert sd.reorder_rows(rp, ci, K).tolist() == want, name
+    rng = np.random.default_rng(11)
+    for _ in range(200):
+        M, K = int(rng.integers(1, 12)), int(rng.integers(1, 140))
+        mask = rng.random((M, K)) < rng.choice([0.05, 0.3, 0.7])
+        rows = [list(np.nonzero(mask[i])[0]) for i in range(M)]
+        rp, ci, _ = pattern_to_csr(rows, K)
+        assert np.array_equal(sd.reorder_rows(rp, ci, K), oracle.reorder(rp, ci, K))
+    for bits in range(512):  # every 3x3 pattern
+        rows = [[c for c in range(3) if bits >> (3 * r + c) & 1] for r in range(3)]
+        rp, ci, _ = pattern_to_csr(rows, 3)
+        assert np.array_equal(sd.reorder_rows(rp, ci, 3), oracle.reorder(rp, ci, 3))
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c4", "w0", "c3"])
+@pytest.mark.parametrize("panel_rows", [4, 8, 16])
+def test_packed_stream_self_check(name, panel_rows):
+    for L in inputs.workload(name, N=4).layers:
+        info = sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K,
+                                  panel_rows=panel_rows)
+        assert info["nnz"] == L.W.nnz and info["M"] == L.W.M and info["K"] == L.W.K
+        assert info["panels"] == -(-L.W.M // panel_rows)
+        assert info["rho"] >= 1.0 and info["fill"] == 1.0
+
+
+def test_permutation_raises_reuse_on_grouped_columns():
+    """Algorithm 1's purpose (Sec. 3.1.2): adjacent rows share columns.  On block-
+    correlated rows the panel reuse factor rho must improve over the identity order."""
+    W = inputs.pattern_grouped8(768, 768, 0.03, inputs.CFG_C5, 0, 0.1)
+    on = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, panel_rows=8)
+    off = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, panel_rows=8,
+                             permute=False)
+    assert on["rho"] > 1.3 * off["rho"]
+
+
+def test_edge_shapes_pack():
+    cases = [
+        ([[]], 5),                 # one empty row
+        ([[0]], 1),                # 1 x 1
+        ([[], [], []], 0),         # K = 0
+        ([[0, 63, 64, 127, 128]], 129),  # chunk boundaries
+        ([list(range(200))] * 3, 200),   # dense rows spanning chunks
+    ]
+    for rows, K in cases:
+        rp, ci, v = pattern_to_csr(rows, K)
+        info = sd.plan_check_host(rp, ci, v, len(rows), K)
+        assert info["nnz"] == len(ci)
+    # M = 0
+    info = sd.plan_check_host(np.zeros(1, np.int32), np.zeros(0, np.int32),
+                              np.zeros(0, np.float32), 0, 7)
+    assert info["panels"] == 0
+
+
+def _expect(code, fn):
+    with pytest.raises(sd.SdnnError) as ei:
+        fn()
+    assert ei.value.code == code, str(ei.value)
+
+
+@pytest.mark.parametrize("entry", ["check", "create", "reorder"])
+def test_bad_csr_rejected(entry):
+    def run(rp, ci, v, M, K):
+        if entry == "check":
+            return sd.plan_check_host(rp, ci, v, M, K)
+        if entry == "create":
+            return sd.Plan(rp, ci, v, M, K)
+        return sd.reorder_rows(rp, ci, K) if len(rp) == M + 1 else None
+
+    v3 = np.ones(3, np.float32)
+    _expect(3, lambda: run(np.array([1, 2, 3], np.int32), np.array([0, 1, 2], np.int32), v3, 2, 4))  # row_ptr[0] != 0
+    _expect(3, lambda: run(np.array([0, 2, 1], np.int32), np.array([0, 1], np.int32), v3, 2, 4))  # non-monotone
+    _expect(3, lambda: run(np.array([0, 2, 3], np.int32), np.array([0, 1, 4], np.int32), v3, 2, 4))  # col >= K
+    _expect(3, lambda: run(np.array([0, 2, 3], np.int32), np.array([0, -1, 2], np.int32), v3, 2, 4))  # col < 0
+    _expect(3, lambda: run(np.array([0, 2, 3], np.int32), np.array([1, 0, 2], np.int32), v3, 2, 4))  # unsorted
+    _expect(3, lambda: run(np.array([0, 2, 3], np.int32), np.array([1, 1, 2], np.int32), v3, 2, 4))  # duplicate
+
+
+def test_bad_dims_and_nulls():
+    L = sd.lib()
+    rp = np.array([0, 1], np.int32)
+    ci = np.array([0], np.int32)
+    v = np.ones(1, np.float32)
+    P = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    perm = np.zeros(1, np.int32)
+    assert L.sdnn_reorder_rows(P(rp), P(ci), -1, 4, P(perm)) == 2
+    assert L.sdnn_reorder_rows(None, P(ci), 1, 4, P(perm)) == 1
+    assert L.sdnn_reorder_rows(P(rp), None, 1, 4, P(perm)) == 1
+    assert L.sdnn_reorder_rows(P(rp), P(ci), 1, 4, None) == 1
+    info = sd.PlanInfo()
+    assert L.sdnn_plan_check_host(P(rp), P(ci), None, 1, 4, None, ctypes.byref(info)) == 1
+    bad = sd.PlanOpts(5, 1)
+    assert L.sdnn_plan_check_host(P(rp), P(ci), P(v), 1, 4, ctypes.byref(bad), None) == 2
+    bad = sd.PlanOpts(8, 3)
+    assert L.sdnn_plan_check_host(P(rp), P(ci), P(v), 1, 4, ctypes.byref(bad), None) == 2
+    assert L.sdnn_plan_create(P(rp), P(ci), P(v), 1, 4, None, None) == 1
+    assert L.sdnn_plan_get_perm(None, P(perm)) == 1
+    assert L.sdnn_plan_info(None, ctypes.byref(info)) == 1
+    assert L.sdnn_spmm(None, None, None, 4, None, 0, None) == 1
+    assert L.sdnn_dense_gemm(None, None, None, -1, 4, 4, None, 0, None) == 2
+    assert L.sdnn_dense_gemm(None, None, None, 0, 4, 4, None, 0, None) == 0  # M = 0: no-op
