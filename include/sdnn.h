@@ -57,7 +57,7 @@ typedef enum {
 } sdnn_epilogue;
 
 /* Options for sdnn_plan_create; pass NULL for the defaults {0, 1}.
- *   panel_rows: rows per register panel (0 = library default; otherwise 4, 8 or 16).
+ *   panel_rows: rows per register panel (0 = library default 4; otherwise 4, 8, 12 or 16).
  *   permute:    1 = apply Algorithm 1 (default), 0 = identity order (ablation). */
 typedef struct {
   int32_t panel_rows;

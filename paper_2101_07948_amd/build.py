@@ -22,6 +22,13 @@ def hipcc() -> str:
 
 
 def build(verbose: bool = False) -> str:
+    # regenerate the inline-assembly inner loop (a pure function of its generator)
+    sys.path.insert(0, os.path.join(HERE, "csrc"))
+    try:
+        import gen_spmm_asm
+        gen_spmm_asm.main()
+    finally:
+        sys.path.pop(0)
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [hipcc()] + HIPCC_FLAGS + ["-o", tmp] + SOURCES
     res = subprocess.run(cmd, capture_output=True, text=True)

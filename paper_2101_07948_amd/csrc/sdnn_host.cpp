@@ -103,13 +103,14 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
     P.panel_rows.assign((size_t)P.npanels * RW, -1);
     for (int32_t i = 0; i < M; ++i) P.panel_rows[i] = perm[i];
     const size_t nseg = (size_t)P.npanels * P.nchunks;
-    P.seg_start.assign(nseg, 0);
+    P.seg_start.assign(nseg + 1, 0);
     P.counts.assign(nseg * RW, 0);
-    P.entries.resize((size_t)P.nnz * 2);
+    P.entries.clear();
+    P.entries.reserve((size_t)(P.nnz + P.nnz / 2 + 64) * 2);
 
     std::vector<int32_t> cursor(RW);
     std::vector<int32_t> mark((size_t)std::max(K, 1), -1);
-    int64_t pos = 0, union_total = 0;
+    int64_t union_total = 0;
     for (int32_t p = 0; p < P.npanels; ++p) {
       for (int32_t r = 0; r < RW; ++r) {
         const int32_t orig = P.panel_rows[(size_t)p * RW + r];
@@ -123,7 +124,9 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
       }
       for (int32_t k = 0; k < P.nchunks; ++k) {
         const int32_t hi = (k + 1) * kChunk;
-        P.seg_start[(size_t)p * P.nchunks + k] = (int32_t)pos;
+        P.seg_start[(size_t)p * P.nchunks + k] = (int32_t)(P.entries.size() / (2 * kGroup));
+        // gather the segment's entries row by row, then write them group-wise
+        std::vector<uint32_t> w, a;
         for (int32_t r = 0; r < RW; ++r) {
           const int32_t orig = P.panel_rows[(size_t)p * RW + r];
           if (orig < 0) continue;
@@ -133,16 +136,30 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
           while (q < end && col_idx[q] < hi) {
             uint32_t wbits;
             memcpy(&wbits, &values[q], 4);
-            P.entries[2 * pos] = wbits;
-            P.entries[2 * pos + 1] = (uint32_t)(col_idx[q] - k * kChunk);
-            ++pos;
+            w.push_back(wbits);
+            a.push_back(((uint32_t)(col_idx[q] - k * kChunk) << 10) | (uint32_t)r);
             ++q;
             ++c;
           }
           cursor[r] = q;
           P.counts[((size_t)p * P.nchunks + k) * RW + r] = (uint16_t)c;
         }
+        while (w.size() % kGroup != 0) {  // zero padding to whole groups
+          w.push_back(0u);
+          a.push_back(0u);
+        }
+        for (size_t g = 0; g < w.size(); g += kGroup) {
+          for (int j = 0; j < kGroup; ++j) P.entries.push_back(w[g + j]);
+          for (int j = 0; j < kGroup; ++j) P.entries.push_back(a[g + j]);
+        }
       }
+    }
+    P.stored = (int64_t)(P.entries.size() / 2);
+    if (P.stored > INT32_MAX - kTailGroups * kGroup) return SDNN_ERR_DIM;
+    P.seg_start[nseg] = (int32_t)(P.stored / kGroup);
+    for (int i = 0; i < kTailGroups * kGroup; ++i) {  // tail padding for the prefetch
+      P.entries.push_back(0u);
+      P.entries.push_back(0u);
     }
     P.rho = union_total ? (double)P.nnz / (double)union_total : 1.0;
   } catch (const std::bad_alloc&) {
@@ -152,43 +169,55 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
 }
 
 // Independent re-walk of a packed stream: every CSR entry must appear exactly once, in
-// its row's panel and chunk, ascending, weight bits unchanged, offsets inside the chunk.
+// its row's panel and chunk, rows in panel order, columns ascending, weight bits
+// unchanged, offsets inside the chunk; each segment ends with fewer than kGroup zero
+// padding entries, and the stream with kTailGroups zero groups.
 static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const float* values,
                          const Packed& P) {
   std::vector<char> seen((size_t)P.nnz, 0);
   std::vector<int32_t> pos_of_row((size_t)std::max(P.M, 1), 0);
   for (int32_t i = 0; i < P.M; ++i) pos_of_row[i] = row_ptr[i];
+  if ((int64_t)P.entries.size() != 2 * (P.stored + kTailGroups * kGroup)) return false;
+  if (P.stored % kGroup != 0) return false;
+  auto weight = [&](int64_t e) { return P.entries[(e / kGroup) * 2 * kGroup + (e % kGroup)]; };
+  auto word = [&](int64_t e) {
+    return P.entries[(e / kGroup) * 2 * kGroup + kGroup + (e % kGroup)];
+  };
   for (int32_t p = 0; p < P.npanels; ++p) {
     for (int32_t k = 0; k < P.nchunks; ++k) {
-      int64_t e = P.seg_start[(size_t)p * P.nchunks + k];
+      const size_t s = (size_t)p * P.nchunks + k;
+      int64_t e = (int64_t)P.seg_start[s] * kGroup;
+      const int64_t end = (int64_t)P.seg_start[s + 1] * kGroup;
+      if (end < e || end > P.stored) return false;
       for (int32_t r = 0; r < P.RW; ++r) {
         const int32_t orig = P.panel_rows[(size_t)p * P.RW + r];
-        const int32_t c = P.counts[((size_t)p * P.nchunks + k) * P.RW + r];
-        if (orig < 0) {
-          if (c != 0) return false;
-          continue;
-        }
+        const int32_t c = P.counts[s * P.RW + r];
+        if (orig < 0 && c != 0) return false;
         for (int32_t j = 0; j < c; ++j, ++e) {
-          if (e < 0 || e >= P.nnz) return false;
-          const uint32_t off = P.entries[2 * e + 1];
+          if (e >= end) return false;
+          const uint32_t wd = word(e);
+          if ((int32_t)(wd & 0x3ffu) != r) return false;
+          if ((wd & 0x300u) != 0u) return false;
+          const uint32_t off = wd >> 10;
           if (off >= (uint32_t)kChunk) return false;
           const int32_t col = k * kChunk + (int32_t)off;
           const int32_t q = pos_of_row[orig]++;
           if (q >= row_ptr[orig + 1] || col_idx[q] != col || seen[q]) return false;
-          uint32_t wbits;
-          memcpy(&wbits, &values[q], 4);
-          if (wbits != P.entries[2 * e]) return false;
+          uint32_t vbits;
+          memcpy(&vbits, &values[q], 4);
+          if (vbits != weight(e)) return false;
           seen[q] = 1;
         }
       }
-      const int64_t next = (k + 1 < P.nchunks) ? P.seg_start[(size_t)p * P.nchunks + k + 1]
-                           : (p + 1 < P.npanels) ? P.seg_start[(size_t)(p + 1) * P.nchunks]
-                                                 : P.nnz;
-      if (e != next) return false;
+      if (end - e >= kGroup) return false;  // at most kGroup-1 padding entries
+      for (; e < end; ++e)
+        if (weight(e) != 0u || word(e) != 0u) return false;
     }
   }
   for (int64_t q = 0; q < P.nnz; ++q)
     if (!seen[q]) return false;
+  for (size_t d = (size_t)(2 * P.stored); d < P.entries.size(); ++d)
+    if (P.entries[d] != 0u) return false;
   std::vector<char> used((size_t)std::max(P.M, 1), 0);
   for (int32_t i = 0; i < P.M; ++i) {
     const int32_t x = P.perm[i];
@@ -199,11 +228,12 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
 }
 
 static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t* RW, int32_t* permute) {
-  *RW = 8;
+  *RW = 4;
   *permute = 1;
   if (opts) {
     if (opts->panel_rows != 0) {
-      if (opts->panel_rows != 4 && opts->panel_rows != 8 && opts->panel_rows != 16)
+      if (opts->panel_rows != 4 && opts->panel_rows != 8 && opts->panel_rows != 12 &&
+          opts->panel_rows != 16)
         return SDNN_ERR_DIM;
       *RW = opts->panel_rows;
     }
@@ -243,7 +273,7 @@ static void fill_info(const Packed& P, int64_t packed_bytes, sdnn_plan_info_t* o
   out->panels = P.npanels;
   out->packed_bytes = packed_bytes;
   out->rho = P.rho;
-  out->fill = 1.0;
+  out->fill = P.stored ? (double)P.nnz / (double)P.stored : 1.0;
   out->panel_rows = P.RW;
   out->k_chunk = kChunk;
 }
@@ -294,7 +324,6 @@ sdnn_status sdnn_plan_check_host(const int32_t* row_ptr, const int32_t* col_idx,
     if (info) {
       const int64_t bytes = align256((int64_t)P.entries.size() * 4) +
                             align256((int64_t)P.seg_start.size() * 4) +
-                            align256((int64_t)P.counts.size() * 2) +
                             align256((int64_t)P.panel_rows.size() * 4);
       fill_info(P, bytes, info);
     }
@@ -331,14 +360,13 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
     plan->npanels = P.npanels;
     plan->nnz = P.nnz;
     plan->rho = P.rho;
-    plan->fill = 1.0;
+    plan->fill = P.stored ? (double)P.nnz / (double)P.stored : 1.0;
     plan->perm = P.perm;
 
     const int64_t b_ent = align256((int64_t)P.entries.size() * 4);
     const int64_t b_seg = align256((int64_t)P.seg_start.size() * 4);
-    const int64_t b_cnt = align256((int64_t)P.counts.size() * 2);
     const int64_t b_rows = align256((int64_t)P.panel_rows.size() * 4);
-    const int64_t total = b_ent + b_seg + b_cnt + b_rows;
+    const int64_t total = b_ent + b_seg + b_rows;
     plan->packed_bytes = total;
     if (total > 0) {
       if (hipMalloc(&plan->d_mem, (size_t)total) != hipSuccess) {
@@ -347,18 +375,15 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
         return SDNN_ERR_ALLOC;
       }
       char* base = (char*)plan->d_mem;
-      plan->d_entries = (const uint2*)base;
+      plan->d_entries = (const uint32_t*)base;
       plan->d_seg = (const int32_t*)(base + b_ent);
-      plan->d_counts = (const uint16_t*)(base + b_ent + b_seg);
-      plan->d_panel_rows = (const int32_t*)(base + b_ent + b_seg + b_cnt);
+      plan->d_panel_rows = (const int32_t*)(base + b_ent + b_seg);
       std::vector<char> host((size_t)total, 0);
       if (!P.entries.empty()) memcpy(host.data(), P.entries.data(), P.entries.size() * 4);
       if (!P.seg_start.empty())
         memcpy(host.data() + b_ent, P.seg_start.data(), P.seg_start.size() * 4);
-      if (!P.counts.empty())
-        memcpy(host.data() + b_ent + b_seg, P.counts.data(), P.counts.size() * 2);
       if (!P.panel_rows.empty())
-        memcpy(host.data() + b_ent + b_seg + b_cnt, P.panel_rows.data(), P.panel_rows.size() * 4);
+        memcpy(host.data() + b_ent + b_seg, P.panel_rows.data(), P.panel_rows.size() * 4);
       if (hipMemcpy(plan->d_mem, host.data(), (size_t)total, hipMemcpyHostToDevice) !=
           hipSuccess) {
         (void)hipGetLastError();

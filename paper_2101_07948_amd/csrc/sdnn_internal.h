@@ -16,22 +16,33 @@ namespace sdnn {
 // tiling of the dense operand, Sec. 3.2.2).  The packed stream is cut at these
 // boundaries, so the value is fixed at plan creation.
 constexpr int kChunk = 64;
+// Stream entries are consumed in groups of kGroup.
+constexpr int kGroup = 4;
+// Columns of C per workgroup tile: 64 lanes x 4 consecutive columns.
+constexpr int kTileCols = 256;
+// Zero groups appended after the last segment: the kernel's stream prefetch may read
+// this many groups past the end of a segment.
+constexpr int kTailGroups = 4;
 
 // Host-side packed form of W in the kernel's traversal order (Sec. 3.2.2: each
 // matrix stored in its own format, read sequentially).
 //
-//   panels of RW consecutive rows of the permuted matrix; for panel p and chunk k
-//   the segment holds, for r = 0..RW-1, the entries of row p*RW+r whose column lies
-//   in [k*kChunk, (k+1)*kChunk), ascending by column.  An entry is two 32-bit words:
-//   the fp32 weight bits and the column offset inside the chunk.
+//   Panels of RW consecutive rows of the permuted matrix.  For panel p and chunk k the
+//   segment holds the entries of rows 0..RW-1 of the panel (row by row, each row in
+//   ascending column order) whose column lies in [k*kChunk, (k+1)*kChunk), padded at
+//   its end with zero entries to whole groups.  A group of kGroup entries is stored as
+//   2*kGroup dwords: the kGroup fp32 weight bits, then kGroup words
+//   (column offset inside the chunk << 10) | r.  The stream ends with kTailGroups zero
+//   groups so that a kernel may prefetch that many groups past the last segment.
 struct Packed {
   int32_t M = 0, K = 0, RW = 0, nchunks = 0, npanels = 0;
-  int64_t nnz = 0;
+  int64_t nnz = 0, stored = 0;     // structural entries, stored entries (with padding)
   std::vector<int32_t> perm;        // [M]   original row at permuted position
   std::vector<int32_t> panel_rows;  // [npanels*RW] original row or -1 (padding)
-  std::vector<int32_t> seg_start;   // [npanels*nchunks] first entry of each segment
-  std::vector<uint16_t> counts;     // [npanels*nchunks*RW] entries per (panel, chunk, row)
-  std::vector<uint32_t> entries;    // [2*nnz] (weight bits, column in chunk)
+  std::vector<int32_t> seg_start;   // [npanels*nchunks + 1] first group of each segment
+  std::vector<uint16_t> counts;     // [npanels*nchunks*RW] real entries per (panel, chunk, row)
+                                    // (host-side only, used by the self-check)
+  std::vector<uint32_t> entries;    // [2*(stored + kTailGroups*kGroup)] dwords
   double rho = 1.0;                 // nnz / sum_p |union of the panel's column sets|
 };
 
@@ -54,10 +65,9 @@ struct sdnn_plan_s {
   int64_t nnz = 0, packed_bytes = 0;
   double rho = 1.0, fill = 1.0;
   std::vector<int32_t> perm;
-  void* d_mem = nullptr;             // one device allocation holding the four arrays
-  const uint2* d_entries = nullptr;  // [nnz]
-  const int32_t* d_seg = nullptr;    // [npanels*nchunks]
-  const uint16_t* d_counts = nullptr;  // [npanels*nchunks*RW]
+  void* d_mem = nullptr;             // one device allocation holding the three arrays
+  const uint32_t* d_entries = nullptr;  // [2*(stored + kTailGroups*kGroup)] dwords
+  const int32_t* d_seg = nullptr;    // [npanels*nchunks + 1] (in groups)
   const int32_t* d_panel_rows = nullptr;  // [npanels*RW]
 };
 

@@ -28,15 +28,13 @@ def tolerance(bound, ref, epi):
 
 
 class Forced:
-    """Forces the kernel variant (columns per lane, waves per workgroup) for a call."""
+    """Forces the launch shape (waves per workgroup) for a call."""
 
-    def __init__(self, V=None, waves=None):
-        self.V, self.waves = V, waves
+    def __init__(self, waves=None):
+        self.waves = waves
 
     def __enter__(self):
-        self.old = {k: os.environ.get(k) for k in ("SDNN_FORCE_V", "SDNN_FORCE_WAVES")}
-        if self.V:
-            os.environ["SDNN_FORCE_V"] = str(self.V)
+        self.old = {k: os.environ.get(k) for k in ("SDNN_FORCE_WAVES",)}
         if self.waves:
             os.environ["SDNN_FORCE_WAVES"] = str(self.waves)
 
@@ -57,10 +55,10 @@ def gpu_spmm(plan, B, bias, epi, stream=None):
     return C.cpu().numpy()
 
 
-def check(row_ptr, col_idx, values, M, K, B, bias, epi, panel_rows=0, permute=True, V=None,
+def check(row_ptr, col_idx, values, M, K, B, bias, epi, panel_rows=0, permute=True,
           waves=None, label=""):
     with sd.Plan(row_ptr, col_idx, values, M, K, panel_rows=panel_rows, permute=permute) as plan:
-        with Forced(V, waves):
+        with Forced(waves):
             got = gpu_spmm(plan, B, bias, epi)
         if permute:
             assert np.array_equal(plan.perm, oracle.reorder(row_ptr, col_idx, K)), label
@@ -117,18 +115,17 @@ def test_ragged_N(N):
     check(W.row_ptr, W.col_idx, W.values, 200, 300, B, bias, "gelu", label=f"N={N}")
 
 
-@pytest.mark.parametrize("V", [1, 2, 4])
-@pytest.mark.parametrize("panel_rows", [4, 8, 16])
+@pytest.mark.parametrize("panel_rows", [4, 8, 12, 16])
 @pytest.mark.parametrize("N", [640, 643])
-def test_kernel_variants(V, panel_rows, N):
-    """Every compiled variant: columns per lane, rows per panel, aligned and unaligned N
-    (16-byte vs 4-byte staging), several K-chunks with a ragged last chunk."""
+def test_kernel_variants(panel_rows, N):
+    """Every compiled variant: rows per panel, aligned and unaligned N (16-byte vs
+    4-byte staging), several K-chunks with a ragged last chunk."""
     M, K = 333, 451
-    W = inputs.pattern_uniform(M, K, 0.12, inputs.CFG_TEST, 100 + V, 0.05)
+    W = inputs.pattern_uniform(M, K, 0.12, inputs.CFG_TEST, 100 + panel_rows, 0.05)
     B = inputs.dense_B(K, N, inputs.CFG_TEST, 100 + N)
     bias = inputs.bias_normal(M, inputs.CFG_TEST, 100, 0.02)
-    check(W.row_ptr, W.col_idx, W.values, M, K, B, bias, "relu", panel_rows=panel_rows, V=V,
-          label=f"V={V} RW={panel_rows} N={N}")
+    check(W.row_ptr, W.col_idx, W.values, M, K, B, bias, "relu", panel_rows=panel_rows,
+          label=f"RW={panel_rows} N={N}")
 
 
 @pytest.mark.parametrize("waves", [1, 3, 16])
