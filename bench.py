@@ -30,7 +30,8 @@ HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, GB/s
 ALU_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
 PACKED_FP32_PEAK_TFLOPS = 157.3
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2101_07948_amd", "csrc", f)
-                  for f in ("sdnn_kernels.hip", "sdnn_host.cpp", "sdnn_internal.h")]
+                  for f in ("sdnn_kernels.hip", "sdnn_host.cpp", "sdnn_internal.h",
+                            "gen_spmm_asm.py", "spmm_asm_gen.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_spmm_w0.json")
 
 
@@ -48,6 +49,38 @@ def measured_traffic():
     except (OSError, ValueError):
         return None
     return t.get("bytes_per_launch") if t.get("kernel_hash") == kernel_hash() else None
+
+
+def _pmc_rows(path, counter):
+    import csv
+    rows = []
+    for r in csv.DictReader(open(path)):
+        if r.get("Counter_Name") == counter:
+            rows.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    return rows
+
+
+def summarize_pmc(fetch_csv, write_csv, N):
+    """Per-launch HBM traffic of the sparse kernel from FETCH_SIZE / WRITE_SIZE (KiB per
+    dispatch), each scaled by what the same counter reads for the calibration copy
+    (an elementwise kernel that reads and writes exactly K*N*4 bytes)."""
+    K = 3072
+    copy_bytes = 4.0 * K * N
+    out = {"kernel_hash": kernel_hash(), "copy_bytes_each_way": copy_bytes}
+    for name, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
+        rows = _pmc_rows(path, counter)
+        spmm = [v for k, v in rows if "spmm_panel_kernel" in k]
+        copy = [v for k, v in rows if "elementwise" in k.lower() and "neg" in k.lower()]
+        if not spmm or not copy:
+            raise SystemExit(f"{path}: need both the spmm kernel and the calibration copy")
+        factor = copy_bytes / (copy[-1] * 1024.0)   # true bytes per counted byte
+        out[name + "_kib_counted_per_launch"] = sum(spmm) / len(spmm)
+        out[name + "_calibration_factor"] = factor
+        out[name + "_bytes_per_launch"] = sum(spmm) / len(spmm) * 1024.0 * factor
+    out["bytes_per_launch"] = out["fetch_bytes_per_launch"] + out["write_bytes_per_launch"]
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
+    print(json.dumps(out))
 
 
 def cpu_baseline(W, B, bias, budget_s: float):
@@ -80,7 +113,17 @@ def main():
                     help="seconds of CPU-oracle timing (0 = skip the cpu_baseline leg)")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense comparison kernel")
     ap.add_argument("--warm", action="store_true", help="reuse one buffer set (cache-warm)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="after timing, run one plain elementwise copy of B (known bytes) so a "
+                         "counter pass can calibrate FETCH_SIZE / WRITE_SIZE")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, "
+                         "WRITE_SIZE) of a --calib-copy run into per-launch HBM bytes and write "
+                         f"{os.path.relpath(TRAFFIC_FILE, ROOT)}")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, N=args.N)
+        return
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested); the operator "
@@ -143,6 +186,12 @@ def main():
     roof["frac_of_packed_fp32_peak"] = round(flop / t / 1e12 / PACKED_FP32_PEAK_TFLOPS, 4)
     roof["alg_bytes"] = int(alg_bytes)
     roof["flop"] = int(flop)
+
+    if args.calib_copy:  # plain copy of known size for counter calibration
+        X = torch.empty_like(Bs[0])
+        torch.neg(Bs[0], out=X)
+        torch.cuda.synchronize()
+        del X
 
     # cache-warm rate on one buffer set (context only)
     warm_ms = None

@@ -144,10 +144,11 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
           cursor[r] = q;
           P.counts[((size_t)p * P.nchunks + k) * RW + r] = (uint16_t)c;
         }
-        while (w.size() % kGroup != 0) {  // zero padding to whole groups
+        while (w.empty() || w.size() % kGroup != 0) {  // zero padding to whole groups
           w.push_back(0u);
           a.push_back(0u);
         }
+        a.back() |= 1u << kSegEndBit;  // last group of the segment
         for (size_t g = 0; g < w.size(); g += kGroup) {
           for (int j = 0; j < kGroup; ++j) P.entries.push_back(w[g + j]);
           for (int j = 0; j < kGroup; ++j) P.entries.push_back(a[g + j]);
@@ -171,7 +172,8 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
 // Independent re-walk of a packed stream: every CSR entry must appear exactly once, in
 // its row's panel and chunk, rows in panel order, columns ascending, weight bits
 // unchanged, offsets inside the chunk; each segment ends with fewer than kGroup zero
-// padding entries, and the stream with kTailGroups zero groups.
+// padding entries (a whole zero group if it is empty) and carries the end flag on its
+// last word, and the stream ends with kTailGroups zero groups.
 static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const float* values,
                          const Packed& P) {
   std::vector<char> seen((size_t)P.nnz, 0);
@@ -189,13 +191,20 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
       int64_t e = (int64_t)P.seg_start[s] * kGroup;
       const int64_t end = (int64_t)P.seg_start[s + 1] * kGroup;
       if (end < e || end > P.stored) return false;
+      if (end - e < kGroup) return false;  // at least one group
+      // the segment-end flag sits exactly on the last word of the last group
+      for (int64_t x = e; x < end; ++x) {
+        const bool flagged = (word(x) >> kSegEndBit) & 1u;
+        if (flagged != (x == end - 1)) return false;
+      }
+      auto plain = [&](int64_t x) { return word(x) & ~(1u << kSegEndBit); };
       for (int32_t r = 0; r < P.RW; ++r) {
         const int32_t orig = P.panel_rows[(size_t)p * P.RW + r];
         const int32_t c = P.counts[s * P.RW + r];
         if (orig < 0 && c != 0) return false;
         for (int32_t j = 0; j < c; ++j, ++e) {
           if (e >= end) return false;
-          const uint32_t wd = word(e);
+          const uint32_t wd = plain(e);
           if ((int32_t)(wd & 0x3ffu) != r) return false;
           if ((wd & 0x300u) != 0u) return false;
           const uint32_t off = wd >> 10;
@@ -209,9 +218,12 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
           seen[q] = 1;
         }
       }
-      if (end - e >= kGroup) return false;  // at most kGroup-1 padding entries
+      // padding: fewer than kGroup entries, or one whole group for an empty segment
+      if (end - e >= kGroup && !(end - e == kGroup && e == end - kGroup &&
+                                 (int64_t)P.seg_start[s] * kGroup == e))
+        return false;
       for (; e < end; ++e)
-        if (weight(e) != 0u || word(e) != 0u) return false;
+        if (weight(e) != 0u || plain(e) != 0u) return false;
     }
   }
   for (int64_t q = 0; q < P.nnz; ++q)

@@ -21,8 +21,10 @@ constexpr int kGroup = 4;
 // Columns of C per workgroup tile: 64 lanes x 4 consecutive columns.
 constexpr int kTileCols = 256;
 // Zero groups appended after the last segment: the kernel's stream prefetch may read
-// this many groups past the end of a segment.
-constexpr int kTailGroups = 4;
+// this many groups past the end of a panel's stream.
+constexpr int kTailGroups = 24;
+// Marks the last group of a segment (in the group's last column word).
+constexpr int kSegEndBit = 9;
 
 // Host-side packed form of W in the kernel's traversal order (Sec. 3.2.2: each
 // matrix stored in its own format, read sequentially).
@@ -30,10 +32,12 @@ constexpr int kTailGroups = 4;
 //   Panels of RW consecutive rows of the permuted matrix.  For panel p and chunk k the
 //   segment holds the entries of rows 0..RW-1 of the panel (row by row, each row in
 //   ascending column order) whose column lies in [k*kChunk, (k+1)*kChunk), padded at
-//   its end with zero entries to whole groups.  A group of kGroup entries is stored as
-//   2*kGroup dwords: the kGroup fp32 weight bits, then kGroup words
-//   (column offset inside the chunk << 10) | r.  The stream ends with kTailGroups zero
-//   groups so that a kernel may prefetch that many groups past the last segment.
+//   its end with zero entries to whole groups, and at least one group long.  A group
+//   of kGroup entries is stored as 2*kGroup dwords: the kGroup fp32 weight bits, then
+//   kGroup words (column offset inside the chunk << 10) | r; bit kSegEndBit of the
+//   group's last word is set on the last group of a segment.  A panel's segments are
+//   stored back to back in chunk order, panels in order, and the stream ends with
+//   kTailGroups zero groups so that a kernel may prefetch that many groups past it.
 struct Packed {
   int32_t M = 0, K = 0, RW = 0, nchunks = 0, npanels = 0;
   int64_t nnz = 0, stored = 0;     // structural entries, stored entries (with padding)

@@ -38,28 +38,28 @@ namespace {
 template <int RW>
 using acc_plane_t = float __attribute__((ext_vector_type(RW)));
 
+// Operands of the assembly K-loop (wave-uniform values go to SGPRs, the rest to VGPRs).
+struct KloopArgs {
+  const uint32_t* stream;  // first group of the wave's panel; null: no panel (the wave
+                           // only stages B and joins the barriers)
+  int32_t nchunks, K;
+  uint32_t row_bytes;      // N * 4
+  uint32_t wave, nwaves;
+  int32_t ncol;            // N - n0 (columns of the tile that exist)
+  uint64_t vbase;          // B[0][n0] + this lane's byte offset in a staged row segment
+  uint32_t vl0, vl1;       // this lane's LDS read address in buffer 0 / 1
+  uint32_t lane;
+};
+
 #include "spmm_asm_gen.h"
 static_assert(kStreamTailGroups <= kTailGroups, "stream tail shorter than the prefetch");
+static_assert(kSegmentEndBit == (1u << kSegEndBit), "segment-end flag mismatch");
 
 __device__ __forceinline__ float activation(float x, int epi) {
   if (epi == SDNN_EPI_RELU) return fmaxf(x, 0.0f);
   if (epi == SDNN_EPI_GELU) return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
   return x;
 }
-
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-
-// Direct global -> LDS copy of `size` bytes per active lane: lane i's bytes land at
-// lds_base + i * size (lds_base is wave-uniform).  The kernel waits for these copies
-// (vmcnt(0)) right before the barrier that publishes the buffer.
-__device__ __forceinline__ void dma16(const float* gptr, lds_ptr_t lds_base) {
-  __builtin_amdgcn_global_load_lds(gptr, lds_base, 16, 0, 0);
-}
-__device__ __forceinline__ void dma4(const float* gptr, lds_ptr_t lds_base) {
-  __builtin_amdgcn_global_load_lds(gptr, lds_base, 4, 0, 0);
-}
-// s_waitcnt vmcnt(0) (gfx9 encoding: expcnt and lgkmcnt fields at their maximum)
-__device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // Scalar launch parameters (the pointers are separate __restrict__ kernel arguments so
 // the compiler may read them through the scalar cache).
@@ -70,37 +70,6 @@ struct SpmmArgs {
   int32_t per_xcd;   // launched grid / 8
   int32_t epi;
 };
-
-// Stages rows [k*kChunk, k*kChunk + kChunk) x columns [n0, n0 + 256) of B into an LDS
-// buffer laid out row-major, 1 KB per row.  Out-of-range rows and columns are skipped:
-// no stream entry refers to such a row, and such columns are never stored.
-template <bool VEC>
-__device__ __forceinline__ void stage_chunk(const float* __restrict__ B, int K, int N, int n0,
-                                            int k, float* buf, int wave, int nwaves, int lane) {
-  constexpr int CHUNK_FLOATS = kChunk * kTileCols;
-  const int k0 = k * kChunk;
-  if (VEC) {
-    // one instruction moves one B row segment: 64 lanes x 16 bytes = 1 KB; the row
-    // pointer is wave-uniform (scalar base), the lane offset a 32-bit vector offset
-    const int col = n0 + lane * 4;
-    const bool col_ok = col < N;
-    for (int row = wave; row < kChunk; row += nwaves) {
-      const int krow = k0 + row;
-      if (krow >= K) break;
-      const float* rowp = B + (size_t)krow * N;
-      if (col_ok) dma16(rowp + col, (lds_ptr_t)(buf + row * kTileCols));
-    }
-  } else {
-    constexpr int INSTS = CHUNK_FLOATS / 64;
-    for (int j = wave; j < INSTS; j += nwaves) {
-      const int q = j * 64 + lane;
-      const int row = q / kTileCols;
-      const int col = n0 + (q - row * kTileCols);
-      const int krow = k0 + row;
-      if (krow < K && col < N) dma4(B + (size_t)krow * N + col, (lds_ptr_t)(buf + j * 64));
-    }
-  }
-}
 
 // RW: rows per panel; VEC: N % 4 == 0 and B, C 16-byte aligned (16-byte staging DMA,
 // vector stores of C).
@@ -128,30 +97,28 @@ __global__ __launch_bounds__(1024) void spmm_panel_kernel(
   const bool active = panel < a.npanels;
   const int n0 = tile * kTileCols;
   const int nchunks = a.nchunks;
+  (void)lane;
 
   acc_plane_t<RW> p0 = {}, p1 = {}, p2 = {}, p3 = {};
   const uint32_t lds_base = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) float*)lds);
-  const uint32_t vl0 = lds_base + (uint32_t)lane * 16u;
-  const uint32_t vl1 = vl0 + (uint32_t)CHUNK_FLOATS * 4u;
-
-  // segment bounds of the wave's panel, read one chunk ahead of their use
-  const int32_t* __restrict__ pseg = segs + (active ? panel * nchunks : 0);
-  int g_lo = nchunks > 0 ? pseg[0] : 0;
-  int g_hi = nchunks > 0 ? pseg[1] : 0;
-  if (nchunks > 0) stage_chunk<VEC>(B, a.K, a.N, n0, 0, lds, wave, nwaves, lane);
-  for (int k = 0; k < nchunks; ++k) {
-    wait_vmcnt0();
-    __syncthreads();  // chunk k is in LDS; every wave is done reading the other buffer
-    if (k + 1 < nchunks)
-      stage_chunk<VEC>(B, a.K, a.N, n0, k + 1, lds + ((k + 1) & 1) * CHUNK_FLOATS, wave, nwaves,
-                       lane);
-    const int g_next = (k + 2 <= nchunks) ? pseg[k + 2] : g_hi;
-    if (active)
-      chunk_fma_asm(p0, p1, p2, p3, entries + (size_t)g_lo * (2 * kGroup), g_hi - g_lo,
-                    (k & 1) ? vl1 : vl0);
-    g_lo = g_hi;
-    g_hi = g_next;
-  }
+  if (lds_base != 0) return;  // the staging code assumes buffers at LDS 0 and 64 KB
+  const uint64_t bcol = (uint64_t)(uintptr_t)(B + n0);
+  KloopArgs ka;
+  ka.stream = active ? entries + (size_t)segs[panel * nchunks] * (2 * kGroup) : nullptr;
+  ka.nchunks = nchunks;
+  ka.K = a.K;
+  ka.row_bytes = (uint32_t)a.N * 4u;
+  ka.wave = (uint32_t)wave;
+  ka.nwaves = (uint32_t)nwaves;
+  ka.ncol = a.N - n0;
+  ka.vbase = bcol + (uint64_t)lane * (VEC ? 16u : 4u);
+  ka.vl0 = lds_base + (uint32_t)lane * 16u;
+  ka.vl1 = ka.vl0 + (uint32_t)CHUNK_FLOATS * 4u;
+  ka.lane = (uint32_t)lane;
+  if (VEC)
+    kloop_vec(p0, p1, p2, p3, ka);
+  else
+    kloop_dword(p0, p1, p2, p3, ka);
 
   if (!active) return;
   const int ncol = n0 + lane * 4;

@@ -158,3 +158,13 @@ def test_bad_dims_and_nulls():
     assert L.sdnn_spmm(None, None, None, 4, None, 0, None) == 1
     assert L.sdnn_dense_gemm(None, None, None, -1, 4, 4, None, 0, None) == 2
     assert L.sdnn_dense_gemm(None, None, None, 0, 4, 4, None, 0, None) == 0  # M = 0: no-op
+
+
+def test_generated_kernel_header_in_sync():
+    """The K-loop assembly header is generated; the committed copy must match."""
+    import importlib.util
+    path = os.path.join(ROOT, "paper_2101_07948_amd", "csrc", "gen_spmm_asm.py")
+    spec = importlib.util.spec_from_file_location("gen_spmm_asm", path)
+    gen = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(gen)
+    assert gen.main(check=True) == 0, "spmm_asm_gen.h is stale: run the package build"
