@@ -56,25 +56,31 @@ def _pmc_rows(path, counter):
     rows = []
     for r in csv.DictReader(open(path)):
         if r.get("Counter_Name") == counter:
-            rows.append((r["Kernel_Name"], float(r["Counter_Value"])))
-    return rows
+            rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+    return sorted(rows)
 
 
 def summarize_pmc(fetch_csv, write_csv, N):
     """Per-launch HBM traffic of the sparse kernel from FETCH_SIZE / WRITE_SIZE (KiB per
-    dispatch), each scaled by what the same counter reads for the calibration copy
-    (an elementwise kernel that reads and writes exactly K*N*4 bytes)."""
+    dispatch), each scaled by what the same counter reads for the calibration copy (an
+    elementwise negation that reads and writes exactly K*N*4 bytes).  Only the sparse
+    launches before the copy count: those are the warm-up and timed steps, each on a
+    buffer set not touched since it was created."""
     K = 3072
     copy_bytes = 4.0 * K * N
     out = {"kernel_hash": kernel_hash(), "copy_bytes_each_way": copy_bytes}
     for name, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
         rows = _pmc_rows(path, counter)
-        spmm = [v for k, v in rows if "spmm_panel_kernel" in k]
-        copy = [v for k, v in rows if "elementwise" in k.lower() and "neg" in k.lower()]
-        if not spmm or not copy:
-            raise SystemExit(f"{path}: need both the spmm kernel and the calibration copy")
-        factor = copy_bytes / (copy[-1] * 1024.0)   # true bytes per counted byte
+        copy = [(d, v) for d, k, v in rows if "elementwise" in k.lower() and "neg" in k.lower()]
+        if not copy:
+            raise SystemExit(f"{path}: no calibration copy dispatch")
+        spmm = [v for d, k, v in rows if "spmm_panel_kernel" in k and d < copy[0][0]]
+        if not spmm:
+            raise SystemExit(f"{path}: no sparse-kernel dispatch before the calibration copy")
+        factor = copy_bytes / (copy[0][1] * 1024.0)   # true bytes per counted byte
+        out[name + "_launches"] = len(spmm)
         out[name + "_kib_counted_per_launch"] = sum(spmm) / len(spmm)
+        out[name + "_copy_kib_counted"] = copy[0][1]
         out[name + "_calibration_factor"] = factor
         out[name + "_bytes_per_launch"] = sum(spmm) / len(spmm) * 1024.0 * factor
     out["bytes_per_launch"] = out["fetch_bytes_per_launch"] + out["write_bytes_per_launch"]
