@@ -1,55 +1,67 @@
-"""Generates spmm_asm_gen.h: the K-loop of the gfx950 panel kernel as inline assembly,
-one function per (panel height RW, staging width).
+"""Generates spmm_asm_gen.h: the inner loops of the gfx950 panel kernel as inline
+assembly.  One consumer routine per panel height RW and one producer routine per
+staging width.
 
-Why generated assembly: the loop keeps a wavefront's RW x 4 output tile in fixed VGPRs
-and selects the row of each nonzero with VGPR index mode (s_set_gpr_idx_*), and it
-software-pipelines scalar loads of the weight stream, LDS reads of B and FMAs across
-rotating register sets that must keep their state across K-chunks.  Compiled code can
-express neither the indexed accumulator nor the persistent rotation.
+Why generated assembly: the consumer keeps a wavefront's RW x 4 output tile in fixed
+VGPRs and selects the row of each nonzero with VGPR index mode (s_set_gpr_idx_*), and
+it software-pipelines scalar loads of the weight stream, LDS reads of B and FMAs
+across rotating register sets.  Compiled code can express neither the indexed
+accumulator nor the rotation.
 
-Stream consumed (see sdnn_internal.h): for each panel, the segments of chunks
-0..nchunks-1 back to back; a segment is >= 1 group; a group is 8 dwords
-[w0 w1 w2 w3 a0 a1 a2 a3], w = fp32 weight bits, a = (column in chunk << 10) | row,
-and bit 9 of a3 marks the last group of a segment.
+Workgroup roles.  Waves 0..nc-1 are consumers (one panel each); waves nc and nc+1
+are producers.  B is staged through a ring of RING slots of CHUNK rows (1 KB per row:
+64 lanes x 16 bytes) at LDS byte address 0; chunk c of B goes to slot c % RING, and
+producer p stages rows [p * CHUNK/2, (p + 1) * CHUNK/2) of every chunk.  There is no
+workgroup barrier inside the loops: the roles synchronise through LDS words
+    ready[p]    number of chunks whose rows producer p has landed in the ring
+    progress[w] lowest chunk consumer w may still read (consumer w writes; the slots
+                of absent consumers hold 0x7fffffff)
+A producer stages its part of chunk c once every progress[w] >= c - RING + 1 (slot
+c % RING no longer read by anyone), keeps up to PMAX chunks in flight, and advances
+its ready word as each lands.  A consumer publishes progress and re-reads the ready
+words only at groups whose sync bit is set; chunk c is there once both exceed c.
+Two producer waves double the bytes in flight per workgroup: one wave alone, waiting
+for each chunk to land, cannot keep the consumers fed.  Every group reads chunks c_lo..c_hi with c_hi - c_lo < RING and
+publishes progress = c_lo before waiting for c_hi, so the slowest consumer's next
+chunk can always be staged: the loops cannot deadlock.  Each wait is also bounded by
+a per-wave poll budget, after which the wave goes on without waiting (the result is
+then wrong, but the kernel ends).
 
-Register plan (pinned in the asm statement):
-  v30             LDS byte address of this lane's 16 bytes in the current B buffer
-  v31             0xfc00 (column-offset mask)
-  v[32:47]        B values of the group being multiplied / being fetched (2 sets of 4 x 4)
-  v[48:63]
-  v[64 + k*RW + r]  accumulator of row r, column 4*lane + k   (k = 0..3)
-  v25             N * 4 (B row stride in bytes); v[26:27] B row address being staged
-  v28, v29        zero offset / sink of the L2 touch loads
-  s[40:79]        ring of NSLOT = 5 stream groups (8 SGPRs each)
-  s[80:81]        address of the next group to fetch
-  s82 phase (position in the unrolled loop), s83 saved m0, s84 next chunk to compute,
-  s85 chunk being staged, s[86:87] column mask, s88 LDS buffer being staged, s89 row,
-  s90 temp, s[92:93] saved exec
-The staging buffers are at LDS byte addresses 0 and 64 KB (the kernel checks this).
-A wave without a panel passes a null stream address: it stages B and takes part in
-every barrier but runs no FMAs.
+Stream consumed (see sdnn_internal.h): per panel, groups of 8 dwords
+[w0 w1 w2 w3 a0 a1 a2 a3]; w = fp32 weight bits; a = (ring row << 10) | row, plus
+c_lo in a2 >> 17, c_hi in a3 >> 18, the sync flag in a3 bit 17 and the end-of-panel
+flag in a3 bit 9.  The ring row field is bits 10..16, so (a & 0x1fc00) | (16 * lane)
+is the LDS address of the lane's 4 B values; VGPR index mode uses only a's low 8 bits.
 
+Consumer register plan (pinned in the asm statement):
+  v31 0x1fc00 (ring-row mask), v28 zero offset and v29 sink of the L2 touch loads,
+  v27 temp, v[32:47] / v[48:63] B values of the group being multiplied / fetched,
+  v[64 + k*RW + r] accumulator of row r, column 4*lane + k (k = 0..3);
+  s[40:79] ring of NSLOT stream groups, s[80:81] next group to fetch, s82 chunks known
+  ready, s83 temp, s84 poll budget, s85 saved m0, s[86:87] saved exec, s88 temp;
+  v26 temp.
 Per group g:
   wait until B of g and stream group g+1 have arrived
+  if g+1 carries the sync bit: publish c_lo(g+1), wait until c_hi(g+1) < ready;
+      if g+1 ends the panel: fetch its B, multiply g and g+1, finish
   address + ds_read_b128 of the 4 B rows of group g+1      (index mode off)
   s_load of stream group g+NSLOT-1 into the slot that group g-1 used
+  vector touch TOUCH_AHEAD bytes ahead (pulls the stream into L2 for the scalar loads)
   for each entry: s_set_gpr_idx_* row; 4 v_fma_f32 into the row's accumulators
   (index mode DST|SRC2: only the accumulator operand is offset by the row)
-  if g ends its segment: leave to the chunk transition, remembering the phase
-Chunk transition (every wave, active or not, executes it once per chunk):
-  wait for this wave's B DMA, s_barrier (all DMA of the chunk landed; every wave is done
-  with the other buffer), DMA of the chunk after the one about to be computed into the
-  free buffer, switch the LDS read base, re-issue the LDS reads of the current group
-  from the new buffer, and re-enter the unrolled loop at the saved phase.
-Scalar loads run NSLOT-2 groups ahead of their first use and continue across chunks.
-Each iteration also issues a vector load (result unused, waited for only at the next
-barrier) TOUCH_AHEAD bytes ahead of the ring pointer: it brings the stream into L2, so
-scalar-cache misses are served from L2 instead of the memory-side cache or HBM.
 The ring and the touch read up to kStreamTailGroups groups past a panel's last
-segment; the stream carries that many zero groups at its end so those reads stay
-inside it, and LDS reads stay inside the B buffer because every column offset is < 64.
+group; the stream carries that many zero groups at its end.
+
+Producer: issues one 16-byte (or four 4-byte) direct global->LDS loads per B row,
+addressed by a scalar row pointer plus the lane's byte offset, with M0 holding the
+LDS row address; rows past K re-stage row K-1 into LDS rows no entry reads.
+
+Hazards the hand-written code must respect (the compiler handles them for compiled
+code): a VALU write of a VGPR followed at once by v_readfirstlane of that VGPR reads
+the old value, so the ready words go from the LDS result straight to SGPRs; a
+VALU-written vcc is read by SALU only after s_nop; an SALU write of M0 is followed by
+at least one instruction before an LDS DMA that uses it.
 """
-import math
 import os
 import sys
 
@@ -57,193 +69,294 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 OUT = os.path.join(HERE, "spmm_asm_gen.h")
 
 NSLOT = 5
-E = tuple(40 + 8 * i for i in range(NSLOT))  # SGPR bases of the stream-group ring
-PTR, PHASE, M0S, KNEXT, DCH, CMASK = 80, 82, 83, 84, 85, 86
-DBUF, DROW, DTMP, DEXEC = 88, 89, 90, 92
-SLAST = 93
+E = tuple(40 + 8 * i for i in range(NSLOT))   # SGPR bases of the stream-group ring
+PTR, SREADY, STMP, SPOLL, M0S, SEXEC, SREADY1 = 80, 82, 83, 84, 85, 86, 88
 VB = (32, 48)                                 # VGPR bases of the two B-value sets
 ACC = 64                                      # first accumulator VGPR
-UNROLL = NSLOT * 2 // math.gcd(NSLOT, 2)
+UNROLL = 10                                   # multiple of NSLOT and of 2
 RW_VARIANTS = (4, 8, 12, 16)
-END_BIT = 9
+END_BIT, SYNC_BIT, LO_SHIFT, HI_SHIFT = 9, 17, 17, 18
+RING_MASK = 0x1FC00
+CHUNK, RING = 32, 4
+PMAX_VEC, PMAX_DWORD = 2, 1                   # chunks in flight per producer variant
 TOUCH_AHEAD = 512  # bytes of stream pulled into L2 ahead of the scalar ring
-PROFILE = False    # scratch builds only: time spent in chunk transitions (%[tbar])
+POLL_BUDGET = 1 << 22   # LDS polls a wave may spend waiting, in total
+INF = 0x7FFFFFFF
+NPROD = 2          # producer waves; producer p stages rows [p, p+1) * CHUNK/NPROD of a chunk
+SLEEP_BEFORE_PUBLISH = 0  # scratch experiments: s_sleep before a ready word is written
+PROFILE = False    # scratch builds only: time consumers spend waiting (%[twait])
 
 
 def address_phase(slot, vb):
     L = []
     for j in range(4):
-        L.append(f"v_and_or_b32 v{vb + 4 * j}, s{slot + 4 + j}, v31, v30")
+        L.append(f"v_and_or_b32 v{vb + 4 * j}, s{slot + 4 + j}, v31, %[vl]")
         L.append(f"ds_read_b128 v[{vb + 4 * j}:{vb + 4 * j + 3}], v{vb + 4 * j}")
     return L
 
 
-def iteration(i, rw):
-    cur, nxt, pre = E[i % NSLOT], E[(i + 1) % NSLOT], E[(i + NSLOT - 1) % NSLOT]
-    vbc, vbn = VB[i % 2], VB[(i + 1) % 2]
-    L = [f".L%=_iter{i}:", "s_waitcnt lgkmcnt(0)"]
-    L += address_phase(nxt, vbn)
-    L.append(f"s_load_dwordx8 s[{pre}:{pre + 7}], s[{PTR}:{PTR + 1}], 0x0")
-    if TOUCH_AHEAD:  # pull the stream line TOUCH_AHEAD bytes ahead into L2 (vector path)
-        L.append(f"global_load_dword v29, v28, s[{PTR}:{PTR + 1}] offset:{TOUCH_AHEAD}")
-    L.append(f"s_add_u32 s{PTR}, s{PTR}, 32")
-    L.append(f"s_addc_u32 s{PTR + 1}, s{PTR + 1}, 0")
+def fmas(slot, vb, rw):
+    L = []
     for j in range(4):
         if j == 0:
-            L.append(f"s_set_gpr_idx_on s{cur + 4}, gpr_idx(DST,SRC2)")
+            L.append(f"s_set_gpr_idx_on s{slot + 4}, gpr_idx(DST,SRC2)")
         else:
-            L.append(f"s_set_gpr_idx_idx s{cur + 4 + j}")
+            L.append(f"s_set_gpr_idx_idx s{slot + 4 + j}")
         for k in range(4):
             p = ACC + k * rw
-            L.append(f"v_fma_f32 v{p}, s{cur + j}, v{vbc + 4 * j + k}, v{p}")
+            L.append(f"v_fma_f32 v{p}, s{slot + j}, v{vb + 4 * j + k}, v{p}")
     L.append("s_set_gpr_idx_off")
-    L.append(f"s_bitcmp1_b32 s{cur + 7}, {END_BIT}")
-    L.append(f"s_cbranch_scc1 .L%=_exit{i}")
     return L
 
 
-def dma(tag, vec):
-    """Stage chunk DCH (if < nch) into buffer DCH & 1: rows wave, wave+nw, ... < 64.
-    The B row address is formed in v[26:27] from the tile base %[vb] (64-bit) and the
-    row stride v25 (one v_mad_u64_u32 per row)."""
-    L = [
-        f"s_cmp_ge_u32 s{DCH}, %[nch]",
-        f"s_cbranch_scc1 .L%=_dmadone{tag}",
-        f"s_and_b32 s{DBUF}, s{DCH}, 1",
-        f"s_lshl_b32 s{DBUF}, s{DBUF}, 16",
-        f"s_mov_b32 s{DROW}, %[wave]",
-        f".L%=_dmaloop{tag}:",
-        f"s_cmp_ge_u32 s{DROW}, 64",
-        f"s_cbranch_scc1 .L%=_dmadone{tag}",
-        f"s_lshl_b32 s{DTMP}, s{DCH}, 6",
-        f"s_add_u32 s{DTMP}, s{DTMP}, s{DROW}",
-        f"s_cmp_ge_u32 s{DTMP}, %[K]",
-        f"s_cbranch_scc1 .L%=_dmadone{tag}",
-        f"v_mad_u64_u32 v[26:27], vcc, s{DTMP}, v25, %[vb]",
-        f"s_lshl_b32 m0, s{DROW}, 10",
-        f"s_add_u32 m0, m0, s{DBUF}",
-    ]
-    if vec:
-        L += [
-            f"s_and_saveexec_b64 s[{DEXEC}:{DEXEC + 1}], s[{CMASK}:{CMASK + 1}]",
-            "s_nop 0",
-            "global_load_lds_dwordx4 v[26:27], off",
-            f"s_mov_b64 exec, s[{DEXEC}:{DEXEC + 1}]",
-        ]
-    else:
-        for q in range(4):
-            if q:
-                L += ["s_add_u32 m0, m0, 0x100", "v_add_co_u32 v26, vcc, 0x100, v26",
-                      "v_addc_co_u32 v27, vcc, 0, v27, vcc"]
-            L += [
-                f"s_sub_i32 s{DTMP}, %[ncol], {64 * q}",
-                f"v_cmp_gt_i32 vcc, s{DTMP}, %[lanev]",
-                f"s_and_saveexec_b64 s[{DEXEC}:{DEXEC + 1}], vcc",
-                "s_nop 0",
-                "global_load_lds_dword v[26:27], off",
-                f"s_mov_b64 exec, s[{DEXEC}:{DEXEC + 1}]",
-            ]
+def lane0_write(addr, vdata):
+    """ds_write_b32 from lane 0 only (all lanes hold the same value)."""
+    return [f"s_mov_b64 s[{SEXEC}:{SEXEC + 1}], exec", "s_mov_b64 exec, 1",
+            f"ds_write_b32 {addr}, {vdata}", f"s_mov_b64 exec, s[{SEXEC}:{SEXEC + 1}]"]
+
+
+def sync(slot, tag):
+    """Publish progress = c_lo of the group in `slot`, then wait until its c_hi has
+    landed (c_hi < min of the producers' ready words), polling while the budget
+    lasts."""
+    assert NPROD == 2  # the poll reads the two ready words with one ds_read_b64
+    L = [f"s_lshr_b32 s{STMP}, s{slot + 6}, {LO_SHIFT}", f"v_mov_b32 v27, s{STMP}"]
+    L += lane0_write("%[pa]", "v27")
+    L += [f"s_lshr_b32 s{STMP}, s{slot + 7}, {HI_SHIFT}"]
+    if PROFILE:
+        L += [f"s_memtime s[{SEXEC}:{SEXEC + 1}]", "s_waitcnt lgkmcnt(0)"]
     L += [
-        f"s_add_u32 s{DROW}, s{DROW}, %[nw]",
-        f"s_branch .L%=_dmaloop{tag}",
-        f".L%=_dmadone{tag}:",
+        f".L%=_poll{tag}:",
+        f"s_cmp_lt_u32 s{STMP}, s{SREADY}",
+        f"s_cbranch_scc1 .L%=_ready{tag}",
+        f"s_cmp_eq_u32 s{SPOLL}, 0",
+        f"s_cbranch_scc1 .L%=_ready{tag}",
+        f"s_sub_u32 s{SPOLL}, s{SPOLL}, 1",
+        # each word goes from the LDS result straight to an SGPR: a VALU write of a
+        # VGPR followed at once by v_readfirstlane of it reads the old value on gfx950
+        "ds_read_b64 v[26:27], %[ra]",
+        "s_waitcnt lgkmcnt(0)",
+        f"v_readfirstlane_b32 s{SREADY}, v26",
+        f"v_readfirstlane_b32 s{SREADY1}, v27",
+        f"s_min_u32 s{SREADY}, s{SREADY}, s{SREADY1}",
+        f"s_cmp_lt_u32 s{STMP}, s{SREADY}",
+        f"s_cbranch_scc1 .L%=_ready{tag}",
+        "s_sleep 1",
+        f"s_branch .L%=_poll{tag}",
+        f".L%=_ready{tag}:",
     ]
+    if PROFILE:  # scratch builds also pin s[94:95]
+        L += ["s_memtime s[94:95]", "s_waitcnt lgkmcnt(0)",
+              f"s_sub_u32 s94, s94, s{SEXEC}", "s_add_u32 %[twait], %[twait], s94"]
     return L
 
 
-def function(rw, vec):
+def consumer(rw):
     L = [
         f"s_mov_b32 s{M0S}, m0",
-        "v_mov_b32 v31, 0xfc00",
+        f"v_mov_b32 v31, {hex(RING_MASK)}",
         "v_mov_b32 v28, 0",
-        "v_mov_b32 v25, %[rs]",
-        f"s_mov_b32 s{KNEXT}, 0",
-        f"s_mov_b32 s{PHASE}, 0",
+        f"s_mov_b32 s{SREADY}, 0",
+        f"s_mov_b32 s{SPOLL}, {hex(POLL_BUDGET)}",
     ]
-    if vec:  # lanes whose 4 columns lie inside N: lane < ncol / 4
-        L += [
-            f"s_lshr_b32 s{DTMP}, %[ncol], 2",
-            f"s_min_u32 s{DTMP}, s{DTMP}, 64",
-            f"s_bfm_b64 s[{CMASK}:{CMASK + 1}], s{DTMP}, 0",
-            f"s_cmp_ge_u32 s{DTMP}, 64",
-            f"s_cselect_b64 s[{CMASK}:{CMASK + 1}], -1, s[{CMASK}:{CMASK + 1}]",
-        ]
-    L += [
-        "s_cmp_eq_u64 %[sp], 0",
-        "s_cbranch_scc1 .L%=_pro_idle",
-    ]
+    if PROFILE:
+        L.append("s_mov_b32 %[twait], 0")
     for g in range(NSLOT - 1):
         L.append(f"s_load_dwordx8 s[{E[g]}:{E[g] + 7}], %[sp], {hex(32 * g)}")
     L += [
         f"s_mov_b64 s[{PTR}:{PTR + 1}], %[sp]",
         f"s_add_u32 s{PTR}, s{PTR}, {32 * (NSLOT - 1)}",
         f"s_addc_u32 s{PTR + 1}, s{PTR + 1}, 0",
-        ".L%=_pro_idle:",
-        f"s_mov_b32 s{DCH}, 0",
+        "s_waitcnt lgkmcnt(0)",
     ]
-    L += dma("p", vec)
-    # chunk transition
-    L += [
-        ".L%=_trans:",
-        f"s_cmp_ge_u32 s{KNEXT}, %[nch]",
-        "s_cbranch_scc1 .L%=_finish",
-    ]
-    if PROFILE:  # cycles spent waiting for the DMA and the barrier
-        L += [f"s_memtime s[{DEXEC}:{DEXEC + 1}]", "s_waitcnt lgkmcnt(0)"]
-    L += [
-        "s_waitcnt vmcnt(0)",
-        "s_barrier",
-    ]
-    if PROFILE:  # scratch builds also pin s[94:95]
-        L += ["s_memtime s[94:95]", "s_waitcnt lgkmcnt(0)",
-              f"s_sub_u32 s94, s94, s{DEXEC}", "s_add_u32 %[tbar], %[tbar], s94"]
-    L += [f"s_add_u32 s{DCH}, s{KNEXT}, 1"]
-    L += dma("t", vec)
-    L += [
-        f"s_bitcmp1_b32 s{KNEXT}, 0",
-        "s_cselect_b64 vcc, -1, 0",
-        "v_cndmask_b32 v30, %[vl0], %[vl1], vcc",
-        f"s_add_u32 s{KNEXT}, s{KNEXT}, 1",
-        "s_cmp_eq_u64 %[sp], 0",
-        "s_cbranch_scc1 .L%=_trans",
-    ]
-    for p in range(UNROLL):
-        L += [f"s_cmp_eq_u32 s{PHASE}, {p}", f"s_cbranch_scc1 .L%=_entry{p}"]
-    L.append("s_branch .L%=_finish")  # unreachable: phase is always < UNROLL
-    for p in range(UNROLL):
-        L.append(f".L%=_entry{p}:")
-        L.append("s_waitcnt lgkmcnt(0)")
-        L += address_phase(E[p % NSLOT], VB[p % 2])
-        L.append(f"s_branch .L%=_iter{p}")
+    L += sync(E[0], "e")   # a panel's first group always carries the sync bit
+    L += address_phase(E[0], VB[0])
+    L += [f"s_bitcmp1_b32 s{E[0] + 7}, {END_BIT}", "s_cbranch_scc0 .L%=_iter0",
+          "s_waitcnt lgkmcnt(0)"]   # the panel is one group
+    L += fmas(E[0], VB[0], rw)
+    L.append("s_branch .L%=_finish")
     for i in range(UNROLL):
-        L += iteration(i, rw)
+        cur, nxt, pre = E[i % NSLOT], E[(i + 1) % NSLOT], E[(i + NSLOT - 1) % NSLOT]
+        vbc, vbn = VB[i % 2], VB[(i + 1) % 2]
+        L += [f".L%=_iter{i}:", "s_waitcnt lgkmcnt(0)",
+              f"s_bitcmp1_b32 s{nxt + 7}, {SYNC_BIT}", f"s_cbranch_scc1 .L%=_sync{i}",
+              f".L%=_ret{i}:"]
+        L += address_phase(nxt, vbn)
+        L.append(f"s_load_dwordx8 s[{pre}:{pre + 7}], s[{PTR}:{PTR + 1}], 0x0")
+        if TOUCH_AHEAD:  # pull the stream line TOUCH_AHEAD bytes ahead into L2
+            L.append(f"global_load_dword v29, v28, s[{PTR}:{PTR + 1}] offset:{TOUCH_AHEAD}")
+        L += [f"s_add_u32 s{PTR}, s{PTR}, 32", f"s_addc_u32 s{PTR + 1}, s{PTR + 1}, 0"]
+        L += fmas(cur, vbc, rw)
     L.append("s_branch .L%=_iter0")
     for i in range(UNROLL):
-        L += [f".L%=_exit{i}:", f"s_mov_b32 s{PHASE}, {(i + 1) % UNROLL}", "s_branch .L%=_trans"]
-    L += [
-        ".L%=_finish:",
-        "s_waitcnt vmcnt(0) lgkmcnt(0)",
-        f"s_mov_b32 m0, s{M0S}",
-    ]
-    if PROFILE:
-        L.insert(0, "s_mov_b32 %[tbar], 0")
+        cur, nxt = E[i % NSLOT], E[(i + 1) % NSLOT]
+        vbc, vbn = VB[i % 2], VB[(i + 1) % 2]
+        L.append(f".L%=_sync{i}:")
+        L += sync(nxt, i)
+        L += [f"s_bitcmp1_b32 s{nxt + 7}, {END_BIT}", f"s_cbranch_scc0 .L%=_ret{i}"]
+        L += address_phase(nxt, vbn)       # group g+1 ends the panel
+        L += fmas(cur, vbc, rw)
+        L.append("s_waitcnt lgkmcnt(0)")
+        L += fmas(nxt, vbn, rw)
+        L.append("s_branch .L%=_finish")
+    L += [".L%=_finish:", f"v_mov_b32 v27, {hex(INF)}"]
+    L += lane0_write("%[pa]", "v27")
+    L += ["s_waitcnt vmcnt(0) lgkmcnt(0)", f"s_mov_b32 m0, s{M0S}"]
     body = "\n".join('      "' + x + '\\n\\t"' for x in L)
     planes = ", ".join(f'"+{{v[{ACC + k * rw}:{ACC + k * rw + rw - 1}]}}"(p{k})' for k in range(4))
-    sregs = [f"s{x}" for x in range(E[0], (95 if PROFILE else SLAST) + 1)]
-    vregs = [f"v{x}" for x in range(25, 64)]
-    # exec is changed only around each DMA and restored right after it
-    clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["vcc", "scc"])
-    suffix = "vec" if vec else "dword"
-    return f"""// RW = {rw}, {"16-byte" if vec else "4-byte"} staging: accumulator planes p0..p3
-__device__ __forceinline__ void kloop_{suffix}(acc_plane_t<{rw}>& p0, acc_plane_t<{rw}>& p1,
+    sregs = [f"s{x}" for x in range(E[0], (95 if PROFILE else SREADY1) + 1)]
+    vregs = [f"v{x}" for x in range(26, 64)]
+    clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["scc"])
+    return f"""// Consumer, RW = {rw}: accumulator planes p0..p3
+__device__ __forceinline__ void consume_rw{rw}(acc_plane_t<{rw}>& p0, acc_plane_t<{rw}>& p1,
                                          acc_plane_t<{rw}>& p2, acc_plane_t<{rw}>& p3,
-                                         const KloopArgs& a) {{
+                                         {'' if PROFILE else 'const '}ConsumerArgs& a) {{
   asm volatile(
 {body}
-      : {planes}{', [tbar] "=&s"(a.tbar)' if PROFILE else ''}
-      : [sp] "s"(a.stream), [nch] "s"(a.nchunks), [rs] "s"(a.row_bytes), [K] "s"(a.K),
-        [wave] "s"(a.wave), [nw] "s"(a.nwaves), [ncol] "s"(a.ncol), [vb] "v"(a.vbase),
-        [vl0] "v"(a.vl0), [vl1] "v"(a.vl1), [lanev] "v"(a.lane)
+      : {planes}{', [twait] "=&s"(a.twait)' if PROFILE else ''}
+      : [sp] "s"(a.stream), [vl] "v"(a.vlane), [pa] "v"(a.prog_addr), [ra] "v"(a.ready_addr)
+      : {clob});
+}}
+"""
+
+
+# producer SGPRs
+PISS, PSIG, PINF, PROW, PNEED, PPOLL, PTMP, PM0 = 40, 41, 42, 43, 44, 45, 46, 47
+PADDR, PEX, PBASE, PKM1 = 48, 50, 52, 54      # 64-bit: PADDR, PEX, PBASE
+PCM = 56                                       # column masks (1 or 4 pairs)
+
+
+def producer(vec):
+    half = CHUNK // NPROD
+    pmax = PMAX_VEC if vec else PMAX_DWORD
+    loads_per_chunk = half if vec else 4 * half
+    assert loads_per_chunk * (pmax - 1) <= 63
+    L = [
+        f"s_mov_b32 s{PM0}, m0",
+        f"s_mov_b32 s{PISS}, 0",
+        f"s_mov_b32 s{PSIG}, 0",
+        f"s_mov_b32 s{PINF}, 0",
+        f"s_mov_b32 s{PPOLL}, {hex(POLL_BUDGET)}",
+        f"s_mov_b64 s[{PBASE}:{PBASE + 1}], %[bb]",
+        f"s_sub_u32 s{PKM1}, %[K], 1",
+    ]
+    # column masks: vec -> lanes whose 4 columns exist (lane < ncol / 4);
+    # dword -> piece q of a row: lanes with 64 q + lane < ncol
+    pieces = 1 if vec else 4
+    for q in range(pieces):
+        m = PCM + 2 * q
+        if vec:
+            L.append(f"s_lshr_b32 s{PTMP}, %[ncol], 2")
+        else:
+            L += [f"s_sub_i32 s{PTMP}, %[ncol], {64 * q}", f"s_max_i32 s{PTMP}, s{PTMP}, 0"]
+        L += [
+            f"s_min_u32 s{PTMP}, s{PTMP}, 64",
+            f"s_bfm_b64 s[{m}:{m + 1}], s{PTMP}, 0",
+            f"s_cmp_ge_u32 s{PTMP}, 64",
+            f"s_cselect_b64 s[{m}:{m + 1}], -1, s[{m}:{m + 1}]",
+        ]
+    L += [
+        ".L%=_loop:",
+        f"s_cmp_ge_u32 s{PSIG}, %[nch]",
+        "s_cbranch_scc1 .L%=_done",
+        f"s_cmp_ge_u32 s{PISS}, %[nch]",
+        "s_cbranch_scc1 .L%=_land",
+        f"s_cmp_ge_u32 s{PINF}, {pmax}",
+        "s_cbranch_scc1 .L%=_land",
+        # slot of chunk `issued` is free once every progress >= issued - RING + 1
+        f"s_sub_i32 s{PNEED}, s{PISS}, {RING - 1}",
+        f"s_cmp_le_i32 s{PNEED}, 0",
+        "s_cbranch_scc1 .L%=_issue",
+        f"s_mov_b64 s[{PEX}:{PEX + 1}], exec",
+        "s_mov_b32 exec_lo, 0xffff",
+        "s_mov_b32 exec_hi, 0",
+        "ds_read_b32 v27, %[pg]",
+        "s_waitcnt lgkmcnt(0)",
+        f"v_cmp_gt_u32 vcc, s{PNEED}, v27",
+        f"s_mov_b64 exec, s[{PEX}:{PEX + 1}]",
+        "s_nop 4",                            # VALU-written vcc read by SALU below
+        "s_cmp_eq_u64 vcc, 0",
+        "s_cbranch_scc1 .L%=_issue",
+        f"s_cmp_eq_u32 s{PINF}, 0",
+        "s_cbranch_scc0 .L%=_land",
+        f"s_cmp_eq_u32 s{PPOLL}, 0",          # budget spent: stage anyway
+        "s_cbranch_scc1 .L%=_issue",
+        f"s_sub_u32 s{PPOLL}, s{PPOLL}, 1",
+        "s_sleep 1",
+        "s_branch .L%=_loop",
+        # stage this producer's rows prow0 .. prow0+half-1 of chunk `issued` into its
+        # slot: LDS row (issued % RING) * CHUNK + prow0 + r; B row min(row, K - 1)
+        ".L%=_issue:",
+        f"s_and_b32 s{PTMP}, s{PISS}, {RING - 1}",
+        f"s_lshl_b32 s{PTMP}, s{PTMP}, {CHUNK.bit_length() - 1 + 10}",
+        "s_lshl_b32 m0, %[prow0], 10",
+        f"s_add_u32 m0, m0, s{PTMP}",
+        f"s_lshl_b32 s{PROW}, s{PISS}, {CHUNK.bit_length() - 1}",
+        f"s_add_u32 s{PROW}, s{PROW}, %[prow0]",
+        f"s_mov_b64 s[{PEX}:{PEX + 1}], exec",
+    ]
+    if vec:
+        L.append(f"s_mov_b64 exec, s[{PCM}:{PCM + 1}]")
+    for r in range(half):
+        L += [
+            f"s_min_u32 s{PTMP}, s{PROW}, s{PKM1}",
+            f"s_mul_i32 s{PADDR}, s{PTMP}, %[rs]",
+            f"s_mul_hi_u32 s{PADDR + 1}, s{PTMP}, %[rs]",
+            f"s_add_u32 s{PADDR}, s{PADDR}, s{PBASE}",
+            f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, s{PBASE + 1}",
+        ]
+        if vec:
+            L += [f"global_load_lds_dwordx4 %[vl], s[{PADDR}:{PADDR + 1}]",
+                  "s_add_u32 m0, m0, 0x400"]
+        else:
+            for q in range(4):
+                m = PCM + 2 * q
+                if q:
+                    L += [f"s_add_u32 s{PADDR}, s{PADDR}, 0x100",
+                          f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, 0"]
+                L += [f"s_mov_b64 exec, s[{m}:{m + 1}]", "s_nop 0",
+                      f"global_load_lds_dword %[vl], s[{PADDR}:{PADDR + 1}]",
+                      "s_add_u32 m0, m0, 0x100"]
+        L.append(f"s_add_u32 s{PROW}, s{PROW}, 1")
+    L += [
+        f"s_mov_b64 exec, s[{PEX}:{PEX + 1}]",
+        f"s_add_u32 s{PISS}, s{PISS}, 1",
+        f"s_add_u32 s{PINF}, s{PINF}, 1",
+        "s_branch .L%=_loop",
+        # wait for the oldest chunk in flight (loads complete in order), publish it
+        ".L%=_land:",
+    ]
+    for n in range(pmax, 1, -1):
+        L += [f"s_cmp_eq_u32 s{PINF}, {n}", f"s_cbranch_scc0 .L%=_land{n}",
+              f"s_waitcnt vmcnt({loads_per_chunk * (n - 1)})", "s_branch .L%=_landed",
+              f".L%=_land{n}:"]
+    L += [
+        "s_waitcnt vmcnt(0)",
+        ".L%=_landed:",
+        f"s_add_u32 s{PSIG}, s{PSIG}, 1",
+        f"s_sub_u32 s{PINF}, s{PINF}, 1",
+        f"v_mov_b32 v27, s{PSIG}",
+        f"s_mov_b64 s[{PEX}:{PEX + 1}], exec",
+        "s_mov_b64 exec, 1",
+        "ds_write_b32 %[ra], v27",
+        f"s_mov_b64 exec, s[{PEX}:{PEX + 1}]",
+        "s_branch .L%=_loop",
+        ".L%=_done:",
+        "s_waitcnt vmcnt(0) lgkmcnt(0)",
+        f"s_mov_b32 m0, s{PM0}",
+    ]
+    body = "\n".join('      "' + x + '\\n\\t"' for x in L)
+    sregs = [f"s{x}" for x in range(PISS, PCM + 2 * pieces)]
+    clob = ", ".join(f'"{r}"' for r in sregs + ["v27", "vcc", "scc"])
+    suffix = "vec" if vec else "dword"
+    return f"""// Producer, {"16-byte" if vec else "4-byte"} staging
+__device__ __forceinline__ void produce_{suffix}(const ProducerArgs& a) {{
+  asm volatile(
+{body}
+      :
+      : [nch] "s"(a.nchunks), [K] "s"(a.K), [rs] "s"(a.row_bytes), [bb] "s"(a.bbase),
+        [ncol] "s"(a.ncol), [prow0] "s"(a.first_row), [vl] "v"(a.vlane),
+        [pg] "v"(a.prog_lane_addr), [ra] "v"(a.ready_addr)
       : {clob});
 }}
 """
@@ -252,14 +365,20 @@ __device__ __forceinline__ void kloop_{suffix}(acc_plane_t<{rw}>& p0, acc_plane_
 def generate() -> str:
     parts = ["// Generated by gen_spmm_asm.py -- do not edit by hand.",
              "#pragma once", "",
-             "// zero groups the stream must carry past its last segment: the scalar ring runs",
+             "// zero groups the stream must carry past its last panel: the scalar ring runs",
              "// NSLOT-1 groups ahead and the L2 touch a further TOUCH_AHEAD bytes",
              f"constexpr int kStreamTailGroups = {NSLOT - 1 + (TOUCH_AHEAD + 31) // 32 + 1};",
-             "// bit of a group's last column word that marks the end of a segment",
-             f"constexpr uint32_t kSegmentEndBit = 1u << {END_BIT};", ""]
+             "// stream and ring layout the loops assume",
+             f"constexpr int kAsmChunk = {CHUNK}, kAsmRing = {RING}, kAsmProducers = {NPROD};",
+             f"constexpr int kAsmEndBit = {END_BIT}, kAsmSyncBit = {SYNC_BIT};",
+             f"constexpr int kAsmLoShift = {LO_SHIFT}, kAsmHiShift = {HI_SHIFT};",
+             f"constexpr uint32_t kAsmRingMask = {hex(RING_MASK)}u;",
+             f"constexpr uint32_t kProgressDone = {hex(INF)}u;",
+             ""]
     for rw in RW_VARIANTS:
-        for vec in (True, False):
-            parts.append(function(rw, vec))
+        parts.append(consumer(rw))
+    for vec in (True, False):
+        parts.append(producer(vec))
     return "\n".join(parts)
 
 

@@ -89,6 +89,32 @@ sdnn_status reorder_bitset(const int32_t* row_ptr, const int32_t* col_idx, int32
   return SDNN_OK;
 }
 
+namespace {
+struct Entry {
+  uint32_t w;      // weight bits
+  uint32_t a;      // ring row << 10 | row
+  int32_t chunk;
+};
+
+// Writes one group (n <= kGroup real entries from e) with its fields.
+void emit_group(std::vector<uint32_t>& out, const Entry* e, int n, bool first, bool last,
+                int32_t* prev_lo, int32_t* prev_hi) {
+  uint32_t w[kGroup], a[kGroup];
+  for (int j = 0; j < kGroup; ++j) {
+    w[j] = j < n ? e[j].w : 0u;            // zero-weight copies of the first entry
+    a[j] = j < n ? e[j].a : e[0].a;
+  }
+  const int32_t lo = e[0].chunk, hi = e[n - 1].chunk;
+  const bool sync = first || last || lo != *prev_lo || hi != *prev_hi;
+  a[2] |= (uint32_t)lo << kLoShift;
+  a[3] |= (uint32_t)hi << kHiShift | (uint32_t)sync << kSyncBit | (uint32_t)last << kEndBit;
+  *prev_lo = lo;
+  *prev_hi = hi;
+  for (int j = 0; j < kGroup; ++j) out.push_back(w[j]);
+  for (int j = 0; j < kGroup; ++j) out.push_back(a[j]);
+}
+}  // namespace
+
 sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* values, int32_t M,
                  int32_t K, int32_t RW, const int32_t* perm, Packed* out) {
   try {
@@ -98,20 +124,21 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
     P.RW = RW;
     P.nnz = M ? row_ptr[M] : 0;
     P.nchunks = (K + kChunk - 1) / kChunk;
+    if (P.nchunks > kMaxChunks) return SDNN_ERR_DIM;
     P.npanels = (M + RW - 1) / RW;
     P.perm.assign(perm, perm + M);
     P.panel_rows.assign((size_t)P.npanels * RW, -1);
     for (int32_t i = 0; i < M; ++i) P.panel_rows[i] = perm[i];
-    const size_t nseg = (size_t)P.npanels * P.nchunks;
-    P.seg_start.assign(nseg + 1, 0);
-    P.counts.assign(nseg * RW, 0);
+    P.panel_start.assign((size_t)P.npanels, -1);
     P.entries.clear();
-    P.entries.reserve((size_t)(P.nnz + P.nnz / 2 + 64) * 2);
+    P.entries.reserve((size_t)(P.nnz + P.nnz / 8 + 64) * 2);
 
     std::vector<int32_t> cursor(RW);
     std::vector<int32_t> mark((size_t)std::max(K, 1), -1);
+    std::vector<Entry> ent;
     int64_t union_total = 0;
     for (int32_t p = 0; p < P.npanels; ++p) {
+      ent.clear();
       for (int32_t r = 0; r < RW; ++r) {
         const int32_t orig = P.panel_rows[(size_t)p * RW + r];
         cursor[r] = orig >= 0 ? row_ptr[orig] : 0;
@@ -122,42 +149,41 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
               ++union_total;
             }
       }
-      for (int32_t k = 0; k < P.nchunks; ++k) {
-        const int32_t hi = (k + 1) * kChunk;
-        P.seg_start[(size_t)p * P.nchunks + k] = (int32_t)(P.entries.size() / (2 * kGroup));
-        // gather the segment's entries row by row, then write them group-wise
-        std::vector<uint32_t> w, a;
+      // the panel's entries in (chunk, row, column) order
+      for (int32_t c = 0; c < P.nchunks; ++c) {
+        const int32_t hi = (c + 1) * kChunk;
+        const uint32_t ring_base = (uint32_t)((c % kRing) * kChunk);
         for (int32_t r = 0; r < RW; ++r) {
           const int32_t orig = P.panel_rows[(size_t)p * RW + r];
           if (orig < 0) continue;
           int32_t q = cursor[r];
           const int32_t end = row_ptr[orig + 1];
-          int32_t c = 0;
-          while (q < end && col_idx[q] < hi) {
-            uint32_t wbits;
-            memcpy(&wbits, &values[q], 4);
-            w.push_back(wbits);
-            a.push_back(((uint32_t)(col_idx[q] - k * kChunk) << 10) | (uint32_t)r);
-            ++q;
-            ++c;
+          for (; q < end && col_idx[q] < hi; ++q) {
+            Entry e;
+            memcpy(&e.w, &values[q], 4);
+            e.a = (ring_base + (uint32_t)(col_idx[q] - c * kChunk)) << kRingRowShift | (uint32_t)r;
+            e.chunk = c;
+            ent.push_back(e);
           }
           cursor[r] = q;
-          P.counts[((size_t)p * P.nchunks + k) * RW + r] = (uint16_t)c;
         }
-        while (w.empty() || w.size() % kGroup != 0) {  // zero padding to whole groups
-          w.push_back(0u);
-          a.push_back(0u);
-        }
-        a.back() |= 1u << kSegEndBit;  // last group of the segment
-        for (size_t g = 0; g < w.size(); g += kGroup) {
-          for (int j = 0; j < kGroup; ++j) P.entries.push_back(w[g + j]);
-          for (int j = 0; j < kGroup; ++j) P.entries.push_back(a[g + j]);
-        }
+      }
+      if (ent.empty()) continue;
+      P.panel_start[p] = (int32_t)(P.entries.size() / (2 * kGroup));
+      int32_t prev_lo = -1, prev_hi = -1;
+      size_t i = 0;
+      bool first = true;
+      while (i < ent.size()) {
+        int n = 1;  // a group never reads more than kRing chunks
+        while (n < kGroup && i + n < ent.size() && ent[i + n].chunk - ent[i].chunk < kRing) ++n;
+        const bool last = i + n == ent.size();
+        emit_group(P.entries, &ent[i], n, first, last, &prev_lo, &prev_hi);
+        first = false;
+        i += n;
       }
     }
     P.stored = (int64_t)(P.entries.size() / 2);
     if (P.stored > INT32_MAX - kTailGroups * kGroup) return SDNN_ERR_DIM;
-    P.seg_start[nseg] = (int32_t)(P.stored / kGroup);
     for (int i = 0; i < kTailGroups * kGroup; ++i) {  // tail padding for the prefetch
       P.entries.push_back(0u);
       P.entries.push_back(0u);
@@ -169,63 +195,93 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
   return SDNN_OK;
 }
 
-// Independent re-walk of a packed stream: every CSR entry must appear exactly once, in
-// its row's panel and chunk, rows in panel order, columns ascending, weight bits
-// unchanged, offsets inside the chunk; each segment ends with fewer than kGroup zero
-// padding entries (a whole zero group if it is empty) and carries the end flag on its
-// last word, and the stream ends with kTailGroups zero groups.
+// Independent re-walk of a packed stream.  Decoding each panel's groups must give
+// back exactly the CSR entries of the panel's rows (weight bits unchanged) in (chunk,
+// row, column) order; every field of every group must be consistent (chunk range at
+// most kRing wide and inside it every entry's chunk, sync and end flags set exactly
+// where the format says, unused bits clear); zero-weight filler copies of a group's
+// first entry may only close a group that ends the panel or that the next entry
+// could not join; and the stream must end with kTailGroups zero groups.
 static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const float* values,
                          const Packed& P) {
-  std::vector<char> seen((size_t)P.nnz, 0);
-  std::vector<int32_t> pos_of_row((size_t)std::max(P.M, 1), 0);
-  for (int32_t i = 0; i < P.M; ++i) pos_of_row[i] = row_ptr[i];
   if ((int64_t)P.entries.size() != 2 * (P.stored + kTailGroups * kGroup)) return false;
   if (P.stored % kGroup != 0) return false;
-  auto weight = [&](int64_t e) { return P.entries[(e / kGroup) * 2 * kGroup + (e % kGroup)]; };
-  auto word = [&](int64_t e) {
-    return P.entries[(e / kGroup) * 2 * kGroup + kGroup + (e % kGroup)];
-  };
+  if ((int64_t)P.panel_start.size() != P.npanels) return false;
+  const int64_t ngroups = P.stored / kGroup;
+  std::vector<char> seen((size_t)P.nnz, 0);
+  int64_t expect_group = 0;  // panels are stored back to back
   for (int32_t p = 0; p < P.npanels; ++p) {
-    for (int32_t k = 0; k < P.nchunks; ++k) {
-      const size_t s = (size_t)p * P.nchunks + k;
-      int64_t e = (int64_t)P.seg_start[s] * kGroup;
-      const int64_t end = (int64_t)P.seg_start[s + 1] * kGroup;
-      if (end < e || end > P.stored) return false;
-      if (end - e < kGroup) return false;  // at least one group
-      // the segment-end flag sits exactly on the last word of the last group
-      for (int64_t x = e; x < end; ++x) {
-        const bool flagged = (word(x) >> kSegEndBit) & 1u;
-        if (flagged != (x == end - 1)) return false;
-      }
-      auto plain = [&](int64_t x) { return word(x) & ~(1u << kSegEndBit); };
+    // the panel's CSR entries in (chunk, row, column) order
+    std::vector<int64_t> want;
+    for (int32_t c = 0; c < P.nchunks; ++c)
       for (int32_t r = 0; r < P.RW; ++r) {
         const int32_t orig = P.panel_rows[(size_t)p * P.RW + r];
-        const int32_t c = P.counts[s * P.RW + r];
-        if (orig < 0 && c != 0) return false;
-        for (int32_t j = 0; j < c; ++j, ++e) {
-          if (e >= end) return false;
-          const uint32_t wd = plain(e);
-          if ((int32_t)(wd & 0x3ffu) != r) return false;
-          if ((wd & 0x300u) != 0u) return false;
-          const uint32_t off = wd >> 10;
-          if (off >= (uint32_t)kChunk) return false;
-          const int32_t col = k * kChunk + (int32_t)off;
-          const int32_t q = pos_of_row[orig]++;
-          if (q >= row_ptr[orig + 1] || col_idx[q] != col || seen[q]) return false;
-          uint32_t vbits;
-          memcpy(&vbits, &values[q], 4);
-          if (vbits != weight(e)) return false;
-          seen[q] = 1;
-        }
+        if (orig < 0) continue;
+        for (int32_t q = row_ptr[orig]; q < row_ptr[orig + 1]; ++q)
+          if (col_idx[q] / kChunk == c) want.push_back(q);
       }
-      // padding: fewer than kGroup entries, or one whole group for an empty segment
-      if (end - e >= kGroup && !(end - e == kGroup && e == end - kGroup &&
-                                 (int64_t)P.seg_start[s] * kGroup == e))
-        return false;
-      for (; e < end; ++e)
-        if (weight(e) != 0u || plain(e) != 0u) return false;
+    if (want.empty()) {
+      if (P.panel_start[p] != -1) return false;
+      continue;
+    }
+    if (P.panel_start[p] != expect_group) return false;
+    size_t k = 0;  // next wanted entry
+    int32_t prev_lo = -1, prev_hi = -1;
+    for (int64_t g = P.panel_start[p];; ++g) {
+      if (g >= ngroups) return false;
+      const uint32_t* w = &P.entries[(size_t)g * 2 * kGroup];
+      const uint32_t* a = w + kGroup;
+      const int32_t lo = (int32_t)(a[2] >> kLoShift), hi = (int32_t)(a[3] >> kHiShift);
+      const bool sync = (a[3] >> kSyncBit) & 1u, last = (a[3] >> kEndBit) & 1u;
+      if (lo > hi || hi - lo >= kRing || hi >= P.nchunks || lo < prev_lo) return false;
+      const bool first = g == P.panel_start[p];
+      if (sync != (first || last || lo != prev_lo || hi != prev_hi)) return false;
+      prev_lo = lo;
+      prev_hi = hi;
+      int nreal = 0;
+      int32_t max_chunk = -1;
+      for (int j = 0; j < kGroup; ++j) {
+        uint32_t fields = a[j] & ((1u << kLoShift) - 1);
+        if (j == 3) fields &= ~(1u << kEndBit);
+        if ((fields >> kRowBits) & ((1u << (kRingRowShift - kRowBits)) - 1)) return false;
+        if (j < 2 && (a[j] >> kLoShift) != 0u) return false;
+        const uint32_t row = fields & ((1u << kRowBits) - 1);
+        const uint32_t ring_row = fields >> kRingRowShift;
+        if (row >= (uint32_t)P.RW || ring_row >= (uint32_t)(kRing * kChunk)) return false;
+        const int32_t slot = (int32_t)ring_row / kChunk;
+        const int32_t chunk = lo + ((slot - lo % kRing) % kRing + kRing) % kRing;
+        const int32_t col = chunk * kChunk + (int32_t)ring_row % kChunk;
+        const bool filler = j > 0 && w[j] == 0u && (fields == (a[0] & ((1u << kLoShift) - 1)));
+        if (filler) {
+          if (nreal == 0) return false;
+          continue;
+        }
+        if (nreal != j) return false;  // fillers only after the real entries
+        ++nreal;
+        if (k >= want.size()) return false;
+        const int64_t q = want[k++];
+        const int32_t orig = P.panel_rows[(size_t)p * P.RW + row];
+        if (orig < 0 || q < row_ptr[orig] || q >= row_ptr[orig + 1]) return false;
+        if (col_idx[q] != col || chunk > hi || seen[q]) return false;
+        uint32_t vbits;
+        memcpy(&vbits, &values[q], 4);
+        if (vbits != w[j]) return false;
+        seen[q] = 1;
+        max_chunk = std::max(max_chunk, chunk);
+      }
+      if (max_chunk != hi) return false;
+      if (last != (k == want.size())) return false;
+      if (nreal < kGroup && !last) {  // cut short: the next entry is too far ahead
+        const int32_t next_chunk = col_idx[want[k]] / kChunk;
+        if (next_chunk - lo < kRing) return false;
+      }
+      if (last) {
+        expect_group = g + 1;
+        break;
+      }
     }
   }
+  if (expect_group != ngroups) return false;
   for (int64_t q = 0; q < P.nnz; ++q)
     if (!seen[q]) return false;
   for (size_t d = (size_t)(2 * P.stored); d < P.entries.size(); ++d)
@@ -335,7 +391,7 @@ sdnn_status sdnn_plan_check_host(const int32_t* row_ptr, const int32_t* col_idx,
     if (!check_packed(row_ptr, col_idx, values, P)) return SDNN_ERR_INTERNAL;
     if (info) {
       const int64_t bytes = align256((int64_t)P.entries.size() * 4) +
-                            align256((int64_t)P.seg_start.size() * 4) +
+                            align256((int64_t)P.panel_start.size() * 4) +
                             align256((int64_t)P.panel_rows.size() * 4);
       fill_info(P, bytes, info);
     }
@@ -376,7 +432,7 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
     plan->perm = P.perm;
 
     const int64_t b_ent = align256((int64_t)P.entries.size() * 4);
-    const int64_t b_seg = align256((int64_t)P.seg_start.size() * 4);
+    const int64_t b_seg = align256((int64_t)P.panel_start.size() * 4);
     const int64_t b_rows = align256((int64_t)P.panel_rows.size() * 4);
     const int64_t total = b_ent + b_seg + b_rows;
     plan->packed_bytes = total;
@@ -388,12 +444,12 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
       }
       char* base = (char*)plan->d_mem;
       plan->d_entries = (const uint32_t*)base;
-      plan->d_seg = (const int32_t*)(base + b_ent);
+      plan->d_panel_start = (const int32_t*)(base + b_ent);
       plan->d_panel_rows = (const int32_t*)(base + b_ent + b_seg);
       std::vector<char> host((size_t)total, 0);
       if (!P.entries.empty()) memcpy(host.data(), P.entries.data(), P.entries.size() * 4);
-      if (!P.seg_start.empty())
-        memcpy(host.data() + b_ent, P.seg_start.data(), P.seg_start.size() * 4);
+      if (!P.panel_start.empty())
+        memcpy(host.data() + b_ent, P.panel_start.data(), P.panel_start.size() * 4);
       if (!P.panel_rows.empty())
         memcpy(host.data() + b_ent + b_seg, P.panel_rows.data(), P.panel_rows.size() * 4);
       if (hipMemcpy(plan->d_mem, host.data(), (size_t)total, hipMemcpyHostToDevice) !=

@@ -12,40 +12,52 @@
 
 namespace sdnn {
 
-// Rows of B staged in LDS per pass over the reduction dimension (the paper's split-K
-// tiling of the dense operand, Sec. 3.2.2).  The packed stream is cut at these
-// boundaries, so the value is fixed at plan creation.
-constexpr int kChunk = 64;
+// Rows of B per LDS staging slot (the paper's split-K tiling of the dense operand,
+// Sec. 3.2.2) and slots in the workgroup's LDS ring.  Chunk c of B (rows
+// [c*kChunk, (c+1)*kChunk)) lives in slot c % kRing while it is in use.
+constexpr int kChunk = 32;
+constexpr int kRing = 4;
 // Stream entries are consumed in groups of kGroup.
 constexpr int kGroup = 4;
 // Columns of C per workgroup tile: 64 lanes x 4 consecutive columns.
 constexpr int kTileCols = 256;
-// Zero groups appended after the last segment: the kernel's stream prefetch may read
+// Zero groups appended after the last panel: the kernel's stream prefetch may read
 // this many groups past the end of a panel's stream.
 constexpr int kTailGroups = 24;
-// Marks the last group of a segment (in the group's last column word).
-constexpr int kSegEndBit = 9;
+// Fields of a group's four address words a0..a3 (see Packed).
+constexpr int kRowBits = 8;         // a_j & 0xff: row inside the panel
+constexpr int kEndBit = 9;          // a3: last group of the panel
+constexpr int kRingRowShift = 10;   // (a_j >> 10) & 0x7f: row of the LDS ring
+constexpr int kSyncBit = 17;        // a3: publish progress / check readiness first
+constexpr int kLoShift = 17;        // a2 >> 17: lowest chunk the group reads
+constexpr int kHiShift = 18;        // a3 >> 18: highest chunk the group reads
+constexpr int kMaxChunks = 1 << 14; // chunk numbers must fit a3's high bits
+static_assert(kRing * kChunk <= 128, "ring rows must fit 7 bits");
 
 // Host-side packed form of W in the kernel's traversal order (Sec. 3.2.2: each
 // matrix stored in its own format, read sequentially).
 //
-//   Panels of RW consecutive rows of the permuted matrix.  For panel p and chunk k the
-//   segment holds the entries of rows 0..RW-1 of the panel (row by row, each row in
-//   ascending column order) whose column lies in [k*kChunk, (k+1)*kChunk), padded at
-//   its end with zero entries to whole groups, and at least one group long.  A group
-//   of kGroup entries is stored as 2*kGroup dwords: the kGroup fp32 weight bits, then
-//   kGroup words (column offset inside the chunk << 10) | r; bit kSegEndBit of the
-//   group's last word is set on the last group of a segment.  A panel's segments are
-//   stored back to back in chunk order, panels in order, and the stream ends with
-//   kTailGroups zero groups so that a kernel may prefetch that many groups past it.
+//   Panels of RW consecutive rows of the permuted matrix.  A panel's entries are
+//   ordered by K-chunk, then by row inside the panel, then by column, and cut into
+//   groups of kGroup.  A group never spans more than kRing chunks: the entry that
+//   would make it do so starts a new group, and a group cut short this way or by the
+//   end of the panel is filled with zero-weight copies of its first entry.  A group
+//   is 2*kGroup dwords: the kGroup fp32 weight bits, then kGroup words
+//       a_j = ((c_j % kRing) * kChunk + col_j - c_j * kChunk) << 10 | row_j
+//   (c_j = chunk of the entry; the shifted part is the entry's B row in the LDS
+//   ring) with extra fields
+//       a2 |= c_lo << 17, a3 |= c_hi << 18 | sync << 17 | end << 9
+//   where c_lo / c_hi are the lowest / highest chunk the group reads, end marks the
+//   panel's last group and sync is set on a panel's first and last groups and
+//   whenever c_lo or c_hi differs from the previous group's.  Panels are stored back
+//   to back; panel_start holds each panel's first group (-1: the panel has no
+//   entries).  The stream ends with kTailGroups zero groups.
 struct Packed {
   int32_t M = 0, K = 0, RW = 0, nchunks = 0, npanels = 0;
   int64_t nnz = 0, stored = 0;     // structural entries, stored entries (with padding)
   std::vector<int32_t> perm;        // [M]   original row at permuted position
   std::vector<int32_t> panel_rows;  // [npanels*RW] original row or -1 (padding)
-  std::vector<int32_t> seg_start;   // [npanels*nchunks + 1] first group of each segment
-  std::vector<uint16_t> counts;     // [npanels*nchunks*RW] real entries per (panel, chunk, row)
-                                    // (host-side only, used by the self-check)
+  std::vector<int32_t> panel_start; // [npanels] first group of the panel, or -1
   std::vector<uint32_t> entries;    // [2*(stored + kTailGroups*kGroup)] dwords
   double rho = 1.0;                 // nnz / sum_p |union of the panel's column sets|
 };
@@ -71,7 +83,7 @@ struct sdnn_plan_s {
   std::vector<int32_t> perm;
   void* d_mem = nullptr;             // one device allocation holding the three arrays
   const uint32_t* d_entries = nullptr;  // [2*(stored + kTailGroups*kGroup)] dwords
-  const int32_t* d_seg = nullptr;    // [npanels*nchunks + 1] (in groups)
+  const int32_t* d_panel_start = nullptr;  // [npanels] (in groups, -1: empty panel)
   const int32_t* d_panel_rows = nullptr;  // [npanels*RW]
 };
 

@@ -6,26 +6,27 @@
 // multiplies it with a row slice of the dense matrix held in registers, accumulating
 // into an output tile kept in registers; the register that a nonzero accumulates into
 // is fixed by generated code per matrix (Sec. 3.2.2, Fig. 3).  On CDNA4:
-//   * a wavefront owns a panel of RW rows of the permuted W and a tile of 256 columns
-//     of C; lane l holds columns 4l..4l+3 of all RW rows in VGPRs;
-//   * the panel's nonzeros of the current K-chunk form one flat stream of (weight,
-//     column, row) entries read with scalar loads, so weights sit in SGPRs; the output
-//     row of each entry selects the accumulator through VGPR index mode instead of
-//     per-matrix generated code;
-//   * the K-chunk of B rows the workgroup needs is staged in LDS (the paper's split-K
-//     tiling of the dense operand), double buffered, by direct global->LDS 16-byte DMA
-//     so staging of chunk k+1 overlaps the FMAs of chunk k; a lane reads its 4 columns
-//     of a B row with one ds_read_b128;
-//   * the inner loop (generated inline assembly, spmm_asm_gen.h) pipelines stream
-//     loads two groups ahead and LDS reads one group ahead of the FMAs;
+//   * a consumer wavefront owns a panel of RW rows of the permuted W and a tile of 256
+//     columns of C; lane l holds columns 4l..4l+3 of all RW rows in VGPRs;
+//   * the panel's nonzeros form one flat stream of (weight, ring row, row) entries
+//     read with scalar loads, so weights sit in SGPRs; the output row of each entry
+//     selects the accumulator through VGPR index mode instead of per-matrix generated
+//     code;
+//   * the rows of B the workgroup needs are staged in LDS (the paper's split-K tiling
+//     of the dense operand) by two producer wavefronts, through a ring of 32-row
+//     slots filled by direct global->LDS 16-byte DMA; a lane reads its 4 columns of a
+//     B row with one ds_read_b128;
+//   * producers and consumers synchronise through LDS words (chunks landed, lowest
+//     chunk each consumer still reads), so no wave ever waits at a workgroup barrier
+//     for the slowest one; the loops are generated inline assembly (spmm_asm_gen.h);
 //   * the bias + activation epilogue is fused and C is written once, coalesced, to
 //     the original (unpermuted) row.
 // Plain FP32 FMA is used throughout (no MFMA: the work is not a dense contraction).
 //
-// Workgroups: one 256-column tile x one row-block of `waves` consecutive panels.  All
-// panels of a row-block share the staged B chunk.  The flat block id is remapped so
-// that all row-blocks of a tile land on one XCD (blocks are dealt to the 8 XCDs round
-// robin), letting them share that XCD's L2 copy of the B tile.
+// Workgroups: one 256-column tile x one row-block of nc consecutive panels, plus the
+// producer waves.  All panels of a row-block share the staged B rows.  The flat block
+// id is remapped so that all row-blocks of a tile land on one XCD (blocks are dealt
+// to the 8 XCDs round robin), letting them share that XCD's L2 copy of the B tile.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -38,22 +39,39 @@ namespace {
 template <int RW>
 using acc_plane_t = float __attribute__((ext_vector_type(RW)));
 
-// Operands of the assembly K-loop (wave-uniform values go to SGPRs, the rest to VGPRs).
-struct KloopArgs {
-  const uint32_t* stream;  // first group of the wave's panel; null: no panel (the wave
-                           // only stages B and joins the barriers)
+// Operands of the assembly loops (wave-uniform values go to SGPRs, the rest to VGPRs).
+struct ConsumerArgs {
+  const uint32_t* stream;  // the panel's first group
+  uint32_t vlane;          // 16 * lane: the lane's byte offset in a staged B row
+  uint32_t prog_addr;      // LDS address of this consumer's progress word
+  uint32_t ready_addr;     // LDS address of the ready word
+};
+struct ProducerArgs {
   int32_t nchunks, K;
   uint32_t row_bytes;      // N * 4
-  uint32_t wave, nwaves;
+  uint64_t bbase;          // address of B[0][n0]
   int32_t ncol;            // N - n0 (columns of the tile that exist)
-  uint64_t vbase;          // B[0][n0] + this lane's byte offset in a staged row segment
-  uint32_t vl0, vl1;       // this lane's LDS read address in buffer 0 / 1
-  uint32_t lane;
+  uint32_t first_row;      // first row of each chunk this producer stages
+  uint32_t vlane;          // the lane's byte offset in a B row segment (16 or 4 * lane)
+  uint32_t prog_lane_addr; // LDS address of progress word `lane` (lanes 0..15)
+  uint32_t ready_addr;     // LDS address of this producer's ready word
 };
 
 #include "spmm_asm_gen.h"
 static_assert(kStreamTailGroups <= kTailGroups, "stream tail shorter than the prefetch");
-static_assert(kSegmentEndBit == (1u << kSegEndBit), "segment-end flag mismatch");
+static_assert(kAsmChunk == kChunk && kAsmRing == kRing, "ring layout mismatch");
+constexpr int kProducers = kAsmProducers;
+static_assert(kAsmEndBit == kEndBit && kAsmSyncBit == kSyncBit && kAsmLoShift == kLoShift &&
+                  kAsmHiShift == kHiShift,
+              "stream fields mismatch");
+static_assert(kAsmRingMask == (uint32_t)(kRing * kChunk - 1) << kRingRowShift,
+              "ring-row mask mismatch");
+
+constexpr int kRingBytes = kRing * kChunk * 1024;
+constexpr int kMaxConsumers = 16 - kProducers;
+// LDS control words after the ring: ready[kProducers] at +0, progress[16] at +64.
+constexpr int kCtlWords = 256;
+static_assert(kProducers <= 16, "ready words overlap the progress words");
 
 __device__ __forceinline__ float activation(float x, int epi) {
   if (epi == SDNN_EPI_RELU) return fmaxf(x, 0.0f);
@@ -72,55 +90,75 @@ struct SpmmArgs {
 };
 
 // RW: rows per panel; VEC: N % 4 == 0 and B, C 16-byte aligned (16-byte staging DMA,
-// vector stores of C).
+// vector stores of C).  blockDim.x = 64 * (consumers + kProducers).
 template <int RW, bool VEC>
 __global__ __launch_bounds__(1024) void spmm_panel_kernel(
-    const uint32_t* __restrict__ entries, const int32_t* __restrict__ segs,
+    const uint32_t* __restrict__ entries, const int32_t* __restrict__ panel_start,
     const int32_t* __restrict__ panel_rows, const float* __restrict__ B, float* __restrict__ C,
     const float* __restrict__ bias, SpmmArgs a) {
-  constexpr int CHUNK_FLOATS = kChunk * kTileCols;
-  // the two staging buffers: [0, 64 KB) and [64 KB, 128 KB) of the workgroup's LDS.
-  // The inner loop forms addresses as (column << 10) | (buffer + 16 * lane), which
-  // needs both buffer bases 64 KB aligned; this is the kernel's only LDS object, so it
-  // starts at offset 0.
-  __shared__ __attribute__((aligned(16))) float lds[2 * CHUNK_FLOATS];
+  // the ring ([0, kRingBytes)) and the control words; the ring must start at LDS 0
+  // (the loops form LDS addresses from the ring-row field alone), which holds because
+  // this is the kernel's only LDS object
+  __shared__ __attribute__((aligned(16))) uint32_t lds[kRingBytes / 4 + kCtlWords];
 
   const int bid = blockIdx.x;
   const int lin = (bid & 7) * a.per_xcd + (bid >> 3);
-  if (lin >= a.total_wg) return;  // whole workgroup leaves before any barrier
+  if (lin >= a.total_wg) return;  // whole workgroup leaves before the barrier
   const int tile = lin / a.n_rb;
   const int rb = lin - tile * a.n_rb;
-  const int nwaves = blockDim.x >> 6;
+  const int nc = (blockDim.x >> 6) - kProducers;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int panel = rb * nwaves + wave;
-  const bool active = panel < a.npanels;
   const int n0 = tile * kTileCols;
-  const int nchunks = a.nchunks;
-  (void)lane;
+  const int prod = wave - nc;  // >= 0: producer index
+  const int panel = rb * nc + wave;
+  const int gstart = (prod < 0 && panel < a.npanels) ? panel_start[panel] : -1;
+
+  const uint32_t lds_base = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) uint32_t*)lds);
+  if (lds_base != 0) return;  // never taken: see above
+  const uint32_t ready_addr = lds_base + kRingBytes;
+  const uint32_t prog0 = ready_addr + 64;
+  uint32_t* ctl = lds + kRingBytes / 4;
+  if (prod >= 0) {
+    if (lane == 0) ctl[prod] = 0u;                                           // nothing landed
+    if (prod == 0 && lane >= nc && lane < 16) ctl[16 + lane] = kProgressDone;  // absent consumers
+  } else if (lane == 0) {
+    ctl[16 + wave] = gstart >= 0 ? 0u : kProgressDone;
+  }
+  __syncthreads();
+
+  if (prod >= 0) {
+    ProducerArgs pa;
+    pa.nchunks = a.nchunks;
+    pa.K = a.K;
+    pa.row_bytes = (uint32_t)a.N * 4u;
+    pa.bbase = (uint64_t)(uintptr_t)(B + n0);
+    pa.ncol = a.N - n0;
+    pa.first_row = (uint32_t)(prod * (kChunk / kProducers));
+    pa.vlane = (uint32_t)lane * (VEC ? 16u : 4u);
+    pa.prog_lane_addr = prog0 + 4u * (uint32_t)(lane & 15);
+    pa.ready_addr = ready_addr + 4u * (uint32_t)prod;
+    if (VEC)
+      produce_vec(pa);
+    else
+      produce_dword(pa);
+    return;
+  }
+  if (panel >= a.npanels) return;
 
   acc_plane_t<RW> p0 = {}, p1 = {}, p2 = {}, p3 = {};
-  const uint32_t lds_base = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) float*)lds);
-  if (lds_base != 0) return;  // the staging code assumes buffers at LDS 0 and 64 KB
-  const uint64_t bcol = (uint64_t)(uintptr_t)(B + n0);
-  KloopArgs ka;
-  ka.stream = active ? entries + (size_t)segs[panel * nchunks] * (2 * kGroup) : nullptr;
-  ka.nchunks = nchunks;
-  ka.K = a.K;
-  ka.row_bytes = (uint32_t)a.N * 4u;
-  ka.wave = (uint32_t)wave;
-  ka.nwaves = (uint32_t)nwaves;
-  ka.ncol = a.N - n0;
-  ka.vbase = bcol + (uint64_t)lane * (VEC ? 16u : 4u);
-  ka.vl0 = lds_base + (uint32_t)lane * 16u;
-  ka.vl1 = ka.vl0 + (uint32_t)CHUNK_FLOATS * 4u;
-  ka.lane = (uint32_t)lane;
-  if (VEC)
-    kloop_vec(p0, p1, p2, p3, ka);
-  else
-    kloop_dword(p0, p1, p2, p3, ka);
+  if (gstart >= 0) {  // a panel without entries only writes epi(bias)
+    ConsumerArgs ca;
+    ca.stream = entries + (size_t)gstart * (2 * kGroup);
+    ca.vlane = (uint32_t)lane * 16u;
+    ca.prog_addr = prog0 + 4u * (uint32_t)wave;
+    ca.ready_addr = ready_addr;
+    if constexpr (RW == 4) consume_rw4(p0, p1, p2, p3, ca);
+    if constexpr (RW == 8) consume_rw8(p0, p1, p2, p3, ca);
+    if constexpr (RW == 12) consume_rw12(p0, p1, p2, p3, ca);
+    if constexpr (RW == 16) consume_rw16(p0, p1, p2, p3, ca);
+  }
 
-  if (!active) return;
   const int ncol = n0 + lane * 4;
 #pragma unroll
   for (int r = 0; r < RW; ++r) {
@@ -143,7 +181,7 @@ __global__ __launch_bounds__(1024) void spmm_panel_kernel(
 
 struct SpmmPtrs {
   const uint32_t* entries;
-  const int32_t* seg;
+  const int32_t* panel_start;
   const int32_t* panel_rows;
   const float* B;
   float* C;
@@ -153,8 +191,8 @@ struct SpmmPtrs {
 template <int RW, bool VEC>
 hipError_t launch_variant(const SpmmPtrs& p, const SpmmArgs& args, int waves, int grid,
                           hipStream_t stream) {
-  hipLaunchKernelGGL((spmm_panel_kernel<RW, VEC>), dim3(grid), dim3(64 * waves), 0, stream,
-                     p.entries, p.seg, p.panel_rows, p.B, p.C, p.bias, args);
+  hipLaunchKernelGGL((spmm_panel_kernel<RW, VEC>), dim3(grid), dim3(64 * (waves + kProducers)), 0, stream,
+                     p.entries, p.panel_start, p.panel_rows, p.B, p.C, p.bias, args);
   return hipGetLastError();
 }
 
@@ -176,11 +214,12 @@ int env_int(const char* name, int dflt) {
 }
 
 struct LaunchCfg {
-  int waves, n_tiles, n_rb;
+  int waves, n_tiles, n_rb;  // waves: consumer waves per workgroup (one more produces)
 };
 
 // Panels per workgroup: enough row-blocks that the grid covers every CU about once
-// (the 128 KB of staging LDS allows one workgroup per CU), at most 16 waves.
+// (the 129 KB of ring and control LDS allows one workgroup per CU), at most
+// kMaxConsumers consumer waves.  SDNN_FORCE_WAVES fixes the consumer count.
 LaunchCfg choose_cfg(const sdnn_plan_s* p, int N) {
   const int target = p->num_cus > 0 ? p->num_cus : 256;
   const int forceW = env_int("SDNN_FORCE_WAVES", 0);
@@ -193,7 +232,7 @@ LaunchCfg choose_cfg(const sdnn_plan_s* p, int N) {
     if (n_rb > p->npanels) n_rb = p->npanels;
     c.waves = (p->npanels + n_rb - 1) / n_rb;
   }
-  if (c.waves > 16) c.waves = 16;
+  if (c.waves > kMaxConsumers) c.waves = kMaxConsumers;
   if (c.waves > p->npanels) c.waves = p->npanels;
   if (c.waves < 1) c.waves = 1;
   c.n_rb = (p->npanels + c.waves - 1) / c.waves;
@@ -205,7 +244,7 @@ LaunchCfg choose_cfg(const sdnn_plan_s* p, int N) {
 hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                        const float* bias, int epi, hipStream_t stream) {
   const LaunchCfg cfg = choose_cfg(p, N);
-  const SpmmPtrs ptrs{p->d_entries, p->d_seg, p->d_panel_rows, B, C, bias};
+  const SpmmPtrs ptrs{p->d_entries, p->d_panel_start, p->d_panel_rows, B, C, bias};
   SpmmArgs args;
   args.K = p->K;
   args.N = N;
