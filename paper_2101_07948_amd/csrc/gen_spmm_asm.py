@@ -27,25 +27,26 @@ chunk can always be staged: the loops cannot deadlock.  Each wait is also bounde
 a per-wave poll budget, after which the wave goes on without waiting (the result is
 then wrong, but the kernel ends).
 
-Stream consumed (see sdnn_internal.h): per panel, groups of 8 dwords
-[w0 w1 w2 w3 a0 a1 a2 a3]; w = fp32 weight bits; a = (ring row << 10) | row, plus
-c_lo in a2 >> 17, c_hi in a3 >> 18, the sync flag in a3 bit 17 and the end-of-panel
-flag in a3 bit 9.  The ring row field is bits 10..16, so (a & 0x1fc00) | (16 * lane)
-is the LDS address of the lane's 4 B values; VGPR index mode uses only a's low 8 bits.
+Stream consumed (see sdnn_internal.h): per panel, groups of 16 dwords (64 bytes,
+one scalar load, one scalar-cache line) [w0..w7 a0..a7]; w = fp32 weight bits;
+a = (ring row << 10) | row, plus c_lo in a6 >> 17, c_hi in a7 >> 18, the sync flag in
+a7 bit 17 and the end-of-panel flag in a7 bit 9.  The ring row field is bits 10..16,
+so (a & 0x1fc00) | (16 * lane) is the LDS address of the lane's 4 B values; VGPR
+index mode uses only a's low 8 bits.
 
 Consumer register plan (pinned in the asm statement):
   v31 0x1fc00 (ring-row mask), v28 zero offset and v29 sink of the L2 touch loads,
-  v27 temp, v[32:47] / v[48:63] B values of the group being multiplied / fetched,
-  v[64 + k*RW + r] accumulator of row r, column 4*lane + k (k = 0..3);
-  s[40:79] ring of NSLOT stream groups, s[80:81] next group to fetch, s82 chunks known
-  ready, s83 temp, s84 poll budget, s85 saved m0, s[86:87] saved exec, s88 temp;
-  v26 temp.
+  v26, v27 temps, v[32:63] / v[64:95] B values of the group being multiplied /
+  fetched, v[96 + k*RW + r] accumulator of row r, column 4*lane + k (k = 0..3);
+  s[36:83] ring of NSLOT = 3 stream groups (16 SGPRs each), s[84:85] next group to
+  fetch, s86 chunks known ready, s87 temp, s88 poll budget, s89 saved m0, s[90:91]
+  saved exec, s92 temp.
 Per group g:
   wait until B of g and stream group g+1 have arrived
   if g+1 carries the sync bit: publish c_lo(g+1), wait until c_hi(g+1) < ready;
       if g+1 ends the panel: fetch its B, multiply g and g+1, finish
-  address + ds_read_b128 of the 4 B rows of group g+1      (index mode off)
   s_load of stream group g+NSLOT-1 into the slot that group g-1 used
+  address + ds_read_b128 of the 8 B rows of group g+1      (index mode off)
   vector touch TOUCH_AHEAD bytes ahead (pulls the stream into L2 for the scalar loads)
   for each entry: s_set_gpr_idx_* row; 4 v_fma_f32 into the row's accumulators
   (index mode DST|SRC2: only the accumulator operand is offset by the row)
@@ -68,40 +69,45 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 OUT = os.path.join(HERE, "spmm_asm_gen.h")
 
-NSLOT = 5
-E = tuple(40 + 8 * i for i in range(NSLOT))   # SGPR bases of the stream-group ring
-PTR, SREADY, STMP, SPOLL, M0S, SEXEC, SREADY1 = 80, 82, 83, 84, 85, 86, 88
-VB = (32, 48)                                 # VGPR bases of the two B-value sets
-ACC = 64                                      # first accumulator VGPR
-UNROLL = 10                                   # multiple of NSLOT and of 2
+G = 8                                         # entries per group (64 bytes)
+NSLOT = 3
+E = tuple(36 + 2 * G * i for i in range(NSLOT))  # SGPR bases of the stream-group ring
+PTR, SREADY, STMP, SPOLL, M0S, SEXEC, SREADY1 = 84, 86, 87, 88, 89, 90, 92
+LOW, HIW = 2 * G - 2, 2 * G - 1               # slot offsets of the c_lo / c_hi words
+VB = (32, 32 + 4 * G)                         # VGPR bases of the two B-value sets
+ACC = 32 + 8 * G                              # first accumulator VGPR
+UNROLL = 6                                    # multiple of NSLOT and of 2
 RW_VARIANTS = (4, 8, 12, 16)
 END_BIT, SYNC_BIT, LO_SHIFT, HI_SHIFT = 9, 17, 17, 18
 RING_MASK = 0x1FC00
 CHUNK, RING = 32, 4
 PMAX_VEC, PMAX_DWORD = 2, 1                   # chunks in flight per producer variant
 TOUCH_AHEAD = 512  # bytes of stream pulled into L2 ahead of the scalar ring
+GROUP_BYTES = 8 * G
 POLL_BUDGET = 1 << 22   # LDS polls a wave may spend waiting, in total
 INF = 0x7FFFFFFF
-NPROD = 2          # producer waves; producer p stages rows [p, p+1) * CHUNK/NPROD of a chunk
+NPROD = 4          # producer waves; producer p stages rows [p, p+1) * CHUNK/NPROD of a chunk
+MAX_CONS = 14      # consumer waves a workgroup can have
+PF_PER_PANEL = 0   # stream lines a producer prefetches per panel and chunk
 SLEEP_BEFORE_PUBLISH = 0  # scratch experiments: s_sleep before a ready word is written
 PROFILE = False    # scratch builds only: time consumers spend waiting (%[twait])
 
 
 def address_phase(slot, vb):
     L = []
-    for j in range(4):
-        L.append(f"v_and_or_b32 v{vb + 4 * j}, s{slot + 4 + j}, v31, %[vl]")
+    for j in range(G):
+        L.append(f"v_and_or_b32 v{vb + 4 * j}, s{slot + G + j}, v31, %[vl]")
         L.append(f"ds_read_b128 v[{vb + 4 * j}:{vb + 4 * j + 3}], v{vb + 4 * j}")
     return L
 
 
 def fmas(slot, vb, rw):
     L = []
-    for j in range(4):
+    for j in range(G):
         if j == 0:
-            L.append(f"s_set_gpr_idx_on s{slot + 4}, gpr_idx(DST,SRC2)")
+            L.append(f"s_set_gpr_idx_on s{slot + G}, gpr_idx(DST,SRC2)")
         else:
-            L.append(f"s_set_gpr_idx_idx s{slot + 4 + j}")
+            L.append(f"s_set_gpr_idx_idx s{slot + G + j}")
         for k in range(4):
             p = ACC + k * rw
             L.append(f"v_fma_f32 v{p}, s{slot + j}, v{vb + 4 * j + k}, v{p}")
@@ -119,12 +125,15 @@ def sync(slot, tag):
     """Publish progress = c_lo of the group in `slot`, then wait until its c_hi has
     landed (c_hi < min of the producers' ready words), polling while the budget
     lasts."""
-    assert NPROD == 2  # the poll reads the two ready words with one ds_read_b64
-    L = [f"s_lshr_b32 s{STMP}, s{slot + 6}, {LO_SHIFT}", f"v_mov_b32 v27, s{STMP}"]
+    assert NPROD in (1, 2, 4)
+    width = {1: "b32", 2: "b64", 4: "b128"}[NPROD]
+    words = [f"v{24 + 4 - NPROD + k}" for k in range(NPROD)]   # v27 | v[26:27] | v[24:27]
+    L = [f"s_lshr_b32 s{STMP}, s{slot + LOW}, {LO_SHIFT}", f"v_mov_b32 v27, s{STMP}"]
     L += lane0_write("%[pa]", "v27")
-    L += [f"s_lshr_b32 s{STMP}, s{slot + 7}, {HI_SHIFT}"]
+    L += [f"s_lshr_b32 s{STMP}, s{slot + HIW}, {HI_SHIFT}"]
     if PROFILE:
         L += [f"s_memtime s[{SEXEC}:{SEXEC + 1}]", "s_waitcnt lgkmcnt(0)"]
+    rng = words[0] if NPROD == 1 else f"v[{24 + 4 - NPROD}:27]"
     L += [
         f".L%=_poll{tag}:",
         f"s_cmp_lt_u32 s{STMP}, s{SREADY}",
@@ -134,11 +143,13 @@ def sync(slot, tag):
         f"s_sub_u32 s{SPOLL}, s{SPOLL}, 1",
         # each word goes from the LDS result straight to an SGPR: a VALU write of a
         # VGPR followed at once by v_readfirstlane of it reads the old value on gfx950
-        "ds_read_b64 v[26:27], %[ra]",
+        f"ds_read_{width} {rng}, %[ra]",
         "s_waitcnt lgkmcnt(0)",
-        f"v_readfirstlane_b32 s{SREADY}, v26",
-        f"v_readfirstlane_b32 s{SREADY1}, v27",
-        f"s_min_u32 s{SREADY}, s{SREADY}, s{SREADY1}",
+        f"v_readfirstlane_b32 s{SREADY}, {words[0]}",
+    ]
+    for w in words[1:]:
+        L += [f"v_readfirstlane_b32 s{SREADY1}, {w}", f"s_min_u32 s{SREADY}, s{SREADY}, s{SREADY1}"]
+    L += [
         f"s_cmp_lt_u32 s{STMP}, s{SREADY}",
         f"s_cbranch_scc1 .L%=_ready{tag}",
         "s_sleep 1",
@@ -162,16 +173,16 @@ def consumer(rw):
     if PROFILE:
         L.append("s_mov_b32 %[twait], 0")
     for g in range(NSLOT - 1):
-        L.append(f"s_load_dwordx8 s[{E[g]}:{E[g] + 7}], %[sp], {hex(32 * g)}")
+        L.append(f"s_load_dwordx16 s[{E[g]}:{E[g] + 2 * G - 1}], %[sp], {hex(GROUP_BYTES * g)}")
     L += [
         f"s_mov_b64 s[{PTR}:{PTR + 1}], %[sp]",
-        f"s_add_u32 s{PTR}, s{PTR}, {32 * (NSLOT - 1)}",
+        f"s_add_u32 s{PTR}, s{PTR}, {GROUP_BYTES * (NSLOT - 1)}",
         f"s_addc_u32 s{PTR + 1}, s{PTR + 1}, 0",
         "s_waitcnt lgkmcnt(0)",
     ]
     L += sync(E[0], "e")   # a panel's first group always carries the sync bit
     L += address_phase(E[0], VB[0])
-    L += [f"s_bitcmp1_b32 s{E[0] + 7}, {END_BIT}", "s_cbranch_scc0 .L%=_iter0",
+    L += [f"s_bitcmp1_b32 s{E[0] + HIW}, {END_BIT}", "s_cbranch_scc0 .L%=_iter0",
           "s_waitcnt lgkmcnt(0)"]   # the panel is one group
     L += fmas(E[0], VB[0], rw)
     L.append("s_branch .L%=_finish")
@@ -179,13 +190,14 @@ def consumer(rw):
         cur, nxt, pre = E[i % NSLOT], E[(i + 1) % NSLOT], E[(i + NSLOT - 1) % NSLOT]
         vbc, vbn = VB[i % 2], VB[(i + 1) % 2]
         L += [f".L%=_iter{i}:", "s_waitcnt lgkmcnt(0)",
-              f"s_bitcmp1_b32 s{nxt + 7}, {SYNC_BIT}", f"s_cbranch_scc1 .L%=_sync{i}",
+              f"s_bitcmp1_b32 s{nxt + HIW}, {SYNC_BIT}", f"s_cbranch_scc1 .L%=_sync{i}",
               f".L%=_ret{i}:"]
-        L += address_phase(nxt, vbn)
-        L.append(f"s_load_dwordx8 s[{pre}:{pre + 7}], s[{PTR}:{PTR + 1}], 0x0")
+        # the next scalar load goes out first, so it has the whole iteration to land
+        L.append(f"s_load_dwordx16 s[{pre}:{pre + 2 * G - 1}], s[{PTR}:{PTR + 1}], 0x0")
         if TOUCH_AHEAD:  # pull the stream line TOUCH_AHEAD bytes ahead into L2
             L.append(f"global_load_dword v29, v28, s[{PTR}:{PTR + 1}] offset:{TOUCH_AHEAD}")
-        L += [f"s_add_u32 s{PTR}, s{PTR}, 32", f"s_addc_u32 s{PTR + 1}, s{PTR + 1}, 0"]
+        L += [f"s_add_u32 s{PTR}, s{PTR}, {GROUP_BYTES}", f"s_addc_u32 s{PTR + 1}, s{PTR + 1}, 0"]
+        L += address_phase(nxt, vbn)
         L += fmas(cur, vbc, rw)
     L.append("s_branch .L%=_iter0")
     for i in range(UNROLL):
@@ -193,7 +205,7 @@ def consumer(rw):
         vbc, vbn = VB[i % 2], VB[(i + 1) % 2]
         L.append(f".L%=_sync{i}:")
         L += sync(nxt, i)
-        L += [f"s_bitcmp1_b32 s{nxt + 7}, {END_BIT}", f"s_cbranch_scc0 .L%=_ret{i}"]
+        L += [f"s_bitcmp1_b32 s{nxt + HIW}, {END_BIT}", f"s_cbranch_scc0 .L%=_ret{i}"]
         L += address_phase(nxt, vbn)       # group g+1 ends the panel
         L += fmas(cur, vbc, rw)
         L.append("s_waitcnt lgkmcnt(0)")
@@ -205,7 +217,7 @@ def consumer(rw):
     body = "\n".join('      "' + x + '\\n\\t"' for x in L)
     planes = ", ".join(f'"+{{v[{ACC + k * rw}:{ACC + k * rw + rw - 1}]}}"(p{k})' for k in range(4))
     sregs = [f"s{x}" for x in range(E[0], (95 if PROFILE else SREADY1) + 1)]
-    vregs = [f"v{x}" for x in range(26, 64)]
+    vregs = [f"v{x}" for x in range(24, ACC)]
     clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["scc"])
     return f"""// Consumer, RW = {rw}: accumulator planes p0..p3
 __device__ __forceinline__ void consume_rw{rw}(acc_plane_t<{rw}>& p0, acc_plane_t<{rw}>& p1,
@@ -224,6 +236,55 @@ __device__ __forceinline__ void consume_rw{rw}(acc_plane_t<{rw}>& p0, acc_plane_
 PISS, PSIG, PINF, PROW, PNEED, PPOLL, PTMP, PM0 = 40, 41, 42, 43, 44, 45, 46, 47
 PADDR, PEX, PBASE, PKM1 = 48, 50, 52, 54      # 64-bit: PADDR, PEX, PBASE
 PCM = 56                                       # column masks (1 or 4 pairs)
+PFA, PFW, PFN, PFD = 64, 66, 67, 68            # 64-bit PFA: prefetch address; panel, count, sink
+PFG = 70                                       # table pairs, 2 SGPRs per prefetched panel
+
+
+def prefetch_stream():
+    """Warm the scalar cache with the stream lines the consumers will read next: for
+    this producer's share of the workgroup's panels (w = %[pw0], %[pw0]+NPROD, ...
+    < %[npw]), load the panel's table pair [first group starting in chunk `issued`,
+    first group of the next chunk) and touch up to PF_PER_PANEL of those groups with a
+    scalar load whose result is discarded.  The consumers reach chunk `issued` a few
+    chunks later, and their own scalar loads then hit.  gfx950 has no scalar prefetch
+    instruction, and a consumer cannot load far ahead itself because each iteration
+    must wait for all of its scalar loads (they share one counter with its LDS reads)."""
+    npan = -(-MAX_CONS // NPROD)
+    assert PFG + 2 * npan <= 94
+    L = [f"s_lshl_b32 s{PFN}, s{PISS}, 2"]          # byte offset of column `issued`
+    for k in range(npan):
+        g = PFG + 2 * k
+        L += [
+            f"s_add_u32 s{PFW}, %[pw0], {k * NPROD}",
+            f"s_mov_b64 s[{g}:{g + 1}], 0",
+            f"s_cmp_ge_u32 s{PFW}, %[npw]",
+            f"s_cbranch_scc1 .L%=_pft{k}",
+            f"s_mul_i32 s{PFW}, s{PFW}, %[tstr]",
+            f"s_add_u32 s{PFW}, s{PFW}, s{PFN}",
+            f"s_add_u32 s{PFA}, s{PFW}, %[tbl_lo]",
+            f"s_addc_u32 s{PFA + 1}, %[tbl_hi], 0",
+            f"s_load_dwordx2 s[{g}:{g + 1}], s[{PFA}:{PFA + 1}], 0x0",
+            f".L%=_pft{k}:",
+        ]
+    L.append("s_waitcnt lgkmcnt(0)")
+    for k in range(npan):
+        g = PFG + 2 * k
+        L += [
+            f"s_sub_u32 s{PFN}, s{g + 1}, s{g}",
+            f"s_min_u32 s{PFN}, s{PFN}, {PF_PER_PANEL}",
+            f".L%=_pfl{k}:",
+            f"s_cmp_eq_u32 s{PFN}, 0",
+            f"s_cbranch_scc1 .L%=_pfe{k}",
+            f"s_lshl_b32 s{PFW}, s{g}, {GROUP_BYTES.bit_length() - 1}",
+            f"s_add_u32 s{PFA}, s{PFW}, %[ent_lo]",
+            f"s_addc_u32 s{PFA + 1}, %[ent_hi], 0",
+            f"s_load_dword s{PFD}, s[{PFA}:{PFA + 1}], 0x0",
+            f"s_add_u32 s{g}, s{g}, 1",
+            f"s_sub_u32 s{PFN}, s{PFN}, 1",
+            f"s_branch .L%=_pfl{k}",
+            f".L%=_pfe{k}:",
+        ]
+    return L
 
 
 def producer(vec):
@@ -318,8 +379,10 @@ def producer(vec):
                       f"global_load_lds_dword %[vl], s[{PADDR}:{PADDR + 1}]",
                       "s_add_u32 m0, m0, 0x100"]
         L.append(f"s_add_u32 s{PROW}, s{PROW}, 1")
+    L.append(f"s_mov_b64 exec, s[{PEX}:{PEX + 1}]")
+    if PF_PER_PANEL:
+        L += prefetch_stream()
     L += [
-        f"s_mov_b64 exec, s[{PEX}:{PEX + 1}]",
         f"s_add_u32 s{PISS}, s{PISS}, 1",
         f"s_add_u32 s{PINF}, s{PINF}, 1",
         "s_branch .L%=_loop",
@@ -346,7 +409,8 @@ def producer(vec):
         f"s_mov_b32 m0, s{PM0}",
     ]
     body = "\n".join('      "' + x + '\\n\\t"' for x in L)
-    sregs = [f"s{x}" for x in range(PISS, PCM + 2 * pieces)]
+    npan = -(-MAX_CONS // NPROD)
+    sregs = [f"s{x}" for x in list(range(PISS, PCM + 2 * pieces)) + list(range(PFA, PFG + 2 * npan))]
     clob = ", ".join(f'"{r}"' for r in sregs + ["v27", "vcc", "scc"])
     suffix = "vec" if vec else "dword"
     return f"""// Producer, {"16-byte" if vec else "4-byte"} staging
@@ -355,8 +419,10 @@ __device__ __forceinline__ void produce_{suffix}(const ProducerArgs& a) {{
 {body}
       :
       : [nch] "s"(a.nchunks), [K] "s"(a.K), [rs] "s"(a.row_bytes), [bb] "s"(a.bbase),
-        [ncol] "s"(a.ncol), [prow0] "s"(a.first_row), [vl] "v"(a.vlane),
-        [pg] "v"(a.prog_lane_addr), [ra] "v"(a.ready_addr)
+        [ncol] "s"(a.ncol), [prow0] "s"(a.first_row), [tbl_lo] "s"(a.tbl_lo),
+        [tbl_hi] "s"(a.tbl_hi), [tstr] "s"(a.tstride), [ent_lo] "s"(a.ent_lo),
+        [ent_hi] "s"(a.ent_hi), [npw] "s"(a.npanels_wg), [pw0] "s"(a.first_panel),
+        [vl] "v"(a.vlane), [pg] "v"(a.prog_lane_addr), [ra] "v"(a.ready_addr)
       : {clob});
 }}
 """
@@ -367,9 +433,11 @@ def generate() -> str:
              "#pragma once", "",
              "// zero groups the stream must carry past its last panel: the scalar ring runs",
              "// NSLOT-1 groups ahead and the L2 touch a further TOUCH_AHEAD bytes",
-             f"constexpr int kStreamTailGroups = {NSLOT - 1 + (TOUCH_AHEAD + 31) // 32 + 1};",
+             f"constexpr int kStreamTailGroups = {NSLOT - 1 + (TOUCH_AHEAD + GROUP_BYTES - 1) // GROUP_BYTES + 1};",
              "// stream and ring layout the loops assume",
              f"constexpr int kAsmChunk = {CHUNK}, kAsmRing = {RING}, kAsmProducers = {NPROD};",
+             f"constexpr int kAsmMaxConsumers = {MAX_CONS};",
+             f"constexpr int kAsmGroup = {G}, kAsmAccBase = {ACC};",
              f"constexpr int kAsmEndBit = {END_BIT}, kAsmSyncBit = {SYNC_BIT};",
              f"constexpr int kAsmLoShift = {LO_SHIFT}, kAsmHiShift = {HI_SHIFT};",
              f"constexpr uint32_t kAsmRingMask = {hex(RING_MASK)}u;",

@@ -106,8 +106,8 @@ void emit_group(std::vector<uint32_t>& out, const Entry* e, int n, bool first, b
   }
   const int32_t lo = e[0].chunk, hi = e[n - 1].chunk;
   const bool sync = first || last || lo != *prev_lo || hi != *prev_hi;
-  a[2] |= (uint32_t)lo << kLoShift;
-  a[3] |= (uint32_t)hi << kHiShift | (uint32_t)sync << kSyncBit | (uint32_t)last << kEndBit;
+  a[kLoWord] |= (uint32_t)lo << kLoShift;
+  a[kHiWord] |= (uint32_t)hi << kHiShift | (uint32_t)sync << kSyncBit | (uint32_t)last << kEndBit;
   *prev_lo = lo;
   *prev_hi = hi;
   for (int j = 0; j < kGroup; ++j) out.push_back(w[j]);
@@ -130,6 +130,7 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
     P.panel_rows.assign((size_t)P.npanels * RW, -1);
     for (int32_t i = 0; i < M; ++i) P.panel_rows[i] = perm[i];
     P.panel_start.assign((size_t)P.npanels, -1);
+    P.chunk_group.assign((size_t)P.npanels * (P.nchunks + 1), 0);
     P.entries.clear();
     P.entries.reserve((size_t)(P.nnz + P.nnz / 8 + 64) * 2);
 
@@ -173,14 +174,20 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
       int32_t prev_lo = -1, prev_hi = -1;
       size_t i = 0;
       bool first = true;
+      int32_t* cg = &P.chunk_group[(size_t)p * (P.nchunks + 1)];
+      int32_t c_next = 0;  // next chunk whose first group is still to be recorded
       while (i < ent.size()) {
         int n = 1;  // a group never reads more than kRing chunks
         while (n < kGroup && i + n < ent.size() && ent[i + n].chunk - ent[i].chunk < kRing) ++n;
         const bool last = i + n == ent.size();
+        const int32_t g = (int32_t)(P.entries.size() / (2 * kGroup));
+        for (; c_next <= ent[i].chunk; ++c_next) cg[c_next] = g;
         emit_group(P.entries, &ent[i], n, first, last, &prev_lo, &prev_hi);
         first = false;
         i += n;
       }
+      const int32_t g_end = (int32_t)(P.entries.size() / (2 * kGroup));
+      for (; c_next <= P.nchunks; ++c_next) cg[c_next] = g_end;
     }
     P.stored = (int64_t)(P.entries.size() / 2);
     if (P.stored > INT32_MAX - kTailGroups * kGroup) return SDNN_ERR_DIM;
@@ -231,8 +238,8 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
       if (g >= ngroups) return false;
       const uint32_t* w = &P.entries[(size_t)g * 2 * kGroup];
       const uint32_t* a = w + kGroup;
-      const int32_t lo = (int32_t)(a[2] >> kLoShift), hi = (int32_t)(a[3] >> kHiShift);
-      const bool sync = (a[3] >> kSyncBit) & 1u, last = (a[3] >> kEndBit) & 1u;
+      const int32_t lo = (int32_t)(a[kLoWord] >> kLoShift), hi = (int32_t)(a[kHiWord] >> kHiShift);
+      const bool sync = (a[kHiWord] >> kSyncBit) & 1u, last = (a[kHiWord] >> kEndBit) & 1u;
       if (lo > hi || hi - lo >= kRing || hi >= P.nchunks || lo < prev_lo) return false;
       const bool first = g == P.panel_start[p];
       if (sync != (first || last || lo != prev_lo || hi != prev_hi)) return false;
@@ -242,9 +249,9 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
       int32_t max_chunk = -1;
       for (int j = 0; j < kGroup; ++j) {
         uint32_t fields = a[j] & ((1u << kLoShift) - 1);
-        if (j == 3) fields &= ~(1u << kEndBit);
+        if (j == kHiWord) fields &= ~(1u << kEndBit);
         if ((fields >> kRowBits) & ((1u << (kRingRowShift - kRowBits)) - 1)) return false;
-        if (j < 2 && (a[j] >> kLoShift) != 0u) return false;
+        if (j < kLoWord && (a[j] >> kLoShift) != 0u) return false;
         const uint32_t row = fields & ((1u << kRowBits) - 1);
         const uint32_t ring_row = fields >> kRingRowShift;
         if (row >= (uint32_t)P.RW || ring_row >= (uint32_t)(kRing * kChunk)) return false;
@@ -282,6 +289,27 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
     }
   }
   if (expect_group != ngroups) return false;
+  // chunk_group[p][c]: the first group of panel p with c_lo >= c
+  if ((int64_t)P.chunk_group.size() != (int64_t)P.npanels * (P.nchunks + 1)) return false;
+  for (int32_t p = 0; p < P.npanels; ++p) {
+    const int32_t* cg = &P.chunk_group[(size_t)p * (P.nchunks + 1)];
+    if (P.panel_start[p] < 0) {
+      for (int32_t c = 0; c <= P.nchunks; ++c)
+        if (cg[c] != 0) return false;
+      continue;
+    }
+    int64_t end = P.panel_start[p];  // one past the panel's last group
+    while (!((P.entries[(size_t)end * 2 * kGroup + kGroup + kHiWord] >> kEndBit) & 1u)) ++end;
+    ++end;
+    auto c_lo = [&](int64_t g) {
+      return (int32_t)(P.entries[(size_t)g * 2 * kGroup + kGroup + kLoWord] >> kLoShift);
+    };
+    int64_t g = P.panel_start[p];
+    for (int32_t c = 0; c <= P.nchunks; ++c) {
+      while (g < end && c_lo(g) < c) ++g;
+      if (cg[c] != g) return false;
+    }
+  }
   for (int64_t q = 0; q < P.nnz; ++q)
     if (!seen[q]) return false;
   for (size_t d = (size_t)(2 * P.stored); d < P.entries.size(); ++d)
@@ -392,7 +420,8 @@ sdnn_status sdnn_plan_check_host(const int32_t* row_ptr, const int32_t* col_idx,
     if (info) {
       const int64_t bytes = align256((int64_t)P.entries.size() * 4) +
                             align256((int64_t)P.panel_start.size() * 4) +
-                            align256((int64_t)P.panel_rows.size() * 4);
+                            align256((int64_t)P.panel_rows.size() * 4) +
+                            align256((int64_t)P.chunk_group.size() * 4);
       fill_info(P, bytes, info);
     }
     return SDNN_OK;
@@ -434,7 +463,8 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
     const int64_t b_ent = align256((int64_t)P.entries.size() * 4);
     const int64_t b_seg = align256((int64_t)P.panel_start.size() * 4);
     const int64_t b_rows = align256((int64_t)P.panel_rows.size() * 4);
-    const int64_t total = b_ent + b_seg + b_rows;
+    const int64_t b_cg = align256((int64_t)P.chunk_group.size() * 4);
+    const int64_t total = b_ent + b_seg + b_rows + b_cg;
     plan->packed_bytes = total;
     if (total > 0) {
       if (hipMalloc(&plan->d_mem, (size_t)total) != hipSuccess) {
@@ -446,12 +476,16 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
       plan->d_entries = (const uint32_t*)base;
       plan->d_panel_start = (const int32_t*)(base + b_ent);
       plan->d_panel_rows = (const int32_t*)(base + b_ent + b_seg);
+      plan->d_chunk_group = (const int32_t*)(base + b_ent + b_seg + b_rows);
       std::vector<char> host((size_t)total, 0);
       if (!P.entries.empty()) memcpy(host.data(), P.entries.data(), P.entries.size() * 4);
       if (!P.panel_start.empty())
         memcpy(host.data() + b_ent, P.panel_start.data(), P.panel_start.size() * 4);
       if (!P.panel_rows.empty())
         memcpy(host.data() + b_ent + b_seg, P.panel_rows.data(), P.panel_rows.size() * 4);
+      if (!P.chunk_group.empty())
+        memcpy(host.data() + b_ent + b_seg + b_rows, P.chunk_group.data(),
+               P.chunk_group.size() * 4);
       if (hipMemcpy(plan->d_mem, host.data(), (size_t)total, hipMemcpyHostToDevice) !=
           hipSuccess) {
         (void)hipGetLastError();

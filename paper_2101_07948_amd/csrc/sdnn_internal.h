@@ -17,20 +17,22 @@ namespace sdnn {
 // [c*kChunk, (c+1)*kChunk)) lives in slot c % kRing while it is in use.
 constexpr int kChunk = 32;
 constexpr int kRing = 4;
-// Stream entries are consumed in groups of kGroup.
-constexpr int kGroup = 4;
+// Stream entries are consumed in groups of kGroup: one group is 64 bytes, one scalar
+// load and one scalar-cache line.
+constexpr int kGroup = 8;
 // Columns of C per workgroup tile: 64 lanes x 4 consecutive columns.
 constexpr int kTileCols = 256;
 // Zero groups appended after the last panel: the kernel's stream prefetch may read
 // this many groups past the end of a panel's stream.
-constexpr int kTailGroups = 24;
-// Fields of a group's four address words a0..a3 (see Packed).
+constexpr int kTailGroups = 16;
+// Fields of a group's address words a_0..a_7 (see Packed); L = kGroup - 1.
 constexpr int kRowBits = 8;         // a_j & 0xff: row inside the panel
-constexpr int kEndBit = 9;          // a3: last group of the panel
+constexpr int kEndBit = 9;          // a_L: last group of the panel
 constexpr int kRingRowShift = 10;   // (a_j >> 10) & 0x7f: row of the LDS ring
-constexpr int kSyncBit = 17;        // a3: publish progress / check readiness first
-constexpr int kLoShift = 17;        // a2 >> 17: lowest chunk the group reads
-constexpr int kHiShift = 18;        // a3 >> 18: highest chunk the group reads
+constexpr int kSyncBit = 17;        // a_L: publish progress / check readiness first
+constexpr int kLoShift = 17;        // a_{L-1} >> 17: lowest chunk the group reads
+constexpr int kHiShift = 18;        // a_L >> 18: highest chunk the group reads
+constexpr int kLoWord = kGroup - 2, kHiWord = kGroup - 1;
 constexpr int kMaxChunks = 1 << 14; // chunk numbers must fit a3's high bits
 static_assert(kRing * kChunk <= 128, "ring rows must fit 7 bits");
 
@@ -45,19 +47,24 @@ static_assert(kRing * kChunk <= 128, "ring rows must fit 7 bits");
 //   is 2*kGroup dwords: the kGroup fp32 weight bits, then kGroup words
 //       a_j = ((c_j % kRing) * kChunk + col_j - c_j * kChunk) << 10 | row_j
 //   (c_j = chunk of the entry; the shifted part is the entry's B row in the LDS
-//   ring) with extra fields
-//       a2 |= c_lo << 17, a3 |= c_hi << 18 | sync << 17 | end << 9
+//   ring) with extra fields in the last two words
+//       a6 |= c_lo << 17, a7 |= c_hi << 18 | sync << 17 | end << 9
 //   where c_lo / c_hi are the lowest / highest chunk the group reads, end marks the
 //   panel's last group and sync is set on a panel's first and last groups and
 //   whenever c_lo or c_hi differs from the previous group's.  Panels are stored back
 //   to back; panel_start holds each panel's first group (-1: the panel has no
-//   entries).  The stream ends with kTailGroups zero groups.
+//   entries) and chunk_group[p][c] the first group of panel p whose c_lo >= c, so that
+//   [chunk_group[p][c], chunk_group[p][c+1]) are the groups starting in chunk c (the
+//   kernel's producers prefetch their stream lines into the scalar cache).  The
+//   stream ends with kTailGroups zero groups.
 struct Packed {
   int32_t M = 0, K = 0, RW = 0, nchunks = 0, npanels = 0;
   int64_t nnz = 0, stored = 0;     // structural entries, stored entries (with padding)
   std::vector<int32_t> perm;        // [M]   original row at permuted position
   std::vector<int32_t> panel_rows;  // [npanels*RW] original row or -1 (padding)
   std::vector<int32_t> panel_start; // [npanels] first group of the panel, or -1
+  std::vector<int32_t> chunk_group; // [npanels][nchunks+1]: first group of the panel whose
+                                    // c_lo >= c (the panel's end for c = nchunks; 0 if empty)
   std::vector<uint32_t> entries;    // [2*(stored + kTailGroups*kGroup)] dwords
   double rho = 1.0;                 // nnz / sum_p |union of the panel's column sets|
 };
@@ -81,10 +88,11 @@ struct sdnn_plan_s {
   int64_t nnz = 0, packed_bytes = 0;
   double rho = 1.0, fill = 1.0;
   std::vector<int32_t> perm;
-  void* d_mem = nullptr;             // one device allocation holding the three arrays
+  void* d_mem = nullptr;             // one device allocation holding the four arrays
   const uint32_t* d_entries = nullptr;  // [2*(stored + kTailGroups*kGroup)] dwords
   const int32_t* d_panel_start = nullptr;  // [npanels] (in groups, -1: empty panel)
   const int32_t* d_panel_rows = nullptr;  // [npanels*RW]
+  const int32_t* d_chunk_group = nullptr; // [npanels*(nchunks+1)]
 };
 
 namespace sdnn {

@@ -55,11 +55,18 @@ struct ProducerArgs {
   uint32_t vlane;          // the lane's byte offset in a B row segment (16 or 4 * lane)
   uint32_t prog_lane_addr; // LDS address of progress word `lane` (lanes 0..15)
   uint32_t ready_addr;     // LDS address of this producer's ready word
+  // scalar-cache prefetch of the consumers' stream (see prefetch_stream)
+  uint32_t tbl_lo, tbl_hi; // chunk_group row of the workgroup's first panel
+  uint32_t tstride;        // bytes per chunk_group row: (nchunks + 1) * 4
+  uint32_t ent_lo, ent_hi; // the entry stream
+  uint32_t npanels_wg;     // panels of this workgroup that exist
+  uint32_t first_panel;    // this producer's first panel (then every kProducers-th)
 };
 
 #include "spmm_asm_gen.h"
 static_assert(kStreamTailGroups <= kTailGroups, "stream tail shorter than the prefetch");
 static_assert(kAsmChunk == kChunk && kAsmRing == kRing, "ring layout mismatch");
+static_assert(kAsmGroup == kGroup, "group size mismatch");
 constexpr int kProducers = kAsmProducers;
 static_assert(kAsmEndBit == kEndBit && kAsmSyncBit == kSyncBit && kAsmLoShift == kLoShift &&
                   kAsmHiShift == kHiShift,
@@ -68,7 +75,11 @@ static_assert(kAsmRingMask == (uint32_t)(kRing * kChunk - 1) << kRingRowShift,
               "ring-row mask mismatch");
 
 constexpr int kRingBytes = kRing * kChunk * 1024;
-constexpr int kMaxConsumers = 16 - kProducers;
+// Threads per workgroup a panel height allows: the accumulators sit above the loop's
+// pinned VGPRs (kAsmAccBase + 4 * RW), so RW >= 8 needs more than the 128 VGPRs that
+// 16 waves per CU leave each wave.
+template <int RW>
+constexpr int max_threads() { return kAsmAccBase + 4 * RW < 128 ? 1024 : 768; }
 // LDS control words after the ring: ready[kProducers] at +0, progress[16] at +64.
 constexpr int kCtlWords = 256;
 static_assert(kProducers <= 16, "ready words overlap the progress words");
@@ -92,10 +103,11 @@ struct SpmmArgs {
 // RW: rows per panel; VEC: N % 4 == 0 and B, C 16-byte aligned (16-byte staging DMA,
 // vector stores of C).  blockDim.x = 64 * (consumers + kProducers).
 template <int RW, bool VEC>
-__global__ __launch_bounds__(1024) void spmm_panel_kernel(
+__global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     const uint32_t* __restrict__ entries, const int32_t* __restrict__ panel_start,
-    const int32_t* __restrict__ panel_rows, const float* __restrict__ B, float* __restrict__ C,
-    const float* __restrict__ bias, SpmmArgs a) {
+    const int32_t* __restrict__ panel_rows, const int32_t* __restrict__ chunk_group,
+    const float* __restrict__ B, float* __restrict__ C, const float* __restrict__ bias,
+    SpmmArgs a) {
   // the ring ([0, kRingBytes)) and the control words; the ring must start at LDS 0
   // (the loops form LDS addresses from the ring-row field alone), which holds because
   // this is the kernel's only LDS object
@@ -138,6 +150,16 @@ __global__ __launch_bounds__(1024) void spmm_panel_kernel(
     pa.vlane = (uint32_t)lane * (VEC ? 16u : 4u);
     pa.prog_lane_addr = prog0 + 4u * (uint32_t)(lane & 15);
     pa.ready_addr = ready_addr + 4u * (uint32_t)prod;
+    const int first = rb * nc;
+    const uint64_t tbl = (uint64_t)(uintptr_t)(chunk_group + (size_t)first * (a.nchunks + 1));
+    const uint64_t ent = (uint64_t)(uintptr_t)entries;
+    pa.tbl_lo = (uint32_t)tbl;
+    pa.tbl_hi = (uint32_t)(tbl >> 32);
+    pa.tstride = (uint32_t)(a.nchunks + 1) * 4u;
+    pa.ent_lo = (uint32_t)ent;
+    pa.ent_hi = (uint32_t)(ent >> 32);
+    pa.npanels_wg = (uint32_t)(a.npanels - first < nc ? a.npanels - first : nc);
+    pa.first_panel = (uint32_t)prod;
     if (VEC)
       produce_vec(pa);
     else
@@ -183,6 +205,7 @@ struct SpmmPtrs {
   const uint32_t* entries;
   const int32_t* panel_start;
   const int32_t* panel_rows;
+  const int32_t* chunk_group;
   const float* B;
   float* C;
   const float* bias;
@@ -192,7 +215,8 @@ template <int RW, bool VEC>
 hipError_t launch_variant(const SpmmPtrs& p, const SpmmArgs& args, int waves, int grid,
                           hipStream_t stream) {
   hipLaunchKernelGGL((spmm_panel_kernel<RW, VEC>), dim3(grid), dim3(64 * (waves + kProducers)), 0, stream,
-                     p.entries, p.panel_start, p.panel_rows, p.B, p.C, p.bias, args);
+                     p.entries, p.panel_start, p.panel_rows, p.chunk_group, p.B, p.C, p.bias,
+                     args);
   return hipGetLastError();
 }
 
@@ -208,20 +232,29 @@ hipError_t launch_rw(int RW, const SpmmPtrs& p, const SpmmArgs& args, int waves,
   return hipErrorInvalidValue;
 }
 
+int max_consumers(int RW) {
+  const int threads = RW == 4 ? max_threads<4>() : RW == 8 ? max_threads<8>()
+                    : RW == 12 ? max_threads<12>() : max_threads<16>();
+  const int c = threads / 64 - kProducers;
+  return c < kAsmMaxConsumers ? c : kAsmMaxConsumers;
+}
+
 int env_int(const char* name, int dflt) {
   const char* s = getenv(name);
   return s ? atoi(s) : dflt;
 }
 
 struct LaunchCfg {
-  int waves, n_tiles, n_rb;  // waves: consumer waves per workgroup (one more produces)
+  int waves, n_tiles, n_rb;  // waves: consumer waves per workgroup (the producers come on top)
 };
 
 // Panels per workgroup: enough row-blocks that the grid covers every CU about once
-// (the 129 KB of ring and control LDS allows one workgroup per CU), at most
-// kMaxConsumers consumer waves.  SDNN_FORCE_WAVES fixes the consumer count.
+// (the 129 KB of ring and control LDS allows one workgroup per CU), at most as many
+// consumer waves as the panel height's register use allows.  SDNN_FORCE_WAVES fixes
+// the consumer count.
 LaunchCfg choose_cfg(const sdnn_plan_s* p, int N) {
   const int target = p->num_cus > 0 ? p->num_cus : 256;
+  const int cap = max_consumers(p->RW);
   const int forceW = env_int("SDNN_FORCE_WAVES", 0);
   LaunchCfg c;
   c.n_tiles = (N + kTileCols - 1) / kTileCols;
@@ -232,7 +265,7 @@ LaunchCfg choose_cfg(const sdnn_plan_s* p, int N) {
     if (n_rb > p->npanels) n_rb = p->npanels;
     c.waves = (p->npanels + n_rb - 1) / n_rb;
   }
-  if (c.waves > kMaxConsumers) c.waves = kMaxConsumers;
+  if (c.waves > cap) c.waves = cap;
   if (c.waves > p->npanels) c.waves = p->npanels;
   if (c.waves < 1) c.waves = 1;
   c.n_rb = (p->npanels + c.waves - 1) / c.waves;
@@ -244,7 +277,8 @@ LaunchCfg choose_cfg(const sdnn_plan_s* p, int N) {
 hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                        const float* bias, int epi, hipStream_t stream) {
   const LaunchCfg cfg = choose_cfg(p, N);
-  const SpmmPtrs ptrs{p->d_entries, p->d_panel_start, p->d_panel_rows, B, C, bias};
+  const SpmmPtrs ptrs{p->d_entries, p->d_panel_start, p->d_panel_rows, p->d_chunk_group,
+                      B, C, bias};
   SpmmArgs args;
   args.K = p->K;
   args.N = N;
