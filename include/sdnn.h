@@ -57,24 +57,32 @@ typedef enum {
 } sdnn_epilogue;
 
 /* Options for sdnn_plan_create; pass NULL for the defaults {0, 1}.
- *   panel_rows: rows per register panel (0 = library default 4; otherwise 4, 8, 12 or 16).
+ *   panel_rows: rows per register panel.  0 (default) packs W twice, with short
+ *               panels of 4 rows and tall panels of 12 rows, and sdnn_spmm picks per
+ *               call: tall panels once a 256-column tile has at least a full
+ *               workgroup of them per compute unit (M * ceil(N / 256) >= 96 * CUs),
+ *               short panels otherwise.  4, 8, 12 or 16 packs that height only.
  *   permute:    1 = apply Algorithm 1 (default), 0 = identity order (ablation). */
 typedef struct {
   int32_t panel_rows;
   int32_t permute;
 } sdnn_plan_opts;
 
-/* Plan statistics.
+/* Plan statistics (of the first packing; the tall_* fields describe the second one,
+ * or are 0 when the plan holds one packing).
  *   panels:       number of row panels (ceil(M / panel_rows)).
- *   packed_bytes: device bytes of the packed weight stream and its indexes.
+ *   packed_bytes: device bytes of every packed weight stream and its indexes.
  *   rho:          nnz / sum over panels of |union of the panel rows' column sets|,
  *                 the reuse an ideal panel kernel gets per staged B row (>= 1).
- *   fill:         nnz / stored stream entries (1.0 = no padding). */
+ *   fill:         nnz / stored stream entries (1.0 = no padding).
+ *   k_chunk:      rows of B per LDS staging slot. */
 typedef struct {
   int32_t M, K;
   int64_t nnz, panels, packed_bytes;
   double rho, fill;
   int32_t panel_rows, k_chunk;
+  int32_t tall_panel_rows, reserved;
+  double tall_rho, tall_fill;
 } sdnn_plan_info_t;
 
 /* Greedy weight-row permutation (Sec. 3.1.2, Algorithm 1), host only, no GPU needed.

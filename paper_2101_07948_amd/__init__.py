@@ -39,7 +39,9 @@ class PlanInfo(ctypes.Structure):
     _fields_ = [("M", ctypes.c_int32), ("K", ctypes.c_int32), ("nnz", ctypes.c_int64),
                 ("panels", ctypes.c_int64), ("packed_bytes", ctypes.c_int64),
                 ("rho", ctypes.c_double), ("fill", ctypes.c_double),
-                ("panel_rows", ctypes.c_int32), ("k_chunk", ctypes.c_int32)]
+                ("panel_rows", ctypes.c_int32), ("k_chunk", ctypes.c_int32),
+                ("tall_panel_rows", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("tall_rho", ctypes.c_double), ("tall_fill", ctypes.c_double)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}

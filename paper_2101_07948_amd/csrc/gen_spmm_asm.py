@@ -8,22 +8,25 @@ it software-pipelines scalar loads of the weight stream, LDS reads of B and FMAs
 across rotating register sets.  Compiled code can express neither the indexed
 accumulator nor the rotation.
 
-Workgroup roles.  Waves 0..nc-1 are consumers (one panel each); waves nc and nc+1
+Workgroup roles.  Waves 0..nc-1 are consumers (one panel each); waves nc..nc+NPROD-1
 are producers.  B is staged through a ring of RING slots of CHUNK rows (1 KB per row:
 64 lanes x 16 bytes) at LDS byte address 0; chunk c of B goes to slot c % RING, and
-producer p stages rows [p * CHUNK/2, (p + 1) * CHUNK/2) of every chunk.  There is no
+producer p stages rows [p, p + 1) * CHUNK/NPROD of every chunk.  There is no
 workgroup barrier inside the loops: the roles synchronise through LDS words
     ready[p]    number of chunks whose rows producer p has landed in the ring
     progress[w] lowest chunk consumer w may still read (consumer w writes; the slots
                 of absent consumers hold 0x7fffffff)
-A producer stages its part of chunk c once every progress[w] >= c - RING + 1 (slot
-c % RING no longer read by anyone), keeps up to PMAX chunks in flight, and advances
-its ready word as each lands.  A consumer publishes progress and re-reads the ready
-words only at groups whose sync bit is set; chunk c is there once both exceed c.
-Two producer waves double the bytes in flight per workgroup: one wave alone, waiting
-for each chunk to land, cannot keep the consumers fed.  Every group reads chunks c_lo..c_hi with c_hi - c_lo < RING and
-publishes progress = c_lo before waiting for c_hi, so the slowest consumer's next
-chunk can always be staged: the loops cannot deadlock.  Each wait is also bounded by
+A producer stages its part of chunk c once c < min(progress) + RING (slot c % RING no
+longer read by anyone; it re-reads the progress words only when it reaches the limit
+it last computed), keeps up to PMAX chunks in flight, and advances its ready word as
+each lands.  A consumer publishes progress and re-reads the ready words only at
+groups whose sync bit is set; chunk c is there once every ready word exceeds c.
+Several producer waves split each chunk so that its loads go out in parallel and the
+per-chunk handshake of any one wave stays short.
+
+Every group reads chunks c_lo..c_hi with c_hi - c_lo < RING and publishes
+progress = c_lo before waiting for c_hi, so the slowest consumer's next chunk can
+always be staged: the loops cannot deadlock.  Each wait is also bounded by
 a per-wave poll budget, after which the wave goes on without waiting (the result is
 then wrong, but the kernel ends).
 
@@ -36,7 +39,7 @@ index mode uses only a's low 8 bits.
 
 Consumer register plan (pinned in the asm statement):
   v31 0x1fc00 (ring-row mask), v28 zero offset and v29 sink of the L2 touch loads,
-  v26, v27 temps, v[32:63] / v[64:95] B values of the group being multiplied /
+  v[24:27] ready words, v30 temp, v[32:63] / v[64:95] B values of the group being multiplied /
   fetched, v[96 + k*RW + r] accumulator of row r, column 4*lane + k (k = 0..3);
   s[36:83] ring of NSLOT = 3 stream groups (16 SGPRs each), s[84:85] next group to
   fetch, s86 chunks known ready, s87 temp, s88 poll budget, s89 saved m0, s[90:91]
@@ -46,16 +49,16 @@ Per group g:
   if g+1 carries the sync bit: publish c_lo(g+1), wait until c_hi(g+1) < ready;
       if g+1 ends the panel: fetch its B, multiply g and g+1, finish
   s_load of stream group g+NSLOT-1 into the slot that group g-1 used
-  address + ds_read_b128 of the 8 B rows of group g+1      (index mode off)
   vector touch TOUCH_AHEAD bytes ahead (pulls the stream into L2 for the scalar loads)
+  address + ds_read_b128 of the 8 B rows of group g+1      (index mode off)
   for each entry: s_set_gpr_idx_* row; 4 v_fma_f32 into the row's accumulators
   (index mode DST|SRC2: only the accumulator operand is offset by the row)
 The ring and the touch read up to kStreamTailGroups groups past a panel's last
 group; the stream carries that many zero groups at its end.
 
-Producer: issues one 16-byte (or four 4-byte) direct global->LDS loads per B row,
-addressed by a scalar row pointer plus the lane's byte offset, with M0 holding the
-LDS row address; rows past K re-stage row K-1 into LDS rows no entry reads.
+Producer: issues one 16-byte (or four 4-byte) direct global->LDS load per B row,
+addressed by a scalar pointer plus a per-lane VGPR offset, with M0 holding the LDS
+row address; rows past K re-stage row K-1 into LDS rows no entry reads.
 
 Hazards the hand-written code must respect (the compiler handles them for compiled
 code): a VALU write of a VGPR followed at once by v_readfirstlane of that VGPR reads
@@ -88,8 +91,6 @@ POLL_BUDGET = 1 << 22   # LDS polls a wave may spend waiting, in total
 INF = 0x7FFFFFFF
 NPROD = 4          # producer waves; producer p stages rows [p, p+1) * CHUNK/NPROD of a chunk
 MAX_CONS = 14      # consumer waves a workgroup can have
-PF_PER_PANEL = 0   # stream lines a producer prefetches per panel and chunk
-SLEEP_BEFORE_PUBLISH = 0  # scratch experiments: s_sleep before a ready word is written
 PROFILE = False    # scratch builds only: time consumers spend waiting (%[twait])
 
 
@@ -121,19 +122,36 @@ def lane0_write(addr, vdata):
             f"ds_write_b32 {addr}, {vdata}", f"s_mov_b64 exec, s[{SEXEC}:{SEXEC + 1}]"]
 
 
+def ready_regs():
+    """VGPRs that receive the producers' ready words: v27 | v[26:27] | v[24:27]."""
+    assert NPROD in (1, 2, 4)
+    width = {1: "b32", 2: "b64", 4: "b128"}[NPROD]
+    words = [f"v{24 + 4 - NPROD + k}" for k in range(NPROD)]
+    rng = words[0] if NPROD == 1 else f"v[{24 + 4 - NPROD}:27]"
+    return width, words, rng
+
+
+def fold_ready():
+    """SREADY = min of the ready words in ready_regs().  Each word goes from the LDS
+    result straight to an SGPR: a VALU write of a VGPR followed at once by
+    v_readfirstlane of it reads the old value on gfx950."""
+    _, words, _ = ready_regs()
+    L = [f"v_readfirstlane_b32 s{SREADY}, {words[0]}"]
+    for w in words[1:]:
+        L += [f"v_readfirstlane_b32 s{SREADY1}, {w}", f"s_min_u32 s{SREADY}, s{SREADY}, s{SREADY1}"]
+    return L
+
+
 def sync(slot, tag):
     """Publish progress = c_lo of the group in `slot`, then wait until its c_hi has
     landed (c_hi < min of the producers' ready words), polling while the budget
     lasts."""
-    assert NPROD in (1, 2, 4)
-    width = {1: "b32", 2: "b64", 4: "b128"}[NPROD]
-    words = [f"v{24 + 4 - NPROD + k}" for k in range(NPROD)]   # v27 | v[26:27] | v[24:27]
-    L = [f"s_lshr_b32 s{STMP}, s{slot + LOW}, {LO_SHIFT}", f"v_mov_b32 v27, s{STMP}"]
-    L += lane0_write("%[pa]", "v27")
+    width, _, rng = ready_regs()
+    L = [f"s_lshr_b32 s{STMP}, s{slot + LOW}, {LO_SHIFT}", f"v_mov_b32 v30, s{STMP}"]
+    L += lane0_write("%[pa]", "v30")
     L += [f"s_lshr_b32 s{STMP}, s{slot + HIW}, {HI_SHIFT}"]
     if PROFILE:
         L += [f"s_memtime s[{SEXEC}:{SEXEC + 1}]", "s_waitcnt lgkmcnt(0)"]
-    rng = words[0] if NPROD == 1 else f"v[{24 + 4 - NPROD}:27]"
     L += [
         f".L%=_poll{tag}:",
         f"s_cmp_lt_u32 s{STMP}, s{SREADY}",
@@ -141,14 +159,10 @@ def sync(slot, tag):
         f"s_cmp_eq_u32 s{SPOLL}, 0",
         f"s_cbranch_scc1 .L%=_ready{tag}",
         f"s_sub_u32 s{SPOLL}, s{SPOLL}, 1",
-        # each word goes from the LDS result straight to an SGPR: a VALU write of a
-        # VGPR followed at once by v_readfirstlane of it reads the old value on gfx950
         f"ds_read_{width} {rng}, %[ra]",
         "s_waitcnt lgkmcnt(0)",
-        f"v_readfirstlane_b32 s{SREADY}, {words[0]}",
     ]
-    for w in words[1:]:
-        L += [f"v_readfirstlane_b32 s{SREADY1}, {w}", f"s_min_u32 s{SREADY}, s{SREADY}, s{SREADY1}"]
+    L += fold_ready()
     L += [
         f"s_cmp_lt_u32 s{STMP}, s{SREADY}",
         f"s_cbranch_scc1 .L%=_ready{tag}",
@@ -211,8 +225,8 @@ def consumer(rw):
         L.append("s_waitcnt lgkmcnt(0)")
         L += fmas(nxt, vbn, rw)
         L.append("s_branch .L%=_finish")
-    L += [".L%=_finish:", f"v_mov_b32 v27, {hex(INF)}"]
-    L += lane0_write("%[pa]", "v27")
+    L += [".L%=_finish:", f"v_mov_b32 v30, {hex(INF)}"]
+    L += lane0_write("%[pa]", "v30")
     L += ["s_waitcnt vmcnt(0) lgkmcnt(0)", f"s_mov_b32 m0, s{M0S}"]
     body = "\n".join('      "' + x + '\\n\\t"' for x in L)
     planes = ", ".join(f'"+{{v[{ACC + k * rw}:{ACC + k * rw + rw - 1}]}}"(p{k})' for k in range(4))
@@ -233,74 +247,106 @@ __device__ __forceinline__ void consume_rw{rw}(acc_plane_t<{rw}>& p0, acc_plane_
 
 
 # producer SGPRs
-PISS, PSIG, PINF, PROW, PNEED, PPOLL, PTMP, PM0 = 40, 41, 42, 43, 44, 45, 46, 47
-PADDR, PEX, PBASE, PKM1 = 48, 50, 52, 54      # 64-bit: PADDR, PEX, PBASE
+PISS, PSIG, PINF, PLIM, PTMP, PPOLL, PROW, PM0 = 40, 41, 42, 43, 44, 45, 46, 47
+PADDR, PEX, PBASE, PCS = 48, 50, 52, 54       # 64-bit each
 PCM = 56                                       # column masks (1 or 4 pairs)
-PFA, PFW, PFN, PFD = 64, 66, 67, 68            # 64-bit PFA: prefetch address; panel, count, sink
-PFG = 70                                       # table pairs, 2 SGPRs per prefetched panel
+PKM1, PLAST = 64, 65
+# producer VGPRs: row offsets of the fast path, progress words, min tree
+VO, VP, VMIN = 32, 40, 56
 
 
-def prefetch_stream():
-    """Warm the scalar cache with the stream lines the consumers will read next: for
-    this producer's share of the workgroup's panels (w = %[pw0], %[pw0]+NPROD, ...
-    < %[npw]), load the panel's table pair [first group starting in chunk `issued`,
-    first group of the next chunk) and touch up to PF_PER_PANEL of those groups with a
-    scalar load whose result is discarded.  The consumers reach chunk `issued` a few
-    chunks later, and their own scalar loads then hit.  gfx950 has no scalar prefetch
-    instruction, and a consumer cannot load far ahead itself because each iteration
-    must wait for all of its scalar loads (they share one counter with its LDS reads)."""
-    npan = -(-MAX_CONS // NPROD)
-    assert PFG + 2 * npan <= 94
-    L = [f"s_lshl_b32 s{PFN}, s{PISS}, 2"]          # byte offset of column `issued`
-    for k in range(npan):
-        g = PFG + 2 * k
+def producer_poll():
+    """Read the 16 progress words and set PLIM = min(progress) + RING: chunks below
+    PLIM have a free slot (every consumer has moved past the chunk that used it)."""
+    L = [f"s_mov_b64 s[{PEX}:{PEX + 1}], exec", "s_mov_b64 exec, 1"]
+    for k in range(4):
+        L.append(f"ds_read_b128 v[{VP + 4 * k}:{VP + 4 * k + 3}], %[pg] offset:{16 * k}")
+    L += ["s_waitcnt lgkmcnt(0)",
+          f"v_min3_u32 v{VMIN}, v{VP}, v{VP + 1}, v{VP + 2}",
+          f"v_min3_u32 v{VMIN + 1}, v{VP + 3}, v{VP + 4}, v{VP + 5}",
+          f"v_min3_u32 v{VMIN + 2}, v{VP + 6}, v{VP + 7}, v{VP + 8}",
+          f"v_min3_u32 v{VMIN + 3}, v{VP + 9}, v{VP + 10}, v{VP + 11}",
+          f"v_min3_u32 v{VMIN + 4}, v{VP + 12}, v{VP + 13}, v{VP + 14}",
+          f"v_min3_u32 v{VMIN}, v{VMIN}, v{VMIN + 1}, v{VMIN + 2}",
+          f"v_min3_u32 v{VMIN + 1}, v{VMIN + 3}, v{VMIN + 4}, v{VP + 15}",
+          f"v_min_u32 v{VMIN}, v{VMIN}, v{VMIN + 1}",
+          "s_nop 4",                           # VALU write, then v_readfirstlane of it
+          f"v_readfirstlane_b32 s{PTMP}, v{VMIN}",
+          f"s_mov_b64 exec, s[{PEX}:{PEX + 1}]",
+          f"s_add_u32 s{PLIM}, s{PTMP}, {RING}"]
+    return L
+
+
+def issue_rows_clamped(vec, half):
+    """Stage rows PROW .. PROW+half-1 of B (each clamped to K-1) at LDS m0, m0+1KB, ..."""
+    L = []
+    pieces = 1 if vec else 4
+    if vec:
+        L.append(f"s_mov_b64 exec, s[{PCM}:{PCM + 1}]")
+    for r in range(half):
         L += [
-            f"s_add_u32 s{PFW}, %[pw0], {k * NPROD}",
-            f"s_mov_b64 s[{g}:{g + 1}], 0",
-            f"s_cmp_ge_u32 s{PFW}, %[npw]",
-            f"s_cbranch_scc1 .L%=_pft{k}",
-            f"s_mul_i32 s{PFW}, s{PFW}, %[tstr]",
-            f"s_add_u32 s{PFW}, s{PFW}, s{PFN}",
-            f"s_add_u32 s{PFA}, s{PFW}, %[tbl_lo]",
-            f"s_addc_u32 s{PFA + 1}, %[tbl_hi], 0",
-            f"s_load_dwordx2 s[{g}:{g + 1}], s[{PFA}:{PFA + 1}], 0x0",
-            f".L%=_pft{k}:",
+            f"s_min_u32 s{PTMP}, s{PROW}, s{PKM1}",
+            f"s_mul_i32 s{PADDR}, s{PTMP}, %[rs]",
+            f"s_mul_hi_u32 s{PADDR + 1}, s{PTMP}, %[rs]",
+            f"s_add_u32 s{PADDR}, s{PADDR}, %[bb_lo]",
+            f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, %[bb_hi]",
         ]
-    L.append("s_waitcnt lgkmcnt(0)")
-    for k in range(npan):
-        g = PFG + 2 * k
-        L += [
-            f"s_sub_u32 s{PFN}, s{g + 1}, s{g}",
-            f"s_min_u32 s{PFN}, s{PFN}, {PF_PER_PANEL}",
-            f".L%=_pfl{k}:",
-            f"s_cmp_eq_u32 s{PFN}, 0",
-            f"s_cbranch_scc1 .L%=_pfe{k}",
-            f"s_lshl_b32 s{PFW}, s{g}, {GROUP_BYTES.bit_length() - 1}",
-            f"s_add_u32 s{PFA}, s{PFW}, %[ent_lo]",
-            f"s_addc_u32 s{PFA + 1}, %[ent_hi], 0",
-            f"s_load_dword s{PFD}, s[{PFA}:{PFA + 1}], 0x0",
-            f"s_add_u32 s{g}, s{g}, 1",
-            f"s_sub_u32 s{PFN}, s{PFN}, 1",
-            f"s_branch .L%=_pfl{k}",
-            f".L%=_pfe{k}:",
-        ]
+        if vec:
+            L += [f"global_load_lds_dwordx4 %[vl], s[{PADDR}:{PADDR + 1}]",
+                  "s_add_u32 m0, m0, 0x400"]
+        else:
+            for q in range(pieces):
+                m = PCM + 2 * q
+                if q:
+                    L += [f"s_add_u32 s{PADDR}, s{PADDR}, 0x100",
+                          f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, 0"]
+                L += [f"s_mov_b64 exec, s[{m}:{m + 1}]", "s_nop 0",
+                      f"global_load_lds_dword %[vl], s[{PADDR}:{PADDR + 1}]",
+                      "s_add_u32 m0, m0, 0x100"]
+        L.append(f"s_add_u32 s{PROW}, s{PROW}, 1")
     return L
 
 
 def producer(vec):
+    """Producer loop.  State: issued (chunks whose loads went out), landed (chunks
+    published in the ready word), in flight = issued - landed <= PMAX, and the cached
+    issue limit PLIM (re-read from the progress words only when issued reaches it).
+    Chunks below PLAST take the fast path: the chunk's base address advances by
+    CHUNK rows per chunk and row r adds the lane's precomputed VGPR offset
+    16 * lane + r * row_bytes, so each row is one DMA and one m0 step.  The last chunk
+    when K is not a multiple of CHUNK, and every chunk of the 4-byte variant, take the
+    clamped path, which re-stages row K-1 for rows past K (LDS rows no entry reads)."""
     half = CHUNK // NPROD
     pmax = PMAX_VEC if vec else PMAX_DWORD
     loads_per_chunk = half if vec else 4 * half
     assert loads_per_chunk * (pmax - 1) <= 63
+    lg_chunk = CHUNK.bit_length() - 1
     L = [
         f"s_mov_b32 s{PM0}, m0",
         f"s_mov_b32 s{PISS}, 0",
         f"s_mov_b32 s{PSIG}, 0",
         f"s_mov_b32 s{PINF}, 0",
+        f"s_mov_b32 s{PLIM}, {RING}",
         f"s_mov_b32 s{PPOLL}, {hex(POLL_BUDGET)}",
-        f"s_mov_b64 s[{PBASE}:{PBASE + 1}], %[bb]",
         f"s_sub_u32 s{PKM1}, %[K], 1",
+        # fast-path state: chunk base B + prow0 * row_bytes, chunk stride CHUNK * row_bytes
+        f"s_mul_i32 s{PBASE}, %[prow0], %[rs]",
+        f"s_mul_hi_u32 s{PBASE + 1}, %[prow0], %[rs]",
+        f"s_add_u32 s{PBASE}, s{PBASE}, %[bb_lo]",
+        f"s_addc_u32 s{PBASE + 1}, s{PBASE + 1}, %[bb_hi]",
+        f"s_lshl_b32 s{PCS}, %[rs], {lg_chunk}",
+        f"s_lshr_b32 s{PCS + 1}, %[rs], {32 - lg_chunk}",
     ]
+    if vec:  # PLAST = nch - 1 if K % CHUNK else nch
+        L += [f"s_and_b32 s{PTMP}, %[K], {CHUNK - 1}",
+              f"s_sub_u32 s{PLAST}, %[nch], 1",
+              f"s_cmp_eq_u32 s{PTMP}, 0",
+              f"s_cselect_b32 s{PLAST}, %[nch], s{PLAST}",
+              f"v_mov_b32 v{VO}, %[vl]"]
+        for r in range(1, half):
+            L.append(f"v_add_u32 v{VO + r}, %[rs], v{VO + r - 1}")
+    else:
+        L.append(f"s_mov_b32 s{PLAST}, 0")
     # column masks: vec -> lanes whose 4 columns exist (lane < ncol / 4);
     # dword -> piece q of a row: lanes with 64 q + lane < ncol
     pieces = 1 if vec else 4
@@ -324,19 +370,12 @@ def producer(vec):
         "s_cbranch_scc1 .L%=_land",
         f"s_cmp_ge_u32 s{PINF}, {pmax}",
         "s_cbranch_scc1 .L%=_land",
-        # slot of chunk `issued` is free once every progress >= issued - RING + 1
-        f"s_sub_i32 s{PNEED}, s{PISS}, {RING - 1}",
-        f"s_cmp_le_i32 s{PNEED}, 0",
+        f"s_cmp_lt_u32 s{PISS}, s{PLIM}",
         "s_cbranch_scc1 .L%=_issue",
-        f"s_mov_b64 s[{PEX}:{PEX + 1}], exec",
-        "s_mov_b32 exec_lo, 0xffff",
-        "s_mov_b32 exec_hi, 0",
-        "ds_read_b32 v27, %[pg]",
-        "s_waitcnt lgkmcnt(0)",
-        f"v_cmp_gt_u32 vcc, s{PNEED}, v27",
-        f"s_mov_b64 exec, s[{PEX}:{PEX + 1}]",
-        "s_nop 4",                            # VALU-written vcc read by SALU below
-        "s_cmp_eq_u64 vcc, 0",
+    ]
+    L += producer_poll()
+    L += [
+        f"s_cmp_lt_u32 s{PISS}, s{PLIM}",
         "s_cbranch_scc1 .L%=_issue",
         f"s_cmp_eq_u32 s{PINF}, 0",
         "s_cbranch_scc0 .L%=_land",
@@ -345,44 +384,34 @@ def producer(vec):
         f"s_sub_u32 s{PPOLL}, s{PPOLL}, 1",
         "s_sleep 1",
         "s_branch .L%=_loop",
-        # stage this producer's rows prow0 .. prow0+half-1 of chunk `issued` into its
-        # slot: LDS row (issued % RING) * CHUNK + prow0 + r; B row min(row, K - 1)
+        # LDS row of the producer's first row of chunk `issued`:
+        # (issued % RING) * CHUNK + prow0
         ".L%=_issue:",
         f"s_and_b32 s{PTMP}, s{PISS}, {RING - 1}",
-        f"s_lshl_b32 s{PTMP}, s{PTMP}, {CHUNK.bit_length() - 1 + 10}",
+        f"s_lshl_b32 s{PTMP}, s{PTMP}, {lg_chunk + 10}",
         "s_lshl_b32 m0, %[prow0], 10",
         f"s_add_u32 m0, m0, s{PTMP}",
-        f"s_lshl_b32 s{PROW}, s{PISS}, {CHUNK.bit_length() - 1}",
-        f"s_add_u32 s{PROW}, s{PROW}, %[prow0]",
         f"s_mov_b64 s[{PEX}:{PEX + 1}], exec",
+        f"s_cmp_lt_u32 s{PISS}, s{PLAST}",
+        "s_cbranch_scc0 .L%=_clamped",
     ]
     if vec:
-        L.append(f"s_mov_b64 exec, s[{PCM}:{PCM + 1}]")
-    for r in range(half):
-        L += [
-            f"s_min_u32 s{PTMP}, s{PROW}, s{PKM1}",
-            f"s_mul_i32 s{PADDR}, s{PTMP}, %[rs]",
-            f"s_mul_hi_u32 s{PADDR + 1}, s{PTMP}, %[rs]",
-            f"s_add_u32 s{PADDR}, s{PADDR}, s{PBASE}",
-            f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, s{PBASE + 1}",
-        ]
-        if vec:
-            L += [f"global_load_lds_dwordx4 %[vl], s[{PADDR}:{PADDR + 1}]",
+        L.append(f"s_mov_b64 exec, s[{PCM}:{PCM + 1}]")   # also spaces the m0 write from the DMA
+        for r in range(half):
+            if r:
+                L.append("s_nop 0")                       # m0 write, then a DMA reading it
+            L += [f"global_load_lds_dwordx4 v{VO + r}, s[{PBASE}:{PBASE + 1}]",
                   "s_add_u32 m0, m0, 0x400"]
-        else:
-            for q in range(4):
-                m = PCM + 2 * q
-                if q:
-                    L += [f"s_add_u32 s{PADDR}, s{PADDR}, 0x100",
-                          f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, 0"]
-                L += [f"s_mov_b64 exec, s[{m}:{m + 1}]", "s_nop 0",
-                      f"global_load_lds_dword %[vl], s[{PADDR}:{PADDR + 1}]",
-                      "s_add_u32 m0, m0, 0x100"]
-        L.append(f"s_add_u32 s{PROW}, s{PROW}, 1")
-    L.append(f"s_mov_b64 exec, s[{PEX}:{PEX + 1}]")
-    if PF_PER_PANEL:
-        L += prefetch_stream()
+        L.append("s_branch .L%=_issued")
+    L += [".L%=_clamped:",
+          f"s_lshl_b32 s{PROW}, s{PISS}, {lg_chunk}",
+          f"s_add_u32 s{PROW}, s{PROW}, %[prow0]"]
+    L += issue_rows_clamped(vec, half)
     L += [
+        ".L%=_issued:",
+        f"s_mov_b64 exec, s[{PEX}:{PEX + 1}]",
+        f"s_add_u32 s{PBASE}, s{PBASE}, s{PCS}",
+        f"s_addc_u32 s{PBASE + 1}, s{PBASE + 1}, s{PCS + 1}",
         f"s_add_u32 s{PISS}, s{PISS}, 1",
         f"s_add_u32 s{PINF}, s{PINF}, 1",
         "s_branch .L%=_loop",
@@ -409,20 +438,18 @@ def producer(vec):
         f"s_mov_b32 m0, s{PM0}",
     ]
     body = "\n".join('      "' + x + '\\n\\t"' for x in L)
-    npan = -(-MAX_CONS // NPROD)
-    sregs = [f"s{x}" for x in list(range(PISS, PCM + 2 * pieces)) + list(range(PFA, PFG + 2 * npan))]
-    clob = ", ".join(f'"{r}"' for r in sregs + ["v27", "vcc", "scc"])
+    sregs = [f"s{x}" for x in list(range(PISS, PCM + 2 * pieces)) + [PKM1, PLAST]]
+    vregs = ["v27"] + [f"v{x}" for x in range(VO, VMIN + 5)]
+    clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["vcc", "scc"])
     suffix = "vec" if vec else "dword"
     return f"""// Producer, {"16-byte" if vec else "4-byte"} staging
 __device__ __forceinline__ void produce_{suffix}(const ProducerArgs& a) {{
   asm volatile(
 {body}
       :
-      : [nch] "s"(a.nchunks), [K] "s"(a.K), [rs] "s"(a.row_bytes), [bb] "s"(a.bbase),
-        [ncol] "s"(a.ncol), [prow0] "s"(a.first_row), [tbl_lo] "s"(a.tbl_lo),
-        [tbl_hi] "s"(a.tbl_hi), [tstr] "s"(a.tstride), [ent_lo] "s"(a.ent_lo),
-        [ent_hi] "s"(a.ent_hi), [npw] "s"(a.npanels_wg), [pw0] "s"(a.first_panel),
-        [vl] "v"(a.vlane), [pg] "v"(a.prog_lane_addr), [ra] "v"(a.ready_addr)
+      : [nch] "s"(a.nchunks), [K] "s"(a.K), [rs] "s"(a.row_bytes), [bb_lo] "s"(a.bbase_lo),
+        [bb_hi] "s"(a.bbase_hi), [ncol] "s"(a.ncol), [prow0] "s"(a.first_row),
+        [vl] "v"(a.vlane), [pg] "v"(a.prog_addr), [ra] "v"(a.ready_addr)
       : {clob});
 }}
 """

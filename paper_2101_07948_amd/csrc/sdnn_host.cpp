@@ -130,7 +130,6 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
     P.panel_rows.assign((size_t)P.npanels * RW, -1);
     for (int32_t i = 0; i < M; ++i) P.panel_rows[i] = perm[i];
     P.panel_start.assign((size_t)P.npanels, -1);
-    P.chunk_group.assign((size_t)P.npanels * (P.nchunks + 1), 0);
     P.entries.clear();
     P.entries.reserve((size_t)(P.nnz + P.nnz / 8 + 64) * 2);
 
@@ -174,20 +173,14 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
       int32_t prev_lo = -1, prev_hi = -1;
       size_t i = 0;
       bool first = true;
-      int32_t* cg = &P.chunk_group[(size_t)p * (P.nchunks + 1)];
-      int32_t c_next = 0;  // next chunk whose first group is still to be recorded
       while (i < ent.size()) {
         int n = 1;  // a group never reads more than kRing chunks
         while (n < kGroup && i + n < ent.size() && ent[i + n].chunk - ent[i].chunk < kRing) ++n;
         const bool last = i + n == ent.size();
-        const int32_t g = (int32_t)(P.entries.size() / (2 * kGroup));
-        for (; c_next <= ent[i].chunk; ++c_next) cg[c_next] = g;
         emit_group(P.entries, &ent[i], n, first, last, &prev_lo, &prev_hi);
         first = false;
         i += n;
       }
-      const int32_t g_end = (int32_t)(P.entries.size() / (2 * kGroup));
-      for (; c_next <= P.nchunks; ++c_next) cg[c_next] = g_end;
     }
     P.stored = (int64_t)(P.entries.size() / 2);
     if (P.stored > INT32_MAX - kTailGroups * kGroup) return SDNN_ERR_DIM;
@@ -289,27 +282,6 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
     }
   }
   if (expect_group != ngroups) return false;
-  // chunk_group[p][c]: the first group of panel p with c_lo >= c
-  if ((int64_t)P.chunk_group.size() != (int64_t)P.npanels * (P.nchunks + 1)) return false;
-  for (int32_t p = 0; p < P.npanels; ++p) {
-    const int32_t* cg = &P.chunk_group[(size_t)p * (P.nchunks + 1)];
-    if (P.panel_start[p] < 0) {
-      for (int32_t c = 0; c <= P.nchunks; ++c)
-        if (cg[c] != 0) return false;
-      continue;
-    }
-    int64_t end = P.panel_start[p];  // one past the panel's last group
-    while (!((P.entries[(size_t)end * 2 * kGroup + kGroup + kHiWord] >> kEndBit) & 1u)) ++end;
-    ++end;
-    auto c_lo = [&](int64_t g) {
-      return (int32_t)(P.entries[(size_t)g * 2 * kGroup + kGroup + kLoWord] >> kLoShift);
-    };
-    int64_t g = P.panel_start[p];
-    for (int32_t c = 0; c <= P.nchunks; ++c) {
-      while (g < end && c_lo(g) < c) ++g;
-      if (cg[c] != g) return false;
-    }
-  }
   for (int64_t q = 0; q < P.nnz; ++q)
     if (!seen[q]) return false;
   for (size_t d = (size_t)(2 * P.stored); d < P.entries.size(); ++d)
@@ -323,15 +295,17 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
   return true;
 }
 
-static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t* RW, int32_t* permute) {
-  *RW = 4;
+// Panel heights to pack: the explicit option, or the short and tall defaults.
+static sdnn_status resolve_opts(const sdnn_plan_opts* opts, std::vector<int32_t>* rws,
+                                int32_t* permute) {
+  *rws = {kShortPanel, kTallPanel};
   *permute = 1;
   if (opts) {
     if (opts->panel_rows != 0) {
       if (opts->panel_rows != 4 && opts->panel_rows != 8 && opts->panel_rows != 12 &&
           opts->panel_rows != 16)
         return SDNN_ERR_DIM;
-      *RW = opts->panel_rows;
+      *rws = {opts->panel_rows};
     }
     if (opts->permute != 0 && opts->permute != 1) return SDNN_ERR_DIM;
     *permute = opts->permute;
@@ -339,10 +313,13 @@ static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t* RW, int32_t
   return SDNN_OK;
 }
 
+// Validation, Algorithm 1 (once) and one packing per panel height.
 static sdnn_status prepare(const int32_t* row_ptr, const int32_t* col_idx, const float* values,
-                           int32_t M, int32_t K, const sdnn_plan_opts* opts, Packed* P) {
-  int32_t RW, permute;
-  sdnn_status st = resolve_opts(opts, &RW, &permute);
+                           int32_t M, int32_t K, const sdnn_plan_opts* opts,
+                           std::vector<Packed>* packs) {
+  std::vector<int32_t> rws;
+  int32_t permute;
+  sdnn_status st = resolve_opts(opts, &rws, &permute);
   if (st != SDNN_OK) return st;
   st = validate_csr(row_ptr, col_idx, M, K);
   if (st != SDNN_OK) return st;
@@ -350,6 +327,7 @@ static sdnn_status prepare(const int32_t* row_ptr, const int32_t* col_idx, const
   std::vector<int32_t> perm;
   try {
     perm.resize(M);
+    packs->assign(rws.size(), Packed());
   } catch (const std::bad_alloc&) {
     return SDNN_ERR_ALLOC;
   }
@@ -359,22 +337,44 @@ static sdnn_status prepare(const int32_t* row_ptr, const int32_t* col_idx, const
   } else {
     for (int32_t i = 0; i < M; ++i) perm[i] = i;
   }
-  return pack(row_ptr, col_idx, values, M, K, RW, perm.data(), P);
+  for (size_t i = 0; i < rws.size(); ++i) {
+    st = pack(row_ptr, col_idx, values, M, K, rws[i], perm.data(), &(*packs)[i]);
+    if (st != SDNN_OK) return st;
+  }
+  return SDNN_OK;
 }
 
-static void fill_info(const Packed& P, int64_t packed_bytes, sdnn_plan_info_t* out) {
+static double fill_of(const Packed& P) {
+  return P.stored ? (double)P.nnz / (double)P.stored : 1.0;
+}
+
+// Statistics of the first packing, plus the tall one's if there is one.
+static void fill_info(const std::vector<Packed>& packs, int64_t packed_bytes,
+                      sdnn_plan_info_t* out) {
+  const Packed& P = packs[0];
   out->M = P.M;
   out->K = P.K;
   out->nnz = P.nnz;
   out->panels = P.npanels;
   out->packed_bytes = packed_bytes;
   out->rho = P.rho;
-  out->fill = P.stored ? (double)P.nnz / (double)P.stored : 1.0;
+  out->fill = fill_of(P);
   out->panel_rows = P.RW;
   out->k_chunk = kChunk;
+  const bool tall = packs.size() > 1;
+  out->tall_panel_rows = tall ? packs[1].RW : 0;
+  out->reserved = 0;
+  out->tall_rho = tall ? packs[1].rho : 0.0;
+  out->tall_fill = tall ? fill_of(packs[1]) : 0.0;
 }
 
 static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
+
+// Device bytes of one packing's three arrays (each 256-byte aligned).
+static int64_t packing_bytes(const Packed& P) {
+  return align256((int64_t)P.entries.size() * 4) + align256((int64_t)P.panel_start.size() * 4) +
+         align256((int64_t)P.panel_rows.size() * 4);
+}
 
 }  // namespace sdnn
 
@@ -413,17 +413,15 @@ sdnn_status sdnn_plan_check_host(const int32_t* row_ptr, const int32_t* col_idx,
                                  const float* values, int32_t M, int32_t K,
                                  const sdnn_plan_opts* opts, sdnn_plan_info_t* info) {
   try {
-    Packed P;
-    sdnn_status st = prepare(row_ptr, col_idx, values, M, K, opts, &P);
+    std::vector<Packed> packs;
+    sdnn_status st = prepare(row_ptr, col_idx, values, M, K, opts, &packs);
     if (st != SDNN_OK) return st;
-    if (!check_packed(row_ptr, col_idx, values, P)) return SDNN_ERR_INTERNAL;
-    if (info) {
-      const int64_t bytes = align256((int64_t)P.entries.size() * 4) +
-                            align256((int64_t)P.panel_start.size() * 4) +
-                            align256((int64_t)P.panel_rows.size() * 4) +
-                            align256((int64_t)P.chunk_group.size() * 4);
-      fill_info(P, bytes, info);
+    int64_t bytes = 0;
+    for (const Packed& P : packs) {
+      if (!check_packed(row_ptr, col_idx, values, P)) return SDNN_ERR_INTERNAL;
+      bytes += packing_bytes(P);
     }
+    if (info) fill_info(packs, bytes, info);
     return SDNN_OK;
   } catch (...) {
     return SDNN_ERR_ALLOC;
@@ -436,8 +434,8 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
   *out = nullptr;
   sdnn_plan_s* plan = nullptr;
   try {
-    Packed P;
-    sdnn_status st = prepare(row_ptr, col_idx, values, M, K, opts, &P);
+    std::vector<Packed> packs;
+    sdnn_status st = prepare(row_ptr, col_idx, values, M, K, opts, &packs);
     if (st != SDNN_OK) return st;
 
     plan = new sdnn_plan_s();
@@ -450,21 +448,16 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
       delete plan;
       return SDNN_ERR_HIP;
     }
-    plan->M = P.M;
-    plan->K = P.K;
-    plan->RW = P.RW;
-    plan->nchunks = P.nchunks;
-    plan->npanels = P.npanels;
-    plan->nnz = P.nnz;
-    plan->rho = P.rho;
-    plan->fill = P.stored ? (double)P.nnz / (double)P.stored : 1.0;
-    plan->perm = P.perm;
+    const Packed& P0 = packs[0];
+    plan->M = P0.M;
+    plan->K = P0.K;
+    plan->nchunks = P0.nchunks;
+    plan->nnz = P0.nnz;
+    plan->perm = P0.perm;
+    plan->npack = (int)packs.size();
 
-    const int64_t b_ent = align256((int64_t)P.entries.size() * 4);
-    const int64_t b_seg = align256((int64_t)P.panel_start.size() * 4);
-    const int64_t b_rows = align256((int64_t)P.panel_rows.size() * 4);
-    const int64_t b_cg = align256((int64_t)P.chunk_group.size() * 4);
-    const int64_t total = b_ent + b_seg + b_rows + b_cg;
+    int64_t total = 0;
+    for (const Packed& P : packs) total += packing_bytes(P);
     plan->packed_bytes = total;
     if (total > 0) {
       if (hipMalloc(&plan->d_mem, (size_t)total) != hipSuccess) {
@@ -472,26 +465,40 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
         delete plan;
         return SDNN_ERR_ALLOC;
       }
-      char* base = (char*)plan->d_mem;
-      plan->d_entries = (const uint32_t*)base;
-      plan->d_panel_start = (const int32_t*)(base + b_ent);
-      plan->d_panel_rows = (const int32_t*)(base + b_ent + b_seg);
-      plan->d_chunk_group = (const int32_t*)(base + b_ent + b_seg + b_rows);
       std::vector<char> host((size_t)total, 0);
-      if (!P.entries.empty()) memcpy(host.data(), P.entries.data(), P.entries.size() * 4);
-      if (!P.panel_start.empty())
-        memcpy(host.data() + b_ent, P.panel_start.data(), P.panel_start.size() * 4);
-      if (!P.panel_rows.empty())
-        memcpy(host.data() + b_ent + b_seg, P.panel_rows.data(), P.panel_rows.size() * 4);
-      if (!P.chunk_group.empty())
-        memcpy(host.data() + b_ent + b_seg + b_rows, P.chunk_group.data(),
-               P.chunk_group.size() * 4);
+      int64_t off = 0;
+      for (size_t i = 0; i < packs.size(); ++i) {
+        const Packed& P = packs[i];
+        DevPacking& d = plan->pk[i];
+        const int64_t b_ent = align256((int64_t)P.entries.size() * 4);
+        const int64_t b_seg = align256((int64_t)P.panel_start.size() * 4);
+        char* base = (char*)plan->d_mem + off;
+        d.RW = P.RW;
+        d.npanels = P.npanels;
+        d.rho = P.rho;
+        d.fill = fill_of(P);
+        d.entries = (const uint32_t*)base;
+        d.panel_start = (const int32_t*)(base + b_ent);
+        d.panel_rows = (const int32_t*)(base + b_ent + b_seg);
+        char* h = host.data() + off;
+        if (!P.entries.empty()) memcpy(h, P.entries.data(), P.entries.size() * 4);
+        if (!P.panel_start.empty())
+          memcpy(h + b_ent, P.panel_start.data(), P.panel_start.size() * 4);
+        if (!P.panel_rows.empty())
+          memcpy(h + b_ent + b_seg, P.panel_rows.data(), P.panel_rows.size() * 4);
+        off += packing_bytes(P);
+      }
       if (hipMemcpy(plan->d_mem, host.data(), (size_t)total, hipMemcpyHostToDevice) !=
           hipSuccess) {
         (void)hipGetLastError();
         (void)hipFree(plan->d_mem);
         delete plan;
         return SDNN_ERR_HIP;
+      }
+    } else {
+      for (size_t i = 0; i < packs.size(); ++i) {
+        plan->pk[i].RW = packs[i].RW;
+        plan->pk[i].npanels = packs[i].npanels;
       }
     }
     *out = plan;
@@ -514,15 +521,21 @@ sdnn_status sdnn_plan_get_perm(sdnn_plan p, int32_t* perm_out) {
 
 sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out) {
   if (!p || !out) return SDNN_ERR_NULL;
+  const DevPacking& d = p->pk[0];
   out->M = p->M;
   out->K = p->K;
   out->nnz = p->nnz;
-  out->panels = p->npanels;
+  out->panels = d.npanels;
   out->packed_bytes = p->packed_bytes;
-  out->rho = p->rho;
-  out->fill = p->fill;
-  out->panel_rows = p->RW;
+  out->rho = d.rho;
+  out->fill = d.fill;
+  out->panel_rows = d.RW;
   out->k_chunk = kChunk;
+  const bool tall = p->npack > 1;
+  out->tall_panel_rows = tall ? p->pk[1].RW : 0;
+  out->reserved = 0;
+  out->tall_rho = tall ? p->pk[1].rho : 0.0;
+  out->tall_fill = tall ? p->pk[1].fill : 0.0;
   return SDNN_OK;
 }
 

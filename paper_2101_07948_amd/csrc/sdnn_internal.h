@@ -53,21 +53,22 @@ static_assert(kRing * kChunk <= 128, "ring rows must fit 7 bits");
 //   panel's last group and sync is set on a panel's first and last groups and
 //   whenever c_lo or c_hi differs from the previous group's.  Panels are stored back
 //   to back; panel_start holds each panel's first group (-1: the panel has no
-//   entries) and chunk_group[p][c] the first group of panel p whose c_lo >= c, so that
-//   [chunk_group[p][c], chunk_group[p][c+1]) are the groups starting in chunk c (the
-//   kernel's producers prefetch their stream lines into the scalar cache).  The
-//   stream ends with kTailGroups zero groups.
+//   entries).  The stream ends with kTailGroups zero groups.
 struct Packed {
   int32_t M = 0, K = 0, RW = 0, nchunks = 0, npanels = 0;
   int64_t nnz = 0, stored = 0;     // structural entries, stored entries (with padding)
   std::vector<int32_t> perm;        // [M]   original row at permuted position
   std::vector<int32_t> panel_rows;  // [npanels*RW] original row or -1 (padding)
   std::vector<int32_t> panel_start; // [npanels] first group of the panel, or -1
-  std::vector<int32_t> chunk_group; // [npanels][nchunks+1]: first group of the panel whose
-                                    // c_lo >= c (the panel's end for c = nchunks; 0 if empty)
   std::vector<uint32_t> entries;    // [2*(stored + kTailGroups*kGroup)] dwords
   double rho = 1.0;                 // nnz / sum_p |union of the panel's column sets|
 };
+
+// Panel heights of the two packings a default plan holds: short panels keep enough
+// waves busy when a tile has few rows per CU; tall panels (used once there are rows
+// for a full workgroup of them per CU) carry more entries per K-chunk and stage each
+// B tile for more rows.
+constexpr int kShortPanel = 4, kTallPanel = 12;
 
 // CSR validation; returns SDNN_OK or SDNN_ERR_*.
 sdnn_status validate_csr(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K);
@@ -78,21 +79,27 @@ sdnn_status reorder_bitset(const int32_t* row_ptr, const int32_t* col_idx, int32
 sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* values, int32_t M,
                  int32_t K, int32_t RW, const int32_t* perm, Packed* out);
 
+// One packing of the plan in device memory.
+struct DevPacking {
+  int32_t RW = 0, npanels = 0;
+  double rho = 1.0, fill = 1.0;
+  const uint32_t* entries = nullptr;      // [2*(stored + kTailGroups*kGroup)] dwords
+  const int32_t* panel_start = nullptr;   // [npanels] (in groups, -1: empty panel)
+  const int32_t* panel_rows = nullptr;    // [npanels*RW]
+};
+
 }  // namespace sdnn
 
 // The plan handle.
 struct sdnn_plan_s {
   int device = -1;
   int num_cus = 0;
-  int32_t M = 0, K = 0, RW = 0, nchunks = 0, npanels = 0;
+  int32_t M = 0, K = 0, nchunks = 0;
   int64_t nnz = 0, packed_bytes = 0;
-  double rho = 1.0, fill = 1.0;
   std::vector<int32_t> perm;
-  void* d_mem = nullptr;             // one device allocation holding the four arrays
-  const uint32_t* d_entries = nullptr;  // [2*(stored + kTailGroups*kGroup)] dwords
-  const int32_t* d_panel_start = nullptr;  // [npanels] (in groups, -1: empty panel)
-  const int32_t* d_panel_rows = nullptr;  // [npanels*RW]
-  const int32_t* d_chunk_group = nullptr; // [npanels*(nchunks+1)]
+  void* d_mem = nullptr;       // one device allocation holding every packing's arrays
+  int npack = 0;               // 1 (explicit panel height) or 2 (short, tall)
+  sdnn::DevPacking pk[2];
 };
 
 namespace sdnn {

@@ -13,9 +13,9 @@
 //     selects the accumulator through VGPR index mode instead of per-matrix generated
 //     code;
 //   * the rows of B the workgroup needs are staged in LDS (the paper's split-K tiling
-//     of the dense operand) by two producer wavefronts, through a ring of 32-row
-//     slots filled by direct global->LDS 16-byte DMA; a lane reads its 4 columns of a
-//     B row with one ds_read_b128;
+//     of the dense operand) by producer wavefronts, through a ring of 32-row slots
+//     filled by direct global->LDS 16-byte DMA; a lane reads its 4 columns of a B row
+//     with one ds_read_b128;
 //   * producers and consumers synchronise through LDS words (chunks landed, lowest
 //     chunk each consumer still reads), so no wave ever waits at a workgroup barrier
 //     for the slowest one; the loops are generated inline assembly (spmm_asm_gen.h);
@@ -49,18 +49,12 @@ struct ConsumerArgs {
 struct ProducerArgs {
   int32_t nchunks, K;
   uint32_t row_bytes;      // N * 4
-  uint64_t bbase;          // address of B[0][n0]
+  uint32_t bbase_lo, bbase_hi;  // address of B[0][n0]
   int32_t ncol;            // N - n0 (columns of the tile that exist)
   uint32_t first_row;      // first row of each chunk this producer stages
   uint32_t vlane;          // the lane's byte offset in a B row segment (16 or 4 * lane)
-  uint32_t prog_lane_addr; // LDS address of progress word `lane` (lanes 0..15)
+  uint32_t prog_addr;      // LDS address of the 16 progress words
   uint32_t ready_addr;     // LDS address of this producer's ready word
-  // scalar-cache prefetch of the consumers' stream (see prefetch_stream)
-  uint32_t tbl_lo, tbl_hi; // chunk_group row of the workgroup's first panel
-  uint32_t tstride;        // bytes per chunk_group row: (nchunks + 1) * 4
-  uint32_t ent_lo, ent_hi; // the entry stream
-  uint32_t npanels_wg;     // panels of this workgroup that exist
-  uint32_t first_panel;    // this producer's first panel (then every kProducers-th)
 };
 
 #include "spmm_asm_gen.h"
@@ -105,8 +99,7 @@ struct SpmmArgs {
 template <int RW, bool VEC>
 __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     const uint32_t* __restrict__ entries, const int32_t* __restrict__ panel_start,
-    const int32_t* __restrict__ panel_rows, const int32_t* __restrict__ chunk_group,
-    const float* __restrict__ B, float* __restrict__ C, const float* __restrict__ bias,
+    const int32_t* __restrict__ panel_rows, const float* __restrict__ B, float* __restrict__ C, const float* __restrict__ bias,
     SpmmArgs a) {
   // the ring ([0, kRingBytes)) and the control words; the ring must start at LDS 0
   // (the loops form LDS addresses from the ring-row field alone), which holds because
@@ -144,22 +137,14 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     pa.nchunks = a.nchunks;
     pa.K = a.K;
     pa.row_bytes = (uint32_t)a.N * 4u;
-    pa.bbase = (uint64_t)(uintptr_t)(B + n0);
+    const uint64_t bb = (uint64_t)(uintptr_t)(B + n0);
+    pa.bbase_lo = (uint32_t)bb;
+    pa.bbase_hi = (uint32_t)(bb >> 32);
     pa.ncol = a.N - n0;
     pa.first_row = (uint32_t)(prod * (kChunk / kProducers));
     pa.vlane = (uint32_t)lane * (VEC ? 16u : 4u);
-    pa.prog_lane_addr = prog0 + 4u * (uint32_t)(lane & 15);
+    pa.prog_addr = prog0;
     pa.ready_addr = ready_addr + 4u * (uint32_t)prod;
-    const int first = rb * nc;
-    const uint64_t tbl = (uint64_t)(uintptr_t)(chunk_group + (size_t)first * (a.nchunks + 1));
-    const uint64_t ent = (uint64_t)(uintptr_t)entries;
-    pa.tbl_lo = (uint32_t)tbl;
-    pa.tbl_hi = (uint32_t)(tbl >> 32);
-    pa.tstride = (uint32_t)(a.nchunks + 1) * 4u;
-    pa.ent_lo = (uint32_t)ent;
-    pa.ent_hi = (uint32_t)(ent >> 32);
-    pa.npanels_wg = (uint32_t)(a.npanels - first < nc ? a.npanels - first : nc);
-    pa.first_panel = (uint32_t)prod;
     if (VEC)
       produce_vec(pa);
     else
@@ -205,7 +190,6 @@ struct SpmmPtrs {
   const uint32_t* entries;
   const int32_t* panel_start;
   const int32_t* panel_rows;
-  const int32_t* chunk_group;
   const float* B;
   float* C;
   const float* bias;
@@ -215,7 +199,7 @@ template <int RW, bool VEC>
 hipError_t launch_variant(const SpmmPtrs& p, const SpmmArgs& args, int waves, int grid,
                           hipStream_t stream) {
   hipLaunchKernelGGL((spmm_panel_kernel<RW, VEC>), dim3(grid), dim3(64 * (waves + kProducers)), 0, stream,
-                     p.entries, p.panel_start, p.panel_rows, p.chunk_group, p.B, p.C, p.bias,
+                     p.entries, p.panel_start, p.panel_rows, p.B, p.C, p.bias,
                      args);
   return hipGetLastError();
 }
@@ -252,9 +236,9 @@ struct LaunchCfg {
 // (the 129 KB of ring and control LDS allows one workgroup per CU), at most as many
 // consumer waves as the panel height's register use allows.  SDNN_FORCE_WAVES fixes
 // the consumer count.
-LaunchCfg choose_cfg(const sdnn_plan_s* p, int N) {
-  const int target = p->num_cus > 0 ? p->num_cus : 256;
-  const int cap = max_consumers(p->RW);
+LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N) {
+  const int target = num_cus > 0 ? num_cus : 256;
+  const int cap = max_consumers(pk.RW);
   const int forceW = env_int("SDNN_FORCE_WAVES", 0);
   LaunchCfg c;
   c.n_tiles = (N + kTileCols - 1) / kTileCols;
@@ -262,28 +246,39 @@ LaunchCfg choose_cfg(const sdnn_plan_s* p, int N) {
     c.waves = forceW;
   } else {
     int n_rb = (target + c.n_tiles - 1) / c.n_tiles;
-    if (n_rb > p->npanels) n_rb = p->npanels;
-    c.waves = (p->npanels + n_rb - 1) / n_rb;
+    if (n_rb > pk.npanels) n_rb = pk.npanels;
+    c.waves = (pk.npanels + n_rb - 1) / n_rb;
   }
   if (c.waves > cap) c.waves = cap;
-  if (c.waves > p->npanels) c.waves = p->npanels;
+  if (c.waves > pk.npanels) c.waves = pk.npanels;
   if (c.waves < 1) c.waves = 1;
-  c.n_rb = (p->npanels + c.waves - 1) / c.waves;
+  c.n_rb = (pk.npanels + c.waves - 1) / c.waves;
   return c;
+}
+
+// The packing a call runs on: the tall one (second) once the tiles hold at least a
+// full workgroup of tall panels per CU, else the first.
+const DevPacking& choose_packing(const sdnn_plan_s* p, int N) {
+  if (p->npack < 2) return p->pk[0];
+  const DevPacking& tall = p->pk[1];
+  const int64_t n_tiles = (N + kTileCols - 1) / kTileCols;
+  const int64_t cus = p->num_cus > 0 ? p->num_cus : 256;
+  const int64_t wg_rows = (int64_t)max_consumers(tall.RW) * tall.RW;
+  return (int64_t)p->M * n_tiles >= wg_rows * cus ? tall : p->pk[0];
 }
 
 }  // namespace
 
 hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                        const float* bias, int epi, hipStream_t stream) {
-  const LaunchCfg cfg = choose_cfg(p, N);
-  const SpmmPtrs ptrs{p->d_entries, p->d_panel_start, p->d_panel_rows, p->d_chunk_group,
-                      B, C, bias};
+  const DevPacking& pk = choose_packing(p, N);
+  const LaunchCfg cfg = choose_cfg(pk, p->num_cus, N);
+  const SpmmPtrs ptrs{pk.entries, pk.panel_start, pk.panel_rows, B, C, bias};
   SpmmArgs args;
   args.K = p->K;
   args.N = N;
   args.nchunks = p->nchunks;
-  args.npanels = p->npanels;
+  args.npanels = pk.npanels;
   args.n_rb = cfg.n_rb;
   const int64_t total = (int64_t)cfg.n_tiles * cfg.n_rb;
   if (total > (int64_t)1 << 30) return hipErrorInvalidValue;
@@ -291,9 +286,12 @@ hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N
   args.total_wg = (int32_t)total;
   args.per_xcd = (int32_t)(grid / 8);
   args.epi = epi;
-  const bool vec = (N % 4 == 0) && (((uintptr_t)B & 15) == 0) && (((uintptr_t)C & 15) == 0);
-  return vec ? launch_rw<true>(p->RW, ptrs, args, cfg.waves, (int)grid, stream)
-             : launch_rw<false>(p->RW, ptrs, args, cfg.waves, (int)grid, stream);
+  // the 16-byte producer addresses a chunk's rows with 32-bit per-lane offsets
+  // 16 * lane + r * 4N (r < kChunk / kProducers)
+  const bool vec = (N % 4 == 0) && (((uintptr_t)B & 15) == 0) && (((uintptr_t)C & 15) == 0) &&
+                   (uint64_t)N * 4u * (kChunk / kProducers) < ((uint64_t)1 << 31);
+  return vec ? launch_rw<true>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream)
+             : launch_rw<false>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
 }
 
 // ---------------------------------------------------------------------------------

@@ -86,6 +86,22 @@ def test_packed_stream_self_check(name, panel_rows):
         assert stored % 4 == 0
 
 
+@pytest.mark.parametrize("name", ["c2", "w0", "c3"])
+def test_default_plan_packs_short_and_tall_panels(name):
+    """With panel_rows = 0 the plan holds a 4-row and a 12-row packing of the same
+    permutation; both pass the stream self-check and tall panels share more columns."""
+    for L in inputs.workload(name, N=4).layers:
+        info = sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K)
+        assert info["panel_rows"] == 4 and info["tall_panel_rows"] == 12
+        assert info["panels"] == -(-L.W.M // 4)
+        assert info["tall_rho"] >= info["rho"] >= 1.0
+        assert 0.0 < info["tall_fill"] <= 1.0 and 0.0 < info["fill"] <= 1.0
+        one = sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K,
+                                 panel_rows=12)
+        assert one["tall_panel_rows"] == 0 and one["rho"] == info["tall_rho"]
+        assert info["packed_bytes"] > one["packed_bytes"]
+
+
 def test_permutation_raises_reuse_on_grouped_columns():
     """Algorithm 1's purpose (Sec. 3.1.2): adjacent rows share columns.  On block-
     correlated rows the panel reuse factor rho must improve over the identity order."""

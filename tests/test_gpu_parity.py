@@ -184,6 +184,21 @@ def test_row_permutation_equivariance_bitexact():
     assert np.array_equal(C2, C1[pi])
 
 
+def test_tall_panels_at_large_N():
+    """M * ceil(N / 256) = 768 * 32 reaches 96 rows per CU on 256 CUs, so the default
+    plan runs its 12-row packing: checked against the oracle, and bit-identical to a
+    4-row-only plan (every row sums its entries in ascending column order either way)."""
+    M, K, N = 768, 1024, 8192
+    W = inputs.pattern_uniform(M, K, 0.1, inputs.CFG_TEST, 21, 0.05)
+    B = inputs.dense_B(K, N, inputs.CFG_TEST, 21)
+    bias = inputs.bias_normal(M, inputs.CFG_TEST, 21, 0.02)
+    got = check(W.row_ptr, W.col_idx, W.values, M, K, B, bias, "relu", label="tall")
+    with sd.Plan.from_csr(W, panel_rows=4) as p4:
+        assert p4.info["tall_panel_rows"] == 0
+        short = gpu_spmm(p4, B, bias, "relu")
+    assert np.array_equal(got, short)
+
+
 def test_permute_off_and_on_agree():
     W = inputs.pattern_grouped8(256, 512, 0.05, inputs.CFG_TEST, 9, 0.05)
     B = inputs.dense_B(512, 256, inputs.CFG_TEST, 9)
