@@ -25,10 +25,11 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, GB/s
-# FP32 FMA issued as single (unpacked) v_fma_f32: 256 CUs x 4 SIMD x 16 lanes x 2 FLOP
-# x 2.4 GHz.  Packed FP32 (157.3 TFLOP/s) is not used by this build.
-ALU_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
-PACKED_FP32_PEAK_TFLOPS = 157.3
+# FP32 vector peak of MI355X: 256 CUs x 128 FP32 FMA lanes per clock x 2 FLOP x 2.4 GHz
+# = 157.3 TFLOP/s.  The kernel issues unpacked v_fma_f32; the machine probe measures
+# unpacked FMAs alone well above half of this figure, so it is the ceiling they are
+# held to.
+ALU_PEAK_TFLOPS = 256 * 128 * 2 * 2.4e9 / 1e12
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2101_07948_amd", "csrc", f)
                   for f in ("sdnn_kernels.hip", "sdnn_host.cpp", "sdnn_internal.h",
                             "gen_spmm_asm.py", "spmm_asm_gen.h")]
@@ -109,6 +110,270 @@ def cpu_baseline(W, B, bias, budget_s: float):
                       f"{per * 1e3:.1f} ms per call"}
 
 
+# ---------------------------------------------------------------------------------
+# Configuration suite: every workload layer (cold / warm), the dense comparison, the
+# Algorithm 1 ablation, the chained C5 stack, the CPU oracle at 1 / 4 / all threads and
+# the machine probes.  Writes a markdown report.
+
+def _launch_times(fn, reps):
+    """Per-launch milliseconds (an event pair around each call) and the mean over one
+    event pair around all reps."""
+    import torch
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(reps)]
+    for i in range(reps):
+        pairs[i][0].record()
+        fn(i)
+        pairs[i][1].record()
+    torch.cuda.synchronize()
+    per = sorted(a.elapsed_time(b) for a, b in pairs)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(reps):
+        fn(i)
+    e1.record()
+    torch.cuda.synchronize()
+    return per, e0.elapsed_time(e1) / reps
+
+
+def _pct(sorted_vals, q):
+    i = min(len(sorted_vals) - 1, max(0, int(round(q * (len(sorted_vals) - 1)))))
+    return sorted_vals[i]
+
+
+def _suite_layers():
+    from paper_2101_07948_amd import inputs
+    out = []
+    def add(label, name, li, N=None, **kw):
+        w = inputs.workload(name, N=N, **kw)
+        out.append((label, w.layers[li], w.N))
+    add("C1 256x256 90% N=64", "c1", 0)
+    add("C2 768x768 90% N=1024", "c2", 0)
+    add("C3 W1 3072x768 94% lognormal, N=4096, GELU", "c3", 0)
+    add("C3 W2 768x3072 94% lognormal, N=4096", "c3", 1)
+    add("C4 512x512 80% N=3136, ReLU", "c4", 0)
+    add("C5 projection 768x768 97% grouped, N=16384", "c5", 0, num_layers=1)
+    add("C5 FFN1 3072x768 97% grouped, N=16384, GELU", "c5", 4, num_layers=1)
+    add("C5 FFN2 768x3072 97% grouped, N=16384", "c5", 5, num_layers=1)
+    for N in (1024, 4096, 16384):
+        add(f"W0 768x3072 90% N={N}", "w0", 0, N=N)
+    return out
+
+
+def _time_layer(plan, L, N, reps=100, warmup=10, cold=True):
+    import torch
+    dev = torch.device("cuda:0")
+    M, K = L.W.M, L.W.K
+    bytes_set = 4 * (K * N + M * N)
+    nsets = min(64, max(1, math.ceil((1 << 30) / bytes_set))) if cold else 1
+    Bs = [torch.randn(K, N, device=dev) for _ in range(nsets)]
+    Cs = [torch.empty(M, N, device=dev) for _ in range(nsets)]
+    bias = torch.from_numpy(L.bias).to(dev) if L.bias is not None else None
+    fn = lambda i: plan.spmm(Bs[i % nsets], Cs[i % nsets], bias, L.epi)
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    per, mean = _launch_times(fn, reps)
+    del Bs, Cs
+    return per, mean, nsets
+
+
+def _packing_used(info, M, N, cus):
+    """Mirror of the launcher's choice (4-row unless the tall packing fills every CU)."""
+    tall = info["tall_panel_rows"]
+    if tall and M * -(-N // 256) >= 8 * tall * cus:
+        return tall, info["tall_rho"]
+    return info["panel_rows"], info["rho"]
+
+
+def run_suite(out_path):
+    import platform
+    import numpy as np
+    import torch
+    import ctypes
+    import oracle
+    import paper_2101_07948_amd as sd
+    from paper_2101_07948_amd import inputs
+
+    dev = torch.device("cuda:0")
+    props = torch.cuda.get_device_properties(0)
+    cus = props.multi_processor_count
+    lines = [f"# Configuration suite on {props.name} ({cus} CUs)", "",
+             f"Command: `python3 bench.py --suite {os.path.relpath(out_path, ROOT)}` "
+             f"(kernel hash {kernel_hash()}).", "",
+             "Times are `sdnn_spmm` alone, inputs resident in HBM.  Cold: (B, C) buffer sets "
+             "rotated (>= 1 GiB in total, at most 64 sets); warm: one set.  Per-launch times "
+             "from an event pair around each of 100 launches after 10 warm-up launches; "
+             "'mean' is one event pair around 100 back-to-back launches.  % ALU is of "
+             f"{ALU_PEAK_TFLOPS:.1f} TFLOP/s (FP32 vector peak), % HBM of {HBM_PEAK_GBS:.0f} GB/s "
+             "(algorithmic bytes 8 nnz + 4 KN + 4 MN + 4 M).", "",
+             "## Every configuration", "",
+             "| layer | nnz | panel rows used | rho | cold median us (p10-p90) | cold mean us | "
+             "warm median us | GFLOP/s (cold mean) | % ALU | alg GB/s | % HBM |",
+             "|---|---|---|---|---|---|---|---|---|---|---|"]
+    timed = {}
+    for label, L, N in _suite_layers():
+        W = L.W
+        with sd.Plan.from_csr(W) as plan:
+            rw, rho = _packing_used(plan.info, W.M, N, cus)
+            per, mean, nsets = _time_layer(plan, L, N)
+            wper, _, _ = _time_layer(plan, L, N, cold=False)
+        flop = 2.0 * W.nnz * N
+        ab = 8.0 * W.nnz + 4.0 * W.K * N + 4.0 * W.M * N + 4.0 * W.M
+        t = mean * 1e-3
+        timed[label] = mean
+        lines.append(f"| {label} | {W.nnz} | {rw} | {rho:.2f} | {_pct(per, .5)*1e3:.1f} "
+                     f"({_pct(per, .1)*1e3:.1f}-{_pct(per, .9)*1e3:.1f}) | {mean*1e3:.1f} | "
+                     f"{_pct(wper, .5)*1e3:.1f} | {flop/t/1e9:.0f} | "
+                     f"{100*flop/t/1e12/ALU_PEAK_TFLOPS:.1f} | {ab/t/1e9:.0f} | "
+                     f"{100*ab/t/1e9/HBM_PEAK_GBS:.1f} |")
+        print(lines[-1], flush=True)
+
+    lines += ["", "## Dense comparison kernel (same layouts and epilogue)", "",
+              "| layer | dense us | dense-equivalent TFLOP/s | % of FP32 peak | "
+              "sparse speedup |", "|---|---|---|---|---|"]
+    for label, L, N in _suite_layers():
+        if not (label.startswith("C2") or label.startswith("C3 W1") or label == "W0 768x3072 90% N=4096"):
+            continue
+        W = L.W
+        Wd = torch.from_numpy(W.to_dense()).to(dev)
+        B = torch.randn(W.K, N, device=dev)
+        C = torch.empty(W.M, N, device=dev)
+        bias = torch.from_numpy(L.bias).to(dev) if L.bias is not None else None
+        fn = lambda i: sd.dense_gemm(Wd, B, C, bias, L.epi)
+        fn(0)
+        torch.cuda.synchronize()
+        _, dmean = _launch_times(fn, 10)
+        tf = 2.0 * W.M * W.K * N / (dmean * 1e-3) / 1e12
+        lines.append(f"| {label} | {dmean*1e3:.1f} | {tf:.1f} | {100*tf/ALU_PEAK_TFLOPS:.1f} | "
+                     f"{dmean/timed[label]:.2f}x |")
+        print(lines[-1], flush=True)
+        del Wd, B, C
+
+    lines += ["", "## Algorithm 1 ablation (permute = 0 vs 1), cold mean", "",
+              "| layer | rho off | rho on | us off | us on | speedup from the permutation |",
+              "|---|---|---|---|---|---|"]
+    for label, L, N in _suite_layers():
+        if not (label.startswith("C2") or label.startswith("C3") or label.startswith("C5")):
+            continue
+        res = {}
+        for perm in (False, True):
+            with sd.Plan.from_csr(L.W, permute=perm) as plan:
+                _, rho = _packing_used(plan.info, L.W.M, N, cus)
+                _, mean, _ = _time_layer(plan, L, N, reps=50)
+            res[perm] = (rho, mean)
+        lines.append(f"| {label} | {res[False][0]:.2f} | {res[True][0]:.2f} | "
+                     f"{res[False][1]*1e3:.1f} | {res[True][1]*1e3:.1f} | "
+                     f"{res[False][1]/res[True][1]:.2f}x |")
+        print(lines[-1], flush=True)
+
+    # the whole C5 stack, chained on the GPU's own activations
+    w = inputs.workload("c5")
+    t0 = time.perf_counter()
+    plans = [sd.Plan.from_csr(L.W) for L in w.layers]
+    prep_s = time.perf_counter() - t0
+    X0 = torch.randn(w.layers[0].W.K, w.N, device=dev)
+    biases = [None if L.bias is None else torch.from_numpy(L.bias).to(dev) for L in w.layers]
+    acts = {768: [torch.empty(768, w.N, device=dev) for _ in range(2)],
+            3072: [torch.empty(3072, w.N, device=dev)]}
+    def forward(_i):
+        X, flip = X0, 0
+        for L, plan, b in zip(w.layers, plans, biases):
+            if L.W.M == 3072:
+                Y = acts[3072][0]
+            else:
+                Y = acts[768][flip]
+                flip ^= 1
+            plan.spmm(X, Y, b, L.epi)
+            X = Y
+    forward(0)
+    torch.cuda.synchronize()
+    _, fmean = _launch_times(forward, 5)
+    flop = sum(2.0 * L.W.nnz * w.N for L in w.layers)
+    for p_ in plans:
+        p_.close()
+    lines += ["", "## C5: 12 encoder layers x 6 sparse products, chained (N = 16384)", "",
+              f"* {len(w.layers)} products, {flop/1e9:.1f} GFLOP per forward; "
+              f"{fmean:.2f} ms per forward = {flop/(fmean*1e-3)/1e12:.1f} TFLOP/s "
+              f"(mean of 5 forwards after one warm-up, activations stay on the GPU).",
+              f"* Preparation of the {len(w.layers)} plans (validation, Algorithm 1, two packings, "
+              f"upload): {prep_s:.2f} s on the host."]
+    print("\n".join(lines[-3:]), flush=True)
+
+    # CPU oracle (fp32 CSR loop) at 1, 4 and all threads on W0 at N = 4096
+    wl = inputs.workload("w0")
+    L = wl.layers[0]
+    cpu_model = "unknown"
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                cpu_model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    avail = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    lines += ["", f"## CPU oracle (fp32 CSR loop, OpenMP over rows) on W0, N = 4096", "",
+              f"Host: {cpu_model}; {avail} CPUs available to the process "
+              f"({platform.machine()}).  Median of 5 calls after 1 warm-up.", "",
+              "| threads | ms per call | GFLOP/s | GPU speedup (cold mean) |", "|---|---|---|---|"]
+    out = np.empty((L.W.M, wl.N), dtype=np.float32)
+    default_threads = oracle.num_threads()
+    for T in sorted({1, 4, default_threads}):
+        oracle.set_num_threads(T)
+        oracle.spmm_f32(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.K, wl.B, L.bias, "none", out=out)
+        ts = []
+        for _ in range(5):
+            t0 = time.perf_counter()
+            oracle.spmm_f32(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.K, wl.B, L.bias, "none", out=out)
+            ts.append(time.perf_counter() - t0)
+        med = sorted(ts)[2]
+        gf = 2.0 * L.W.nnz * wl.N / med / 1e9
+        lines.append(f"| {T} | {med*1e3:.1f} | {gf:.1f} | "
+                     f"{med/(timed['W0 768x3072 90% N=4096']*1e-3):.0f}x |")
+        print(lines[-1], flush=True)
+    oracle.set_num_threads(default_threads)
+
+    # machine probes next to the datasheet peaks
+    plib = ctypes.CDLL(os.path.join(ROOT, "paper_2101_07948_amd", "libsdnn_probes.so"))
+    plib.sdnn_probe_out_floats.restype = ctypes.c_int64
+    for f in (plib.sdnn_probe_fma, plib.sdnn_probe_lds_read):
+        f.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+        f.restype = ctypes.c_int32
+    pout = torch.empty(int(plib.sdnn_probe_out_floats()), device=dev)
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    def probe(f, iters):
+        assert f(iters, ctypes.c_void_p(pout.data_ptr()), stream) == 0
+    probe(plib.sdnn_probe_fma, 100)
+    torch.cuda.synchronize()
+    fi = 20000
+    _, fms = _launch_times(lambda i: probe(plib.sdnn_probe_fma, fi), 5)
+    fma_tf = pout.numel() * fi * 16 * 2 / (fms * 1e-3) / 1e12
+    li = 4000
+    _, lms = _launch_times(lambda i: probe(plib.sdnn_probe_lds_read, li), 5)
+    lds_bytes = 256 * 16 * li * 8 * 1024
+    lds_cu = lds_bytes / 256 / (lms * 1e-3)
+    x = torch.empty(1 << 28, device=dev)
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    _, cms = _launch_times(lambda i: y.copy_(x), 10)
+    hbm = 2.0 * x.numel() * 4 / (cms * 1e-3) / 1e9
+    del x, y
+    lines += ["", "## Machine probes (measured next to the datasheet peaks)", "",
+              "| probe | measured | datasheet | fraction |", "|---|---|---|---|",
+              f"| HBM stream copy (1 GiB read + 1 GiB write) | {hbm:.0f} GB/s | "
+              f"{HBM_PEAK_GBS:.0f} GB/s | {hbm/HBM_PEAK_GBS:.2f} |",
+              f"| unpacked FP32 FMA loop (v_fmaak_f32, 8 chains per thread, 16 waves per CU) | "
+              f"{fma_tf:.1f} TFLOP/s | {ALU_PEAK_TFLOPS:.1f} TFLOP/s | {fma_tf/ALU_PEAK_TFLOPS:.2f} |",
+              f"| LDS ds_read_b128 of 1 KB rows (16 waves per CU) | {lds_cu/1e9:.0f} GB/s per CU "
+              f"= {lds_cu/2.4e9:.0f} B/clk at 2.4 GHz | 512 B/clk: one 4-byte B value per "
+              f"FMA at the FP32 peak | {lds_cu/2.4e9/512:.2f} |"]
+    print("\n".join(lines[-5:]), flush=True)
+    text = "\n".join(lines) + "\n"
+    os.makedirs(os.path.dirname(os.path.abspath(out_path)), exist_ok=True)
+    open(out_path, "w").write(text)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,7 +391,14 @@ def main():
                     help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, "
                          "WRITE_SIZE) of a --calib-copy run into per-launch HBM bytes and write "
                          f"{os.path.relpath(TRAFFIC_FILE, ROOT)}")
+    ap.add_argument("--suite", metavar="OUT_MD",
+                    help="time every configuration, the dense comparison, the Algorithm 1 "
+                         "ablation, the chained C5 stack, the CPU oracle at 1/4/all threads "
+                         "and the machine probes; write a markdown report to OUT_MD")
     args = ap.parse_args()
+    if args.suite:
+        run_suite(args.suite)
+        return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, N=args.N)
         return
@@ -189,7 +461,6 @@ def main():
     traffic = measured_traffic()
     roof["traffic"] = traffic
     roof["hbm_frac"] = round(gbs / HBM_PEAK_GBS, 4)
-    roof["frac_of_packed_fp32_peak"] = round(flop / t / 1e12 / PACKED_FP32_PEAK_TFLOPS, 4)
     roof["alg_bytes"] = int(alg_bytes)
     roof["flop"] = int(flop)
 

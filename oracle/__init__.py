@@ -51,6 +51,8 @@ def load(path: str) -> ctypes.CDLL:
     lib.oracle_spmm_f32.restype = ctypes.c_int
     lib.oracle_reorder.argtypes = [i32, i32, p, p, p]
     lib.oracle_reorder.restype = ctypes.c_int
+    lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_num_threads.restype = None
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     return lib
@@ -120,4 +122,9 @@ def reorder(row_ptr, col_idx, K, lib=None):
 
 def num_threads() -> int:
     return int(_lib().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """OpenMP threads of later oracle calls (timing only)."""
+    _lib().oracle_set_num_threads(int(n))
 

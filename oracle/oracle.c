@@ -177,3 +177,12 @@ int oracle_num_threads(void) {
   return 1;
 #endif
 }
+
+/* Sets the OpenMP thread count of later calls (n >= 1); for timing at chosen counts. */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}

@@ -1,4 +1,5 @@
-"""Builds libsdnn.so (the gfx950 HIP kernels + C ABI) in place with hipcc."""
+"""Builds libsdnn.so (the gfx950 HIP kernels + C ABI) and libsdnn_probes.so (the
+measurement probes of include/sdnn_probes.h) in place with hipcc."""
 from __future__ import annotations
 
 import os
@@ -8,6 +9,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(HERE, "libsdnn.so")
 SOURCES = [os.path.join(HERE, "csrc", "sdnn_host.cpp"), os.path.join(HERE, "csrc", "sdnn_kernels.hip")]
+PROBES_LIB = os.path.join(HERE, "libsdnn_probes.so")
+PROBES_SOURCES = [os.path.join(HERE, "csrc", "sdnn_probes.hip")]
 
 # -packed-fp32-ops: keep the compiler from forming packed FP32 instructions.
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-Wall",
@@ -29,15 +32,16 @@ def build(verbose: bool = False) -> str:
         gen_spmm_asm.main()
     finally:
         sys.path.pop(0)
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc()] + HIPCC_FLAGS + ["-o", tmp] + SOURCES
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("hipcc failed building libsdnn.so")
-    if verbose:
-        sys.stderr.write(res.stderr)
-    os.replace(tmp, LIB)
+    for lib, sources in ((LIB, SOURCES), (PROBES_LIB, PROBES_SOURCES)):
+        tmp = lib + ".tmp%d" % os.getpid()
+        cmd = [hipcc()] + HIPCC_FLAGS + ["-o", tmp] + sources
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            sys.stderr.write(res.stdout + res.stderr)
+            raise RuntimeError(f"hipcc failed building {os.path.basename(lib)}")
+        if verbose:
+            sys.stderr.write(res.stderr)
+        os.replace(tmp, lib)
     return LIB
 
 

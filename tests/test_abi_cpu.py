@@ -15,8 +15,8 @@ from conftest import ROOT, pattern_to_csr, load_reorder_examples
 from paper_2101_07948_amd import inputs
 
 
-def header_functions():
-    text = open(os.path.join(ROOT, "include", "sdnn.h")).read()
+def header_functions(header="sdnn.h"):
+    text = open(os.path.join(ROOT, "include", header)).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(sdnn_[a-z_]+)\s*\(", text)))
 
@@ -27,6 +27,17 @@ def test_library_exports_every_header_symbol():
     assert "sdnn_spmm" in names and "sdnn_plan_create" in names
     for n in names:
         assert hasattr(L, n), f"libsdnn.so does not export {n}"
+
+
+def test_probe_library_exports_every_header_symbol():
+    path = os.path.join(ROOT, "paper_2101_07948_amd", "libsdnn_probes.so")
+    L = ctypes.CDLL(path)
+    names = header_functions("sdnn_probes.h")
+    assert names == ["sdnn_probe_fma", "sdnn_probe_lds_read", "sdnn_probe_out_floats"]
+    for n in names:
+        assert hasattr(L, n), f"libsdnn_probes.so does not export {n}"
+    L.sdnn_probe_out_floats.restype = ctypes.c_int64
+    assert L.sdnn_probe_out_floats() == 256 * 1024
 
 
 def test_status_strings():
