@@ -292,13 +292,28 @@ def run_suite(out_path):
     flop = sum(2.0 * L.W.nnz * w.N for L in w.layers)
     for p_ in plans:
         p_.close()
+    # the same chain in permuted space: every activation stays in its producer's row
+    # order and the next plan takes that order as in_perm (the last writes the original)
+    plans, prev = [], None
+    for i, L in enumerate(w.layers):
+        last = i == len(w.layers) - 1
+        plans.append(sd.Plan.from_csr(L.W, out_permuted=not last, in_perm=prev))
+        prev = None if last else plans[-1].perm
+    forward(0)
+    torch.cuda.synchronize()
+    _, pmean = _launch_times(forward, 5)
+    for p_ in plans:
+        p_.close()
     lines += ["", "## C5: 12 encoder layers x 6 sparse products, chained (N = 16384)", "",
               f"* {len(w.layers)} products, {flop/1e9:.1f} GFLOP per forward; "
               f"{fmean:.2f} ms per forward = {flop/(fmean*1e-3)/1e12:.1f} TFLOP/s "
               f"(mean of 5 forwards after one warm-up, activations stay on the GPU).",
+              f"* In permuted space (each activation left in its producer's Algorithm 1 row "
+              f"order, the next plan built with in_perm): {pmean:.2f} ms per forward "
+              f"= {flop/(pmean*1e-3)/1e12:.1f} TFLOP/s.",
               f"* Preparation of the {len(w.layers)} plans (validation, Algorithm 1, two packings, "
               f"upload): {prep_s:.2f} s on the host."]
-    print("\n".join(lines[-3:]), flush=True)
+    print("\n".join(lines[-4:]), flush=True)
 
     # CPU oracle (fp32 CSR loop) at 1, 4 and all threads on W0 at N = 4096
     wl = inputs.workload("w0")

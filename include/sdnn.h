@@ -56,16 +56,28 @@ typedef enum {
   SDNN_EPI_GELU = 2  /* 0.5 * x * (1 + erf(x / sqrt(2))) */
 } sdnn_epilogue;
 
-/* Options for sdnn_plan_create; pass NULL for the defaults {0, 1}.
- *   panel_rows: rows per register panel.  0 (default) packs W twice, with short
- *               panels of 4 rows and tall panels of 12 rows, and sdnn_spmm picks per
- *               call: tall panels once a 256-column tile has at least a full
- *               workgroup of them per compute unit (M * ceil(N / 256) >= 96 * CUs),
- *               short panels otherwise.  4, 8, 12 or 16 packs that height only.
- *   permute:    1 = apply Algorithm 1 (default), 0 = identity order (ablation). */
+/* Options for sdnn_plan_create; pass NULL for the defaults {0, 1, 0, NULL}.
+ *   panel_rows:   rows per register panel.  0 (default) packs W twice, with short
+ *                 panels of 4 rows and tall panels of 12 rows, and sdnn_spmm picks per
+ *                 call: tall panels once a 256-column tile has at least a full
+ *                 workgroup of them per compute unit (M * ceil(N / 256) >= 96 * CUs),
+ *                 short panels otherwise.  4, 8, 12 or 16 packs that height only.
+ *   permute:      1 = apply Algorithm 1 (default), 0 = identity order (ablation).
+ *   out_permuted: 0 (default) = C row i is output row i; 1 = C is written in the
+ *                 plan's permuted row order, C row i = output row perm[i] (Sec. 3.1.2:
+ *                 the rows stay permuted and the next layer's columns compensate).
+ *                 The bias is always given in the original row order.
+ *   in_perm:      NULL (default) = B row c is input feature c; otherwise K int32 (host,
+ *                 read during the call only), a permutation of 0..K-1 giving the order
+ *                 of B's rows: B row i holds input feature in_perm[i].  Pass the
+ *                 previous layer's perm when that layer used out_permuted = 1.
+ *                 Not a permutation: SDNN_ERR_DIM. */
 typedef struct {
   int32_t panel_rows;
   int32_t permute;
+  int32_t out_permuted;
+  int32_t reserved;
+  const int32_t* in_perm;
 } sdnn_plan_opts;
 
 /* Plan statistics (of the first packing; the tall_* fields describe the second one,
@@ -83,6 +95,7 @@ typedef struct {
   int32_t panel_rows, k_chunk;
   int32_t tall_panel_rows, reserved;
   double tall_rho, tall_fill;
+  int32_t out_permuted, in_permuted;  /* the plan's options (in_permuted: in_perm given) */
 } sdnn_plan_info_t;
 
 /* Greedy weight-row permutation (Sec. 3.1.2, Algorithm 1), host only, no GPU needed.
@@ -125,6 +138,8 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out);
  *   C:    device, M x N row-major fp32, written once, in the ORIGINAL row order.
  *   N:    columns of B and C, any N >= 0 (N = 0 or M = 0 is a no-op).
  *   bias: device, M fp32 in original row order, or NULL (treated as zeros).
+ *   With out_permuted plans, C row i is output row perm[i] (see sdnn_plan_opts); with
+ *   in_perm plans, B's rows are in that order.
  * Asynchronous: no allocation, no synchronisation, no pointer retained.  A plan may
  * be used from several streams at once.  B must not overlap C or bias; the bias may
  * not overlap C (SDNN_ERR_DIM).  Device faults surface at the caller's next sync.

@@ -32,7 +32,9 @@ class SdnnError(RuntimeError):
 
 
 class PlanOpts(ctypes.Structure):
-    _fields_ = [("panel_rows", ctypes.c_int32), ("permute", ctypes.c_int32)]
+    _fields_ = [("panel_rows", ctypes.c_int32), ("permute", ctypes.c_int32),
+                ("out_permuted", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("in_perm", ctypes.c_void_p)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -41,7 +43,8 @@ class PlanInfo(ctypes.Structure):
                 ("rho", ctypes.c_double), ("fill", ctypes.c_double),
                 ("panel_rows", ctypes.c_int32), ("k_chunk", ctypes.c_int32),
                 ("tall_panel_rows", ctypes.c_int32), ("reserved", ctypes.c_int32),
-                ("tall_rho", ctypes.c_double), ("tall_fill", ctypes.c_double)]
+                ("tall_rho", ctypes.c_double), ("tall_fill", ctypes.c_double),
+                ("out_permuted", ctypes.c_int32), ("in_permuted", ctypes.c_int32)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -96,8 +99,14 @@ def _np_ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
-def _opts(panel_rows: int, permute: bool) -> PlanOpts:
-    return PlanOpts(int(panel_rows), 1 if permute else 0)
+def _opts(K: int, panel_rows: int, permute: bool, out_permuted: bool = False, in_perm=None):
+    """PlanOpts plus the in_perm array it points to (kept alive by the caller)."""
+    keep = None if in_perm is None else _i32(in_perm)
+    if keep is not None and keep.shape != (int(K),):
+        raise ValueError(f"in_perm must hold K = {K} entries, got shape {keep.shape}")
+    o = PlanOpts(int(panel_rows), 1 if permute else 0, 1 if out_permuted else 0, 0,
+                 None if keep is None else keep.ctypes.data)
+    return o, keep
 
 
 def reorder_rows(row_ptr, col_idx, K: int) -> np.ndarray:
@@ -111,11 +120,11 @@ def reorder_rows(row_ptr, col_idx, K: int) -> np.ndarray:
 
 
 def plan_check_host(row_ptr, col_idx, values, M: int, K: int, panel_rows: int = 0,
-                    permute: bool = True) -> dict:
+                    permute: bool = True, out_permuted: bool = False, in_perm=None) -> dict:
     """Host-only self-check of the preparation stage; returns the plan statistics."""
     row_ptr, col_idx, values = _i32(row_ptr), _i32(col_idx), _f32(values)
     info = PlanInfo()
-    o = _opts(panel_rows, permute)
+    o, _keep = _opts(K, panel_rows, permute, out_permuted, in_perm)
     _check(lib().sdnn_plan_check_host(_np_ptr(row_ptr), _np_ptr(col_idx), _np_ptr(values), M, K,
                                       ctypes.byref(o), ctypes.byref(info)),
            "sdnn_plan_check_host")
@@ -153,11 +162,14 @@ class Plan:
     """
 
     def __init__(self, row_ptr, col_idx, values, M: int, K: int, panel_rows: int = 0,
-                 permute: bool = True):
+                 permute: bool = True, out_permuted: bool = False, in_perm=None):
+        """out_permuted: write C in the plan's permuted row order (C[i] = output row
+        perm[i]); in_perm: the order of B's rows (B[i] = input feature in_perm[i]),
+        e.g. the previous layer's perm when that layer used out_permuted."""
         row_ptr, col_idx, values = _i32(row_ptr), _i32(col_idx), _f32(values)
         self.M, self.K = int(M), int(K)
         h = ctypes.c_void_p()
-        o = _opts(panel_rows, permute)
+        o, _keep = _opts(self.K, panel_rows, permute, out_permuted, in_perm)
         self._lib = lib()
         _check(self._lib.sdnn_plan_create(_np_ptr(row_ptr), _np_ptr(col_idx), _np_ptr(values),
                                           self.M, self.K, ctypes.byref(o), ctypes.byref(h)),

@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <utility>
 #include <new>
 #include <vector>
 
@@ -295,31 +296,85 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
   return true;
 }
 
+// Resolved plan options.
+struct Options {
+  std::vector<int32_t> rws;      // panel heights to pack
+  int32_t permute = 1;           // apply Algorithm 1
+  int32_t out_permuted = 0;      // store C in the permuted row order
+  const int32_t* in_perm = nullptr;  // order of B's rows (NULL: original)
+};
+
 // Panel heights to pack: the explicit option, or the short and tall defaults.
-static sdnn_status resolve_opts(const sdnn_plan_opts* opts, std::vector<int32_t>* rws,
-                                int32_t* permute) {
-  *rws = {kShortPanel, kTallPanel};
-  *permute = 1;
-  if (opts) {
-    if (opts->panel_rows != 0) {
-      if (opts->panel_rows != 4 && opts->panel_rows != 8 && opts->panel_rows != 12 &&
-          opts->panel_rows != 16)
-        return SDNN_ERR_DIM;
-      *rws = {opts->panel_rows};
+static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* o) {
+  o->rws = {kShortPanel, kTallPanel};
+  if (!opts) return SDNN_OK;
+  if (opts->panel_rows != 0) {
+    if (opts->panel_rows != 4 && opts->panel_rows != 8 && opts->panel_rows != 12 &&
+        opts->panel_rows != 16)
+      return SDNN_ERR_DIM;
+    o->rws = {opts->panel_rows};
+  }
+  if (opts->permute != 0 && opts->permute != 1) return SDNN_ERR_DIM;
+  if (opts->out_permuted != 0 && opts->out_permuted != 1) return SDNN_ERR_DIM;
+  o->permute = opts->permute;
+  o->out_permuted = opts->out_permuted;
+  o->in_perm = opts->in_perm;
+  if (o->in_perm) {  // must be a permutation of 0..K-1
+    std::vector<char> seen((size_t)std::max(K, 1), 0);
+    for (int32_t i = 0; i < K; ++i) {
+      const int32_t x = o->in_perm[i];
+      if (x < 0 || x >= K || seen[x]) return SDNN_ERR_DIM;
+      seen[x] = 1;
     }
-    if (opts->permute != 0 && opts->permute != 1) return SDNN_ERR_DIM;
-    *permute = opts->permute;
   }
   return SDNN_OK;
 }
 
-// Validation, Algorithm 1 (once) and one packing per panel height.
+// The CSR a plan packs: the caller's, or (with in_perm) the same rows with column c
+// renamed to its position in B's row order, pos[c] (in_perm[pos[c]] = c), re-sorted
+// within each row.  W'[r][pos[c]] = W[r][c] makes W' * B_given = W * B when
+// B_given[i] = B[in_perm[i]] (Sec. 3.1.2: the next layer's columns absorb the previous
+// layer's row permutation).
+struct CsrView {
+  const int32_t* row_ptr = nullptr;
+  const int32_t* col_idx = nullptr;
+  const float* values = nullptr;
+  std::vector<int32_t> cols;     // storage when relabelled
+  std::vector<float> vals;
+};
+
+static void relabel_columns(const int32_t* row_ptr, const int32_t* col_idx, const float* values,
+                            int32_t M, int32_t K, const int32_t* in_perm, CsrView* v) {
+  std::vector<int32_t> pos((size_t)std::max(K, 1));
+  for (int32_t i = 0; i < K; ++i) pos[in_perm[i]] = i;
+  const int64_t nnz = M ? row_ptr[M] : 0;
+  v->cols.resize((size_t)nnz);
+  v->vals.resize((size_t)nnz);
+  std::vector<std::pair<int32_t, float>> row;
+  for (int32_t r = 0; r < M; ++r) {
+    row.clear();
+    for (int32_t q = row_ptr[r]; q < row_ptr[r + 1]; ++q)
+      row.emplace_back(pos[col_idx[q]], values ? values[q] : 0.0f);
+    std::sort(row.begin(), row.end(),
+              [](const std::pair<int32_t, float>& a, const std::pair<int32_t, float>& b) {
+                return a.first < b.first;
+              });
+    for (size_t k = 0; k < row.size(); ++k) {
+      v->cols[(size_t)row_ptr[r] + k] = row[k].first;
+      v->vals[(size_t)row_ptr[r] + k] = row[k].second;
+    }
+  }
+  v->row_ptr = row_ptr;
+  v->col_idx = v->cols.data();
+  v->values = v->vals.data();
+}
+
+// Validation, column relabelling (with in_perm), Algorithm 1 (once: its keys do not
+// depend on column names) and one packing per panel height.  *csr is what was packed.
 static sdnn_status prepare(const int32_t* row_ptr, const int32_t* col_idx, const float* values,
                            int32_t M, int32_t K, const sdnn_plan_opts* opts,
-                           std::vector<Packed>* packs) {
-  std::vector<int32_t> rws;
-  int32_t permute;
-  sdnn_status st = resolve_opts(opts, &rws, &permute);
+                           std::vector<Packed>* packs, CsrView* csr, Options* o) {
+  sdnn_status st = resolve_opts(opts, K, o);
   if (st != SDNN_OK) return st;
   st = validate_csr(row_ptr, col_idx, M, K);
   if (st != SDNN_OK) return st;
@@ -327,18 +382,26 @@ static sdnn_status prepare(const int32_t* row_ptr, const int32_t* col_idx, const
   std::vector<int32_t> perm;
   try {
     perm.resize(M);
-    packs->assign(rws.size(), Packed());
+    packs->assign(o->rws.size(), Packed());
+    if (o->in_perm) {
+      relabel_columns(row_ptr, col_idx, values, M, K, o->in_perm, csr);
+    } else {
+      csr->row_ptr = row_ptr;
+      csr->col_idx = col_idx;
+      csr->values = values;
+    }
   } catch (const std::bad_alloc&) {
     return SDNN_ERR_ALLOC;
   }
-  if (permute) {
-    st = reorder_bitset(row_ptr, col_idx, M, K, perm.data());
+  if (o->permute) {
+    st = reorder_bitset(csr->row_ptr, csr->col_idx, M, K, perm.data());
     if (st != SDNN_OK) return st;
   } else {
     for (int32_t i = 0; i < M; ++i) perm[i] = i;
   }
-  for (size_t i = 0; i < rws.size(); ++i) {
-    st = pack(row_ptr, col_idx, values, M, K, rws[i], perm.data(), &(*packs)[i]);
+  for (size_t i = 0; i < o->rws.size(); ++i) {
+    st = pack(csr->row_ptr, csr->col_idx, csr->values, M, K, o->rws[i], perm.data(),
+              &(*packs)[i]);
     if (st != SDNN_OK) return st;
   }
   return SDNN_OK;
@@ -350,7 +413,7 @@ static double fill_of(const Packed& P) {
 
 // Statistics of the first packing, plus the tall one's if there is one.
 static void fill_info(const std::vector<Packed>& packs, int64_t packed_bytes,
-                      sdnn_plan_info_t* out) {
+                      const Options& o, sdnn_plan_info_t* out) {
   const Packed& P = packs[0];
   out->M = P.M;
   out->K = P.K;
@@ -366,6 +429,8 @@ static void fill_info(const std::vector<Packed>& packs, int64_t packed_bytes,
   out->reserved = 0;
   out->tall_rho = tall ? packs[1].rho : 0.0;
   out->tall_fill = tall ? fill_of(packs[1]) : 0.0;
+  out->out_permuted = o.out_permuted;
+  out->in_permuted = o.in_perm ? 1 : 0;
 }
 
 static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
@@ -414,14 +479,16 @@ sdnn_status sdnn_plan_check_host(const int32_t* row_ptr, const int32_t* col_idx,
                                  const sdnn_plan_opts* opts, sdnn_plan_info_t* info) {
   try {
     std::vector<Packed> packs;
-    sdnn_status st = prepare(row_ptr, col_idx, values, M, K, opts, &packs);
+    CsrView csr;
+    Options o;
+    sdnn_status st = prepare(row_ptr, col_idx, values, M, K, opts, &packs, &csr, &o);
     if (st != SDNN_OK) return st;
     int64_t bytes = 0;
     for (const Packed& P : packs) {
-      if (!check_packed(row_ptr, col_idx, values, P)) return SDNN_ERR_INTERNAL;
+      if (!check_packed(csr.row_ptr, csr.col_idx, csr.values, P)) return SDNN_ERR_INTERNAL;
       bytes += packing_bytes(P);
     }
-    if (info) fill_info(packs, bytes, info);
+    if (info) fill_info(packs, bytes, o, info);
     return SDNN_OK;
   } catch (...) {
     return SDNN_ERR_ALLOC;
@@ -435,7 +502,9 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
   sdnn_plan_s* plan = nullptr;
   try {
     std::vector<Packed> packs;
-    sdnn_status st = prepare(row_ptr, col_idx, values, M, K, opts, &packs);
+    CsrView csr;
+    Options o;
+    sdnn_status st = prepare(row_ptr, col_idx, values, M, K, opts, &packs, &csr, &o);
     if (st != SDNN_OK) return st;
 
     plan = new sdnn_plan_s();
@@ -455,6 +524,8 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
     plan->nnz = P0.nnz;
     plan->perm = P0.perm;
     plan->npack = (int)packs.size();
+    plan->out_permuted = o.out_permuted;
+    plan->in_permuted = o.in_perm ? 1 : 0;
 
     int64_t total = 0;
     for (const Packed& P : packs) total += packing_bytes(P);
@@ -536,6 +607,8 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out) {
   out->reserved = 0;
   out->tall_rho = tall ? p->pk[1].rho : 0.0;
   out->tall_fill = tall ? p->pk[1].fill : 0.0;
+  out->out_permuted = p->out_permuted;
+  out->in_permuted = p->in_permuted;
   return SDNN_OK;
 }
 

@@ -99,6 +99,8 @@ struct sdnn_plan_s {
   std::vector<int32_t> perm;
   void* d_mem = nullptr;       // one device allocation holding every packing's arrays
   int npack = 0;               // 1 (explicit panel height) or 2 (short, tall)
+  int32_t out_permuted = 0;    // C rows stored in the permuted order
+  int32_t in_permuted = 0;     // W's columns renamed to a caller-given order of B's rows
   sdnn::DevPacking pk[2];
 };
 

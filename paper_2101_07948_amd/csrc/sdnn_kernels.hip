@@ -92,6 +92,7 @@ struct SpmmArgs {
   int32_t total_wg;  // real workgroups (n_tiles * n_rb)
   int32_t per_xcd;   // launched grid / 8
   int32_t epi;
+  int32_t out_permuted;  // store permuted row i at row i instead of at its source row
 };
 
 // RW: rows per panel; VEC: N % 4 == 0 and B, C 16-byte aligned (16-byte staging DMA,
@@ -172,7 +173,7 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     const int orig = panel_rows[panel * RW + r];
     if (orig < 0) continue;
     const float bb = bias ? bias[orig] : 0.0f;
-    float* crow = C + (size_t)orig * a.N;
+    float* crow = C + (size_t)(a.out_permuted ? panel * RW + r : orig) * a.N;
     const float v[4] = {p0[r], p1[r], p2[r], p3[r]};
     if (VEC && ncol + 4 <= a.N) {
       *reinterpret_cast<float4*>(crow + ncol) =
@@ -286,6 +287,7 @@ hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N
   args.total_wg = (int32_t)total;
   args.per_xcd = (int32_t)(grid / 8);
   args.epi = epi;
+  args.out_permuted = p->out_permuted;
   // the 16-byte producer addresses a chunk's rows with 32-bit per-lane offsets
   // 16 * lane + r * 4N (r < kChunk / kProducers)
   const bool vec = (N % 4 == 0) && (((uintptr_t)B & 15) == 0) && (((uintptr_t)C & 15) == 0) &&

@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import paper_2101_07948_amd as sd
-from conftest import ROOT, pattern_to_csr, load_reorder_examples
+from conftest import ROOT, dense_to_csr, pattern_to_csr, load_reorder_examples
 from paper_2101_07948_amd import inputs
 
 
@@ -111,6 +111,57 @@ def test_default_plan_packs_short_and_tall_panels(name):
                                  panel_rows=12)
         assert one["tall_panel_rows"] == 0 and one["rho"] == info["tall_rho"]
         assert info["packed_bytes"] > one["packed_bytes"]
+
+
+def test_in_perm_relabels_columns():
+    """A plan told that B's rows arrive in the order in_perm (the previous layer's
+    permuted output, Sec. 3.1.2) packs W with column c renamed to its position in that
+    order; the packed stream passes its self-check against the renamed CSR, and the
+    statistics (panels, rho, fill) do not depend on column names."""
+    W = inputs.pattern_grouped8(256, 384, 0.05, inputs.CFG_TEST, 31, 0.05)
+    pi = np.random.default_rng(31).permutation(384).astype(np.int32)
+    base = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K)
+    got = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, in_perm=pi,
+                             out_permuted=True)
+    assert got["in_permuted"] == 1 and got["out_permuted"] == 1
+    assert base["in_permuted"] == 0 and base["out_permuted"] == 0
+    for k in ("panels", "rho", "tall_rho"):
+        assert got[k] == base[k]
+
+
+def test_algorithm1_ignores_column_names():
+    """Algorithm 1's keys (overlap with the last placed row, nnz, index) are invariant
+    under renaming columns, so a plan built on B's permuted row order keeps the
+    permutation of the original matrix."""
+    W = inputs.pattern_grouped8(200, 320, 0.06, inputs.CFG_TEST, 32, 0.05)
+    pi = np.random.default_rng(32).permutation(320)
+    Wd = W.to_dense()
+    rp, ci, v = dense_to_csr(Wd[:, pi])        # column i of W' is column pi[i] of W
+    assert np.array_equal(oracle.reorder(rp, ci, 320), oracle.reorder(W.row_ptr, W.col_idx, 320))
+    assert np.array_equal(sd.reorder_rows(rp, ci, 320), sd.reorder_rows(W.row_ptr, W.col_idx, 320))
+
+
+def test_bad_permutation_options_rejected():
+    W = inputs.pattern_uniform(64, 96, 0.1, inputs.CFG_TEST, 33, 0.05)
+    bad = np.arange(96, dtype=np.int32)
+    bad[5] = 6  # duplicate
+    with pytest.raises(sd.SdnnError) as e:
+        sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, in_perm=bad)
+    assert e.value.code == 2
+    bad = np.arange(96, dtype=np.int32)
+    bad[0] = 96  # out of range
+    with pytest.raises(sd.SdnnError) as e:
+        sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, in_perm=bad)
+    assert e.value.code == 2
+    with pytest.raises(ValueError):
+        sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, in_perm=np.arange(95))
+    o = sd.PlanOpts(0, 1, 2, 0, None)
+    info = sd.PlanInfo()
+    L = sd.lib()
+    rc = L.sdnn_plan_check_host(W.row_ptr.ctypes.data, W.col_idx.ctypes.data,
+                                W.values.ctypes.data, W.M, W.K, ctypes.byref(o),
+                                ctypes.byref(info))
+    assert rc == 2
 
 
 def test_permutation_raises_reuse_on_grouped_columns():

@@ -199,6 +199,50 @@ def test_tall_panels_at_large_N():
     assert np.array_equal(got, short)
 
 
+def test_out_permuted_writes_rows_in_plan_order():
+    """out_permuted only moves the store: C row i is output row perm[i], bit for bit."""
+    W = inputs.pattern_uniform(300, 500, 0.1, inputs.CFG_TEST, 41, 0.05)
+    B = inputs.dense_B(500, 643, inputs.CFG_TEST, 41)
+    bias = inputs.bias_normal(300, inputs.CFG_TEST, 41, 0.02)
+    with sd.Plan.from_csr(W) as p0, sd.Plan.from_csr(W, out_permuted=True) as p1:
+        assert p1.info["out_permuted"] == 1
+        assert np.array_equal(p1.perm, p0.perm)
+        C0 = gpu_spmm(p0, B, bias, "gelu")
+        C1 = gpu_spmm(p1, B, bias, "gelu")
+        assert np.array_equal(C1, C0[p1.perm])
+
+
+@pytest.mark.parametrize("N", [1024, 16384])
+def test_chain_in_permuted_space(N):
+    """Cross-layer compensation (Sec. 3.1.2): C5's first encoder layer chained with every
+    intermediate activation left in its producer's row order; each plan takes the
+    previous plan's perm as in_perm, the last one writes the original order.  Each layer
+    is checked against the oracle on the un-permuted input, rows permuted as stored."""
+    w = inputs.workload("c5", N=N, num_layers=1)
+    X = torch.from_numpy(w.B).to(DEV)
+    prev = None
+    for i, L in enumerate(w.layers):
+        last = i == len(w.layers) - 1
+        with sd.Plan.from_csr(L.W, out_permuted=not last, in_perm=prev) as plan:
+            Y = torch.full((L.W.M, N), float("nan"), device=DEV)
+            bt = None if L.bias is None else torch.from_numpy(L.bias).to(DEV)
+            plan.spmm(X, Y, bt, L.epi)
+            torch.cuda.synchronize()
+            x = X.cpu().numpy()
+            x_orig = x if prev is None else np.empty_like(x)
+            if prev is not None:
+                x_orig[prev] = x          # B row j holds input feature prev[j]
+            ref, bound = oracle.spmm_f64(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.K, x_orig,
+                                         L.bias, L.epi)
+            order = np.arange(L.W.M) if last else plan.perm
+            got = Y.cpu().numpy().astype(np.float64)
+            err = np.abs(got - ref[order])
+            tol = tolerance(bound[order], ref[order], L.epi)
+            assert not (~(err <= tol)).any(), f"layer {i}: worst err/tol {np.nanmax(err / tol):.3g}"
+            prev = None if last else plan.perm
+        X = Y
+
+
 def test_permute_off_and_on_agree():
     W = inputs.pattern_grouped8(256, 512, 0.05, inputs.CFG_TEST, 9, 0.05)
     B = inputs.dense_B(512, 256, inputs.CFG_TEST, 9)
