@@ -13,6 +13,9 @@ Functions (each cites the passage of the paper it follows):
 * :func:`spmm_f32` -- the same loops with a float accumulator (timed CPU baseline).
 * :func:`reorder` -- Algorithm 1 of Sec. 3.1.2 (greedy weight-row permutation) with
   the tie-break reading (overlap desc, nonzero count desc, row index asc).
+* :func:`conv3x3_f64` -- the sparse 3x3 convolution of Sec. 3.2.3 (stride 1, zero
+  padding 1, the paper's benchmark setting of Sec. 4.1) by its definition, in double;
+  filters as an OC x (IC*9) CSR (column ``i*9 + ky*3 + kx``), activations IC x H x W x NB.
 """
 from __future__ import annotations
 
@@ -51,6 +54,8 @@ def load(path: str) -> ctypes.CDLL:
     lib.oracle_spmm_f32.restype = ctypes.c_int
     lib.oracle_reorder.argtypes = [i32, i32, p, p, p]
     lib.oracle_reorder.restype = ctypes.c_int
+    lib.oracle_conv3x3_f64.argtypes = [i32, i32, i32, i32, i32, p, p, p, p, p, i32, p, p]
+    lib.oracle_conv3x3_f64.restype = ctypes.c_int
     lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
     lib.oracle_set_num_threads.restype = None
     lib.oracle_num_threads.argtypes = []
@@ -107,6 +112,23 @@ def spmm_f32(row_ptr, col_idx, values, K, B, bias=None, epi="none", out=None, li
     _lib(lib).oracle_spmm_f32(M, K, N, _ptr(row_ptr), _ptr(col_idx), _ptr(values), _ptr(B),
                            _ptr(bias), EPI[epi], _ptr(C))
     return C
+
+
+def conv3x3_f64(row_ptr, col_idx, values, X, bias=None, epi="none", with_bound=True, lib=None):
+    """Reference sparse 3x3 convolution (stride 1, zero padding 1) in double.  ``X`` is
+    (IC, H, W, NB); the filters are an OC x (IC*9) CSR.  Returns ``(C, bound)`` of shape
+    (OC, H, W, NB); ``bound`` is ``sum |w| |x|`` over the taps (None if not asked)."""
+    row_ptr, col_idx, values = _csr(row_ptr, col_idx, values)
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    IC, H, W, NB = (int(d) for d in X.shape)
+    OC = row_ptr.shape[0] - 1
+    assert col_idx.size == 0 or int(col_idx.max()) < IC * 9
+    bias = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    C = np.empty((OC, H, W, NB), dtype=np.float64)
+    bound = np.empty((OC, H, W, NB), dtype=np.float64) if with_bound else None
+    _lib(lib).oracle_conv3x3_f64(OC, IC, H, W, NB, _ptr(row_ptr), _ptr(col_idx), _ptr(values),
+                                 _ptr(X), _ptr(bias), EPI[epi], _ptr(C), _ptr(bound))
+    return C, bound
 
 
 def reorder(row_ptr, col_idx, K, lib=None):

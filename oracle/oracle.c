@@ -21,6 +21,17 @@
  *                    order; it is the CPU baseline that the benchmark times.  No
  *                    blocking, no intrinsics, no BLAS; OpenMP splits rows only.
  *
+ *   oracle_conv3x3_f64  The sparse 3x3 convolution of Sec. 3.2.3 (stride 1, zero padding
+ *                    of 1, as in the paper's convolution benchmark, Sec. 4.1) by its
+ *                    definition: for output channel o, pixel (y, x) and image b,
+ *                        C[o][y][x][b] = act( sum over the stored filter taps (i, ky, kx)
+ *                            of filter o of  w * X[i][y + ky - 1][x + kx - 1][b]
+ *                            (zero outside the image)  + bias[o] )
+ *                    in double.  The filters are an OC x (IC * 9) CSR whose column is
+ *                    i * 9 + ky * 3 + kx (the paper's OC by IC x Fx x Fy filter matrix);
+ *                    activations are IC x H x W x NB (channel, row, column, image).
+ *                    Also returns sum |w * x| per output element.
+ *
  *   oracle_reorder   The greedy weight-row permutation of Sec. 3.1.2 (Algorithm 1):
  *                    the first row is the one with the most nonzeros, and each next
  *                    row is the remaining row whose nonzero column set overlaps most
@@ -105,6 +116,38 @@ int oracle_spmm_f32(int32_t M, int32_t K, int32_t N, const int32_t* row_ptr,
     }
     const float bi = bias ? bias[i] : 0.0f;
     for (int32_t n = 0; n < N; ++n) acc[n] = act_f32(acc[n] + bi, epi);
+  }
+  return 0;
+}
+
+/* Sparse 3x3 convolution, stride 1, padding 1, by its definition (see the header).
+ * X is IC x H x W x NB, C_out and bound_out are OC x H x W x NB doubles.  Returns 0. */
+int oracle_conv3x3_f64(int32_t OC, int32_t IC, int32_t H, int32_t W, int32_t NB,
+                       const int32_t* row_ptr, const int32_t* col_idx, const float* values,
+                       const float* X, const float* bias, int32_t epi, double* C_out,
+                       double* bound_out) {
+  (void)IC;
+  const size_t plane = (size_t)H * W * NB;
+#pragma omp parallel for schedule(static)
+  for (int32_t o = 0; o < OC; ++o) {
+    const double bo = bias ? (double)bias[o] : 0.0;
+    for (int32_t y = 0; y < H; ++y)
+      for (int32_t x = 0; x < W; ++x)
+        for (int32_t b = 0; b < NB; ++b) {
+          double acc = 0.0, bnd = 0.0;
+          for (int32_t p = row_ptr[o]; p < row_ptr[o + 1]; ++p) {
+            const int32_t tap = col_idx[p];
+            const int32_t i = tap / 9, ky = (tap % 9) / 3, kx = tap % 3;
+            int32_t yy = y + ky - 1, xx = x + kx - 1;
+            if (yy < 0 || yy >= H || xx < 0 || xx >= W) continue;
+            const double t = (double)values[p] * (double)X[i * plane + ((size_t)yy * W + xx) * NB + b];
+            acc += t;
+            bnd += fabs(t);
+          }
+          const size_t at = (size_t)o * plane + ((size_t)y * W + x) * NB + b;
+          C_out[at] = act_f64(acc + bo, epi);
+          if (bound_out) bound_out[at] = bnd;
+        }
   }
   return 0;
 }

@@ -200,8 +200,91 @@ def check_reorder(lib=None):
     return fails
 
 
+def _conv_filters(rng, OC, IC, density):
+    """Random sparse 3x3 filters as (CSR over columns i*9 + ky*3 + kx, dense OC x IC x 3 x 3)."""
+    F = rng.standard_normal((OC, IC, 3, 3)).astype(np.float32)
+    F[rng.random(F.shape) >= density] = 0.0
+    rp, ci, v = dense_to_csr(F.reshape(OC, IC * 9))
+    return rp, ci, v, F
+
+
+def _conv_numpy(F, X):
+    """Zero-padded 3x3 convolution by slicing a padded copy (NumPy float64)."""
+    IC, H, W, NB = X.shape
+    Xp = np.pad(X.astype(np.float64), ((0, 0), (1, 1), (1, 1), (0, 0)))
+    out = np.zeros((F.shape[0], H, W, NB))
+    for ky in range(3):
+        for kx in range(3):
+            win = Xp[:, ky:ky + H, kx:kx + W, :]            # X[i][y+ky-1][x+kx-1][b]
+            out += np.einsum("oi,iyxb->oyxb", F[:, :, ky, kx].astype(np.float64), win)
+    return out
+
+
+def check_conv(lib=None):
+    """Sparse 3x3 convolution (stride 1, padding 1) against: a padded-slice NumPy
+    convolution on random tiny shapes (values and the |w||x| bound); all-ones filters on
+    an all-ones input (4, 6 or 9 taps in range, times IC); a centre-tap-only filter,
+    which is the pointwise product W_c @ X (the SpMM reference, bit for bit); and a
+    one-hot input, which places the filter taps mirrored around the hot pixel."""
+    fails = []
+    rng = np.random.default_rng(2024)
+    for trial in range(40):
+        OC, IC = (int(v) for v in rng.integers(1, 6, size=2))
+        H, W = (int(v) for v in rng.integers(1, 7, size=2))
+        NB = int(rng.integers(1, 5))
+        epi = ["none", "relu", "gelu"][trial % 3]
+        rp, ci, v, F = _conv_filters(rng, OC, IC, [0.1, 0.5, 1.0][trial % 3])
+        X = rng.standard_normal((IC, H, W, NB)).astype(np.float32)
+        bias = rng.standard_normal(OC).astype(np.float32) if trial % 2 else None
+        C, bound = oracle.conv3x3_f64(rp, ci, v, X, bias, epi, lib=lib)
+        ref = _conv_numpy(F, X)
+        if bias is not None:
+            ref = ref + bias.astype(np.float64)[:, None, None, None]
+        ref = _act_np(ref, epi)
+        ref_bound = _conv_numpy(np.abs(F), np.abs(X))
+        if not np.all(np.abs(C - ref) <= 1e-12 * (ref_bound + np.abs(ref) + 1.0)):
+            fails.append(f"conv value mismatch OC={OC} IC={IC} H={H} W={W} NB={NB} {epi}")
+        if not np.all(np.abs(bound - ref_bound) <= 1e-12 * (ref_bound + 1.0)):
+            fails.append(f"conv bound mismatch OC={OC} IC={IC} H={H} W={W}")
+    # all-ones: every in-range tap contributes 1 per input channel
+    for H, W, IC in ((1, 1, 2), (2, 5, 3), (4, 4, 1), (6, 3, 2)):
+        rp, ci, v = dense_to_csr(np.ones((2, IC * 9), np.float32))
+        C, _ = oracle.conv3x3_f64(rp, ci, v, np.ones((IC, H, W, 2), np.float32), lib=lib)
+        ny = np.array([min(H - 1, y + 1) - max(0, y - 1) + 1 for y in range(H)])
+        nx = np.array([min(W - 1, x + 1) - max(0, x - 1) + 1 for x in range(W)])
+        want = IC * ny[:, None] * nx[None, :]
+        if not all(np.array_equal(C[o, :, :, b], want) for o in range(2) for b in range(2)):
+            fails.append(f"all-ones conv != in-range tap count x IC (H={H} W={W})")
+    # centre tap only: a pointwise product
+    OC, IC, H, W, NB = 4, 3, 5, 4, 3
+    Wc = rng.standard_normal((OC, IC)).astype(np.float32)
+    F = np.zeros((OC, IC, 3, 3), np.float32)
+    F[:, :, 1, 1] = Wc
+    rp, ci, v = dense_to_csr(F.reshape(OC, IC * 9))
+    X = rng.standard_normal((IC, H, W, NB)).astype(np.float32)
+    C, _ = oracle.conv3x3_f64(rp, ci, v, X, lib=lib)
+    rp1, ci1, v1 = dense_to_csr(Wc)
+    P, _ = oracle.spmm_f64(rp1, ci1, v1, IC, X.reshape(IC, -1))
+    if not np.array_equal(C.reshape(OC, -1), P):
+        fails.append("centre-tap conv != pointwise product")
+    # one-hot input at (i0, y0, x0, b0): C[o][y][x][b0] = F[o][i0][y0 - y + 1][x0 - x + 1]
+    OC, IC, H, W, NB = 3, 2, 5, 6, 2
+    rp, ci, v, F = _conv_filters(rng, OC, IC, 1.0)
+    i0, y0, x0, b0 = 1, 2, 3, 1
+    X = np.zeros((IC, H, W, NB), np.float32)
+    X[i0, y0, x0, b0] = 1.0
+    C, _ = oracle.conv3x3_f64(rp, ci, v, X, lib=lib)
+    want = np.zeros((OC, H, W, NB))
+    for y in range(y0 - 1, y0 + 2):
+        for x in range(x0 - 1, x0 + 2):
+            want[:, y, x, b0] = F[:, i0, y0 - y + 1, x0 - x + 1]
+    if not np.array_equal(C, want):
+        fails.append("one-hot conv does not place the mirrored filter taps")
+    return fails
+
+
 ALL_CHECKS = [check_bruteforce, check_special_cases, check_gelu_table, check_invariants,
-              check_reorder]
+              check_reorder, check_conv]
 
 
 def run_all(lib=None):

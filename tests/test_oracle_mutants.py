@@ -35,6 +35,14 @@ MUTANTS = [
     ("reorder_last_index_ties", "(ov == best_ov && xn > best_nnz)", "(ov == best_ov && xn >= best_nnz)"),
     ("reorder_merge_wrong_advance", "} else if (a[i] < b[j]) {", "} else if (a[i] > b[j]) {"),
     ("reorder_fewest_overlap", "if (ov > best_ov ||", "if (best_ov < 0 || ov < best_ov ||"),
+    ("conv_flipped_rows", "int32_t yy = y + ky - 1, xx = x + kx - 1;",
+     "int32_t yy = y - ky + 1, xx = x + kx - 1;"),
+    ("conv_swapped_taps", "const int32_t i = tap / 9, ky = (tap % 9) / 3, kx = tap % 3;",
+     "const int32_t i = tap / 9, ky = tap % 3, kx = (tap % 9) / 3;"),
+    ("conv_clamped_border", "if (yy < 0 || yy >= H || xx < 0 || xx >= W) continue;",
+     "if (yy < 0 || yy >= H || xx < 0 || xx >= W) { yy = yy < 0 ? 0 : (yy >= H ? H - 1 : yy); xx = xx < 0 ? 0 : (xx >= W ? W - 1 : xx); }"),
+    ("conv_bias_dropped", "C_out[at] = act_f64(acc + bo, epi);", "C_out[at] = act_f64(acc, epi);"),
+    ("conv_first_image", "X[i * plane + ((size_t)yy * W + xx) * NB + b]", "X[i * plane + ((size_t)yy * W + xx) * NB]"),
 ]
 
 
