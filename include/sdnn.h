@@ -147,6 +147,27 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out);
 sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
                       sdnn_epilogue epi, void* stream);
 
+/* Sparse 3x3 convolution, stride 1, zero padding 1 (Sec. 3.2.3: direct convolution as
+ * an SpMM whose dense operand is a virtual matrix built on the fly from the input; the
+ * paper's convolution benchmark, Sec. 4.1, uses this filter size and padding):
+ *     C[o][y][x][b] = act( sum_{i,ky,kx} F[o][i][ky][kx] * X[i][y+ky-1][x+kx-1][b]
+ *                          + bias[o] )       (X is zero outside the image)
+ *   p:    a plan created from the filters as an OC x (IC * 9) CSR whose column is
+ *         i * 9 + ky * 3 + kx (M = OC, K = IC * 9), without in_perm.
+ *   X:    device, IC x H x W x NB fp32 (channel, image row, image column, image),
+ *         16-byte aligned, read only.
+ *   C:    device, OC x H x W x NB fp32, same layout (a following layer takes it as its
+ *         X), 16-byte aligned; with an out_permuted plan its channels are in perm order.
+ *   NB:   images per call, a multiple of 4 (a lane's four columns are four images of
+ *         one pixel).  H = 0, W = 0 or NB = 0 is a no-op.
+ *   bias: device, OC fp32, or NULL.
+ * Same stream, allocation and concurrency semantics as sdnn_spmm.
+ * Errors: SDNN_ERR_NULL; SDNN_ERR_DIM (K not a multiple of 9, in_perm plan, NB % 4 != 0,
+ * misaligned or overlapping buffers, H * W * NB * 4 >= 2^31); SDNN_ERR_DEVICE;
+ * SDNN_ERR_HIP. */
+sdnn_status sdnn_conv3x3(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
+                         int32_t NB, const float* bias, sdnn_epilogue epi, void* stream);
+
 /* Frees the plan and its device memory.  NULL is a no-op. */
 void sdnn_plan_destroy(sdnn_plan p);
 

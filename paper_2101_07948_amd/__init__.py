@@ -75,8 +75,10 @@ def lib() -> ctypes.CDLL:
         L.sdnn_plan_destroy.argtypes = [p]
         L.sdnn_plan_destroy.restype = None
         L.sdnn_dense_gemm.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
+        L.sdnn_conv3x3.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
         for fn in ("sdnn_reorder_rows", "sdnn_plan_check_host", "sdnn_plan_create",
-                   "sdnn_plan_get_perm", "sdnn_plan_info", "sdnn_spmm", "sdnn_dense_gemm"):
+                   "sdnn_plan_get_perm", "sdnn_plan_info", "sdnn_spmm", "sdnn_dense_gemm",
+                   "sdnn_conv3x3"):
             getattr(L, fn).restype = ctypes.c_int
         _lib_handle = L
     return _lib_handle
@@ -197,6 +199,22 @@ class Plan:
         info = PlanInfo()
         _check(self._lib.sdnn_plan_info(self.handle, ctypes.byref(info)), "sdnn_plan_info")
         return info.as_dict()
+
+    def conv3x3(self, X, C, bias=None, epi: str = "none", stream=None):
+        """Sparse 3x3 convolution (stride 1, padding 1) on the GPU: the plan holds the
+        filters as an OC x (IC*9) CSR (column i*9 + ky*3 + kx); X is (IC, H, W, NB) and C
+        is (OC, H, W, NB), both contiguous fp32 on the device; NB % 4 == 0."""
+        if X.dim() != 4 or C.dim() != 4:
+            raise ValueError("X and C must be 4-d (channels, H, W, images)")
+        IC, H, W, NB = (int(d) for d in X.shape)
+        if IC * 9 != self.K:
+            raise ValueError(f"X has {IC} channels; the plan's K = {self.K} needs {self.K // 9}")
+        px = _dev_ptr(X, "X", (IC, H, W, NB))
+        pc = _dev_ptr(C, "C", (self.M, H, W, NB))
+        pbias = _dev_ptr(bias, "bias", (self.M,), allow_none=True)
+        _check(self._lib.sdnn_conv3x3(self.handle, px, pc, H, W, NB, pbias, EPI[epi],
+                                      _stream_handle(stream)), "sdnn_conv3x3")
+        return C
 
     def spmm(self, B, C, bias=None, epi: str = "none", stream=None):
         """C = act(W @ B + bias) on the GPU, enqueued on `stream` (default: current)."""

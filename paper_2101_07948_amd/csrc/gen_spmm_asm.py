@@ -307,17 +307,99 @@ def issue_rows_clamped(vec, half):
     return L
 
 
-def producer(vec):
-    """Producer loop.  State: issued (chunks whose loads went out), landed (chunks
-    published in the ready word), in flight = issued - landed <= PMAX, and the cached
-    issue limit PLIM (re-read from the progress words only when issued reaches it).
-    Chunks below PLAST take the fast path: the chunk's base address advances by
-    CHUNK rows per chunk and row r adds the lane's precomputed VGPR offset
+# conv producer SGPRs: tap of the current row, LDS row address, 64-bit temps
+PIC, PKY, PKX, PRL, PDL, PMT, PMU = 66, 67, 68, 69, 70, 72, 74
+VZ, VA = 36, 32        # conv producer: v[36:39] zeros, v32 LDS address of a zero fill
+CONV_OPERANDS = (
+    ',\n        [rstep] "s"(a.row_step), [cstep] "s"(a.col_step),'
+    ' [c0step] "s"(a.row_step + a.col_step),\n'
+    '        [plane] "s"(a.plane_bytes), [ic] "s"(a.in_channels), [vn] "v"(a.col_bytes),\n'
+    '        [r0] "s"(a.rowmask[0]), [r1] "s"(a.rowmask[1]), [r2] "s"(a.rowmask[2]),\n'
+    '        [c0] "s"(a.colmask[0]), [c1] "s"(a.colmask[1]), [c2] "s"(a.colmask[2])')
+
+
+def issue_rows_conv(half):
+    """Stage rows k0 .. k0+half-1 of the virtual B of a 3x3 convolution (stride 1,
+    padding 1).  Row k is input channel k / 9 shifted by tap (ky, kx) = ((k % 9) / 3,
+    k % 3): lane l's four columns n = n0 + 4l .. n0 + 4l + 3 are four images of one pixel
+    (y, x), so they come from X + ic * plane + (n + ((ky-1) * W + (kx-1)) * NB) * 4, one
+    16-byte segment, when (y + ky - 1, x + kx - 1) lies in the image, and are zero
+    otherwise.  Valid lanes: the DMA (exec = live & rowmask[ky] & colmask[kx]); invalid
+    live lanes: a ds_write of zeros to the same LDS row.  Rows past K re-stage the last
+    row.  Before the first row PIC/PKY/PKX hold the tap of row k0."""
+    L = []
+    for r in range(half):
+        L += [
+            # row address: X + ic * plane + ((ky - 1) * W + (kx - 1)) * NB * 4
+            f"s_mul_i32 s{PDL}, s{PKY}, %[rstep]",
+            f"s_mul_i32 s{PTMP}, s{PKX}, %[cstep]",
+            f"s_add_u32 s{PDL}, s{PDL}, s{PTMP}",
+            f"s_sub_u32 s{PDL}, s{PDL}, %[c0step]",
+            f"s_ashr_i32 s{PDL + 1}, s{PDL}, 31",
+            f"s_mul_i32 s{PADDR}, s{PIC}, %[plane]",
+            f"s_mul_hi_u32 s{PADDR + 1}, s{PIC}, %[plane]",
+            f"s_add_u32 s{PADDR}, s{PADDR}, s{PDL}",
+            f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, s{PDL + 1}",
+            f"s_add_u32 s{PADDR}, s{PADDR}, %[bb_lo]",
+            f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, %[bb_hi]",
+            # lanes whose source pixel lies in the image
+            f"s_cmp_eq_u32 s{PKY}, 0",
+            f"s_cselect_b64 s[{PMT}:{PMT + 1}], %[r0], %[r1]",
+            f"s_cmp_eq_u32 s{PKY}, 2",
+            f"s_cselect_b64 s[{PMT}:{PMT + 1}], %[r2], s[{PMT}:{PMT + 1}]",
+            f"s_cmp_eq_u32 s{PKX}, 0",
+            f"s_cselect_b64 s[{PMU}:{PMU + 1}], %[c0], %[c1]",
+            f"s_cmp_eq_u32 s{PKX}, 2",
+            f"s_cselect_b64 s[{PMU}:{PMU + 1}], %[c2], s[{PMU}:{PMU + 1}]",
+            f"s_and_b64 s[{PMT}:{PMT + 1}], s[{PMT}:{PMT + 1}], s[{PMU}:{PMU + 1}]",
+            f"s_and_b64 s[{PMT}:{PMT + 1}], s[{PMT}:{PMT + 1}], s[{PCM}:{PCM + 1}]",
+            # live lanes outside the image: zeros
+            f"s_andn2_b64 exec, s[{PCM}:{PCM + 1}], s[{PMT}:{PMT + 1}]",
+            f"s_cbranch_execz .L%=_cz{r}",
+            f"v_add_u32 v{VA}, s{PRL}, %[vl]",
+            f"ds_write_b128 v{VA}, v[{VZ}:{VZ + 3}]",
+            f".L%=_cz{r}:",
+            f"s_mov_b64 exec, s[{PMT}:{PMT + 1}]",
+            f"s_cbranch_execz .L%=_cd{r}",
+            f"global_load_lds_dwordx4 %[vn], s[{PADDR}:{PADDR + 1}]",
+            f".L%=_cd{r}:",
+            f"s_add_u32 s{PRL}, s{PRL}, 0x400",
+            f"s_mov_b32 m0, s{PRL}",
+            # next tap; past the last input channel keep re-staging its last row
+            f"s_add_u32 s{PKX}, s{PKX}, 1",
+            f"s_cmp_eq_u32 s{PKX}, 3",
+            f"s_cselect_b32 s{PKX}, 0, s{PKX}",
+            f"s_cselect_b32 s{PTMP}, 1, 0",
+            f"s_add_u32 s{PKY}, s{PKY}, s{PTMP}",
+            f"s_cmp_eq_u32 s{PKY}, 3",
+            f"s_cselect_b32 s{PKY}, 0, s{PKY}",
+            f"s_cselect_b32 s{PTMP}, 1, 0",
+            f"s_add_u32 s{PIC}, s{PIC}, s{PTMP}",
+            f"s_cmp_ge_u32 s{PIC}, %[ic]",
+            f"s_cbranch_scc0 .L%=_cn{r}",
+            f"s_sub_u32 s{PIC}, %[ic], 1",
+            f"s_mov_b32 s{PKY}, 2",
+            f"s_mov_b32 s{PKX}, 2",
+            f".L%=_cn{r}:",
+        ]
+    return L
+
+
+def producer(kind):
+    """Producer loop (kind: "vec" 16-byte rows, "dword" 4-byte pieces, "conv" the virtual
+    B of a 3x3 convolution).  State: issued (chunks whose loads went out), landed
+    (chunks published in the ready word), in flight = issued - landed <= PMAX, and the
+    cached issue limit PLIM (re-read from the progress words only when issued reaches
+    it).  vec: chunks below PLAST take the fast path: the chunk's base address advances
+    by CHUNK rows per chunk and row r adds the lane's precomputed VGPR offset
     16 * lane + r * row_bytes, so each row is one DMA and one m0 step.  The last chunk
     when K is not a multiple of CHUNK, and every chunk of the 4-byte variant, take the
-    clamped path, which re-stages row K-1 for rows past K (LDS rows no entry reads)."""
+    clamped path, which re-stages row K-1 for rows past K (LDS rows no entry reads).
+    conv: one chunk in flight (a row may issue no DMA, so landing waits for all loads)."""
+    vec = kind in ("vec", "conv")
+    conv = kind == "conv"
     half = CHUNK // NPROD
-    pmax = PMAX_VEC if vec else PMAX_DWORD
+    pmax = 1 if conv else (PMAX_VEC if vec else PMAX_DWORD)
     loads_per_chunk = half if vec else 4 * half
     assert loads_per_chunk * (pmax - 1) <= 63
     lg_chunk = CHUNK.bit_length() - 1
@@ -337,7 +419,7 @@ def producer(vec):
         f"s_lshl_b32 s{PCS}, %[rs], {lg_chunk}",
         f"s_lshr_b32 s{PCS + 1}, %[rs], {32 - lg_chunk}",
     ]
-    if vec:  # PLAST = nch - 1 if K % CHUNK else nch
+    if kind == "vec":  # PLAST = nch - 1 if K % CHUNK else nch
         L += [f"s_and_b32 s{PTMP}, %[K], {CHUNK - 1}",
               f"s_sub_u32 s{PLAST}, %[nch], 1",
               f"s_cmp_eq_u32 s{PTMP}, 0",
@@ -347,6 +429,8 @@ def producer(vec):
             L.append(f"v_add_u32 v{VO + r}, %[rs], v{VO + r - 1}")
     else:
         L.append(f"s_mov_b32 s{PLAST}, 0")
+    if conv:
+        L += [f"v_mov_b32 v{VZ + q}, 0" for q in range(4)]
     # column masks: vec -> lanes whose 4 columns exist (lane < ncol / 4);
     # dword -> piece q of a row: lanes with 64 q + lane < ncol
     pieces = 1 if vec else 4
@@ -392,21 +476,43 @@ def producer(vec):
         "s_lshl_b32 m0, %[prow0], 10",
         f"s_add_u32 m0, m0, s{PTMP}",
         f"s_mov_b64 s[{PEX}:{PEX + 1}], exec",
-        f"s_cmp_lt_u32 s{PISS}, s{PLAST}",
-        "s_cbranch_scc0 .L%=_clamped",
     ]
-    if vec:
-        L.append(f"s_mov_b64 exec, s[{PCM}:{PCM + 1}]")   # also spaces the m0 write from the DMA
-        for r in range(half):
-            if r:
-                L.append("s_nop 0")                       # m0 write, then a DMA reading it
-            L += [f"global_load_lds_dwordx4 v{VO + r}, s[{PBASE}:{PBASE + 1}]",
-                  "s_add_u32 m0, m0, 0x400"]
+    if conv:
+        # tap of row k0 = issued * CHUNK + prow0 (k0 / 9 by a multiply-high), clamped
+        # to the last row when k0 >= K
+        L += [
+            f"s_mov_b32 s{PRL}, m0",
+            f"s_lshl_b32 s{PTMP}, s{PISS}, {lg_chunk}",
+            f"s_add_u32 s{PTMP}, s{PTMP}, %[prow0]",
+            f"s_min_u32 s{PTMP}, s{PTMP}, s{PKM1}",
+            f"s_mul_hi_u32 s{PIC}, s{PTMP}, 0x38e38e39",
+            f"s_lshr_b32 s{PIC}, s{PIC}, 1",
+            f"s_mul_i32 s{PKX}, s{PIC}, 9",
+            f"s_sub_u32 s{PKX}, s{PTMP}, s{PKX}",
+            f"s_cmp_ge_u32 s{PKX}, 3",
+            f"s_cselect_b32 s{PKY}, 1, 0",
+            f"s_cmp_ge_u32 s{PKX}, 6",
+            f"s_cselect_b32 s{PTMP}, 1, 0",
+            f"s_add_u32 s{PKY}, s{PKY}, s{PTMP}",
+            f"s_mul_i32 s{PTMP}, s{PKY}, 3",
+            f"s_sub_u32 s{PKX}, s{PKX}, s{PTMP}",
+        ]
+        L += issue_rows_conv(half)
         L.append("s_branch .L%=_issued")
-    L += [".L%=_clamped:",
-          f"s_lshl_b32 s{PROW}, s{PISS}, {lg_chunk}",
-          f"s_add_u32 s{PROW}, s{PROW}, %[prow0]"]
-    L += issue_rows_clamped(vec, half)
+    else:
+        L += [f"s_cmp_lt_u32 s{PISS}, s{PLAST}", "s_cbranch_scc0 .L%=_clamped"]
+        if vec:
+            L.append(f"s_mov_b64 exec, s[{PCM}:{PCM + 1}]")   # also spaces the m0 write from the DMA
+            for r in range(half):
+                if r:
+                    L.append("s_nop 0")                       # m0 write, then a DMA reading it
+                L += [f"global_load_lds_dwordx4 v{VO + r}, s[{PBASE}:{PBASE + 1}]",
+                      "s_add_u32 m0, m0, 0x400"]
+            L.append("s_branch .L%=_issued")
+        L += [".L%=_clamped:",
+              f"s_lshl_b32 s{PROW}, s{PISS}, {lg_chunk}",
+              f"s_add_u32 s{PROW}, s{PROW}, %[prow0]"]
+        L += issue_rows_clamped(vec, half)
     L += [
         ".L%=_issued:",
         f"s_mov_b64 exec, s[{PEX}:{PEX + 1}]",
@@ -439,17 +545,20 @@ def producer(vec):
     ]
     body = "\n".join('      "' + x + '\\n\\t"' for x in L)
     sregs = [f"s{x}" for x in list(range(PISS, PCM + 2 * pieces)) + [PKM1, PLAST]]
+    if conv:
+        sregs += [f"s{x}" for x in range(PIC, PMU + 2)]
     vregs = ["v27"] + [f"v{x}" for x in range(VO, VMIN + 5)]
     clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["vcc", "scc"])
-    suffix = "vec" if vec else "dword"
-    return f"""// Producer, {"16-byte" if vec else "4-byte"} staging
-__device__ __forceinline__ void produce_{suffix}(const ProducerArgs& a) {{
+    title = {"vec": "16-byte staging", "dword": "4-byte staging",
+             "conv": "the virtual B of a 3x3 convolution"}[kind]
+    return f"""// Producer, {title}
+__device__ __forceinline__ void produce_{kind}(const ProducerArgs& a) {{
   asm volatile(
 {body}
       :
       : [nch] "s"(a.nchunks), [K] "s"(a.K), [rs] "s"(a.row_bytes), [bb_lo] "s"(a.bbase_lo),
         [bb_hi] "s"(a.bbase_hi), [ncol] "s"(a.ncol), [prow0] "s"(a.first_row),
-        [vl] "v"(a.vlane), [pg] "v"(a.prog_addr), [ra] "v"(a.ready_addr)
+        [vl] "v"(a.vlane), [pg] "v"(a.prog_addr), [ra] "v"(a.ready_addr){CONV_OPERANDS if conv else ""}
       : {clob});
 }}
 """
@@ -472,8 +581,8 @@ def generate() -> str:
              ""]
     for rw in RW_VARIANTS:
         parts.append(consumer(rw))
-    for vec in (True, False):
-        parts.append(producer(vec))
+    for kind in ("vec", "dword", "conv"):
+        parts.append(producer(kind))
     return "\n".join(parts)
 
 

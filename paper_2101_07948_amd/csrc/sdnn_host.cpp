@@ -652,6 +652,34 @@ sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const fl
   }
 }
 
+sdnn_status sdnn_conv3x3(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
+                         int32_t NB, const float* bias, sdnn_epilogue epi, void* stream) {
+  if (!p) return SDNN_ERR_NULL;
+  if (H < 0 || W < 0 || NB < 0) return SDNN_ERR_DIM;
+  if (epi != SDNN_EPI_NONE && epi != SDNN_EPI_RELU && epi != SDNN_EPI_GELU) return SDNN_ERR_DIM;
+  if (p->K % 9 != 0 || p->K == 0 || p->in_permuted) return SDNN_ERR_DIM;
+  if (NB % 4 != 0) return SDNN_ERR_DIM;
+  const int64_t N = (int64_t)H * W * NB;
+  if (p->M == 0 || N == 0) return SDNN_OK;
+  // 32-bit column and channel-plane byte offsets in the staging loop
+  if (N * 4 >= ((int64_t)1 << 31) || (int64_t)(p->K / 9) * N * 4 >= ((int64_t)1 << 40))
+    return SDNN_ERR_DIM;
+  if (!X || !C) return SDNN_ERR_NULL;
+  if ((((uintptr_t)X | (uintptr_t)C) & 15) != 0) return SDNN_ERR_DIM;
+  const int64_t xbytes = (int64_t)(p->K / 9) * N * 4, cbytes = (int64_t)p->M * N * 4;
+  if (ranges_overlap(X, xbytes, C, cbytes)) return SDNN_ERR_DIM;
+  if (ranges_overlap(bias, (int64_t)p->M * 4, C, cbytes)) return SDNN_ERR_DIM;
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return SDNN_ERR_HIP;
+  if (cur != p->device) return SDNN_ERR_DEVICE;
+  try {
+    hipError_t e = launch_conv3x3(p, X, C, H, W, NB, bias, (int)epi, (hipStream_t)stream);
+    return e == hipSuccess ? SDNN_OK : SDNN_ERR_HIP;
+  } catch (...) {
+    return SDNN_ERR_HIP;
+  }
+}
+
 sdnn_status sdnn_dense_gemm(const float* W, const float* B, float* C, int32_t M, int32_t K,
                             int32_t N, const float* bias, sdnn_epilogue epi, void* stream) {
   if (M < 0 || K < 0 || N < 0) return SDNN_ERR_DIM;

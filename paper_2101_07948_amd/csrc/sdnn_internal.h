@@ -108,6 +108,8 @@ namespace sdnn {
 // Kernel launchers (sdnn_kernels.hip).  Arguments are already checked.
 hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                        const float* bias, int epi, hipStream_t stream);
+hipError_t launch_conv3x3(const sdnn_plan_s* p, const float* X, float* C, int32_t H, int32_t W,
+                          int32_t NB, const float* bias, int epi, hipStream_t stream);
 hipError_t launch_dense(const float* W, const float* B, float* C, int32_t M, int32_t K, int32_t N,
                         const float* bias, int epi, hipStream_t stream);
 }  // namespace sdnn

@@ -55,6 +55,13 @@ struct ProducerArgs {
   uint32_t vlane;          // the lane's byte offset in a B row segment (16 or 4 * lane)
   uint32_t prog_addr;      // LDS address of the 16 progress words
   uint32_t ready_addr;     // LDS address of this producer's ready word
+  // virtual B of a 3x3 convolution (bbase is then X itself)
+  uint32_t row_step, col_step;  // bytes between image rows (W * NB * 4), columns (NB * 4)
+  uint32_t plane_bytes;         // bytes per input channel (H * W * NB * 4)
+  uint32_t in_channels;         // IC = K / 9
+  uint32_t col_bytes;           // 4 * (n0 + 4 * lane): the lane's first column in a plane
+  uint64_t rowmask[3];          // lanes whose pixel row y + ky - 1 lies in the image
+  uint64_t colmask[3];          // lanes whose pixel column x + kx - 1 lies in the image
 };
 
 #include "spmm_asm_gen.h"
@@ -93,11 +100,16 @@ struct SpmmArgs {
   int32_t per_xcd;   // launched grid / 8
   int32_t epi;
   int32_t out_permuted;  // store permuted row i at row i instead of at its source row
+  int32_t H, W, NB;      // image geometry of a 3x3 convolution (B is then the input X)
 };
 
-// RW: rows per panel; VEC: N % 4 == 0 and B, C 16-byte aligned (16-byte staging DMA,
-// vector stores of C).  blockDim.x = 64 * (consumers + kProducers).
-template <int RW, bool VEC>
+// Producer kinds: 4-byte staging (any N), 16-byte staging (N % 4 == 0, aligned), the
+// virtual B of a 3x3 convolution (16-byte segments of an IC x H x W x NB input).
+enum { kStageDword = 0, kStageVec = 1, kStageConv = 2 };
+
+// RW: rows per panel; STAGE: the producer kind (16-byte kinds also store C as float4:
+// N % 4 == 0 and B, C 16-byte aligned).  blockDim.x = 64 * (consumers + kProducers).
+template <int RW, int STAGE>
 __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     const uint32_t* __restrict__ entries, const int32_t* __restrict__ panel_start,
     const int32_t* __restrict__ panel_rows, const float* __restrict__ B, float* __restrict__ C, const float* __restrict__ bias,
@@ -143,13 +155,33 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     pa.bbase_hi = (uint32_t)(bb >> 32);
     pa.ncol = a.N - n0;
     pa.first_row = (uint32_t)(prod * (kChunk / kProducers));
-    pa.vlane = (uint32_t)lane * (VEC ? 16u : 4u);
+    pa.vlane = (uint32_t)lane * (STAGE != kStageDword ? 16u : 4u);
     pa.prog_addr = prog0;
     pa.ready_addr = ready_addr + 4u * (uint32_t)prod;
-    if (VEC)
+    if constexpr (STAGE == kStageConv) {
+      // lane l's columns n0 + 4l .. + 3: four images of pixel (y, x)
+      const uint64_t xb = (uint64_t)(uintptr_t)B;
+      pa.bbase_lo = (uint32_t)xb;
+      pa.bbase_hi = (uint32_t)(xb >> 32);
+      pa.row_step = (uint32_t)a.W * (uint32_t)a.NB * 4u;
+      pa.col_step = (uint32_t)a.NB * 4u;
+      pa.plane_bytes = (uint32_t)a.H * pa.row_step;
+      pa.in_channels = (uint32_t)(a.K / 9);
+      const int n = n0 + 4 * lane;
+      pa.col_bytes = 4u * (uint32_t)n;
+      const bool live = n < a.N;
+      const int q = n / a.NB, y = q / a.W, x = q - y * a.W;
+#pragma unroll
+      for (int t = 0; t < 3; ++t) {
+        pa.rowmask[t] = __ballot(live && (unsigned)(y + t - 1) < (unsigned)a.H);
+        pa.colmask[t] = __ballot(live && (unsigned)(x + t - 1) < (unsigned)a.W);
+      }
+      produce_conv(pa);
+    } else if constexpr (STAGE == kStageVec) {
       produce_vec(pa);
-    else
+    } else {
       produce_dword(pa);
+    }
     return;
   }
   if (panel >= a.npanels) return;
@@ -175,7 +207,7 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     const float bb = bias ? bias[orig] : 0.0f;
     float* crow = C + (size_t)(a.out_permuted ? panel * RW + r : orig) * a.N;
     const float v[4] = {p0[r], p1[r], p2[r], p3[r]};
-    if (VEC && ncol + 4 <= a.N) {
+    if (STAGE != kStageDword && ncol + 4 <= a.N) {
       *reinterpret_cast<float4*>(crow + ncol) =
           make_float4(activation(v[0] + bb, a.epi), activation(v[1] + bb, a.epi),
                       activation(v[2] + bb, a.epi), activation(v[3] + bb, a.epi));
@@ -196,23 +228,23 @@ struct SpmmPtrs {
   const float* bias;
 };
 
-template <int RW, bool VEC>
+template <int RW, int STAGE>
 hipError_t launch_variant(const SpmmPtrs& p, const SpmmArgs& args, int waves, int grid,
                           hipStream_t stream) {
-  hipLaunchKernelGGL((spmm_panel_kernel<RW, VEC>), dim3(grid), dim3(64 * (waves + kProducers)), 0, stream,
+  hipLaunchKernelGGL((spmm_panel_kernel<RW, STAGE>), dim3(grid), dim3(64 * (waves + kProducers)), 0, stream,
                      p.entries, p.panel_start, p.panel_rows, p.B, p.C, p.bias,
                      args);
   return hipGetLastError();
 }
 
-template <bool VEC>
+template <int STAGE>
 hipError_t launch_rw(int RW, const SpmmPtrs& p, const SpmmArgs& args, int waves, int grid,
                      hipStream_t stream) {
   switch (RW) {
-    case 4: return launch_variant<4, VEC>(p, args, waves, grid, stream);
-    case 8: return launch_variant<8, VEC>(p, args, waves, grid, stream);
-    case 12: return launch_variant<12, VEC>(p, args, waves, grid, stream);
-    case 16: return launch_variant<16, VEC>(p, args, waves, grid, stream);
+    case 4: return launch_variant<4, STAGE>(p, args, waves, grid, stream);
+    case 8: return launch_variant<8, STAGE>(p, args, waves, grid, stream);
+    case 12: return launch_variant<12, STAGE>(p, args, waves, grid, stream);
+    case 16: return launch_variant<16, STAGE>(p, args, waves, grid, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -270,8 +302,10 @@ const DevPacking& choose_packing(const sdnn_plan_s* p, int N) {
 
 }  // namespace
 
-hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
-                       const float* bias, int epi, hipStream_t stream) {
+namespace {
+hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
+                         const float* bias, int epi, const int32_t* conv_hwn,
+                         hipStream_t stream) {
   const DevPacking& pk = choose_packing(p, N);
   const LaunchCfg cfg = choose_cfg(pk, p->num_cus, N);
   const SpmmPtrs ptrs{pk.entries, pk.panel_start, pk.panel_rows, B, C, bias};
@@ -288,12 +322,28 @@ hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N
   args.per_xcd = (int32_t)(grid / 8);
   args.epi = epi;
   args.out_permuted = p->out_permuted;
+  args.H = conv_hwn ? conv_hwn[0] : 0;
+  args.W = conv_hwn ? conv_hwn[1] : 0;
+  args.NB = conv_hwn ? conv_hwn[2] : 0;
+  if (conv_hwn) return launch_rw<kStageConv>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
   // the 16-byte producer addresses a chunk's rows with 32-bit per-lane offsets
   // 16 * lane + r * 4N (r < kChunk / kProducers)
   const bool vec = (N % 4 == 0) && (((uintptr_t)B & 15) == 0) && (((uintptr_t)C & 15) == 0) &&
                    (uint64_t)N * 4u * (kChunk / kProducers) < ((uint64_t)1 << 31);
-  return vec ? launch_rw<true>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream)
-             : launch_rw<false>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
+  return vec ? launch_rw<kStageVec>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream)
+             : launch_rw<kStageDword>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
+}
+}  // namespace
+
+hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
+                       const float* bias, int epi, hipStream_t stream) {
+  return launch_panels(p, B, C, N, bias, epi, nullptr, stream);
+}
+
+hipError_t launch_conv3x3(const sdnn_plan_s* p, const float* X, float* C, int32_t H, int32_t W,
+                          int32_t NB, const float* bias, int epi, hipStream_t stream) {
+  const int32_t hwn[3] = {H, W, NB};
+  return launch_panels(p, X, C, H * W * NB, bias, epi, hwn, stream);
 }
 
 // ---------------------------------------------------------------------------------

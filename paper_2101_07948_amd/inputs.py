@@ -32,6 +32,7 @@ SEED = 210107948
 
 # workload ids used in the seed
 CFG_W0, CFG_C1, CFG_C2, CFG_C3, CFG_C4, CFG_C5, CFG_S, CFG_TEST = 0, 1, 2, 3, 4, 5, 6, 7
+CFG_CONV = 8
 T_PATTERN, T_VALUES, T_B, T_BIAS = 0, 1, 2, 3
 
 
@@ -254,3 +255,29 @@ def workload(name: str, N: Optional[int] = None, num_layers: Optional[int] = Non
                                     "gelu" if j == 4 else "none"))
         return Workload(name, layers, dense_B(768, N, CFG_C5, 0), N)
     raise KeyError(name)
+
+
+@dataclasses.dataclass
+class ConvLayer:
+    """A sparse 3x3 convolution (stride 1, padding 1): filters as an OC x (IC*9) CSR whose
+    column is i*9 + ky*3 + kx, input X of shape (IC, H, W, NB), bias, epilogue."""
+    F: CSR
+    X: np.ndarray
+    bias: Optional[np.ndarray]
+    epi: str
+
+    @property
+    def shape(self):
+        IC, H, W, NB = self.X.shape
+        return self.F.M, IC, H, W, NB
+
+
+def conv_layer(OC: int, IC: int, H: int, W: int, NB: int, sparsity: float, layer: int = 0,
+               epi: str = "none", cfg: int = CFG_CONV) -> ConvLayer:
+    """The paper's convolution benchmark problems (Sec. 4.1): 3x3 filters, padding 1,
+    random sparsity generated like the SpMM suite (a uniformly random support of exactly
+    round(d * OC * IC * 9) taps, d = 1 - sparsity), values N(0, 0.05); input N(0, 1) in
+    channel, row, column, image order; bias N(0, 0.02)."""
+    F = pattern_uniform(OC, IC * 9, 1.0 - sparsity, cfg, layer, 0.05)
+    X = rng_for(cfg, layer, T_B).standard_normal((IC, H, W, NB), dtype=np.float32)
+    return ConvLayer(F, X, bias_normal(OC, cfg, layer, 0.02), epi)
