@@ -315,6 +315,46 @@ def run_suite(out_path):
               f"upload): {prep_s:.2f} s on the host."]
     print("\n".join(lines[-4:]), flush=True)
 
+    # sparse 3x3 convolutions shaped like the paper's benchmark (Sec. 4.1): IC, OC in
+    # 32..256, images 7..56, padding 1, 90 / 95 %; 16 images per call on the GPU
+    lines += ["", "## Sparse 3x3 convolution (stride 1, padding 1), 16 images per call", "",
+              "Filters uniform-random at the stated sparsity; input (IC, H, W, 16).  Dense: "
+              "the comparison GEMM on the dense filters times a materialised im2col matrix "
+              "(building it is not timed).", "",
+              "| OC x IC, image | sparsity | nnz | us (cold mean) | GFLOP/s | % ALU | "
+              "dense us | speedup |", "|---|---|---|---|---|---|---|---|"]
+    for OC, IC, HW in ((64, 64, 56), (128, 128, 28), (256, 256, 14), (256, 256, 7)):
+        for sp in (0.9, 0.95):
+            L = inputs.conv_layer(OC, IC, HW, HW, 16, sp, layer=OC + HW)
+            N = HW * HW * 16
+            nsets = min(64, max(1, math.ceil((1 << 30) / (4 * (IC + OC) * N))))
+            Xs = [torch.from_numpy(L.X).to(dev)] + [torch.randn(IC, HW, HW, 16, device=dev)
+                                                     for _ in range(nsets - 1)]
+            Cs = [torch.empty(OC, HW, HW, 16, device=dev) for _ in range(nsets)]
+            bias = torch.from_numpy(L.bias).to(dev)
+            with sd.Plan.from_csr(L.F) as plan:
+                fn = lambda i: plan.conv3x3(Xs[i % nsets], Cs[i % nsets], bias)
+                for i in range(10):
+                    fn(i)
+                torch.cuda.synchronize()
+                _, mean = _launch_times(fn, 100)
+            Xp = np.pad(L.X, ((0, 0), (1, 1), (1, 1), (0, 0)))
+            cols = np.stack([Xp[:, ky:ky + HW, kx:kx + HW, :] for ky in range(3) for kx in range(3)],
+                            axis=1).reshape(IC * 9, N)
+            Bd = torch.from_numpy(np.ascontiguousarray(cols)).to(dev)
+            Wd = torch.from_numpy(L.F.to_dense()).to(dev)
+            Cd = torch.empty(OC, N, device=dev)
+            dfn = lambda i: sd.dense_gemm(Wd, Bd, Cd, bias)
+            dfn(0)
+            torch.cuda.synchronize()
+            _, dmean = _launch_times(dfn, 10)
+            flop = 2.0 * L.F.nnz * N
+            lines.append(f"| {OC} x {IC}, {HW}x{HW} | {int(sp*100)} % | {L.F.nnz} | {mean*1e3:.1f} | "
+                         f"{flop/(mean*1e-3)/1e9:.0f} | {100*flop/(mean*1e-3)/1e12/ALU_PEAK_TFLOPS:.1f} | "
+                         f"{dmean*1e3:.1f} | {dmean/mean:.2f}x |")
+            print(lines[-1], flush=True)
+            del Xs, Cs, Bd, Wd, Cd
+
     # CPU oracle (fp32 CSR loop) at 1, 4 and all threads on W0 at N = 4096
     wl = inputs.workload("w0")
     L = wl.layers[0]

@@ -307,81 +307,91 @@ def issue_rows_clamped(vec, half):
     return L
 
 
-# conv producer SGPRs: tap of the current row, LDS row address, 64-bit temps
-PIC, PKY, PKX, PRL, PDL, PMT, PMU = 66, 67, 68, 69, 70, 72, 74
-VZ, VA = 36, 32        # conv producer: v[36:39] zeros, v32 LDS address of a zero fill
+# conv producer SGPRs: row bases (X + ic * plane + (ky - 1) * row_step, 64-bit, ky = 0..2),
+# LDS row address, rows of the chunk below K, mask temp
+RB, PRL, PNV, PMT, PXB = (66, 68, 70), 72, 73, 74, 76   # PXB: X itself (64-bit)
+VZ, VA, VN = 36, 32, 33  # v[36:39] zeros, v32 zero-fill address, v33..v35 column offsets (the
+                         # progress poll uses v40 and up)
 CONV_OPERANDS = (
-    ',\n        [rstep] "s"(a.row_step), [cstep] "s"(a.col_step),'
-    ' [c0step] "s"(a.row_step + a.col_step),\n'
-    '        [plane] "s"(a.plane_bytes), [ic] "s"(a.in_channels), [vn] "v"(a.col_bytes),\n'
+    ',\n        [rstep] "s"(a.row_step), [cstep] "s"(a.col_step), [plane] "s"(a.plane_bytes),\n'
+    '        [vn] "v"(a.col_bytes), [dummy] "s"(a.dummy_lds),\n'
     '        [r0] "s"(a.rowmask[0]), [r1] "s"(a.rowmask[1]), [r2] "s"(a.rowmask[2]),\n'
     '        [c0] "s"(a.colmask[0]), [c1] "s"(a.colmask[1]), [c2] "s"(a.colmask[2])')
 
 
 def issue_rows_conv(half):
     """Stage rows k0 .. k0+half-1 of the virtual B of a 3x3 convolution (stride 1,
-    padding 1).  Row k is input channel k / 9 shifted by tap (ky, kx) = ((k % 9) / 3,
-    k % 3): lane l's four columns n = n0 + 4l .. n0 + 4l + 3 are four images of one pixel
-    (y, x), so they come from X + ic * plane + (n + ((ky-1) * W + (kx-1)) * NB) * 4, one
-    16-byte segment, when (y + ky - 1, x + kx - 1) lies in the image, and are zero
-    otherwise.  Valid lanes: the DMA (exec = live & rowmask[ky] & colmask[kx]); invalid
-    live lanes: a ds_write of zeros to the same LDS row.  Rows past K re-stage the last
-    row.  Before the first row PIC/PKY/PKX hold the tap of row k0."""
-    L = []
-    for r in range(half):
-        L += [
-            # row address: X + ic * plane + ((ky - 1) * W + (kx - 1)) * NB * 4
-            f"s_mul_i32 s{PDL}, s{PKY}, %[rstep]",
-            f"s_mul_i32 s{PTMP}, s{PKX}, %[cstep]",
-            f"s_add_u32 s{PDL}, s{PDL}, s{PTMP}",
-            f"s_sub_u32 s{PDL}, s{PDL}, %[c0step]",
-            f"s_ashr_i32 s{PDL + 1}, s{PDL}, 31",
-            f"s_mul_i32 s{PADDR}, s{PIC}, %[plane]",
-            f"s_mul_hi_u32 s{PADDR + 1}, s{PIC}, %[plane]",
-            f"s_add_u32 s{PADDR}, s{PADDR}, s{PDL}",
-            f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, s{PDL + 1}",
-            f"s_add_u32 s{PADDR}, s{PADDR}, %[bb_lo]",
-            f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, %[bb_hi]",
-            # lanes whose source pixel lies in the image
-            f"s_cmp_eq_u32 s{PKY}, 0",
-            f"s_cselect_b64 s[{PMT}:{PMT + 1}], %[r0], %[r1]",
-            f"s_cmp_eq_u32 s{PKY}, 2",
-            f"s_cselect_b64 s[{PMT}:{PMT + 1}], %[r2], s[{PMT}:{PMT + 1}]",
-            f"s_cmp_eq_u32 s{PKX}, 0",
-            f"s_cselect_b64 s[{PMU}:{PMU + 1}], %[c0], %[c1]",
-            f"s_cmp_eq_u32 s{PKX}, 2",
-            f"s_cselect_b64 s[{PMU}:{PMU + 1}], %[c2], s[{PMU}:{PMU + 1}]",
-            f"s_and_b64 s[{PMT}:{PMT + 1}], s[{PMT}:{PMT + 1}], s[{PMU}:{PMU + 1}]",
-            f"s_and_b64 s[{PMT}:{PMT + 1}], s[{PMT}:{PMT + 1}], s[{PCM}:{PCM + 1}]",
-            # live lanes outside the image: zeros
-            f"s_andn2_b64 exec, s[{PCM}:{PCM + 1}], s[{PMT}:{PMT + 1}]",
-            f"s_cbranch_execz .L%=_cz{r}",
-            f"v_add_u32 v{VA}, s{PRL}, %[vl]",
-            f"ds_write_b128 v{VA}, v[{VZ}:{VZ + 3}]",
-            f".L%=_cz{r}:",
-            f"s_mov_b64 exec, s[{PMT}:{PMT + 1}]",
-            f"s_cbranch_execz .L%=_cd{r}",
-            f"global_load_lds_dwordx4 %[vn], s[{PADDR}:{PADDR + 1}]",
-            f".L%=_cd{r}:",
-            f"s_add_u32 s{PRL}, s{PRL}, 0x400",
-            f"s_mov_b32 m0, s{PRL}",
-            # next tap; past the last input channel keep re-staging its last row
-            f"s_add_u32 s{PKX}, s{PKX}, 1",
-            f"s_cmp_eq_u32 s{PKX}, 3",
-            f"s_cselect_b32 s{PKX}, 0, s{PKX}",
-            f"s_cselect_b32 s{PTMP}, 1, 0",
-            f"s_add_u32 s{PKY}, s{PKY}, s{PTMP}",
-            f"s_cmp_eq_u32 s{PKY}, 3",
-            f"s_cselect_b32 s{PKY}, 0, s{PKY}",
-            f"s_cselect_b32 s{PTMP}, 1, 0",
-            f"s_add_u32 s{PIC}, s{PIC}, s{PTMP}",
-            f"s_cmp_ge_u32 s{PIC}, %[ic]",
-            f"s_cbranch_scc0 .L%=_cn{r}",
-            f"s_sub_u32 s{PIC}, %[ic], 1",
-            f"s_mov_b32 s{PKY}, 2",
-            f"s_mov_b32 s{PKX}, 2",
-            f".L%=_cn{r}:",
-        ]
+    padding 1).  Row k is input channel k / 9 shifted by tap t = k % 9, (ky, kx) =
+    (t / 3, t % 3): lane l's four columns n = n0 + 4l .. n0 + 4l + 3 are four images of
+    one pixel (y, x), so they are the 16 bytes at
+        RB[ky] + 4 n + (kx - 1) * NB * 4,   RB[ky] = X + ic * plane + (ky - 1) * W * NB * 4
+    when (y + ky - 1, x + kx - 1) lies in the image, and zero otherwise.  The taps of a
+    chunk's rows follow from t0 = k0 % 9, so the rows are generated once per t0 with
+    static taps: the lane mask is rowmask[ky] & colmask[kx], the address is a row base
+    plus one of three per-lane offsets, and the channel (the three row bases) advances
+    after tap 8.  In-image lanes get the DMA, live lanes outside the image get zeros
+    written to LDS; every row issues exactly one DMA (a one-lane load into a scratch
+    LDS word when the row has no in-image lane or lies past K), so a chunk is always
+    `half` loads and two chunks can be in flight."""
+    lg_chunk = CHUNK.bit_length() - 1
+    L = [
+        f"s_mov_b32 s{PRL}, m0",
+        # k0 = issued * CHUNK + prow0; rows of the chunk below K
+        f"s_lshl_b32 s{PTMP}, s{PISS}, {lg_chunk}",
+        f"s_add_u32 s{PTMP}, s{PTMP}, %[prow0]",
+        f"s_sub_i32 s{PNV}, %[K], s{PTMP}",
+        f"s_max_i32 s{PNV}, s{PNV}, 0",
+        f"s_min_i32 s{PNV}, s{PNV}, {half}",
+        # ic0 = k0 / 9 (multiply-high), t0 = k0 - 9 ic0
+        f"s_mul_hi_u32 s{PROW}, s{PTMP}, 0x38e38e39",
+        f"s_lshr_b32 s{PROW}, s{PROW}, 1",
+        f"s_mul_i32 s{PADDR}, s{PROW}, 9",
+        f"s_sub_u32 s{PTMP}, s{PTMP}, s{PADDR}",
+        # row bases of channel ic0
+        f"s_mul_i32 s{RB[1]}, s{PROW}, %[plane]",
+        f"s_mul_hi_u32 s{RB[1] + 1}, s{PROW}, %[plane]",
+        f"s_add_u32 s{RB[1]}, s{RB[1]}, %[bb_lo]",
+        f"s_addc_u32 s{RB[1] + 1}, s{RB[1] + 1}, %[bb_hi]",
+        f"s_sub_u32 s{RB[0]}, s{RB[1]}, %[rstep]",
+        f"s_subb_u32 s{RB[0] + 1}, s{RB[1] + 1}, 0",
+        f"s_add_u32 s{RB[2]}, s{RB[1]}, %[rstep]",
+        f"s_addc_u32 s{RB[2] + 1}, s{RB[1] + 1}, 0",
+    ]
+    for t0 in range(9):
+        L += [f"s_cmp_eq_u32 s{PTMP}, {t0}", f"s_cbranch_scc1 .L%=_cv{t0}"]
+    L.append("s_branch .L%=_issued")          # unreachable: t0 < 9
+    for t0 in range(9):
+        L.append(f".L%=_cv{t0}:")
+        for r in range(half):
+            t = (t0 + r) % 9
+            ky, kx = t // 3, t % 3
+            tag = f"{t0}_{r}"
+            L += [
+                f"s_cmp_lt_u32 s{PNV}, {r + 1}",           # row past K
+                f"s_cbranch_scc1 .L%=_cy{tag}",
+                f"s_and_b64 s[{PMT}:{PMT + 1}], %[r{ky}], %[c{kx}]",
+                f"s_andn2_b64 exec, s[{PCM}:{PCM + 1}], s[{PMT}:{PMT + 1}]",
+                f"s_cbranch_execz .L%=_cz{tag}",
+                f"v_add_u32 v{VA}, s{PRL}, %[vl]",
+                f"ds_write_b128 v{VA}, v[{VZ}:{VZ + 3}]",
+                f".L%=_cz{tag}:",
+                f"s_mov_b64 exec, s[{PMT}:{PMT + 1}]",
+                f"s_cbranch_execz .L%=_cy{tag}",
+                f"global_load_lds_dwordx4 v{VN + kx}, s[{RB[ky]}:{RB[ky] + 1}]",
+                f"s_branch .L%=_cn{tag}",
+                f".L%=_cy{tag}:",                          # one-lane load to scratch LDS
+                "s_mov_b32 m0, %[dummy]",
+                "s_mov_b64 exec, 1",
+                "s_nop 0",
+                f"global_load_lds_dwordx4 %[vl], s[{PXB}:{PXB + 1}]",
+                f".L%=_cn{tag}:",
+                f"s_add_u32 s{PRL}, s{PRL}, 0x400",
+                f"s_mov_b32 m0, s{PRL}",
+            ]
+            if t == 8 and r < half - 1:                    # next channel
+                for b in RB:
+                    L += [f"s_add_u32 s{b}, s{b}, %[plane]", f"s_addc_u32 s{b + 1}, s{b + 1}, 0"]
+        L.append("s_branch .L%=_issued")
     return L
 
 
@@ -395,11 +405,11 @@ def producer(kind):
     16 * lane + r * row_bytes, so each row is one DMA and one m0 step.  The last chunk
     when K is not a multiple of CHUNK, and every chunk of the 4-byte variant, take the
     clamped path, which re-stages row K-1 for rows past K (LDS rows no entry reads).
-    conv: one chunk in flight (a row may issue no DMA, so landing waits for all loads)."""
+    conv: rows as in issue_rows_conv, `half` loads per chunk like vec."""
     vec = kind in ("vec", "conv")
     conv = kind == "conv"
     half = CHUNK // NPROD
-    pmax = 1 if conv else (PMAX_VEC if vec else PMAX_DWORD)
+    pmax = PMAX_VEC if vec else PMAX_DWORD
     loads_per_chunk = half if vec else 4 * half
     assert loads_per_chunk * (pmax - 1) <= 63
     lg_chunk = CHUNK.bit_length() - 1
@@ -431,6 +441,11 @@ def producer(kind):
         L.append(f"s_mov_b32 s{PLAST}, 0")
     if conv:
         L += [f"v_mov_b32 v{VZ + q}, 0" for q in range(4)]
+        L += [f"v_subrev_u32 v{VN}, %[cstep], %[vn]",      # 4 n - NB * 4 (kx = 0)
+              f"v_mov_b32 v{VN + 1}, %[vn]",                # 4 n           (kx = 1)
+              f"v_add_u32 v{VN + 2}, %[cstep], %[vn]",      # 4 n + NB * 4  (kx = 2)
+              f"s_mov_b32 s{PXB}, %[bb_lo]",
+              f"s_mov_b32 s{PXB + 1}, %[bb_hi]"]
     # column masks: vec -> lanes whose 4 columns exist (lane < ncol / 4);
     # dword -> piece q of a row: lanes with 64 q + lane < ncol
     pieces = 1 if vec else 4
@@ -478,27 +493,7 @@ def producer(kind):
         f"s_mov_b64 s[{PEX}:{PEX + 1}], exec",
     ]
     if conv:
-        # tap of row k0 = issued * CHUNK + prow0 (k0 / 9 by a multiply-high), clamped
-        # to the last row when k0 >= K
-        L += [
-            f"s_mov_b32 s{PRL}, m0",
-            f"s_lshl_b32 s{PTMP}, s{PISS}, {lg_chunk}",
-            f"s_add_u32 s{PTMP}, s{PTMP}, %[prow0]",
-            f"s_min_u32 s{PTMP}, s{PTMP}, s{PKM1}",
-            f"s_mul_hi_u32 s{PIC}, s{PTMP}, 0x38e38e39",
-            f"s_lshr_b32 s{PIC}, s{PIC}, 1",
-            f"s_mul_i32 s{PKX}, s{PIC}, 9",
-            f"s_sub_u32 s{PKX}, s{PTMP}, s{PKX}",
-            f"s_cmp_ge_u32 s{PKX}, 3",
-            f"s_cselect_b32 s{PKY}, 1, 0",
-            f"s_cmp_ge_u32 s{PKX}, 6",
-            f"s_cselect_b32 s{PTMP}, 1, 0",
-            f"s_add_u32 s{PKY}, s{PKY}, s{PTMP}",
-            f"s_mul_i32 s{PTMP}, s{PKY}, 3",
-            f"s_sub_u32 s{PKX}, s{PKX}, s{PTMP}",
-        ]
         L += issue_rows_conv(half)
-        L.append("s_branch .L%=_issued")
     else:
         L += [f"s_cmp_lt_u32 s{PISS}, s{PLAST}", "s_cbranch_scc0 .L%=_clamped"]
         if vec:
@@ -546,7 +541,7 @@ def producer(kind):
     body = "\n".join('      "' + x + '\\n\\t"' for x in L)
     sregs = [f"s{x}" for x in list(range(PISS, PCM + 2 * pieces)) + [PKM1, PLAST]]
     if conv:
-        sregs += [f"s{x}" for x in range(PIC, PMU + 2)]
+        sregs += [f"s{x}" for x in range(RB[0], PXB + 2)]
     vregs = ["v27"] + [f"v{x}" for x in range(VO, VMIN + 5)]
     clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["vcc", "scc"])
     title = {"vec": "16-byte staging", "dword": "4-byte staging",

@@ -58,8 +58,8 @@ struct ProducerArgs {
   // virtual B of a 3x3 convolution (bbase is then X itself)
   uint32_t row_step, col_step;  // bytes between image rows (W * NB * 4), columns (NB * 4)
   uint32_t plane_bytes;         // bytes per input channel (H * W * NB * 4)
-  uint32_t in_channels;         // IC = K / 9
   uint32_t col_bytes;           // 4 * (n0 + 4 * lane): the lane's first column in a plane
+  uint32_t dummy_lds;           // 16 bytes of LDS no one reads (one-lane filler loads)
   uint64_t rowmask[3];          // lanes whose pixel row y + ky - 1 lies in the image
   uint64_t colmask[3];          // lanes whose pixel column x + kx - 1 lies in the image
 };
@@ -81,8 +81,10 @@ constexpr int kRingBytes = kRing * kChunk * 1024;
 // 16 waves per CU leave each wave.
 template <int RW>
 constexpr int max_threads() { return kAsmAccBase + 4 * RW < 128 ? 1024 : 768; }
-// LDS control words after the ring: ready[kProducers] at +0, progress[16] at +64.
+// LDS control words after the ring: ready[kProducers] at +0, progress[16] at +64, and
+// 16 bytes per producer at +512 that the convolution producer's filler loads write.
 constexpr int kCtlWords = 256;
+static_assert(512 + 16 * kProducers <= kCtlWords * 4, "filler words outside the control area");
 static_assert(kProducers <= 16, "ready words overlap the progress words");
 
 __device__ __forceinline__ float activation(float x, int epi) {
@@ -166,7 +168,7 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
       pa.row_step = (uint32_t)a.W * (uint32_t)a.NB * 4u;
       pa.col_step = (uint32_t)a.NB * 4u;
       pa.plane_bytes = (uint32_t)a.H * pa.row_step;
-      pa.in_channels = (uint32_t)(a.K / 9);
+      pa.dummy_lds = ready_addr + 512u + 16u * (uint32_t)prod;
       const int n = n0 + 4 * lane;
       pa.col_bytes = 4u * (uint32_t)n;
       const bool live = n < a.N;
