@@ -62,7 +62,11 @@ typedef enum {
  *                 call: tall panels once a 256-column tile has at least a full
  *                 workgroup of them per compute unit (M * ceil(N / 256) >= 96 * CUs),
  *                 short panels otherwise.  4, 8, 12 or 16 packs that height only.
- *   permute:      1 = apply Algorithm 1 (default), 0 = identity order (ablation).
+ *   permute:      1 = apply Algorithm 1 (default), 0 = identity order (ablation),
+ *                 2 = panel-balancing order: rows, by nonzero count descending, each
+ *                 go to the 4-row panel with the fewest nonzeros so far that has room,
+ *                 so that every panel (and every 12-row panel) carries about the same
+ *                 work.
  *   out_permuted: 0 (default) = C row i is output row i; 1 = C is written in the
  *                 plan's permuted row order, C row i = output row perm[i] (Sec. 3.1.2:
  *                 the rows stay permuted and the next layer's columns compensate).

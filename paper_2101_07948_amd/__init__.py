@@ -106,7 +106,11 @@ def _opts(K: int, panel_rows: int, permute: bool, out_permuted: bool = False, in
     keep = None if in_perm is None else _i32(in_perm)
     if keep is not None and keep.shape != (int(K),):
         raise ValueError(f"in_perm must hold K = {K} entries, got shape {keep.shape}")
-    o = PlanOpts(int(panel_rows), 1 if permute else 0, 1 if out_permuted else 0, 0,
+    if isinstance(permute, str):   # "identity", "algorithm1" or "balanced"
+        mode = {"identity": 0, "algorithm1": 1, "balanced": 2}[permute]
+    else:
+        mode = (1 if permute else 0) if isinstance(permute, bool) else int(permute)
+    o = PlanOpts(int(panel_rows), mode, 1 if out_permuted else 0, 0,
                  None if keep is None else keep.ctypes.data)
     return o, keep
 

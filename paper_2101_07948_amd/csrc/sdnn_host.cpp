@@ -314,7 +314,7 @@ static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* 
       return SDNN_ERR_DIM;
     o->rws = {opts->panel_rows};
   }
-  if (opts->permute != 0 && opts->permute != 1) return SDNN_ERR_DIM;
+  if (opts->permute < 0 || opts->permute > 2) return SDNN_ERR_DIM;
   if (opts->out_permuted != 0 && opts->out_permuted != 1) return SDNN_ERR_DIM;
   o->permute = opts->permute;
   o->out_permuted = opts->out_permuted;
@@ -328,6 +328,43 @@ static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* 
     }
   }
   return SDNN_OK;
+}
+
+// Row order that balances the panels' work (plan option permute = 2): rows are taken
+// by nonzero count (descending, ties by index) and each goes to the 4-row panel with
+// the fewest nonzeros so far among those with room (ties: lower panel), the greedy
+// longest-first rule for equal-size bins.  Position p * kShortPanel + r holds panel
+// p's r-th row, so a tall panel (kTallPanel = 3 * kShortPanel consecutive positions)
+// is three balanced short panels.
+static void balanced_order(const int32_t* row_ptr, int32_t M, int32_t* perm_out) {
+  std::vector<int32_t> rows((size_t)M);
+  for (int32_t i = 0; i < M; ++i) rows[i] = i;
+  std::stable_sort(rows.begin(), rows.end(), [&](int32_t a, int32_t b) {
+    return row_ptr[a + 1] - row_ptr[a] > row_ptr[b + 1] - row_ptr[b];
+  });
+  const int32_t P = (M + kShortPanel - 1) / kShortPanel;
+  std::vector<int32_t> fill((size_t)std::max(P, 1), 0);
+  // min-heap of (nonzeros so far, panel) over panels with room
+  std::vector<std::pair<int64_t, int32_t>> heap;
+  heap.reserve((size_t)P);
+  for (int32_t p = 0; p < P; ++p) heap.emplace_back(0, p);
+  auto greater = [](const std::pair<int64_t, int32_t>& a, const std::pair<int64_t, int32_t>& b) {
+    return a > b;
+  };
+  std::make_heap(heap.begin(), heap.end(), greater);
+  for (int32_t j = 0; j < M; ++j) {
+    std::pop_heap(heap.begin(), heap.end(), greater);
+    std::pair<int64_t, int32_t> top = heap.back();
+    heap.pop_back();
+    const int32_t p = top.second, r = rows[j];
+    perm_out[(size_t)p * kShortPanel + fill[p]] = r;
+    ++fill[p];
+    const int32_t cap = (p == P - 1) ? M - (P - 1) * kShortPanel : kShortPanel;
+    if (fill[p] < cap) {
+      heap.emplace_back(top.first + (row_ptr[r + 1] - row_ptr[r]), p);
+      std::push_heap(heap.begin(), heap.end(), greater);
+    }
+  }
 }
 
 // The CSR a plan packs: the caller's, or (with in_perm) the same rows with column c
@@ -393,9 +430,11 @@ static sdnn_status prepare(const int32_t* row_ptr, const int32_t* col_idx, const
   } catch (const std::bad_alloc&) {
     return SDNN_ERR_ALLOC;
   }
-  if (o->permute) {
+  if (o->permute == 1) {
     st = reorder_bitset(csr->row_ptr, csr->col_idx, M, K, perm.data());
     if (st != SDNN_OK) return st;
+  } else if (o->permute == 2) {
+    balanced_order(csr->row_ptr, M, perm.data());
   } else {
     for (int32_t i = 0; i < M; ++i) perm[i] = i;
   }

@@ -243,6 +243,31 @@ def test_chain_in_permuted_space(N):
         X = Y
 
 
+def test_balanced_order():
+    """permute = 2 gives each row, longest first, to the 4-row panel with the fewest
+    nonzeros so far: a permutation whose panels carry nearly equal work on the
+    lognormal C3 layers, with results equal to the oracle's (and bit-identical to the
+    identity order, since each row still sums its entries in ascending column order)."""
+    w = inputs.workload("c3", N=4)
+    for i, L in enumerate(w.layers):
+        W = L.W
+        B = inputs.dense_B(W.K, 1024, inputs.CFG_TEST, 51 + i)
+        with sd.Plan.from_csr(W, permute="balanced") as pb, \
+                sd.Plan.from_csr(W, permute=False) as p0:
+            perm = pb.perm
+            assert np.array_equal(np.sort(perm), np.arange(W.M))
+            nnz = np.diff(W.row_ptr)[perm]
+            panels = nnz[: W.M // 4 * 4].reshape(-1, 4).sum(axis=1)
+            # a panel can do no better than its heaviest row plus the lightest rows
+            bound = max(1.02 * panels.mean(), nnz.max() + np.sort(nnz)[:3].sum())
+            assert panels.max() <= bound + 4
+            got = gpu_spmm(pb, B, L.bias, L.epi)
+            ident = gpu_spmm(p0, B, L.bias, L.epi)
+        assert np.array_equal(got, ident)
+        ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, W.K, B, L.bias, L.epi)
+        assert np.all(np.abs(got - ref) <= tolerance(bound, ref, L.epi))
+
+
 def test_permute_off_and_on_agree():
     W = inputs.pattern_grouped8(256, 512, 0.05, inputs.CFG_TEST, 9, 0.05)
     B = inputs.dense_B(512, 256, inputs.CFG_TEST, 9)
