@@ -34,7 +34,8 @@
 extern "C" {
 #endif
 
-/* Opaque plan; immutable after creation. */
+/* Opaque plan; immutable after creation except for the launch shapes that
+ * sdnn_plan_tune records. */
 typedef struct sdnn_plan_s* sdnn_plan;
 
 typedef enum {
@@ -150,6 +151,19 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out);
  * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM, SDNN_ERR_DEVICE, SDNN_ERR_HIP. */
 sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
                       sdnn_epilogue epi, void* stream);
+
+/* Per-plan variant selection by timing (the paper's preparation stage chooses the best
+ * kernel implementation per operator, Sec. 3.1): times sdnn_spmm at this N for every
+ * packing the plan holds with several consumer-wave counts per workgroup, on the
+ * caller's B (K x N) and C (M x N, overwritten with unspecified values), and records
+ * the fastest in the plan; later sdnn_spmm calls with the same N use it (up to 8 N
+ * values are kept).  Blocking (synchronises `stream`).  Must not run concurrently with
+ * any other call on the same plan.  Results of sdnn_spmm do not depend on the shape.
+ * On success *panel_rows and *waves (either may be NULL) hold the chosen shape.
+ * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM (N <= 0, M = 0, B overlapping C),
+ * SDNN_ERR_DEVICE, SDNN_ERR_HIP. */
+sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, void* stream,
+                           int32_t* panel_rows, int32_t* waves);
 
 /* Sparse 3x3 convolution, stride 1, zero padding 1 (Sec. 3.2.3: direct convolution as
  * an SpMM whose dense operand is a virtual matrix built on the fly from the input; the

@@ -76,9 +76,10 @@ def lib() -> ctypes.CDLL:
         L.sdnn_plan_destroy.restype = None
         L.sdnn_dense_gemm.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
         L.sdnn_conv3x3.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
+        L.sdnn_plan_tune.argtypes = [p, p, p, i32, p, p, p]
         for fn in ("sdnn_reorder_rows", "sdnn_plan_check_host", "sdnn_plan_create",
                    "sdnn_plan_get_perm", "sdnn_plan_info", "sdnn_spmm", "sdnn_dense_gemm",
-                   "sdnn_conv3x3"):
+                   "sdnn_conv3x3", "sdnn_plan_tune"):
             getattr(L, fn).restype = ctypes.c_int
         _lib_handle = L
     return _lib_handle
@@ -203,6 +204,21 @@ class Plan:
         info = PlanInfo()
         _check(self._lib.sdnn_plan_info(self.handle, ctypes.byref(info)), "sdnn_plan_info")
         return info.as_dict()
+
+    def tune(self, N: int, B=None, C=None, stream=None) -> dict:
+        """Times the plan's launch shapes at this N (on B / C, allocated here when not
+        given) and records the fastest for later spmm calls with the same N."""
+        import torch
+        if B is None:
+            B = torch.randn(self.K, N, device="cuda")
+        if C is None:
+            C = torch.empty(self.M, N, device="cuda")
+        pb = _dev_ptr(B, "B", (self.K, N))
+        pc = _dev_ptr(C, "C", (self.M, N))
+        rw, waves = ctypes.c_int32(), ctypes.c_int32()
+        _check(self._lib.sdnn_plan_tune(self.handle, pb, pc, int(N), _stream_handle(stream),
+                                        ctypes.byref(rw), ctypes.byref(waves)), "sdnn_plan_tune")
+        return {"panel_rows": rw.value, "waves": waves.value}
 
     def conv3x3(self, X, C, bias=None, epi: str = "none", stream=None):
         """Sparse 3x3 convolution (stride 1, padding 1) on the GPU: the plan holds the

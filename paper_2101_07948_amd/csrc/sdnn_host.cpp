@@ -691,6 +691,28 @@ sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const fl
   }
 }
 
+sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, void* stream,
+                           int32_t* panel_rows, int32_t* waves) {
+  if (!p) return SDNN_ERR_NULL;
+  if (N <= 0) return SDNN_ERR_DIM;
+  if (p->M == 0) return SDNN_ERR_DIM;
+  if (!C || (p->K > 0 && !B)) return SDNN_ERR_NULL;
+  const int64_t bbytes = (int64_t)p->K * N * 4, cbytes = (int64_t)p->M * N * 4;
+  if (ranges_overlap(B, bbytes, C, cbytes)) return SDNN_ERR_DIM;
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return SDNN_ERR_HIP;
+  if (cur != p->device) return SDNN_ERR_DEVICE;
+  try {
+    TunedShape chosen;
+    if (tune_spmm(p, B, C, N, (hipStream_t)stream, &chosen) != hipSuccess) return SDNN_ERR_HIP;
+    if (panel_rows) *panel_rows = p->pk[chosen.pack].RW;
+    if (waves) *waves = chosen.waves;
+    return SDNN_OK;
+  } catch (...) {
+    return SDNN_ERR_HIP;
+  }
+}
+
 sdnn_status sdnn_conv3x3(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
                          int32_t NB, const float* bias, sdnn_epilogue epi, void* stream) {
   if (!p) return SDNN_ERR_NULL;

@@ -79,6 +79,13 @@ sdnn_status reorder_bitset(const int32_t* row_ptr, const int32_t* col_idx, int32
 sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* values, int32_t M,
                  int32_t K, int32_t RW, const int32_t* perm, Packed* out);
 
+// A launch shape sdnn_plan_tune measured fastest for one N: which packing, and how many
+// consumer waves per workgroup.
+struct TunedShape {
+  int32_t N = 0, pack = 0, waves = 0;
+};
+constexpr int kTunedSlots = 8;
+
 // One packing of the plan in device memory.
 struct DevPacking {
   int32_t RW = 0, npanels = 0;
@@ -102,6 +109,8 @@ struct sdnn_plan_s {
   int32_t out_permuted = 0;    // C rows stored in the permuted order
   int32_t in_permuted = 0;     // W's columns renamed to a caller-given order of B's rows
   sdnn::DevPacking pk[2];
+  sdnn::TunedShape tuned[sdnn::kTunedSlots];  // filled by sdnn_plan_tune
+  int32_t ntuned = 0;
 };
 
 namespace sdnn {
@@ -110,6 +119,10 @@ hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N
                        const float* bias, int epi, hipStream_t stream);
 hipError_t launch_conv3x3(const sdnn_plan_s* p, const float* X, float* C, int32_t H, int32_t W,
                           int32_t NB, const float* bias, int epi, hipStream_t stream);
+// Times every candidate launch shape of the plan at N on the given buffers (blocking)
+// and records the fastest in p->tuned.
+hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStream_t stream,
+                     TunedShape* chosen);
 hipError_t launch_dense(const float* W, const float* B, float* C, int32_t M, int32_t K, int32_t N,
                         const float* bias, int epi, hipStream_t stream);
 }  // namespace sdnn

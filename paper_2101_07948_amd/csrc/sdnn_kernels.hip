@@ -31,6 +31,9 @@
 #include <stdint.h>
 #include <stdlib.h>
 
+#include <algorithm>
+#include <vector>
+
 #include "sdnn_internal.h"
 
 namespace sdnn {
@@ -305,11 +308,20 @@ const DevPacking& choose_packing(const sdnn_plan_s* p, int N) {
 }  // namespace
 
 namespace {
+// `shape` (packing index and consumer waves) overrides the plan's tuned or heuristic
+// choice when non-null.
 hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                          const float* bias, int epi, const int32_t* conv_hwn,
-                         hipStream_t stream) {
-  const DevPacking& pk = choose_packing(p, N);
-  const LaunchCfg cfg = choose_cfg(pk, p->num_cus, N);
+                         const TunedShape* shape, hipStream_t stream) {
+  if (!shape)
+    for (int i = 0; i < p->ntuned; ++i)
+      if (p->tuned[i].N == N) shape = &p->tuned[i];
+  const DevPacking& pk = shape ? p->pk[shape->pack] : choose_packing(p, N);
+  LaunchCfg cfg = choose_cfg(pk, p->num_cus, N);
+  if (shape) {
+    cfg.waves = shape->waves;
+    cfg.n_rb = (pk.npanels + cfg.waves - 1) / cfg.waves;
+  }
   const SpmmPtrs ptrs{pk.entries, pk.panel_start, pk.panel_rows, B, C, bias};
   SpmmArgs args;
   args.K = p->K;
@@ -339,13 +351,58 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
 
 hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                        const float* bias, int epi, hipStream_t stream) {
-  return launch_panels(p, B, C, N, bias, epi, nullptr, stream);
+  return launch_panels(p, B, C, N, bias, epi, nullptr, nullptr, stream);
+}
+
+hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStream_t stream,
+                     TunedShape* chosen) {
+  // candidates: every packing, each with its register-limited consumer count and
+  // three fewer-wave shapes, plus the heuristic's own choice
+  std::vector<TunedShape> cands;
+  for (int k = 0; k < p->npack; ++k) {
+    const int cap = std::min(max_consumers(p->pk[k].RW), p->pk[k].npanels);
+    const int heur = choose_cfg(p->pk[k], p->num_cus, N).waves;
+    for (int w : {cap, (3 * cap) / 4, cap / 2, cap / 4, heur}) {
+      if (w < 1) continue;
+      bool dup = false;
+      for (const TunedShape& t : cands) dup |= (t.pack == k && t.waves == w);
+      if (!dup) cands.push_back(TunedShape{N, k, w});
+    }
+  }
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  hipError_t err = hipEventCreate(&e0);
+  if (err == hipSuccess) err = hipEventCreate(&e1);
+  float best = -1.0f;
+  for (size_t i = 0; i < cands.size() && err == hipSuccess; ++i) {
+    for (int r = 0; r < 2 && err == hipSuccess; ++r)   // warm-up
+      err = launch_panels(p, B, C, N, nullptr, 0, nullptr, &cands[i], stream);
+    if (err == hipSuccess) err = hipEventRecord(e0, stream);
+    for (int r = 0; r < 5 && err == hipSuccess; ++r)
+      err = launch_panels(p, B, C, N, nullptr, 0, nullptr, &cands[i], stream);
+    if (err == hipSuccess) err = hipEventRecord(e1, stream);
+    if (err == hipSuccess) err = hipEventSynchronize(e1);
+    float ms = 0.0f;
+    if (err == hipSuccess) err = hipEventElapsedTime(&ms, e0, e1);
+    if (err == hipSuccess && (best < 0.0f || ms < best)) {
+      best = ms;
+      *chosen = cands[i];
+    }
+  }
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (err != hipSuccess) return err;
+  int slot = -1;
+  for (int i = 0; i < p->ntuned; ++i)
+    if (p->tuned[i].N == N) slot = i;
+  if (slot < 0) slot = p->ntuned < kTunedSlots ? p->ntuned++ : (int)(N % kTunedSlots);
+  p->tuned[slot] = *chosen;
+  return hipSuccess;
 }
 
 hipError_t launch_conv3x3(const sdnn_plan_s* p, const float* X, float* C, int32_t H, int32_t W,
                           int32_t NB, const float* bias, int epi, hipStream_t stream) {
   const int32_t hwn[3] = {H, W, NB};
-  return launch_panels(p, X, C, H * W * NB, bias, epi, hwn, stream);
+  return launch_panels(p, X, C, H * W * NB, bias, epi, hwn, nullptr, stream);
 }
 
 // ---------------------------------------------------------------------------------

@@ -268,6 +268,26 @@ def test_balanced_order():
         assert np.all(np.abs(got - ref) <= tolerance(bound, ref, L.epi))
 
 
+def test_plan_tune():
+    """sdnn_plan_tune times the plan's launch shapes at one N and records the fastest;
+    later calls at that N use it and give bit-identical results (each row still sums in
+    ascending column order), other N keep the heuristic."""
+    w = inputs.workload("c2")
+    L = w.layers[0]
+    with sd.Plan.from_csr(L.W) as plan:
+        before = gpu_spmm(plan, w.B, L.bias, L.epi)
+        shape = plan.tune(w.N)
+        assert shape["panel_rows"] in (4, 12) and 1 <= shape["waves"] <= 12
+        after = gpu_spmm(plan, w.B, L.bias, L.epi)
+        assert np.array_equal(before, after)
+        B2 = inputs.dense_B(L.W.K, 300, inputs.CFG_TEST, 61)
+        other = gpu_spmm(plan, B2, L.bias, L.epi)
+    ref, bound = oracle.spmm_f64(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.K, w.B, L.bias, L.epi)
+    assert np.all(np.abs(after - ref) <= tolerance(bound, ref, L.epi))
+    ref2, bound2 = oracle.spmm_f64(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.K, B2, L.bias, L.epi)
+    assert np.all(np.abs(other - ref2) <= tolerance(bound2, ref2, L.epi))
+
+
 def test_permute_off_and_on_agree():
     W = inputs.pattern_grouped8(256, 512, 0.05, inputs.CFG_TEST, 9, 0.05)
     B = inputs.dense_B(512, 256, inputs.CFG_TEST, 9)
