@@ -190,6 +190,20 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
       P.entries.push_back(0u);
     }
     P.rho = union_total ? (double)P.nnz / (double)union_total : 1.0;
+    // workgroup order: panels by stored groups, heaviest first (ties: lower panel), so
+    // that consecutive panels -- one workgroup's -- carry similar work and the heaviest
+    // workgroups are dispatched first
+    std::vector<int64_t> groups((size_t)P.npanels, 0);
+    for (int32_t p = 0; p < P.npanels; ++p) {
+      if (P.panel_start[p] < 0) continue;
+      int64_t g = P.panel_start[p];
+      while (!((P.entries[(size_t)g * 2 * kGroup + kGroup + kHiWord] >> kEndBit) & 1u)) ++g;
+      groups[p] = g + 1 - P.panel_start[p];
+    }
+    P.panel_order.resize((size_t)P.npanels);
+    for (int32_t p = 0; p < P.npanels; ++p) P.panel_order[p] = p;
+    std::stable_sort(P.panel_order.begin(), P.panel_order.end(),
+                     [&](int32_t a, int32_t b) { return groups[a] > groups[b]; });
   } catch (const std::bad_alloc&) {
     return SDNN_ERR_ALLOC;
   }
@@ -283,6 +297,25 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
     }
   }
   if (expect_group != ngroups) return false;
+  // panel_order: a permutation of the panels, by stored groups (descending)
+  if ((int64_t)P.panel_order.size() != P.npanels) return false;
+  {
+    std::vector<char> used((size_t)std::max(P.npanels, 1), 0);
+    int64_t prev = INT64_MAX;
+    for (int32_t j = 0; j < P.npanels; ++j) {
+      const int32_t p = P.panel_order[j];
+      if (p < 0 || p >= P.npanels || used[p]) return false;
+      used[p] = 1;
+      int64_t g = 0;
+      if (P.panel_start[p] >= 0) {
+        int64_t e = P.panel_start[p];
+        while (!((P.entries[(size_t)e * 2 * kGroup + kGroup + kHiWord] >> kEndBit) & 1u)) ++e;
+        g = e + 1 - P.panel_start[p];
+      }
+      if (g > prev) return false;
+      prev = g;
+    }
+  }
   for (int64_t q = 0; q < P.nnz; ++q)
     if (!seen[q]) return false;
   for (size_t d = (size_t)(2 * P.stored); d < P.entries.size(); ++d)
@@ -477,7 +510,7 @@ static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 // Device bytes of one packing's three arrays (each 256-byte aligned).
 static int64_t packing_bytes(const Packed& P) {
   return align256((int64_t)P.entries.size() * 4) + align256((int64_t)P.panel_start.size() * 4) +
-         align256((int64_t)P.panel_rows.size() * 4);
+         align256((int64_t)P.panel_rows.size() * 4) + align256((int64_t)P.panel_order.size() * 4);
 }
 
 }  // namespace sdnn
@@ -582,6 +615,7 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
         DevPacking& d = plan->pk[i];
         const int64_t b_ent = align256((int64_t)P.entries.size() * 4);
         const int64_t b_seg = align256((int64_t)P.panel_start.size() * 4);
+        const int64_t b_rows = align256((int64_t)P.panel_rows.size() * 4);
         char* base = (char*)plan->d_mem + off;
         d.RW = P.RW;
         d.npanels = P.npanels;
@@ -590,12 +624,19 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
         d.entries = (const uint32_t*)base;
         d.panel_start = (const int32_t*)(base + b_ent);
         d.panel_rows = (const int32_t*)(base + b_ent + b_seg);
+        d.panel_pos = (const int32_t*)(base + b_ent + b_seg + b_rows);
+        // panel tables in workgroup (slot) order: slot j is panel panel_order[j]
         char* h = host.data() + off;
         if (!P.entries.empty()) memcpy(h, P.entries.data(), P.entries.size() * 4);
-        if (!P.panel_start.empty())
-          memcpy(h + b_ent, P.panel_start.data(), P.panel_start.size() * 4);
-        if (!P.panel_rows.empty())
-          memcpy(h + b_ent + b_seg, P.panel_rows.data(), P.panel_rows.size() * 4);
+        int32_t* hs = (int32_t*)(h + b_ent);
+        int32_t* hr = (int32_t*)(h + b_ent + b_seg);
+        int32_t* hp = (int32_t*)(h + b_ent + b_seg + b_rows);
+        for (int32_t j = 0; j < P.npanels; ++j) {
+          const int32_t q = P.panel_order[j];
+          hs[j] = P.panel_start[q];
+          memcpy(hr + (size_t)j * P.RW, P.panel_rows.data() + (size_t)q * P.RW, 4 * (size_t)P.RW);
+          hp[j] = q;
+        }
         off += packing_bytes(P);
       }
       if (hipMemcpy(plan->d_mem, host.data(), (size_t)total, hipMemcpyHostToDevice) !=

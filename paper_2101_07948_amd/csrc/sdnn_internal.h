@@ -60,6 +60,7 @@ struct Packed {
   std::vector<int32_t> perm;        // [M]   original row at permuted position
   std::vector<int32_t> panel_rows;  // [npanels*RW] original row or -1 (padding)
   std::vector<int32_t> panel_start; // [npanels] first group of the panel, or -1
+  std::vector<int32_t> panel_order; // [npanels] panels by stored groups, heaviest first
   std::vector<uint32_t> entries;    // [2*(stored + kTailGroups*kGroup)] dwords
   double rho = 1.0;                 // nnz / sum_p |union of the panel's column sets|
 };
@@ -93,6 +94,9 @@ struct DevPacking {
   const uint32_t* entries = nullptr;      // [2*(stored + kTailGroups*kGroup)] dwords
   const int32_t* panel_start = nullptr;   // [npanels] (in groups, -1: empty panel)
   const int32_t* panel_rows = nullptr;    // [npanels*RW]
+  const int32_t* panel_pos = nullptr;     // [npanels] panel index of each slot
+  // (panel_start and panel_rows are uploaded in slot order: slot j holds panel
+  // panel_pos[j], the j-th heaviest; workgroups take consecutive slots)
 };
 
 }  // namespace sdnn

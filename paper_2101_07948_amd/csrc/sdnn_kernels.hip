@@ -20,7 +20,11 @@
 //     chunk each consumer still reads), so no wave ever waits at a workgroup barrier
 //     for the slowest one; the loops are generated inline assembly (spmm_asm_gen.h);
 //   * the bias + activation epilogue is fused and C is written once, coalesced, to
-//     the original (unpermuted) row.
+//     the original (unpermuted) row, or to the permuted position when the plan keeps
+//     rows permuted for the next layer (Sec. 3.1.2);
+//   * the same kernel computes a sparse 3x3 convolution (Sec. 3.2.3, direct
+//     convolution): a third producer kind stages the rows of the virtual dense operand
+//     (input channel x filter tap) straight from the input activations.
 // Plain FP32 FMA is used throughout (no MFMA: the work is not a dense contraction).
 //
 // Workgroups: one 256-column tile x one row-block of nc consecutive panels, plus the
@@ -117,7 +121,8 @@ enum { kStageDword = 0, kStageVec = 1, kStageConv = 2 };
 template <int RW, int STAGE>
 __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     const uint32_t* __restrict__ entries, const int32_t* __restrict__ panel_start,
-    const int32_t* __restrict__ panel_rows, const float* __restrict__ B, float* __restrict__ C, const float* __restrict__ bias,
+    const int32_t* __restrict__ panel_rows, const int32_t* __restrict__ panel_pos,
+    const float* __restrict__ B, float* __restrict__ C, const float* __restrict__ bias,
     SpmmArgs a) {
   // the ring ([0, kRingBytes)) and the control words; the ring must start at LDS 0
   // (the loops form LDS addresses from the ring-row field alone), which holds because
@@ -210,7 +215,7 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     const int orig = panel_rows[panel * RW + r];
     if (orig < 0) continue;
     const float bb = bias ? bias[orig] : 0.0f;
-    float* crow = C + (size_t)(a.out_permuted ? panel * RW + r : orig) * a.N;
+    float* crow = C + (size_t)(a.out_permuted ? panel_pos[panel] * RW + r : orig) * a.N;
     const float v[4] = {p0[r], p1[r], p2[r], p3[r]};
     if (STAGE != kStageDword && ncol + 4 <= a.N) {
       *reinterpret_cast<float4*>(crow + ncol) =
@@ -228,6 +233,7 @@ struct SpmmPtrs {
   const uint32_t* entries;
   const int32_t* panel_start;
   const int32_t* panel_rows;
+  const int32_t* panel_pos;
   const float* B;
   float* C;
   const float* bias;
@@ -237,7 +243,7 @@ template <int RW, int STAGE>
 hipError_t launch_variant(const SpmmPtrs& p, const SpmmArgs& args, int waves, int grid,
                           hipStream_t stream) {
   hipLaunchKernelGGL((spmm_panel_kernel<RW, STAGE>), dim3(grid), dim3(64 * (waves + kProducers)), 0, stream,
-                     p.entries, p.panel_start, p.panel_rows, p.B, p.C, p.bias,
+                     p.entries, p.panel_start, p.panel_rows, p.panel_pos, p.B, p.C, p.bias,
                      args);
   return hipGetLastError();
 }
@@ -322,7 +328,7 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
     cfg.waves = shape->waves;
     cfg.n_rb = (pk.npanels + cfg.waves - 1) / cfg.waves;
   }
-  const SpmmPtrs ptrs{pk.entries, pk.panel_start, pk.panel_rows, B, C, bias};
+  const SpmmPtrs ptrs{pk.entries, pk.panel_start, pk.panel_rows, pk.panel_pos, B, C, bias};
   SpmmArgs args;
   args.K = p->K;
   args.N = N;
