@@ -169,6 +169,39 @@ def test_edge_cases():
               label=f"M={M} K={K}")
 
 
+def test_large_shapes():
+    """Long K (3125 chunks: the stream spans the whole ring many times over), many rows
+    with few columns, and one row with every column set."""
+    rng = np.random.default_rng(71)
+    for (M, K, N, d) in ((24, 100000, 96, 0.02), (20000, 96, 260, 0.1), (1, 4096, 512, 1.0)):
+        rp, ci, v, _ = random_csr(rng, M, K, d)
+        B = rng.standard_normal((K, N)).astype(np.float32)
+        check(rp, ci, v, M, K, B, rng.standard_normal(M).astype(np.float32), "none",
+              label=f"M={M} K={K} N={N}")
+
+
+def test_c5_full_stack_sampled_columns():
+    """The whole C5 workload: 12 encoder layers x 6 products, 97 % block-correlated, at
+    N = 16384 on the GPU, chained on its own outputs.  Columns are independent, so the
+    oracle follows the same chain on 256 sampled columns: each layer's GPU output on
+    those columns is checked against the oracle applied to the GPU's previous output."""
+    w = inputs.workload("c5", N=16384)
+    cols = np.sort(np.random.default_rng(72).choice(w.N, 256, replace=False))
+    X = torch.from_numpy(w.B).to(DEV)
+    for i, L in enumerate(w.layers):
+        with sd.Plan.from_csr(L.W) as plan:
+            Y = torch.empty((L.W.M, w.N), device=DEV)
+            bt = None if L.bias is None else torch.from_numpy(L.bias).to(DEV)
+            plan.spmm(X, Y, bt, L.epi)
+            torch.cuda.synchronize()
+        xs = X[:, cols].cpu().numpy()
+        ref, bound = oracle.spmm_f64(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.K, xs, L.bias, L.epi)
+        got = Y[:, cols].cpu().numpy().astype(np.float64)
+        tol = tolerance(bound, ref, L.epi)
+        assert np.all(np.abs(got - ref) <= tol), f"C5 product {i}: worst {np.max(np.abs(got - ref) / tol):.3g}"
+        X = Y
+
+
 def test_row_permutation_equivariance_bitexact():
     """Each row sums its entries in ascending column order whatever panel it lands in,
     so permuting W's rows permutes C's rows exactly."""
