@@ -9,6 +9,11 @@ Infinity Cache cannot hold a step's operands from the previous visit.
 Prints one JSON line.  Extra keys: roofline (the kernel against its bounding peak),
 cpu_baseline (the CPU oracle's fp32 CSR loop on the host cores), dense comparison
 kernel time, warm-cache rate.
+
+Other modes: --suite OUT.md times every configuration (cold/warm, median and p10/p90),
+the dense comparison, the row-order ablation, the chained C5 stack in both row spaces,
+the sparse 3x3 convolutions, the CPU oracle at 1/4/all threads and the machine probes;
+--summarize-pmc turns two rocprofv3 counter passes into profiles/traffic_spmm_w0.json.
 """
 from __future__ import annotations
 
