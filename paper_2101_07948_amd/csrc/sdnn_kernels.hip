@@ -276,37 +276,56 @@ struct LaunchCfg {
   int waves, n_tiles, n_rb;  // waves: consumer waves per workgroup (the producers come on top)
 };
 
-// Panels per workgroup: enough row-blocks that the grid covers every CU about once
-// (the 129 KB of ring and control LDS allows one workgroup per CU), at most as many
-// consumer waves as the panel height's register use allows.  SDNN_FORCE_WAVES fixes
-// the consumer count.
+// The 129 KB of ring and control LDS allow one workgroup per CU, so a grid of G
+// workgroups runs in ceil(G / CUs) rounds, and a partly filled last round costs as
+// much as a full one.
+int64_t rounds_of(int64_t n_tiles, int npanels, int waves, int target) {
+  const int64_t wgs = n_tiles * ((npanels + waves - 1) / waves);
+  return (wgs + target - 1) / target;
+}
+
+// Consumer waves per workgroup: the fewest rounds that the register-limited consumer
+// count allows, and within that many rounds the smallest workgroups (fewest panels
+// each, so the most workgroups share the work).  SDNN_FORCE_WAVES fixes the count.
 LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N) {
   const int target = num_cus > 0 ? num_cus : 256;
-  const int cap = max_consumers(pk.RW);
+  int cap = max_consumers(pk.RW);
+  if (cap > pk.npanels) cap = pk.npanels;
+  if (cap < 1) cap = 1;
   const int forceW = env_int("SDNN_FORCE_WAVES", 0);
   LaunchCfg c;
   c.n_tiles = (N + kTileCols - 1) / kTileCols;
   if (forceW > 0) {
-    c.waves = forceW;
+    c.waves = forceW < cap ? forceW : cap;
   } else {
-    int n_rb = (target + c.n_tiles - 1) / c.n_tiles;
-    if (n_rb > pk.npanels) n_rb = pk.npanels;
-    c.waves = (pk.npanels + n_rb - 1) / n_rb;
+    const int64_t fewest = rounds_of(c.n_tiles, pk.npanels, cap, target);
+    c.waves = cap;
+    for (int w = 1; w < cap; ++w)
+      if (rounds_of(c.n_tiles, pk.npanels, w, target) == fewest) {
+        c.waves = w;
+        break;
+      }
   }
-  if (c.waves > cap) c.waves = cap;
-  if (c.waves > pk.npanels) c.waves = pk.npanels;
-  if (c.waves < 1) c.waves = 1;
   c.n_rb = (pk.npanels + c.waves - 1) / c.waves;
   return c;
 }
 
-// The packing a call runs on: the tall one (second) once the tiles hold at least a
-// full workgroup of tall panels per CU, else the first.
-const DevPacking& choose_packing(const sdnn_plan_s* p, int N) {
+// The packing a call runs on.  A product: the tall one (second) once the tiles hold
+// at least a full workgroup of tall panels per CU, else the first.  A convolution,
+// whose workgroups are bound by staging its shifted input rows rather than by their
+// panels: the packing that needs fewer rounds, the first on a tie.
+const DevPacking& choose_packing(const sdnn_plan_s* p, int N, bool conv) {
   if (p->npack < 2) return p->pk[0];
   const DevPacking& tall = p->pk[1];
   const int64_t n_tiles = (N + kTileCols - 1) / kTileCols;
-  const int64_t cus = p->num_cus > 0 ? p->num_cus : 256;
+  const int cus = p->num_cus > 0 ? p->num_cus : 256;
+  if (conv) {
+    const LaunchCfg s = choose_cfg(p->pk[0], cus, N), t = choose_cfg(tall, cus, N);
+    return rounds_of(n_tiles, tall.npanels, t.waves, cus) <
+                   rounds_of(n_tiles, p->pk[0].npanels, s.waves, cus)
+               ? tall
+               : p->pk[0];
+  }
   const int64_t wg_rows = (int64_t)max_consumers(tall.RW) * tall.RW;
   return (int64_t)p->M * n_tiles >= wg_rows * cus ? tall : p->pk[0];
 }
@@ -315,14 +334,15 @@ const DevPacking& choose_packing(const sdnn_plan_s* p, int N) {
 
 namespace {
 // `shape` (packing index and consumer waves) overrides the plan's tuned or heuristic
-// choice when non-null.
+// choice when non-null.  Tuned shapes were timed on products, so a convolution, whose
+// staging differs, keeps the heuristic.
 hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                          const float* bias, int epi, const int32_t* conv_hwn,
                          const TunedShape* shape, hipStream_t stream) {
-  if (!shape)
+  if (!shape && !conv_hwn)
     for (int i = 0; i < p->ntuned; ++i)
       if (p->tuned[i].N == N) shape = &p->tuned[i];
-  const DevPacking& pk = shape ? p->pk[shape->pack] : choose_packing(p, N);
+  const DevPacking& pk = shape ? p->pk[shape->pack] : choose_packing(p, N, conv_hwn != nullptr);
   LaunchCfg cfg = choose_cfg(pk, p->num_cus, N);
   if (shape) {
     cfg.waves = shape->waves;

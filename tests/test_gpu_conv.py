@@ -62,13 +62,23 @@ def test_conv_parity(OC, IC, H, W, NB, sparsity, epi):
 
 
 def test_conv_tall_panels_and_out_permuted():
-    """OC * ceil(N / 256) = 96 * 256 reaches the tall-panel threshold on 256 CUs; the
-    out_permuted plan writes output channels in its permutation order."""
+    """96 channels over 256 column tiles: 4-row panels need two rounds of workgroups on
+    256 CUs, 12-row panels one, so the call runs on the tall packing; the out_permuted
+    plan writes output channels in its permutation order."""
     L = inputs.conv_layer(96, 16, 32, 32, 64, 0.9, layer=5, epi="relu")
     got = check_conv(L, "tall")
     gotp = check_conv(L, "tall permuted", out_permuted=True)
     with sd.Plan.from_csr(L.F) as plan:
         assert np.array_equal(gotp, got[plan.perm])
+
+
+@pytest.mark.parametrize("OC,IC,HW", [(64, 64, 56), (128, 128, 28), (256, 256, 14)])
+def test_conv_benchmark_shapes(OC, IC, HW):
+    """The timed convolution shapes (16 images, 90 %): 64 x 64 on 56 x 56 runs on the
+    tall packing (one round of workgroups instead of two), 128 x 128 on 28 x 28 on
+    4-row panels with enough consumer waves per workgroup to fit one round."""
+    L = inputs.conv_layer(OC, IC, HW, HW, 16, 0.9, layer=OC + HW)
+    check_conv(L, f"{OC}x{IC} {HW}x{HW}x16")
 
 
 def test_conv_chain():
