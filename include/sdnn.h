@@ -67,7 +67,10 @@ typedef enum {
  *                 2 = panel-balancing order: rows, by nonzero count descending, each
  *                 go to the 4-row panel with the fewest nonzeros so far that has room,
  *                 so that every panel (and every 12-row panel) carries about the same
- *                 work.
+ *                 work.  3 = panel-union greedy: 4-row panels filled in turn, each
+ *                 headed by the remaining row with the most nonzeros and continued
+ *                 by the remaining row with the largest overlap with the union of
+ *                 the panel's column sets so far (ties: more nonzeros, lower index).
  *   out_permuted: 0 (default) = C row i is output row i; 1 = C is written in the
  *                 plan's permuted row order, C row i = output row perm[i] (Sec. 3.1.2:
  *                 the rows stay permuted and the next layer's columns compensate).
@@ -111,6 +114,17 @@ typedef struct {
  * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM, SDNN_ERR_CSR, SDNN_ERR_ALLOC. */
 sdnn_status sdnn_reorder_rows(const int32_t* row_ptr, const int32_t* col_idx, int32_t M,
                               int32_t K, int32_t* perm_out);
+
+/* The row order a plan with option `permute` uses (see sdnn_plan_opts), host only, no
+ * GPU needed: 0 identity, 1 Algorithm 1 (as sdnn_reorder_rows), 2 panel-balancing,
+ * 3 panel-union greedy.  Sec. 3.1.2 notes that other reorderings (hashing,
+ * clustering) performed comparably to Algorithm 1; orders 2 and 3 are two such
+ * alternatives aimed at the 4-row panels the kernel runs.  perm_out[i] is the
+ * original row placed at position i; M entries, caller-owned.
+ * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM (negative sizes, permute outside 0..3),
+ * SDNN_ERR_CSR, SDNN_ERR_ALLOC. */
+sdnn_status sdnn_row_order(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K,
+                           int32_t permute, int32_t* perm_out);
 
 /* Preparation stage (Sec. 2.1, Sec. 3.1.2, Sec. 3.2.2).  Validates the host CSR,
  * computes the row permutation, packs W into the kernel's traversal-ordered stream

@@ -65,6 +65,7 @@ def lib() -> ctypes.CDLL:
         L.sdnn_status_str.argtypes = [ctypes.c_int]
         L.sdnn_status_str.restype = ctypes.c_char_p
         L.sdnn_reorder_rows.argtypes = [p, p, i32, i32, p]
+        L.sdnn_row_order.argtypes = [p, p, i32, i32, i32, p]
         L.sdnn_plan_check_host.argtypes = [p, p, p, i32, i32, ctypes.POINTER(PlanOpts),
                                            ctypes.POINTER(PlanInfo)]
         L.sdnn_plan_create.argtypes = [p, p, p, i32, i32, ctypes.POINTER(PlanOpts),
@@ -77,7 +78,7 @@ def lib() -> ctypes.CDLL:
         L.sdnn_dense_gemm.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
         L.sdnn_conv3x3.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
         L.sdnn_plan_tune.argtypes = [p, p, p, i32, p, p, p]
-        for fn in ("sdnn_reorder_rows", "sdnn_plan_check_host", "sdnn_plan_create",
+        for fn in ("sdnn_reorder_rows", "sdnn_row_order", "sdnn_plan_check_host", "sdnn_plan_create",
                    "sdnn_plan_get_perm", "sdnn_plan_info", "sdnn_spmm", "sdnn_dense_gemm",
                    "sdnn_conv3x3", "sdnn_plan_tune"):
             getattr(L, fn).restype = ctypes.c_int
@@ -102,15 +103,23 @@ def _np_ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
+ORDERS = {"identity": 0, "algorithm1": 1, "balanced": 2, "panel_union": 3}
+
+
+def _order_mode(permute) -> int:
+    """Plan option `permute` from a name in ORDERS, a bool (Algorithm 1 or identity)
+    or its number."""
+    if isinstance(permute, str):
+        return ORDERS[permute]
+    return (1 if permute else 0) if isinstance(permute, bool) else int(permute)
+
+
 def _opts(K: int, panel_rows: int, permute: bool, out_permuted: bool = False, in_perm=None):
     """PlanOpts plus the in_perm array it points to (kept alive by the caller)."""
     keep = None if in_perm is None else _i32(in_perm)
     if keep is not None and keep.shape != (int(K),):
         raise ValueError(f"in_perm must hold K = {K} entries, got shape {keep.shape}")
-    if isinstance(permute, str):   # "identity", "algorithm1" or "balanced"
-        mode = {"identity": 0, "algorithm1": 1, "balanced": 2}[permute]
-    else:
-        mode = (1 if permute else 0) if isinstance(permute, bool) else int(permute)
+    mode = _order_mode(permute)
     o = PlanOpts(int(panel_rows), mode, 1 if out_permuted else 0, 0,
                  None if keep is None else keep.ctypes.data)
     return o, keep
@@ -123,6 +132,17 @@ def reorder_rows(row_ptr, col_idx, K: int) -> np.ndarray:
     perm = np.empty(M, dtype=np.int32)
     _check(lib().sdnn_reorder_rows(_np_ptr(row_ptr), _np_ptr(col_idx), M, K, _np_ptr(perm)),
            "sdnn_reorder_rows")
+    return perm
+
+
+def row_order(row_ptr, col_idx, K: int, permute="algorithm1") -> np.ndarray:
+    """The row order of plan option `permute` (a name in ORDERS or its number),
+    computed by the library on the host: perm[i] is the original row at position i."""
+    row_ptr, col_idx = _i32(row_ptr), _i32(col_idx)
+    M = row_ptr.shape[0] - 1
+    perm = np.empty(M, dtype=np.int32)
+    _check(lib().sdnn_row_order(_np_ptr(row_ptr), _np_ptr(col_idx), M, K,
+                                _order_mode(permute), _np_ptr(perm)), "sdnn_row_order")
     return perm
 
 

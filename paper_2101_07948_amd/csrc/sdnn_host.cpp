@@ -332,7 +332,7 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
 // Resolved plan options.
 struct Options {
   std::vector<int32_t> rws;      // panel heights to pack
-  int32_t permute = 1;           // apply Algorithm 1
+  int32_t permute = 1;           // row order: Algorithm 1 (see row_order)
   int32_t out_permuted = 0;      // store C in the permuted row order
   const int32_t* in_perm = nullptr;  // order of B's rows (NULL: original)
 };
@@ -347,7 +347,7 @@ static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* 
       return SDNN_ERR_DIM;
     o->rws = {opts->panel_rows};
   }
-  if (opts->permute < 0 || opts->permute > 2) return SDNN_ERR_DIM;
+  if (opts->permute < 0 || opts->permute > 3) return SDNN_ERR_DIM;
   if (opts->out_permuted != 0 && opts->out_permuted != 1) return SDNN_ERR_DIM;
   o->permute = opts->permute;
   o->out_permuted = opts->out_permuted;
@@ -439,7 +439,83 @@ static void relabel_columns(const int32_t* row_ptr, const int32_t* col_idx, cons
   v->values = v->vals.data();
 }
 
-// Validation, column relabelling (with in_perm), Algorithm 1 (once: its keys do not
+// Panel-union greedy order (plan option permute = 3), a panel-aware variant of
+// Algorithm 1: positions are filled one 4-row panel at a time; a panel's first row is
+// the remaining row with the most nonzeros, and each further row is the remaining row
+// whose column set overlaps most with the union of the column sets already in the
+// panel (Algorithm 1 compares with the previous row only).  Ties: more nonzeros, then
+// the lower original index.  A tall panel is three consecutive short panels.
+static sdnn_status panel_union_order(const int32_t* row_ptr, const int32_t* col_idx, int32_t M,
+                                     int32_t K, int32_t* perm_out) {
+  if (M == 0) return SDNN_OK;
+  const int64_t words = std::max<int64_t>((K + 63) / 64, 1);
+  std::vector<uint64_t> bits, uni;
+  std::vector<int32_t> remaining;
+  try {
+    bits.assign((size_t)M * (size_t)words, 0);
+    uni.assign((size_t)words, 0);
+    remaining.resize(M);
+  } catch (const std::bad_alloc&) {
+    return SDNN_ERR_ALLOC;
+  }
+  for (int32_t i = 0; i < M; ++i) {
+    uint64_t* row = bits.data() + (size_t)i * words;
+    for (int32_t p = row_ptr[i]; p < row_ptr[i + 1]; ++p)
+      row[col_idx[p] >> 6] |= 1ull << (col_idx[p] & 63);
+  }
+  auto nnz = [&](int32_t x) { return row_ptr[x + 1] - row_ptr[x]; };
+  // remaining rows in ascending index order, so a strict improvement keeps the lower
+  // index among equal keys
+  int32_t nrem = M;
+  for (int32_t x = 0; x < M; ++x) remaining[x] = x;
+  for (int32_t i = 0; i < M; ++i) {
+    const bool head = i % kShortPanel == 0;
+    if (head) std::fill(uni.begin(), uni.end(), 0ull);
+    int32_t best_pos = 0, best_ov = -1, best_nnz = -1;
+    for (int32_t j = 0; j < nrem; ++j) {
+      const int32_t x = remaining[j];
+      int32_t ov = 0;
+      if (!head) {
+        const uint64_t* row = bits.data() + (size_t)x * words;
+        for (int64_t w = 0; w < words; ++w) ov += __builtin_popcountll(uni[w] & row[w]);
+      }
+      const int32_t nx = nnz(x);
+      if (ov > best_ov || (ov == best_ov && nx > best_nnz)) {
+        best_pos = j;
+        best_ov = ov;
+        best_nnz = nx;
+      }
+    }
+    const int32_t pick = remaining[best_pos];
+    perm_out[i] = pick;
+    const uint64_t* row = bits.data() + (size_t)pick * words;
+    for (int64_t w = 0; w < words; ++w) uni[w] |= row[w];
+    memmove(remaining.data() + best_pos, remaining.data() + best_pos + 1,
+            sizeof(int32_t) * (size_t)(nrem - best_pos - 1));
+    --nrem;
+  }
+  return SDNN_OK;
+}
+
+// The row order of plan option `permute` (0 identity, 1 Algorithm 1, 2 panel-balancing,
+// 3 panel-union greedy) for a validated CSR.
+static sdnn_status row_order(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K,
+                             int32_t permute, int32_t* perm_out) {
+  switch (permute) {
+    case 1:
+      return reorder_bitset(row_ptr, col_idx, M, K, perm_out);
+    case 2:
+      balanced_order(row_ptr, M, perm_out);
+      return SDNN_OK;
+    case 3:
+      return panel_union_order(row_ptr, col_idx, M, K, perm_out);
+    default:
+      for (int32_t i = 0; i < M; ++i) perm_out[i] = i;
+      return SDNN_OK;
+  }
+}
+
+// Validation, column relabelling (with in_perm), the row order (once: its keys do not
 // depend on column names) and one packing per panel height.  *csr is what was packed.
 static sdnn_status prepare(const int32_t* row_ptr, const int32_t* col_idx, const float* values,
                            int32_t M, int32_t K, const sdnn_plan_opts* opts,
@@ -463,14 +539,8 @@ static sdnn_status prepare(const int32_t* row_ptr, const int32_t* col_idx, const
   } catch (const std::bad_alloc&) {
     return SDNN_ERR_ALLOC;
   }
-  if (o->permute == 1) {
-    st = reorder_bitset(csr->row_ptr, csr->col_idx, M, K, perm.data());
-    if (st != SDNN_OK) return st;
-  } else if (o->permute == 2) {
-    balanced_order(csr->row_ptr, M, perm.data());
-  } else {
-    for (int32_t i = 0; i < M; ++i) perm[i] = i;
-  }
+  st = row_order(csr->row_ptr, csr->col_idx, M, K, o->permute, perm.data());
+  if (st != SDNN_OK) return st;
   for (size_t i = 0; i < o->rws.size(); ++i) {
     st = pack(csr->row_ptr, csr->col_idx, csr->values, M, K, o->rws[i], perm.data(),
               &(*packs)[i]);
@@ -531,6 +601,19 @@ const char* sdnn_status_str(sdnn_status s) {
     case SDNN_ERR_INTERNAL: return "SDNN_ERR_INTERNAL: packed stream failed its self-check";
   }
   return "SDNN_ERR_UNKNOWN";
+}
+
+sdnn_status sdnn_row_order(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K,
+                           int32_t permute, int32_t* perm_out) {
+  if (M < 0 || K < 0 || permute < 0 || permute > 3) return SDNN_ERR_DIM;
+  if (M > 0 && !perm_out) return SDNN_ERR_NULL;
+  sdnn_status st = validate_csr(row_ptr, col_idx, M, K);
+  if (st != SDNN_OK) return st;
+  try {
+    return row_order(row_ptr, col_idx, M, K, permute, perm_out);
+  } catch (...) {
+    return SDNN_ERR_ALLOC;
+  }
 }
 
 sdnn_status sdnn_reorder_rows(const int32_t* row_ptr, const int32_t* col_idx, int32_t M,
