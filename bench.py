@@ -12,7 +12,8 @@ kernel time, warm-cache rate.
 
 Other modes: --suite OUT.md times every configuration (cold/warm, median and p10/p90),
 the dense comparison, the row-order ablation, the chained C5 stack in both row spaces,
-the sparse 3x3 convolutions, the CPU oracle at 1/4/all threads and the machine probes;
+the sparse 3x3 convolutions, the paper-shaped kernel problems, the CPU oracle at 1/4/all
+threads and the machine probes;
 --summarize-pmc turns two rocprofv3 counter passes into profiles/traffic_spmm_w0.json.
 """
 from __future__ import annotations
@@ -183,6 +184,17 @@ def _time_layer(plan, L, N, reps=100, warmup=10, cold=True):
     return per, mean, nsets
 
 
+def _blas_time(Wd, B, C, reps=20):
+    """Mean ms of the vendor FP32 GEMM (torch.mm into C, TF32 off): a comparator only."""
+    import torch
+    torch.backends.cuda.matmul.allow_tf32 = False
+    fn = lambda i: torch.mm(Wd, B, out=C)
+    fn(0)
+    torch.cuda.synchronize()
+    _, mean = _launch_times(fn, reps)
+    return mean
+
+
 def _packing_used(info, M, N, cus):
     """Mirror of the launcher's choice (4-row unless the tall packing fills every CU)."""
     tall = info["tall_panel_rows"]
@@ -234,9 +246,11 @@ def run_suite(out_path):
                      f"{100*ab/t/1e9/HBM_PEAK_GBS:.1f} |")
         print(lines[-1], flush=True)
 
-    lines += ["", "## Dense comparison kernel (same layouts and epilogue)", "",
+    lines += ["", "## Dense comparison: the library's FP32 GEMM kernel (same layouts and epilogue) "
+              "and the vendor BLAS (torch.mm, FP32, TF32 off; GEMM only)", "",
               "| layer | dense us | dense-equivalent TFLOP/s | % of FP32 peak | "
-              "sparse speedup |", "|---|---|---|---|---|"]
+              "sparse speedup | BLAS us | BLAS TFLOP/s | speedup over BLAS |",
+              "|---|---|---|---|---|---|---|---|"]
     for label, L, N in _suite_layers():
         if not (label.startswith("C2") or label.startswith("C3 W1") or label == "W0 768x3072 90% N=4096"):
             continue
@@ -249,9 +263,12 @@ def run_suite(out_path):
         fn(0)
         torch.cuda.synchronize()
         _, dmean = _launch_times(fn, 10)
+        bmean = _blas_time(Wd, B, C)
         tf = 2.0 * W.M * W.K * N / (dmean * 1e-3) / 1e12
+        btf = 2.0 * W.M * W.K * N / (bmean * 1e-3) / 1e12
         lines.append(f"| {label} | {dmean*1e3:.1f} | {tf:.1f} | {100*tf/ALU_PEAK_TFLOPS:.1f} | "
-                     f"{dmean/timed[label]:.2f}x |")
+                     f"{dmean/timed[label]:.2f}x | {bmean*1e3:.1f} | {btf:.1f} | "
+                     f"{bmean/timed[label]:.2f}x |")
         print(lines[-1], flush=True)
         del Wd, B, C
 
@@ -328,10 +345,11 @@ def run_suite(out_path):
     # 32..256, images 7..56, padding 1, 90 / 95 %; 16 images per call on the GPU
     lines += ["", "## Sparse 3x3 convolution (stride 1, padding 1), 16 images per call", "",
               "Filters uniform-random at the stated sparsity; input (IC, H, W, 16).  Dense: "
-              "the comparison GEMM on the dense filters times a materialised im2col matrix "
-              "(building it is not timed).", "",
+              "the library's comparison GEMM, and the vendor BLAS (torch.mm, FP32), on the "
+              "dense filters times a materialised im2col matrix (building it is not timed).", "",
               "| OC x IC, image | sparsity | nnz | us (cold mean) | GFLOP/s | % ALU | "
-              "dense us | speedup |", "|---|---|---|---|---|---|---|---|"]
+              "dense us | speedup | BLAS us | speedup over BLAS |",
+              "|---|---|---|---|---|---|---|---|---|---|"]
     for OC, IC, HW in ((64, 64, 56), (128, 128, 28), (256, 256, 14), (256, 256, 7)):
         for sp in (0.9, 0.95):
             L = inputs.conv_layer(OC, IC, HW, HW, 16, sp, layer=OC + HW)
@@ -357,12 +375,45 @@ def run_suite(out_path):
             dfn(0)
             torch.cuda.synchronize()
             _, dmean = _launch_times(dfn, 10)
+            bmean = _blas_time(Wd, Bd, Cd)
             flop = 2.0 * L.F.nnz * N
             lines.append(f"| {OC} x {IC}, {HW}x{HW} | {int(sp*100)} % | {L.F.nnz} | {mean*1e3:.1f} | "
                          f"{flop/(mean*1e-3)/1e9:.0f} | {100*flop/(mean*1e-3)/1e12/ALU_PEAK_TFLOPS:.1f} | "
-                         f"{dmean*1e3:.1f} | {dmean/mean:.2f}x |")
+                         f"{dmean*1e3:.1f} | {dmean/mean:.2f}x | {bmean*1e3:.1f} | {bmean/mean:.2f}x |")
             print(lines[-1], flush=True)
             del Xs, Cs, Bd, Wd, Cd
+
+    # the paper's kernel problems (Sec. 4.1): square M = K from 256 to 2048, 70-95 %
+    # sparse by magnitude threshold of a Gaussian matrix, three batch widths
+    lines += ["", "## Paper-shaped kernel problems (Sec. 4.1): M = K, Gaussian magnitude threshold", "",
+              "Each cell: sparse GFLOP/s (cold mean of 50 launches) and, in brackets, the speedup "
+              "over the library's dense kernel and over the vendor BLAS (torch.mm, FP32) on a "
+              "dense W of the same shape.", "",
+              "| M = K | N | " + " | ".join(f"{int(sp*100)} %" for sp in inputs.S_SPARSITIES) +
+              " | dense TFLOP/s | BLAS TFLOP/s |",
+              "|---|---|" + "---|" * len(inputs.S_SPARSITIES) + "---|---|"]
+    for MK in (256, 512, 1024, 2048):
+        for N in (128, 512, 2048):
+            B = torch.randn(MK, N, device=dev)
+            C = torch.empty(MK, N, device=dev)
+            Wd = torch.randn(MK, MK, device=dev)
+            dfn = lambda i: sd.dense_gemm(Wd, B, C)
+            dfn(0)
+            torch.cuda.synchronize()
+            _, dmean = _launch_times(dfn, 10)
+            bmean = _blas_time(Wd, B, C)
+            cells = []
+            for sp in inputs.S_SPARSITIES:
+                L = inputs.s_layer(MK, MK, sp)
+                with sd.Plan.from_csr(L.W) as plan:
+                    _, mean, _ = _time_layer(plan, L, N, reps=50)
+                cells.append(f"{2.0 * L.W.nnz * N / (mean * 1e-3) / 1e9:.0f} "
+                             f"({dmean / mean:.1f}x, {bmean / mean:.1f}x)")
+            lines.append(f"| {MK} | {N} | " + " | ".join(cells) +
+                         f" | {2.0 * MK * MK * N / (dmean * 1e-3) / 1e12:.1f} | "
+                         f"{2.0 * MK * MK * N / (bmean * 1e-3) / 1e12:.1f} |")
+            print(lines[-1], flush=True)
+            del B, C, Wd
 
     # CPU oracle (fp32 CSR loop) at 1, 4 and all threads on W0 at N = 4096
     wl = inputs.workload("w0")
@@ -456,9 +507,10 @@ def main():
                          "WRITE_SIZE) of a --calib-copy run into per-launch HBM bytes and write "
                          f"{os.path.relpath(TRAFFIC_FILE, ROOT)}")
     ap.add_argument("--suite", metavar="OUT_MD",
-                    help="time every configuration, the dense comparison, the Algorithm 1 "
-                         "ablation, the chained C5 stack, the CPU oracle at 1/4/all threads "
-                         "and the machine probes; write a markdown report to OUT_MD")
+                    help="time every configuration, the dense comparison, the row-order "
+                         "ablation, the chained C5 stack, the convolutions, the paper-shaped "
+                         "kernel problems, the CPU oracle at 1/4/all threads and the machine "
+                         "probes; write a markdown report to OUT_MD")
     args = ap.parse_args()
     if args.suite:
         run_suite(args.suite)

@@ -257,6 +257,17 @@ def workload(name: str, N: Optional[int] = None, num_layers: Optional[int] = Non
     raise KeyError(name)
 
 
+S_SPARSITIES = (0.70, 0.80, 0.90, 0.95)
+
+
+def s_layer(M: int, K: int, sparsity: float) -> Layer:
+    """A paper-shaped kernel problem (Sec. 4.1: M, K from 256 to 2048, 70-95 % sparse):
+    the unit-Gaussian survivors of a magnitude threshold, no bias, no activation."""
+    grade = S_SPARSITIES.index(sparsity) if sparsity in S_SPARSITIES else 9
+    layer = (M // 256) * 1000 + (K // 256) * 10 + grade
+    return Layer(pattern_gauss_threshold(M, K, sparsity, CFG_S, layer), None, "none")
+
+
 @dataclasses.dataclass
 class ConvLayer:
     """A sparse 3x3 convolution (stride 1, padding 1): filters as an OC x (IC*9) CSR whose

@@ -107,6 +107,17 @@ def test_c5_first_encoder_layer_chain():
                   label=f"c5 layer {i}")
 
 
+@pytest.mark.parametrize("MK,sparsity,N", [(1024, 0.70, 128), (2048, 0.90, 512),
+                                            (512, 0.80, 2048), (256, 0.95, 130)])
+def test_paper_shaped_problems(MK, sparsity, N):
+    """The paper's kernel problems (Sec. 4.1): square W, the unit-Gaussian survivors of a
+    magnitude threshold at 70-95 % sparsity, batch widths 128-2048 (130: a ragged one)."""
+    L = inputs.s_layer(MK, MK, sparsity)
+    B = inputs.dense_B(MK, N, inputs.CFG_S, MK + N)
+    check(L.W.row_ptr, L.W.col_idx, L.W.values, MK, MK, B, None, "none",
+          label=f"S {MK} {sparsity} N={N}")
+
+
 @pytest.mark.parametrize("N", [1, 2, 3, 63, 64, 65, 255, 256, 257, 1000, 3136])
 def test_ragged_N(N):
     W = inputs.pattern_uniform(200, 300, 0.1, inputs.CFG_TEST, N, 0.05)

@@ -48,3 +48,15 @@ def test_gauss_threshold_keeps_largest():
     dense = inputs.rng_for(inputs.CFG_S, 0, inputs.T_PATTERN).standard_normal((32, 48))
     thr = np.sort(np.abs(dense).ravel())[-W.nnz]
     assert np.all(np.abs(W.values) >= np.float32(thr) * (1 - 1e-6))
+
+
+def test_paper_shaped_layers():
+    """s_layer: exact nonzero counts at every grade and a distinct seed per grade (the
+    threshold itself is pinned by test_gauss_threshold_keeps_largest)."""
+    seen = set()
+    for sp in inputs.S_SPARSITIES:
+        L = inputs.s_layer(256, 512, sp)
+        assert L.W.nnz == inputs.exact_nnz(256, 512, 1.0 - sp)
+        assert L.bias is None and L.epi == "none"
+        seen.add(L.W.values[:8].tobytes())
+    assert len(seen) == len(inputs.S_SPARSITIES)
