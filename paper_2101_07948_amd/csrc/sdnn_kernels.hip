@@ -84,10 +84,10 @@ static_assert(kAsmRingMask == (uint32_t)(kRing * kChunk - 1) << kRingRowShift,
 
 constexpr int kRingBytes = kRing * kChunk * 1024;
 // Threads per workgroup a panel height allows: the accumulators sit above the loop's
-// pinned VGPRs (kAsmAccBase + 4 * RW), so RW >= 8 needs more than the 128 VGPRs that
-// 16 waves per CU leave each wave.
+// pinned VGPRs and end at v[kAsmAccBase + 4 * RW - 1], so RW <= 8 fits the 128 VGPRs
+// that 16 waves per CU leave each wave, and RW >= 12 needs 12 waves per CU.
 template <int RW>
-constexpr int max_threads() { return kAsmAccBase + 4 * RW < 128 ? 1024 : 768; }
+constexpr int max_threads() { return kAsmAccBase + 4 * RW <= 128 ? 1024 : 768; }
 // LDS control words after the ring: ready[kProducers] at +0, progress[16] at +64, and
 // 16 bytes per producer at +512 that the convolution producer's filler loads write.
 constexpr int kCtlWords = 256;
