@@ -159,8 +159,9 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out);
  *   bias: device, M fp32 in original row order, or NULL (treated as zeros).
  *   With out_permuted plans, C row i is output row perm[i] (see sdnn_plan_opts); with
  *   in_perm plans, B's rows are in that order.
- * Asynchronous: no allocation, no synchronisation, no pointer retained.  A plan may
- * be used from several streams at once.  B must not overlap C or bias; the bias may
+ * Asynchronous: no allocation, no synchronisation, no pointer retained, so a call may
+ * be captured in a HIP graph and replayed.  A plan may be used from several streams at
+ * once.  B must not overlap C or bias; the bias may
  * not overlap C (SDNN_ERR_DIM).  Device faults surface at the caller's next sync.
  * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM, SDNN_ERR_DEVICE, SDNN_ERR_HIP. */
 sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,

@@ -349,6 +349,40 @@ def test_permute_off_and_on_agree():
     assert (np.abs(C0 - ref) <= 1e-5 * bound + 1e-6).all()
 
 
+def test_graph_capture_replays():
+    """sdnn_spmm neither allocates nor synchronises, so a call can be captured in a HIP
+    graph: replayed several times, with eager work and synchronisations between the
+    replays, every replay gives the eager result bit for bit."""
+    M, K, N = 700, 500, 1000
+    W = inputs.pattern_uniform(M, K, 0.1, inputs.CFG_TEST, 77, 0.05)
+    B = torch.from_numpy(inputs.dense_B(K, N, inputs.CFG_TEST, 77)).to(DEV)
+    bias = torch.from_numpy(inputs.bias_normal(M, inputs.CFG_TEST, 77, 0.02)).to(DEV)
+    with sd.Plan.from_csr(W) as plan:
+        C_eager = torch.empty(M, N, device=DEV)
+        plan.spmm(B, C_eager, bias, "gelu")
+        torch.cuda.synchronize()
+        C = torch.empty(M, N, device=DEV)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):  # a first call off the default stream before capture
+            plan.spmm(B, C, bias, "gelu")
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            plan.spmm(B, C, bias, "gelu")
+        for rep in range(4):
+            C.fill_(float("nan"))
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(C, C_eager), f"replay {rep}"
+    ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, K, B.cpu().numpy(),
+                                 bias.cpu().numpy(), "gelu")
+    err = np.abs(C_eager.cpu().numpy().astype(np.float64) - ref)
+    assert (err <= tolerance(bound, ref, "gelu")).all()
+
+
 def test_streams_and_concurrency():
     W = inputs.pattern_uniform(512, 512, 0.1, inputs.CFG_TEST, 11, 0.05)
     B1 = inputs.dense_B(512, 1024, inputs.CFG_TEST, 11)
