@@ -272,24 +272,25 @@ def run_suite(out_path):
         print(lines[-1], flush=True)
         del Wd, B, C
 
+    orders = (0, 1, 2, 3, 4, 5)
     lines += ["", "## Row order ablation: identity (permute = 0), Algorithm 1 (1), panel-"
-              "balancing (2), panel-union greedy (3); cold mean; rho of the packing the "
-              "call runs on", "",
-              "| layer | rho 0 | rho 1 | rho 2 | rho 3 | us 0 | us 1 | us 2 | us 3 | "
-              "speedup of Algorithm 1 |",
-              "|---|---|---|---|---|---|---|---|---|---|"]
+              "balancing (2), panel-union greedy (3), MinHash clustering (4), bin-then-"
+              "greedy (5); cold mean; rho of the packing the call runs on", "",
+              "| layer | " + " | ".join(f"rho {k}" for k in orders) + " | " +
+              " | ".join(f"us {k}" for k in orders) + " | speedup of Algorithm 1 |",
+              "|---|" + "---|" * (2 * len(orders) + 1)]
     for label, L, N in _suite_layers():
         if not (label.startswith("C2") or label.startswith("C3") or label.startswith("C5")
                 or label == "W0 768x3072 90% N=4096"):
             continue
         res = {}
-        for perm in (0, 1, 2, 3):
+        for perm in orders:
             with sd.Plan.from_csr(L.W, permute=perm) as plan:
                 _, rho = _packing_used(plan.info, L.W.M, N, cus)
                 _, mean, _ = _time_layer(plan, L, N, reps=50)
             res[perm] = (rho, mean)
-        lines.append(f"| {label} | " + " | ".join(f"{res[k][0]:.2f}" for k in range(4)) + " | "
-                     + " | ".join(f"{res[k][1]*1e3:.1f}" for k in range(4)) + " | "
+        lines.append(f"| {label} | " + " | ".join(f"{res[k][0]:.2f}" for k in orders) + " | "
+                     + " | ".join(f"{res[k][1]*1e3:.1f}" for k in orders) + " | "
                      f"{res[0][1]/res[1][1]:.2f}x |")
         print(lines[-1], flush=True)
 

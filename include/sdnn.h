@@ -71,6 +71,10 @@ typedef enum {
  *                 headed by the remaining row with the most nonzeros and continued
  *                 by the remaining row with the largest overlap with the union of
  *                 the panel's column sets so far (ties: more nonzeros, lower index).
+ *                 4 = MinHash clustering (locality-sensitive hashing): rows sorted by
+ *                 a 4-word MinHash signature of their column sets, then nonzeros
+ *                 descending, then index.  5 = bin-then-greedy: rows binned by
+ *                 floor(log2(nnz + 1)), densest bin first, Algorithm 1 within each bin.
  *   out_permuted: 0 (default) = C row i is output row i; 1 = C is written in the
  *                 plan's permuted row order, C row i = output row perm[i] (Sec. 3.1.2:
  *                 the rows stay permuted and the next layer's columns compensate).
@@ -117,11 +121,11 @@ sdnn_status sdnn_reorder_rows(const int32_t* row_ptr, const int32_t* col_idx, in
 
 /* The row order a plan with option `permute` uses (see sdnn_plan_opts), host only, no
  * GPU needed: 0 identity, 1 Algorithm 1 (as sdnn_reorder_rows), 2 panel-balancing,
- * 3 panel-union greedy.  Sec. 3.1.2 notes that other reorderings (hashing,
- * clustering) performed comparably to Algorithm 1; orders 2 and 3 are two such
- * alternatives aimed at the 4-row panels the kernel runs.  perm_out[i] is the
- * original row placed at position i; M entries, caller-owned.
- * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM (negative sizes, permute outside 0..3),
+ * 3 panel-union greedy, 4 MinHash clustering, 5 bin-then-greedy (see sdnn_plan_opts).
+ * Sec. 3.1.2 notes that other reorderings (hashing, clustering) performed comparably
+ * to Algorithm 1; orders 2-5 are such alternatives.  perm_out[i] is the original row
+ * placed at position i; M entries, caller-owned.
+ * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM (negative sizes, permute outside 0..5),
  * SDNN_ERR_CSR, SDNN_ERR_ALLOC. */
 sdnn_status sdnn_row_order(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K,
                            int32_t permute, int32_t* perm_out);

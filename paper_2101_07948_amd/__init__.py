@@ -103,7 +103,8 @@ def _np_ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
-ORDERS = {"identity": 0, "algorithm1": 1, "balanced": 2, "panel_union": 3}
+ORDERS = {"identity": 0, "algorithm1": 1, "balanced": 2, "panel_union": 3, "minhash": 4,
+          "bin_greedy": 5}
 
 
 def _order_mode(permute) -> int:

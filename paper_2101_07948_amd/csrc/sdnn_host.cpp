@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <array>
 #include <utility>
 #include <new>
 #include <vector>
@@ -347,7 +348,7 @@ static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* 
       return SDNN_ERR_DIM;
     o->rws = {opts->panel_rows};
   }
-  if (opts->permute < 0 || opts->permute > 3) return SDNN_ERR_DIM;
+  if (opts->permute < 0 || opts->permute > 5) return SDNN_ERR_DIM;
   if (opts->out_permuted != 0 && opts->out_permuted != 1) return SDNN_ERR_DIM;
   o->permute = opts->permute;
   o->out_permuted = opts->out_permuted;
@@ -497,8 +498,79 @@ static sdnn_status panel_union_order(const int32_t* row_ptr, const int32_t* col_
   return SDNN_OK;
 }
 
+// MurmurHash3's 32-bit finalizer (Appleby): a bijective avalanche mix of one word.
+static uint32_t fmix32(uint32_t h) {
+  h ^= h >> 16;
+  h *= 0x85ebca6bu;
+  h ^= h >> 13;
+  h *= 0xc2b2ae35u;
+  h ^= h >> 16;
+  return h;
+}
+
+// MinHash clustering order (plan option permute = 4), a locality-sensitive-hashing
+// order: row r's signature is (m_0(r), .., m_3(r)) with m_t(r) = min over its columns c
+// of fmix32(c ^ kMinHashSeed[t]) (0xffffffff for an empty row); two rows agree on each
+// m_t with probability equal to the Jaccard similarity of their column sets, so sorting
+// rows by signature (then nonzeros descending, then index) places rows with similar
+// column sets together, and rows with equal column sets consecutively.
+static const uint32_t kMinHashSeed[4] = {0x9e3779b9u, 0x7f4a7c15u, 0x94d049bbu, 0xbf58476du};
+
+static void minhash_order(const int32_t* row_ptr, const int32_t* col_idx, int32_t M,
+                          int32_t* perm_out) {
+  std::vector<std::array<uint32_t, 4>> sig((size_t)M);
+  for (int32_t r = 0; r < M; ++r) {
+    std::array<uint32_t, 4> m = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
+    for (int32_t q = row_ptr[r]; q < row_ptr[r + 1]; ++q)
+      for (int t = 0; t < 4; ++t) m[t] = std::min(m[t], fmix32((uint32_t)col_idx[q] ^ kMinHashSeed[t]));
+    sig[r] = m;
+  }
+  for (int32_t i = 0; i < M; ++i) perm_out[i] = i;
+  std::sort(perm_out, perm_out + M, [&](int32_t a, int32_t b) {
+    if (sig[a] != sig[b]) return sig[a] < sig[b];
+    const int32_t na = row_ptr[a + 1] - row_ptr[a], nb = row_ptr[b + 1] - row_ptr[b];
+    return na != nb ? na > nb : a < b;
+  });
+}
+
+// Bin-then-greedy order (plan option permute = 5): rows are binned by nonzero count,
+// bin floor(log2(nnz + 1)), the densest bin first, and Algorithm 1 orders the rows of
+// each bin among themselves (first the bin's densest row, then repeatedly the bin's
+// remaining row with the largest overlap with the row placed last; ties: more
+// nonzeros, then the lower index).  Panels then hold rows of similar length.
+static sdnn_status bin_greedy_order(const int32_t* row_ptr, const int32_t* col_idx, int32_t M,
+                                    int32_t K, int32_t* perm_out) {
+  auto bin_of = [&](int32_t r) {
+    uint32_t n = (uint32_t)(row_ptr[r + 1] - row_ptr[r]) + 1u;
+    int b = 0;
+    while (n >>= 1) ++b;
+    return b;
+  };
+  std::vector<std::vector<int32_t>> bins(33);
+  for (int32_t r = 0; r < M; ++r) bins[bin_of(r)].push_back(r);
+  int32_t at = 0;
+  std::vector<int32_t> sub_ptr, sub_col, sub_perm;
+  for (int b = 32; b >= 0; --b) {
+    const std::vector<int32_t>& rows = bins[b];
+    if (rows.empty()) continue;
+    // the bin's rows as a CSR of their own (ascending original index), Algorithm 1 on it
+    sub_ptr.assign(1, 0);
+    sub_col.clear();
+    for (int32_t r : rows) {
+      sub_col.insert(sub_col.end(), col_idx + row_ptr[r], col_idx + row_ptr[r + 1]);
+      sub_ptr.push_back((int32_t)sub_col.size());
+    }
+    sub_perm.resize(rows.size());
+    sdnn_status st = reorder_bitset(sub_ptr.data(), sub_col.data(), (int32_t)rows.size(), K,
+                                    sub_perm.data());
+    if (st != SDNN_OK) return st;
+    for (int32_t x : sub_perm) perm_out[at++] = rows[x];
+  }
+  return SDNN_OK;
+}
+
 // The row order of plan option `permute` (0 identity, 1 Algorithm 1, 2 panel-balancing,
-// 3 panel-union greedy) for a validated CSR.
+// 3 panel-union greedy, 4 MinHash clustering, 5 bin-then-greedy) for a validated CSR.
 static sdnn_status row_order(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K,
                              int32_t permute, int32_t* perm_out) {
   switch (permute) {
@@ -509,6 +581,11 @@ static sdnn_status row_order(const int32_t* row_ptr, const int32_t* col_idx, int
       return SDNN_OK;
     case 3:
       return panel_union_order(row_ptr, col_idx, M, K, perm_out);
+    case 4:
+      minhash_order(row_ptr, col_idx, M, perm_out);
+      return SDNN_OK;
+    case 5:
+      return bin_greedy_order(row_ptr, col_idx, M, K, perm_out);
     default:
       for (int32_t i = 0; i < M; ++i) perm_out[i] = i;
       return SDNN_OK;
@@ -605,7 +682,7 @@ const char* sdnn_status_str(sdnn_status s) {
 
 sdnn_status sdnn_row_order(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K,
                            int32_t permute, int32_t* perm_out) {
-  if (M < 0 || K < 0 || permute < 0 || permute > 3) return SDNN_ERR_DIM;
+  if (M < 0 || K < 0 || permute < 0 || permute > 5) return SDNN_ERR_DIM;
   if (M > 0 && !perm_out) return SDNN_ERR_NULL;
   sdnn_status st = validate_csr(row_ptr, col_idx, M, K);
   if (st != SDNN_OK) return st;

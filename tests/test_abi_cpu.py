@@ -231,7 +231,7 @@ def test_bad_dims_and_nulls():
     assert L.sdnn_plan_check_host(P(rp), P(ci), None, 1, 4, None, ctypes.byref(info)) == 1
     bad = sd.PlanOpts(5, 1)
     assert L.sdnn_plan_check_host(P(rp), P(ci), P(v), 1, 4, ctypes.byref(bad), None) == 2
-    bad = sd.PlanOpts(8, 4)
+    bad = sd.PlanOpts(8, 6)
     assert L.sdnn_plan_check_host(P(rp), P(ci), P(v), 1, 4, ctypes.byref(bad), None) == 2
     assert L.sdnn_plan_create(P(rp), P(ci), P(v), 1, 4, None, None) == 1
     assert L.sdnn_plan_get_perm(None, P(perm)) == 1

@@ -341,7 +341,7 @@ def test_permute_off_and_on_agree():
     with sd.Plan.from_csr(W, permute=False) as p0:
         assert np.array_equal(p0.perm, np.arange(256))
         C0 = gpu_spmm(p0, B, None, "none")
-    for mode in ("algorithm1", "balanced", "panel_union"):
+    for mode in ("algorithm1", "balanced", "panel_union", "minhash", "bin_greedy"):
         with sd.Plan.from_csr(W, permute=mode) as p:
             assert np.array_equal(p.perm, sd.row_order(W.row_ptr, W.col_idx, W.K, mode))
             assert np.array_equal(gpu_spmm(p, B, None, "none"), C0), mode

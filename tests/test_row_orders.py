@@ -1,10 +1,11 @@
-"""CPU tests of the library's alternative row orders (plan option permute = 2 and 3;
+"""CPU tests of the library's alternative row orders (plan option permute = 2 to 5;
 Sec. 3.1.2 notes that reorderings other than Algorithm 1 performed comparably), by
 their defining properties, through the host-only entry point sdnn_row_order.  No GPU
 is touched.  Algorithm 1 itself (permute = 1) is pinned against the oracle elsewhere."""
 import numpy as np
 import pytest
 
+import oracle
 import paper_2101_07948_amd as sd
 from conftest import pattern_to_csr
 from paper_2101_07948_amd import inputs
@@ -44,7 +45,8 @@ def assert_panel_union_picks(row_ptr, col_idx, perm, upto=None):
         union |= sets[best]
 
 
-@pytest.mark.parametrize("mode", ["identity", "algorithm1", "balanced", "panel_union"])
+@pytest.mark.parametrize("mode", ["identity", "algorithm1", "balanced", "panel_union", "minhash",
+                                  "bin_greedy"])
 def test_orders_are_permutations(mode):
     for M, K, d, seed in [(1, 1, 1.0, 1), (3, 5, 0.0, 2), (7, 9, 0.4, 3), (61, 47, 0.15, 4),
                           (130, 300, 0.05, 5)]:
@@ -135,7 +137,7 @@ def test_balanced_order_evens_panel_work():
 
 def test_row_order_rejects_bad_arguments():
     W = random_csr(8, 8, 0.5, 11)
-    for mode in (-1, 4):
+    for mode in (-1, 6):
         with pytest.raises(sd.SdnnError) as e:
             sd.row_order(W.row_ptr, W.col_idx, 8, mode)
         assert e.value.code == 2
@@ -146,11 +148,56 @@ def test_row_order_rejects_bad_arguments():
             sd.row_order(W.row_ptr, bad, 8, "panel_union")
         assert e.value.code == 3
     with pytest.raises(sd.SdnnError) as e:
-        sd.plan_check_host(W.row_ptr, W.col_idx, W.values, 8, 8, permute=4)
+        sd.plan_check_host(W.row_ptr, W.col_idx, W.values, 8, 8, permute=6)
     assert e.value.code == 2
 
 
-@pytest.mark.parametrize("mode", ["balanced", "panel_union"])
+def fmix32(h):
+    """MurmurHash3's 32-bit finalizer, written from its published definition."""
+    h ^= h >> 16
+    h = (h * 0x85EBCA6B) & 0xFFFFFFFF
+    h ^= h >> 13
+    h = (h * 0xC2B2AE35) & 0xFFFFFFFF
+    h ^= h >> 16
+    return h
+
+
+def test_minhash_order_replays_its_definition():
+    """permute = 4: rows sorted by (min over columns of fmix32(c ^ seed_t), t = 0..3), then
+    nonzeros descending, then index; rows with equal column sets end up consecutive."""
+    seeds = (0x9E3779B9, 0x7F4A7C15, 0x94D049BB, 0xBF58476D)
+    for M, K, d, seed in [(40, 30, 0.2, 12), (120, 200, 0.05, 13)]:
+        W = random_csr(M, K, d, seed)
+        sets = row_sets(W.row_ptr, W.col_idx)
+        sig = [tuple(min((fmix32(c ^ t) for c in cs), default=0xFFFFFFFF) for t in seeds)
+               for cs in sets]
+        want = sorted(range(M), key=lambda r: (sig[r], -len(sets[r]), r))
+        assert sd.row_order(W.row_ptr, W.col_idx, K, "minhash").tolist() == want
+    rows = [[1, 5, 9], [2, 3], [1, 5, 9], [7], [2, 3], [1, 5, 9], [4, 8]]
+    rp, ci, _ = pattern_to_csr(rows, 10)
+    perm = sd.row_order(rp, ci, 10, "minhash").tolist()
+    for group in ([0, 2, 5], [1, 4]):
+        where = sorted(perm.index(r) for r in group)
+        assert where == list(range(where[0], where[0] + len(group)))
+
+
+def test_bin_greedy_order_is_algorithm1_within_bins():
+    """permute = 5: bins floor(log2(nnz + 1)), densest first, each ordered by the oracle's
+    Algorithm 1 on the bin's rows alone."""
+    for M, K, d, seed in [(50, 60, 0.15, 14), (97, 128, 0.3, 15)]:
+        W = random_csr(M, K, d, seed)
+        nnz = np.diff(W.row_ptr)
+        bins = np.floor(np.log2(nnz + 1)).astype(int)
+        want = []
+        for b in sorted(set(bins.tolist()), reverse=True):
+            rows = np.flatnonzero(bins == b)
+            sub = [W.col_idx[W.row_ptr[r]:W.row_ptr[r + 1]].tolist() for r in rows]
+            rp, ci, _ = pattern_to_csr(sub, K)
+            want += rows[oracle.reorder(rp, ci, K)].tolist()
+        assert sd.row_order(W.row_ptr, W.col_idx, K, "bin_greedy").tolist() == want
+
+
+@pytest.mark.parametrize("mode", ["balanced", "panel_union", "minhash", "bin_greedy"])
 def test_orders_pack_and_self_check(mode):
     for name in ("c2", "c4"):
         W = inputs.workload(name, N=4).layers[0].W
