@@ -27,8 +27,11 @@ per-chunk handshake of any one wave stays short.
 Every group reads chunks c_lo..c_hi with c_hi - c_lo < RING and publishes
 progress = c_lo before waiting for c_hi, so the slowest consumer's next chunk can
 always be staged: the loops cannot deadlock.  Each wait is also bounded by
-a per-wave poll budget, after which the wave goes on without waiting (the result is
-then wrong, but the kernel ends).
+a per-wave poll budget (a launch argument), after which the wave goes on without
+waiting, so the kernel always ends.  Going on is never silent: a producer that stages
+past the ring limit first sets the workgroup's overrun word, and a consumer whose
+budget ran out, or that finds the overrun word set when it finishes, replaces its
+whole panel's results with NaN.
 
 Stream consumed (see sdnn_internal.h): per panel, groups of 16 dwords (64 bytes,
 one scalar load, one scalar-cache line) [w0..w7 a0..a7]; w = fp32 weight bits;
@@ -87,7 +90,6 @@ CHUNK, RING = 32, 4
 PMAX_VEC, PMAX_DWORD = 2, 1                   # chunks in flight per producer variant
 TOUCH_AHEAD = 512  # bytes of stream pulled into L2 ahead of the scalar ring
 GROUP_BYTES = 8 * G
-POLL_BUDGET = 1 << 22   # LDS polls a wave may spend waiting, in total
 INF = 0x7FFFFFFF
 NPROD = 4          # producer waves; producer p stages rows [p, p+1) * CHUNK/NPROD of a chunk
 MAX_CONS = 14      # consumer waves a workgroup can have
@@ -182,7 +184,7 @@ def consumer(rw):
         f"v_mov_b32 v31, {hex(RING_MASK)}",
         "v_mov_b32 v28, 0",
         f"s_mov_b32 s{SREADY}, 0",
-        f"s_mov_b32 s{SPOLL}, {hex(POLL_BUDGET)}",
+        f"s_mov_b32 s{SPOLL}, %[budget]",
     ]
     if PROFILE:
         L.append("s_mov_b32 %[twait], 0")
@@ -225,7 +227,16 @@ def consumer(rw):
         L.append("s_waitcnt lgkmcnt(0)")
         L += fmas(nxt, vbn, rw)
         L.append("s_branch .L%=_finish")
-    L += [".L%=_finish:", f"v_mov_b32 v30, {hex(INF)}"]
+    # a wave that went on without waiting, or whose chunks a producer may have
+    # overwritten, leaves NaN instead of unchecked values
+    L += [".L%=_finish:",
+          f"s_cmp_eq_u32 s{SPOLL}, 0", "s_cbranch_scc1 .L%=_poison",
+          "ds_read_b32 v30, %[ov]", "s_waitcnt lgkmcnt(0)",
+          f"v_readfirstlane_b32 s{STMP}, v30",
+          f"s_cmp_eq_u32 s{STMP}, 0", "s_cbranch_scc1 .L%=_clean",
+          ".L%=_poison:"]
+    L += [f"v_mov_b32 v{ACC + x}, 0x7fc00000" for x in range(4 * rw)]
+    L += [".L%=_clean:", f"v_mov_b32 v30, {hex(INF)}"]
     L += lane0_write("%[pa]", "v30")
     L += ["s_waitcnt vmcnt(0) lgkmcnt(0)", f"s_mov_b32 m0, s{M0S}"]
     body = "\n".join('      "' + x + '\\n\\t"' for x in L)
@@ -240,7 +251,8 @@ __device__ __forceinline__ void consume_rw{rw}(acc_plane_t<{rw}>& p0, acc_plane_
   asm volatile(
 {body}
       : {planes}{', [twait] "=&s"(a.twait)' if PROFILE else ''}
-      : [sp] "s"(a.stream), [vl] "v"(a.vlane), [pa] "v"(a.prog_addr), [ra] "v"(a.ready_addr)
+      : [sp] "s"(a.stream), [vl] "v"(a.vlane), [pa] "v"(a.prog_addr), [ra] "v"(a.ready_addr),
+        [budget] "s"(a.poll_budget), [ov] "v"(a.overrun_addr)
       : {clob});
 }}
 """
@@ -419,7 +431,7 @@ def producer(kind):
         f"s_mov_b32 s{PSIG}, 0",
         f"s_mov_b32 s{PINF}, 0",
         f"s_mov_b32 s{PLIM}, {RING}",
-        f"s_mov_b32 s{PPOLL}, {hex(POLL_BUDGET)}",
+        f"s_mov_b32 s{PPOLL}, %[budget]",
         f"s_sub_u32 s{PKM1}, %[K], 1",
         # fast-path state: chunk base B + prow0 * row_bytes, chunk stride CHUNK * row_bytes
         f"s_mul_i32 s{PBASE}, %[prow0], %[rs]",
@@ -479,10 +491,19 @@ def producer(kind):
         f"s_cmp_eq_u32 s{PINF}, 0",
         "s_cbranch_scc0 .L%=_land",
         f"s_cmp_eq_u32 s{PPOLL}, 0",          # budget spent: stage anyway
-        "s_cbranch_scc1 .L%=_issue",
+        "s_cbranch_scc1 .L%=_overrun",
         f"s_sub_u32 s{PPOLL}, s{PPOLL}, 1",
         "s_sleep 1",
         "s_branch .L%=_loop",
+        # staging past the limit may overwrite a slot still being read: say so in the
+        # overrun word (landed before the load goes out) and go on to issue
+        ".L%=_overrun:",
+        "v_mov_b32 v27, 1",
+        f"s_mov_b64 s[{PEX}:{PEX + 1}], exec",
+        "s_mov_b64 exec, 1",
+        "ds_write_b32 %[ov], v27",
+        "s_waitcnt lgkmcnt(0)",
+        f"s_mov_b64 exec, s[{PEX}:{PEX + 1}]",
         # LDS row of the producer's first row of chunk `issued`:
         # (issued % RING) * CHUNK + prow0
         ".L%=_issue:",
@@ -553,7 +574,8 @@ __device__ __forceinline__ void produce_{kind}(const ProducerArgs& a) {{
       :
       : [nch] "s"(a.nchunks), [K] "s"(a.K), [rs] "s"(a.row_bytes), [bb_lo] "s"(a.bbase_lo),
         [bb_hi] "s"(a.bbase_hi), [ncol] "s"(a.ncol), [prow0] "s"(a.first_row),
-        [vl] "v"(a.vlane), [pg] "v"(a.prog_addr), [ra] "v"(a.ready_addr){CONV_OPERANDS if conv else ""}
+        [vl] "v"(a.vlane), [pg] "v"(a.prog_addr), [ra] "v"(a.ready_addr),
+        [budget] "s"(a.poll_budget), [ov] "v"(a.overrun_addr){CONV_OPERANDS if conv else ""}
       : {clob});
 }}
 """

@@ -52,6 +52,8 @@ struct ConsumerArgs {
   uint32_t vlane;          // 16 * lane: the lane's byte offset in a staged B row
   uint32_t prog_addr;      // LDS address of this consumer's progress word
   uint32_t ready_addr;     // LDS address of the ready word
+  uint32_t poll_budget;    // failed readiness checks the wave may poll through in total
+  uint32_t overrun_addr;   // LDS address of the workgroup's overrun word
 };
 struct ProducerArgs {
   int32_t nchunks, K;
@@ -62,6 +64,8 @@ struct ProducerArgs {
   uint32_t vlane;          // the lane's byte offset in a B row segment (16 or 4 * lane)
   uint32_t prog_addr;      // LDS address of the 16 progress words
   uint32_t ready_addr;     // LDS address of this producer's ready word
+  uint32_t poll_budget;    // failed ring-limit checks the wave may poll through in total
+  uint32_t overrun_addr;   // LDS address of the workgroup's overrun word
   // virtual B of a 3x3 convolution (bbase is then X itself)
   uint32_t row_step, col_step;  // bytes between image rows (W * NB * 4), columns (NB * 4)
   uint32_t plane_bytes;         // bytes per input channel (H * W * NB * 4)
@@ -83,13 +87,17 @@ static_assert(kAsmRingMask == (uint32_t)(kRing * kChunk - 1) << kRingRowShift,
               "ring-row mask mismatch");
 
 constexpr int kRingBytes = kRing * kChunk * 1024;
+// Failed checks a wave may poll through before it goes on without waiting (results then
+// turn to NaN, never silently wrong); SDNN_POLL_BUDGET overrides it (tests only).
+constexpr int kPollBudget = 1 << 22;
 // Threads per workgroup a panel height allows: the accumulators sit above the loop's
 // pinned VGPRs and end at v[kAsmAccBase + 4 * RW - 1], so RW <= 8 fits the 128 VGPRs
 // that 16 waves per CU leave each wave, and RW >= 12 needs 12 waves per CU.
 template <int RW>
 constexpr int max_threads() { return kAsmAccBase + 4 * RW <= 128 ? 1024 : 768; }
-// LDS control words after the ring: ready[kProducers] at +0, progress[16] at +64, and
-// 16 bytes per producer at +512 that the convolution producer's filler loads write.
+// LDS control words after the ring: ready[kProducers] at +0, progress[16] at +64, the
+// overrun word at +128 (nonzero once a producer staged past the ring limit), and 16
+// bytes per producer at +512 that the convolution producer's filler loads write.
 constexpr int kCtlWords = 256;
 static_assert(512 + 16 * kProducers <= kCtlWords * 4, "filler words outside the control area");
 static_assert(kProducers <= 16, "ready words overlap the progress words");
@@ -110,6 +118,7 @@ struct SpmmArgs {
   int32_t epi;
   int32_t out_permuted;  // store permuted row i at row i instead of at its source row
   int32_t H, W, NB;      // image geometry of a 3x3 convolution (B is then the input X)
+  uint32_t poll_budget;  // failed readiness / ring-limit checks a wave may poll through
 };
 
 // Producer kinds: 4-byte staging (any N), 16-byte staging (N % 4 == 0, aligned), the
@@ -146,9 +155,11 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
   if (lds_base != 0) return;  // never taken: see above
   const uint32_t ready_addr = lds_base + kRingBytes;
   const uint32_t prog0 = ready_addr + 64;
+  const uint32_t overrun_addr = ready_addr + 128;
   uint32_t* ctl = lds + kRingBytes / 4;
   if (prod >= 0) {
     if (lane == 0) ctl[prod] = 0u;                                           // nothing landed
+    if (prod == 0 && lane == 0) ctl[32] = 0u;                                // no overrun
     if (prod == 0 && lane >= nc && lane < 16) ctl[16 + lane] = kProgressDone;  // absent consumers
   } else if (lane == 0) {
     ctl[16 + wave] = gstart >= 0 ? 0u : kProgressDone;
@@ -168,6 +179,8 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     pa.vlane = (uint32_t)lane * (STAGE != kStageDword ? 16u : 4u);
     pa.prog_addr = prog0;
     pa.ready_addr = ready_addr + 4u * (uint32_t)prod;
+    pa.poll_budget = a.poll_budget;
+    pa.overrun_addr = overrun_addr;
     if constexpr (STAGE == kStageConv) {
       // lane l's columns n0 + 4l .. + 3: four images of pixel (y, x)
       const uint64_t xb = (uint64_t)(uintptr_t)B;
@@ -203,6 +216,8 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     ca.vlane = (uint32_t)lane * 16u;
     ca.prog_addr = prog0 + 4u * (uint32_t)wave;
     ca.ready_addr = ready_addr;
+    ca.poll_budget = a.poll_budget;
+    ca.overrun_addr = overrun_addr;
     if constexpr (RW == 4) consume_rw4(p0, p1, p2, p3, ca);
     if constexpr (RW == 8) consume_rw8(p0, p1, p2, p3, ca);
     if constexpr (RW == 12) consume_rw12(p0, p1, p2, p3, ca);
@@ -365,6 +380,10 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
   args.H = conv_hwn ? conv_hwn[0] : 0;
   args.W = conv_hwn ? conv_hwn[1] : 0;
   args.NB = conv_hwn ? conv_hwn[2] : 0;
+  {
+    const int budget = env_int("SDNN_POLL_BUDGET", kPollBudget);
+    args.poll_budget = budget > 0 ? (uint32_t)budget : 0u;
+  }
   if (conv_hwn) return launch_rw<kStageConv>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
   // the 16-byte producer addresses a chunk's rows with 32-bit per-lane offsets
   // 16 * lane + r * 4N (r < kChunk / kProducers)

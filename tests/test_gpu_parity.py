@@ -349,6 +349,34 @@ def test_permute_off_and_on_agree():
     assert (np.abs(C0 - ref) <= 1e-5 * bound + 1e-6).all()
 
 
+@pytest.mark.parametrize("budget", [0, 2, 64])
+def test_spent_poll_budget_turns_results_to_nan(budget):
+    """Every wait in the kernel is bounded by a poll budget, here forced tiny from the
+    host: a consumer that stops waiting, or whose staged chunks a producer may have
+    overwritten, writes NaN for its panel.  Every output is within the oracle's bound or
+    NaN, never a finite wrong value; with no budget at all every panel is NaN."""
+    M, K, N = 512, 2048, 4096
+    W = inputs.pattern_uniform(M, K, 0.1, inputs.CFG_TEST, 90, 0.05)
+    B = inputs.dense_B(K, N, inputs.CFG_TEST, 90)
+    bias = inputs.bias_normal(M, inputs.CFG_TEST, 90, 0.02)
+    old = os.environ.get("SDNN_POLL_BUDGET")
+    os.environ["SDNN_POLL_BUDGET"] = str(budget)
+    try:
+        with sd.Plan.from_csr(W) as plan:
+            got = gpu_spmm(plan, B, bias, "none")
+    finally:
+        if old is None:
+            os.environ.pop("SDNN_POLL_BUDGET", None)
+        else:
+            os.environ["SDNN_POLL_BUDGET"] = old
+    ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, K, B, bias, "none")
+    err = np.abs(got.astype(np.float64) - ref)
+    ok = (err <= tolerance(bound, ref, "none")) | np.isnan(got)
+    assert ok.all(), f"{int((~ok).sum())} finite outputs out of tolerance"
+    if budget == 0:
+        assert np.isnan(got).all()
+
+
 def test_graph_capture_replays():
     """sdnn_spmm neither allocates nor synchronises, so a call can be captured in a HIP
     graph: replayed several times, with eager work and synchronisations between the
