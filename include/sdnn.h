@@ -57,7 +57,7 @@ typedef enum {
   SDNN_EPI_GELU = 2  /* 0.5 * x * (1 + erf(x / sqrt(2))) */
 } sdnn_epilogue;
 
-/* Options for sdnn_plan_create; pass NULL for the defaults {0, 1, 0, NULL}.
+/* Options for sdnn_plan_create; pass NULL for the defaults {0, 1, 0, 0, NULL}.
  *   panel_rows:   rows per register panel.  0 (default) packs W twice, with short
  *                 panels of 4 rows and tall panels of 12 rows, and sdnn_spmm picks per
  *                 call: tall panels once a 256-column tile has at least a full
@@ -79,6 +79,12 @@ typedef enum {
  *                 plan's permuted row order, C row i = output row perm[i] (Sec. 3.1.2:
  *                 the rows stay permuted and the next layer's columns compensate).
  *                 The bias is always given in the original row order.
+ *   split_chunks: 0 (default) = no K-segments.  S > 0 cuts K into segments of S chunks
+ *                 (S * k_chunk rows of B; nseg = ceil(ceil(K / k_chunk) / S) segments)
+ *                 so that sdnn_spmm_split / sdnn_conv3x3_split can give each segment
+ *                 of a tile its own workgroup (the split-K tiling of Sec. 3.2.2
+ *                 extended across workgroups).  Such plans also serve sdnn_spmm and
+ *                 sdnn_conv3x3, unsplit.  Negative: SDNN_ERR_DIM.
  *   in_perm:      NULL (default) = B row c is input feature c; otherwise K int32 (host,
  *                 read during the call only), a permutation of 0..K-1 giving the order
  *                 of B's rows: B row i holds input feature in_perm[i].  Pass the
@@ -88,7 +94,7 @@ typedef struct {
   int32_t panel_rows;
   int32_t permute;
   int32_t out_permuted;
-  int32_t reserved;
+  int32_t split_chunks;
   const int32_t* in_perm;
 } sdnn_plan_opts;
 
@@ -99,13 +105,15 @@ typedef struct {
  *   rho:          nnz / sum over panels of |union of the panel rows' column sets|,
  *                 the reuse an ideal panel kernel gets per staged B row (>= 1).
  *   fill:         nnz / stored stream entries (1.0 = no padding).
- *   k_chunk:      rows of B per LDS staging slot. */
+ *   k_chunk:      rows of B per LDS staging slot.
+ *   splits:       K-segments of a plan created with split_chunks > 0 (else 0); the
+ *                 workspace of a K-split call holds splits * M * N floats. */
 typedef struct {
   int32_t M, K;
   int64_t nnz, panels, packed_bytes;
   double rho, fill;
   int32_t panel_rows, k_chunk;
-  int32_t tall_panel_rows, reserved;
+  int32_t tall_panel_rows, splits;
   double tall_rho, tall_fill;
   int32_t out_permuted, in_permuted;  /* the plan's options (in_permuted: in_perm given) */
 } sdnn_plan_info_t;
@@ -171,6 +179,25 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out);
 sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
                       sdnn_epilogue epi, void* stream);
 
+/* K-split execution (Sec. 3.2.2 splits K into tiles that a block walks in turn; here the
+ * K-segments of a tile also go to different workgroups, which fills the device when
+ * M * ceil(N / 256) alone gives too few workgroups).  Same result contract, layouts and
+ * stream semantics as sdnn_spmm; the plan must have been created with split_chunks > 0.
+ * Each workgroup writes its segment's partial product (no bias, no epilogue) to
+ * workspace[s][row][n]; a second kernel on the same stream sums the segments in order
+ * s = 0, 1, ..., adds the bias and applies epi into C.  Results can differ from
+ * sdnn_spmm in rounding only (another summation order).
+ *   workspace:        device, at least splits * M * N fp32 (sdnn_plan_info), 16-byte
+ *                     aligned, clear of B, C and bias; scratch of this call only (its
+ *                     contents afterwards are unspecified).  Not touched, and may be NULL,
+ *                     when the plan has one K-segment: the call is then sdnn_spmm.
+ *   workspace_floats: its size in floats.
+ * Errors: as sdnn_spmm, plus SDNN_ERR_DIM (plan without split_chunks, workspace too
+ * small, misaligned or overlapping) and SDNN_ERR_NULL (workspace NULL with splits > 1). */
+sdnn_status sdnn_spmm_split(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
+                            sdnn_epilogue epi, float* workspace, int64_t workspace_floats,
+                            void* stream);
+
 /* Per-plan variant selection by timing (the paper's preparation stage chooses the best
  * kernel implementation per operator, Sec. 3.1): times sdnn_spmm at this N for every
  * packing the plan holds with several consumer-wave counts per workgroup, on the
@@ -204,6 +231,12 @@ sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, voi
  * SDNN_ERR_HIP. */
 sdnn_status sdnn_conv3x3(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
                          int32_t NB, const float* bias, sdnn_epilogue epi, void* stream);
+
+/* K-split variant of sdnn_conv3x3 (N = H * W * NB columns), with the workspace
+ * contract of sdnn_spmm_split.  Errors: as sdnn_conv3x3 and sdnn_spmm_split. */
+sdnn_status sdnn_conv3x3_split(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
+                               int32_t NB, const float* bias, sdnn_epilogue epi, float* workspace,
+                               int64_t workspace_floats, void* stream);
 
 /* Frees the plan and its device memory.  NULL is a no-op. */
 void sdnn_plan_destroy(sdnn_plan p);

@@ -33,7 +33,7 @@ class SdnnError(RuntimeError):
 
 class PlanOpts(ctypes.Structure):
     _fields_ = [("panel_rows", ctypes.c_int32), ("permute", ctypes.c_int32),
-                ("out_permuted", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("out_permuted", ctypes.c_int32), ("split_chunks", ctypes.c_int32),
                 ("in_perm", ctypes.c_void_p)]
 
 
@@ -42,7 +42,7 @@ class PlanInfo(ctypes.Structure):
                 ("panels", ctypes.c_int64), ("packed_bytes", ctypes.c_int64),
                 ("rho", ctypes.c_double), ("fill", ctypes.c_double),
                 ("panel_rows", ctypes.c_int32), ("k_chunk", ctypes.c_int32),
-                ("tall_panel_rows", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("tall_panel_rows", ctypes.c_int32), ("splits", ctypes.c_int32),
                 ("tall_rho", ctypes.c_double), ("tall_fill", ctypes.c_double),
                 ("out_permuted", ctypes.c_int32), ("in_permuted", ctypes.c_int32)]
 
@@ -78,9 +78,12 @@ def lib() -> ctypes.CDLL:
         L.sdnn_dense_gemm.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
         L.sdnn_conv3x3.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
         L.sdnn_plan_tune.argtypes = [p, p, p, i32, p, p, p]
+        i64 = ctypes.c_int64
+        L.sdnn_spmm_split.argtypes = [p, p, p, i32, p, ctypes.c_int, p, i64, p]
+        L.sdnn_conv3x3_split.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p, i64, p]
         for fn in ("sdnn_reorder_rows", "sdnn_row_order", "sdnn_plan_check_host", "sdnn_plan_create",
                    "sdnn_plan_get_perm", "sdnn_plan_info", "sdnn_spmm", "sdnn_dense_gemm",
-                   "sdnn_conv3x3", "sdnn_plan_tune"):
+                   "sdnn_conv3x3", "sdnn_plan_tune", "sdnn_spmm_split", "sdnn_conv3x3_split"):
             getattr(L, fn).restype = ctypes.c_int
         _lib_handle = L
     return _lib_handle
@@ -115,13 +118,14 @@ def _order_mode(permute) -> int:
     return (1 if permute else 0) if isinstance(permute, bool) else int(permute)
 
 
-def _opts(K: int, panel_rows: int, permute: bool, out_permuted: bool = False, in_perm=None):
+def _opts(K: int, panel_rows: int, permute: bool, out_permuted: bool = False, in_perm=None,
+          split_chunks: int = 0):
     """PlanOpts plus the in_perm array it points to (kept alive by the caller)."""
     keep = None if in_perm is None else _i32(in_perm)
     if keep is not None and keep.shape != (int(K),):
         raise ValueError(f"in_perm must hold K = {K} entries, got shape {keep.shape}")
     mode = _order_mode(permute)
-    o = PlanOpts(int(panel_rows), mode, 1 if out_permuted else 0, 0,
+    o = PlanOpts(int(panel_rows), mode, 1 if out_permuted else 0, int(split_chunks),
                  None if keep is None else keep.ctypes.data)
     return o, keep
 
@@ -148,11 +152,12 @@ def row_order(row_ptr, col_idx, K: int, permute="algorithm1") -> np.ndarray:
 
 
 def plan_check_host(row_ptr, col_idx, values, M: int, K: int, panel_rows: int = 0,
-                    permute: bool = True, out_permuted: bool = False, in_perm=None) -> dict:
+                    permute: bool = True, out_permuted: bool = False, in_perm=None,
+                    split_chunks: int = 0) -> dict:
     """Host-only self-check of the preparation stage; returns the plan statistics."""
     row_ptr, col_idx, values = _i32(row_ptr), _i32(col_idx), _f32(values)
     info = PlanInfo()
-    o, _keep = _opts(K, panel_rows, permute, out_permuted, in_perm)
+    o, _keep = _opts(K, panel_rows, permute, out_permuted, in_perm, split_chunks)
     _check(lib().sdnn_plan_check_host(_np_ptr(row_ptr), _np_ptr(col_idx), _np_ptr(values), M, K,
                                       ctypes.byref(o), ctypes.byref(info)),
            "sdnn_plan_check_host")
@@ -190,14 +195,16 @@ class Plan:
     """
 
     def __init__(self, row_ptr, col_idx, values, M: int, K: int, panel_rows: int = 0,
-                 permute: bool = True, out_permuted: bool = False, in_perm=None):
+                 permute: bool = True, out_permuted: bool = False, in_perm=None,
+                 split_chunks: int = 0):
         """out_permuted: write C in the plan's permuted row order (C[i] = output row
         perm[i]); in_perm: the order of B's rows (B[i] = input feature in_perm[i]),
-        e.g. the previous layer's perm when that layer used out_permuted."""
+        e.g. the previous layer's perm when that layer used out_permuted; split_chunks:
+        K-segments of that many staging chunks for spmm_split / conv3x3_split."""
         row_ptr, col_idx, values = _i32(row_ptr), _i32(col_idx), _f32(values)
         self.M, self.K = int(M), int(K)
         h = ctypes.c_void_p()
-        o, _keep = _opts(self.K, panel_rows, permute, out_permuted, in_perm)
+        o, _keep = _opts(self.K, panel_rows, permute, out_permuted, in_perm, split_chunks)
         self._lib = lib()
         _check(self._lib.sdnn_plan_create(_np_ptr(row_ptr), _np_ptr(col_idx), _np_ptr(values),
                                           self.M, self.K, ctypes.byref(o), ctypes.byref(h)),
@@ -255,6 +262,48 @@ class Plan:
         pbias = _dev_ptr(bias, "bias", (self.M,), allow_none=True)
         _check(self._lib.sdnn_conv3x3(self.handle, px, pc, H, W, NB, pbias, EPI[epi],
                                       _stream_handle(stream)), "sdnn_conv3x3")
+        return C
+
+    def workspace_floats(self, N: int) -> int:
+        """Floats of the workspace a K-split call at N columns needs (splits * M * N)."""
+        return int(self.info["splits"]) * self.M * int(N)
+
+    def _workspace(self, ws, N: int):
+        import torch
+        need = self.workspace_floats(N) if int(self.info["splits"]) > 1 else 0
+        if ws is None:
+            ws = torch.empty(max(need, 1), device="cuda")
+        if not isinstance(ws, torch.Tensor) or ws.device.type != "cuda" or \
+                ws.dtype != torch.float32 or not ws.is_contiguous():
+            raise TypeError("workspace must be a contiguous float32 CUDA/HIP tensor")
+        return ctypes.c_void_p(ws.data_ptr()), int(ws.numel())
+
+    def spmm_split(self, B, C, bias=None, epi: str = "none", workspace=None, stream=None):
+        """spmm with each K-segment of a tile in its own workgroup (plans created with
+        split_chunks > 0); workspace: a float32 device tensor of at least
+        workspace_floats(N) elements (allocated here when None)."""
+        N = int(B.shape[1]) if B is not None and B.dim() == 2 else int(C.shape[1])
+        pb = _dev_ptr(B, "B", (self.K, N))
+        pc = _dev_ptr(C, "C", (self.M, N))
+        pbias = _dev_ptr(bias, "bias", (self.M,), allow_none=True)
+        pw, nw = self._workspace(workspace, N)
+        _check(self._lib.sdnn_spmm_split(self.handle, pb, pc, N, pbias, EPI[epi], pw, nw,
+                                         _stream_handle(stream)), "sdnn_spmm_split")
+        return C
+
+    def conv3x3_split(self, X, C, bias=None, epi: str = "none", workspace=None, stream=None):
+        """conv3x3 with K-segments in separate workgroups (see spmm_split)."""
+        if X.dim() != 4 or C.dim() != 4:
+            raise ValueError("X and C must be 4-d (channels, H, W, images)")
+        IC, H, W, NB = (int(d) for d in X.shape)
+        if IC * 9 != self.K:
+            raise ValueError(f"X has {IC} channels; the plan's K = {self.K} needs {self.K // 9}")
+        px = _dev_ptr(X, "X", (IC, H, W, NB))
+        pc = _dev_ptr(C, "C", (self.M, H, W, NB))
+        pbias = _dev_ptr(bias, "bias", (self.M,), allow_none=True)
+        pw, nw = self._workspace(workspace, H * W * NB)
+        _check(self._lib.sdnn_conv3x3_split(self.handle, px, pc, H, W, NB, pbias, EPI[epi], pw,
+                                            nw, _stream_handle(stream)), "sdnn_conv3x3_split")
         return C
 
     def spmm(self, B, C, bias=None, epi: str = "none", stream=None):

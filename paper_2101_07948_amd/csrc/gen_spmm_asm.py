@@ -198,7 +198,7 @@ def consumer(rw):
     ]
     L += sync(E[0], "e")   # a panel's first group always carries the sync bit
     L += address_phase(E[0], VB[0])
-    L += [f"s_bitcmp1_b32 s{E[0] + HIW}, {END_BIT}", "s_cbranch_scc0 .L%=_iter0",
+    L += [f"s_and_b32 s{STMP}, s{E[0] + HIW}, %[em]", "s_cbranch_scc0 .L%=_iter0",
           "s_waitcnt lgkmcnt(0)"]   # the panel is one group
     L += fmas(E[0], VB[0], rw)
     L.append("s_branch .L%=_finish")
@@ -221,7 +221,7 @@ def consumer(rw):
         vbc, vbn = VB[i % 2], VB[(i + 1) % 2]
         L.append(f".L%=_sync{i}:")
         L += sync(nxt, i)
-        L += [f"s_bitcmp1_b32 s{nxt + HIW}, {END_BIT}", f"s_cbranch_scc0 .L%=_ret{i}"]
+        L += [f"s_and_b32 s{STMP}, s{nxt + HIW}, %[em]", f"s_cbranch_scc0 .L%=_ret{i}"]
         L += address_phase(nxt, vbn)       # group g+1 ends the panel
         L += fmas(cur, vbc, rw)
         L.append("s_waitcnt lgkmcnt(0)")
@@ -252,7 +252,7 @@ __device__ __forceinline__ void consume_rw{rw}(acc_plane_t<{rw}>& p0, acc_plane_
 {body}
       : {planes}{', [twait] "=&s"(a.twait)' if PROFILE else ''}
       : [sp] "s"(a.stream), [vl] "v"(a.vlane), [pa] "v"(a.prog_addr), [ra] "v"(a.ready_addr),
-        [budget] "s"(a.poll_budget), [ov] "v"(a.overrun_addr)
+        [budget] "s"(a.poll_budget), [ov] "v"(a.overrun_addr), [em] "s"(a.end_mask)
       : {clob});
 }}
 """
@@ -427,25 +427,25 @@ def producer(kind):
     lg_chunk = CHUNK.bit_length() - 1
     L = [
         f"s_mov_b32 s{PM0}, m0",
-        f"s_mov_b32 s{PISS}, 0",
-        f"s_mov_b32 s{PSIG}, 0",
+        f"s_mov_b32 s{PISS}, %[fc]",
+        f"s_mov_b32 s{PSIG}, %[fc]",
         f"s_mov_b32 s{PINF}, 0",
-        f"s_mov_b32 s{PLIM}, {RING}",
+        f"s_add_u32 s{PLIM}, %[fc], {RING}",
         f"s_mov_b32 s{PPOLL}, %[budget]",
         f"s_sub_u32 s{PKM1}, %[K], 1",
-        # fast-path state: chunk base B + prow0 * row_bytes, chunk stride CHUNK * row_bytes
-        f"s_mul_i32 s{PBASE}, %[prow0], %[rs]",
-        f"s_mul_hi_u32 s{PBASE + 1}, %[prow0], %[rs]",
+        # fast-path state: chunk base B + (c0 * CHUNK + prow0) * row_bytes, chunk stride
+        # CHUNK * row_bytes
+        f"s_lshl_b32 s{PTMP}, %[fc], {lg_chunk}",
+        f"s_add_u32 s{PTMP}, s{PTMP}, %[prow0]",
+        f"s_mul_i32 s{PBASE}, s{PTMP}, %[rs]",
+        f"s_mul_hi_u32 s{PBASE + 1}, s{PTMP}, %[rs]",
         f"s_add_u32 s{PBASE}, s{PBASE}, %[bb_lo]",
         f"s_addc_u32 s{PBASE + 1}, s{PBASE + 1}, %[bb_hi]",
         f"s_lshl_b32 s{PCS}, %[rs], {lg_chunk}",
         f"s_lshr_b32 s{PCS + 1}, %[rs], {32 - lg_chunk}",
     ]
-    if kind == "vec":  # PLAST = nch - 1 if K % CHUNK else nch
-        L += [f"s_and_b32 s{PTMP}, %[K], {CHUNK - 1}",
-              f"s_sub_u32 s{PLAST}, %[nch], 1",
-              f"s_cmp_eq_u32 s{PTMP}, 0",
-              f"s_cselect_b32 s{PLAST}, %[nch], s{PLAST}",
+    if kind == "vec":  # PLAST = K / CHUNK: chunks below it hold CHUNK rows of B
+        L += [f"s_lshr_b32 s{PLAST}, %[K], {lg_chunk}",
               f"v_mov_b32 v{VO}, %[vl]"]
         for r in range(1, half):
             L.append(f"v_add_u32 v{VO + r}, %[rs], v{VO + r - 1}")
@@ -575,7 +575,7 @@ __device__ __forceinline__ void produce_{kind}(const ProducerArgs& a) {{
       : [nch] "s"(a.nchunks), [K] "s"(a.K), [rs] "s"(a.row_bytes), [bb_lo] "s"(a.bbase_lo),
         [bb_hi] "s"(a.bbase_hi), [ncol] "s"(a.ncol), [prow0] "s"(a.first_row),
         [vl] "v"(a.vlane), [pg] "v"(a.prog_addr), [ra] "v"(a.ready_addr),
-        [budget] "s"(a.poll_budget), [ov] "v"(a.overrun_addr){CONV_OPERANDS if conv else ""}
+        [budget] "s"(a.poll_budget), [ov] "v"(a.overrun_addr), [fc] "s"(a.first_chunk){CONV_OPERANDS if conv else ""}
       : {clob});
 }}
 """

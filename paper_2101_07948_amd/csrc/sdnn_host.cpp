@@ -100,16 +100,18 @@ struct Entry {
 
 // Writes one group (n <= kGroup real entries from e) with its fields.
 void emit_group(std::vector<uint32_t>& out, const Entry* e, int n, bool first, bool last,
-                int32_t* prev_lo, int32_t* prev_hi) {
+                bool seg_end, int32_t* prev_lo, int32_t* prev_hi) {
   uint32_t w[kGroup], a[kGroup];
   for (int j = 0; j < kGroup; ++j) {
     w[j] = j < n ? e[j].w : 0u;            // zero-weight copies of the first entry
     a[j] = j < n ? e[j].a : e[0].a;
   }
   const int32_t lo = e[0].chunk, hi = e[n - 1].chunk;
-  const bool sync = first || last || lo != *prev_lo || hi != *prev_hi;
+  // the consumer looks for the end bits only on groups that carry the sync bit
+  const bool sync = first || last || seg_end || lo != *prev_lo || hi != *prev_hi;
   a[kLoWord] |= (uint32_t)lo << kLoShift;
-  a[kHiWord] |= (uint32_t)hi << kHiShift | (uint32_t)sync << kSyncBit | (uint32_t)last << kEndBit;
+  a[kHiWord] |= (uint32_t)hi << kHiShift | (uint32_t)sync << kSyncBit | (uint32_t)last << kEndBit |
+                (uint32_t)seg_end << kSegEndBit;
   *prev_lo = lo;
   *prev_hi = hi;
   for (int j = 0; j < kGroup; ++j) out.push_back(w[j]);
@@ -118,7 +120,7 @@ void emit_group(std::vector<uint32_t>& out, const Entry* e, int n, bool first, b
 }  // namespace
 
 sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* values, int32_t M,
-                 int32_t K, int32_t RW, const int32_t* perm, Packed* out) {
+                 int32_t K, int32_t RW, const int32_t* perm, int32_t split_chunks, Packed* out) {
   try {
     Packed& P = *out;
     P.M = M;
@@ -132,6 +134,10 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
     P.panel_rows.assign((size_t)P.npanels * RW, -1);
     for (int32_t i = 0; i < M; ++i) P.panel_rows[i] = perm[i];
     P.panel_start.assign((size_t)P.npanels, -1);
+    P.split_chunks = split_chunks;
+    P.nseg = split_chunks > 0 ? std::max(1, (P.nchunks + split_chunks - 1) / split_chunks) : 1;
+    if (split_chunks > 0) P.seg_start.assign((size_t)P.npanels * P.nseg, -1);
+    auto seg_of = [&](int32_t c) { return split_chunks > 0 ? c / split_chunks : 0; };
     P.entries.clear();
     P.entries.reserve((size_t)(P.nnz + P.nnz / 8 + 64) * 2);
 
@@ -176,10 +182,19 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
       size_t i = 0;
       bool first = true;
       while (i < ent.size()) {
-        int n = 1;  // a group never reads more than kRing chunks
-        while (n < kGroup && i + n < ent.size() && ent[i + n].chunk - ent[i].chunk < kRing) ++n;
+        // a group never reads more than kRing chunks, nor two K-segments
+        const int32_t seg = seg_of(ent[i].chunk);
+        int n = 1;
+        while (n < kGroup && i + n < ent.size() && ent[i + n].chunk - ent[i].chunk < kRing &&
+               seg_of(ent[i + n].chunk) == seg)
+          ++n;
         const bool last = i + n == ent.size();
-        emit_group(P.entries, &ent[i], n, first, last, &prev_lo, &prev_hi);
+        const bool seg_first = first || seg_of(ent[i - 1].chunk) != seg;
+        const bool seg_end = last || seg_of(ent[i + n].chunk) != seg;
+        if (split_chunks > 0 && seg_first)
+          P.seg_start[(size_t)p * P.nseg + seg] = (int32_t)(P.entries.size() / (2 * kGroup));
+        emit_group(P.entries, &ent[i], n, first || (split_chunks > 0 && seg_first), last,
+                   split_chunks > 0 && seg_end, &prev_lo, &prev_hi);
         first = false;
         i += n;
       }
@@ -223,6 +238,12 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
   if ((int64_t)P.entries.size() != 2 * (P.stored + kTailGroups * kGroup)) return false;
   if (P.stored % kGroup != 0) return false;
   if ((int64_t)P.panel_start.size() != P.npanels) return false;
+  const bool split = P.split_chunks > 0;
+  auto seg_of = [&](int32_t c) { return split ? c / P.split_chunks : 0; };
+  if (split ? (P.nseg != std::max(1, (P.nchunks + P.split_chunks - 1) / P.split_chunks) ||
+               (int64_t)P.seg_start.size() != (int64_t)P.npanels * P.nseg)
+            : (P.nseg != 1 || !P.seg_start.empty()))
+    return false;
   const int64_t ngroups = P.stored / kGroup;
   std::vector<char> seen((size_t)P.nnz, 0);
   int64_t expect_group = 0;  // panels are stored back to back
@@ -238,8 +259,11 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
       }
     if (want.empty()) {
       if (P.panel_start[p] != -1) return false;
+      for (int32_t sg = 0; split && sg < P.nseg; ++sg)
+        if (P.seg_start[(size_t)p * P.nseg + sg] != -1) return false;
       continue;
     }
+    std::vector<int64_t> seg_first(split ? (size_t)P.nseg : 0, -1);
     if (P.panel_start[p] != expect_group) return false;
     size_t k = 0;  // next wanted entry
     int32_t prev_lo = -1, prev_hi = -1;
@@ -249,16 +273,19 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
       const uint32_t* a = w + kGroup;
       const int32_t lo = (int32_t)(a[kLoWord] >> kLoShift), hi = (int32_t)(a[kHiWord] >> kHiShift);
       const bool sync = (a[kHiWord] >> kSyncBit) & 1u, last = (a[kHiWord] >> kEndBit) & 1u;
+      const bool seg_end = (a[kHiWord] >> kSegEndBit) & 1u;
       if (lo > hi || hi - lo >= kRing || hi >= P.nchunks || lo < prev_lo) return false;
+      if (seg_of(hi) != seg_of(lo)) return false;
       const bool first = g == P.panel_start[p];
-      if (sync != (first || last || lo != prev_lo || hi != prev_hi)) return false;
+      if (sync != (first || last || seg_end || lo != prev_lo || hi != prev_hi)) return false;
+      if (split && seg_first[seg_of(lo)] < 0) seg_first[seg_of(lo)] = g;
       prev_lo = lo;
       prev_hi = hi;
       int nreal = 0;
       int32_t max_chunk = -1;
       for (int j = 0; j < kGroup; ++j) {
         uint32_t fields = a[j] & ((1u << kLoShift) - 1);
-        if (j == kHiWord) fields &= ~(1u << kEndBit);
+        if (j == kHiWord) fields &= ~(1u << kEndBit | 1u << kSegEndBit);
         if ((fields >> kRowBits) & ((1u << (kRingRowShift - kRowBits)) - 1)) return false;
         if (j < kLoWord && (a[j] >> kLoShift) != 0u) return false;
         const uint32_t row = fields & ((1u << kRowBits) - 1);
@@ -287,15 +314,18 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
       }
       if (max_chunk != hi) return false;
       if (last != (k == want.size())) return false;
-      if (nreal < kGroup && !last) {  // cut short: the next entry is too far ahead
-        const int32_t next_chunk = col_idx[want[k]] / kChunk;
-        if (next_chunk - lo < kRing) return false;
-      }
+      // cut short: the next entry is too far ahead or in the next K-segment
+      const int32_t next_chunk = last ? -1 : col_idx[want[k]] / kChunk;
+      if (nreal < kGroup && !last && next_chunk - lo < kRing && seg_of(next_chunk) == seg_of(lo))
+        return false;
+      if (seg_end != (split && (last || seg_of(next_chunk) != seg_of(lo)))) return false;
       if (last) {
         expect_group = g + 1;
         break;
       }
     }
+    for (int32_t sg = 0; split && sg < P.nseg; ++sg)
+      if (P.seg_start[(size_t)p * P.nseg + sg] != seg_first[sg]) return false;
   }
   if (expect_group != ngroups) return false;
   // panel_order: a permutation of the panels, by stored groups (descending)
@@ -335,6 +365,7 @@ struct Options {
   std::vector<int32_t> rws;      // panel heights to pack
   int32_t permute = 1;           // row order: Algorithm 1 (see row_order)
   int32_t out_permuted = 0;      // store C in the permuted row order
+  int32_t split_chunks = 0;      // chunks per K-segment (0: no K-segments)
   const int32_t* in_perm = nullptr;  // order of B's rows (NULL: original)
 };
 
@@ -350,6 +381,8 @@ static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* 
   }
   if (opts->permute < 0 || opts->permute > 5) return SDNN_ERR_DIM;
   if (opts->out_permuted != 0 && opts->out_permuted != 1) return SDNN_ERR_DIM;
+  if (opts->split_chunks < 0) return SDNN_ERR_DIM;
+  o->split_chunks = opts->split_chunks;
   o->permute = opts->permute;
   o->out_permuted = opts->out_permuted;
   o->in_perm = opts->in_perm;
@@ -620,7 +653,7 @@ static sdnn_status prepare(const int32_t* row_ptr, const int32_t* col_idx, const
   if (st != SDNN_OK) return st;
   for (size_t i = 0; i < o->rws.size(); ++i) {
     st = pack(csr->row_ptr, csr->col_idx, csr->values, M, K, o->rws[i], perm.data(),
-              &(*packs)[i]);
+              o->split_chunks, &(*packs)[i]);
     if (st != SDNN_OK) return st;
   }
   return SDNN_OK;
@@ -645,7 +678,7 @@ static void fill_info(const std::vector<Packed>& packs, int64_t packed_bytes,
   out->k_chunk = kChunk;
   const bool tall = packs.size() > 1;
   out->tall_panel_rows = tall ? packs[1].RW : 0;
-  out->reserved = 0;
+  out->splits = P.split_chunks > 0 ? P.nseg : 0;
   out->tall_rho = tall ? packs[1].rho : 0.0;
   out->tall_fill = tall ? fill_of(packs[1]) : 0.0;
   out->out_permuted = o.out_permuted;
@@ -657,7 +690,8 @@ static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 // Device bytes of one packing's three arrays (each 256-byte aligned).
 static int64_t packing_bytes(const Packed& P) {
   return align256((int64_t)P.entries.size() * 4) + align256((int64_t)P.panel_start.size() * 4) +
-         align256((int64_t)P.panel_rows.size() * 4) + align256((int64_t)P.panel_order.size() * 4);
+         align256((int64_t)P.panel_rows.size() * 4) + align256((int64_t)P.panel_order.size() * 4) +
+         align256((int64_t)P.seg_start.size() * 4);
 }
 
 }  // namespace sdnn
@@ -757,10 +791,14 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
     plan->perm = P0.perm;
     plan->npack = (int)packs.size();
     plan->out_permuted = o.out_permuted;
+    plan->split_chunks = o.split_chunks;
     plan->in_permuted = o.in_perm ? 1 : 0;
 
     int64_t total = 0;
     for (const Packed& P : packs) total += packing_bytes(P);
+    // a K-segmented plan's reduction adds the bias through perm (out_permuted plans)
+    const int64_t perm_off = total;
+    if (o.split_chunks > 0) total += align256((int64_t)M * 4);
     plan->packed_bytes = total;
     if (total > 0) {
       if (hipMalloc(&plan->d_mem, (size_t)total) != hipSuccess) {
@@ -785,6 +823,10 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
         d.panel_start = (const int32_t*)(base + b_ent);
         d.panel_rows = (const int32_t*)(base + b_ent + b_seg);
         d.panel_pos = (const int32_t*)(base + b_ent + b_seg + b_rows);
+        const int64_t b_pos = align256((int64_t)P.panel_order.size() * 4);
+        d.nseg = P.nseg;
+        d.seg_start = P.seg_start.empty() ? nullptr
+                                          : (const int32_t*)(base + b_ent + b_seg + b_rows + b_pos);
         // panel tables in workgroup (slot) order: slot j is panel panel_order[j]
         char* h = host.data() + off;
         if (!P.entries.empty()) memcpy(h, P.entries.data(), P.entries.size() * 4);
@@ -796,8 +838,15 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
           hs[j] = P.panel_start[q];
           memcpy(hr + (size_t)j * P.RW, P.panel_rows.data() + (size_t)q * P.RW, 4 * (size_t)P.RW);
           hp[j] = q;
+          if (!P.seg_start.empty())
+            memcpy((int32_t*)(h + b_ent + b_seg + b_rows + b_pos) + (size_t)j * P.nseg,
+                   P.seg_start.data() + (size_t)q * P.nseg, 4 * (size_t)P.nseg);
         }
         off += packing_bytes(P);
+      }
+      if (o.split_chunks > 0 && M > 0) {
+        memcpy(host.data() + perm_off, P0.perm.data(), (size_t)M * 4);
+        plan->d_perm = (const int32_t*)((char*)plan->d_mem + perm_off);
       }
       if (hipMemcpy(plan->d_mem, host.data(), (size_t)total, hipMemcpyHostToDevice) !=
           hipSuccess) {
@@ -844,7 +893,7 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out) {
   out->k_chunk = kChunk;
   const bool tall = p->npack > 1;
   out->tall_panel_rows = tall ? p->pk[1].RW : 0;
-  out->reserved = 0;
+  out->splits = p->split_chunks > 0 ? d.nseg : 0;
   out->tall_rho = tall ? p->pk[1].rho : 0.0;
   out->tall_fill = tall ? p->pk[1].fill : 0.0;
   out->out_permuted = p->out_permuted;
@@ -870,26 +919,62 @@ static bool ranges_overlap(const void* a, int64_t abytes, const void* b, int64_t
   return a0 < b0 + (uintptr_t)bbytes && b0 < a0 + (uintptr_t)abytes;
 }
 
-sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
-                      sdnn_epilogue epi, void* stream) {
+// Checks of a K-split call's workspace: nseg * M * N floats, 16-byte aligned, clear of
+// the call's other buffers.  A plan with one K-segment needs none.
+static sdnn_status check_workspace(const sdnn_plan_s* p, int64_t N, const float* ws,
+                                   int64_t ws_floats, const void* in, int64_t inbytes,
+                                   const float* C, const float* bias) {
+  if (p->split_chunks <= 0) return SDNN_ERR_DIM;
+  const int64_t nseg = p->pk[0].nseg;
+  if (nseg == 1) return SDNN_OK;
+  if (!ws) return SDNN_ERR_NULL;
+  const int64_t need = nseg * p->M * N;
+  if (ws_floats < need || ((uintptr_t)ws & 15) != 0) return SDNN_ERR_DIM;
+  const int64_t wbytes = need * 4;
+  if (ranges_overlap(ws, wbytes, in, inbytes) || ranges_overlap(ws, wbytes, C, p->M * N * 4) ||
+      ranges_overlap(ws, wbytes, bias, (int64_t)p->M * 4))
+    return SDNN_ERR_DIM;
+  return SDNN_OK;
+}
+
+static sdnn_status spmm_entry(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
+                              sdnn_epilogue epi, float* ws, int64_t ws_floats, bool split,
+                              void* stream) {
   if (!p) return SDNN_ERR_NULL;
   if (N < 0) return SDNN_ERR_DIM;
   if (epi != SDNN_EPI_NONE && epi != SDNN_EPI_RELU && epi != SDNN_EPI_GELU) return SDNN_ERR_DIM;
+  if (split && p->split_chunks <= 0) return SDNN_ERR_DIM;
   if (p->M == 0 || N == 0) return SDNN_OK;
   if (!C) return SDNN_ERR_NULL;
   if (p->K > 0 && !B) return SDNN_ERR_NULL;
   const int64_t bbytes = (int64_t)p->K * N * 4, cbytes = (int64_t)p->M * N * 4;
   if (ranges_overlap(B, bbytes, C, cbytes)) return SDNN_ERR_DIM;
   if (ranges_overlap(bias, (int64_t)p->M * 4, C, cbytes)) return SDNN_ERR_DIM;
+  if (split) {
+    const sdnn_status st = check_workspace(p, N, ws, ws_floats, B, bbytes, C, bias);
+    if (st != SDNN_OK) return st;
+  }
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess) return SDNN_ERR_HIP;
   if (cur != p->device) return SDNN_ERR_DEVICE;
   try {
-    hipError_t e = launch_spmm(p, B, C, N, bias, (int)epi, (hipStream_t)stream);
+    hipError_t e = split ? launch_spmm_split(p, B, C, N, bias, (int)epi, ws, (hipStream_t)stream)
+                         : launch_spmm(p, B, C, N, bias, (int)epi, (hipStream_t)stream);
     return e == hipSuccess ? SDNN_OK : SDNN_ERR_HIP;
   } catch (...) {
     return SDNN_ERR_HIP;
   }
+}
+
+sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
+                      sdnn_epilogue epi, void* stream) {
+  return spmm_entry(p, B, C, N, bias, epi, nullptr, 0, false, stream);
+}
+
+sdnn_status sdnn_spmm_split(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
+                            sdnn_epilogue epi, float* workspace, int64_t workspace_floats,
+                            void* stream) {
+  return spmm_entry(p, B, C, N, bias, epi, workspace, workspace_floats, true, stream);
 }
 
 sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, void* stream,
@@ -914,13 +999,15 @@ sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, voi
   }
 }
 
-sdnn_status sdnn_conv3x3(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
-                         int32_t NB, const float* bias, sdnn_epilogue epi, void* stream) {
+static sdnn_status conv_entry(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
+                              int32_t NB, const float* bias, sdnn_epilogue epi, float* ws,
+                              int64_t ws_floats, bool split, void* stream) {
   if (!p) return SDNN_ERR_NULL;
   if (H < 0 || W < 0 || NB < 0) return SDNN_ERR_DIM;
   if (epi != SDNN_EPI_NONE && epi != SDNN_EPI_RELU && epi != SDNN_EPI_GELU) return SDNN_ERR_DIM;
   if (p->K % 9 != 0 || p->K == 0 || p->in_permuted) return SDNN_ERR_DIM;
   if (NB % 4 != 0) return SDNN_ERR_DIM;
+  if (split && p->split_chunks <= 0) return SDNN_ERR_DIM;
   const int64_t N = (int64_t)H * W * NB;
   if (p->M == 0 || N == 0) return SDNN_OK;
   // 32-bit column and channel-plane byte offsets in the staging loop
@@ -931,15 +1018,32 @@ sdnn_status sdnn_conv3x3(sdnn_plan p, const float* X, float* C, int32_t H, int32
   const int64_t xbytes = (int64_t)(p->K / 9) * N * 4, cbytes = (int64_t)p->M * N * 4;
   if (ranges_overlap(X, xbytes, C, cbytes)) return SDNN_ERR_DIM;
   if (ranges_overlap(bias, (int64_t)p->M * 4, C, cbytes)) return SDNN_ERR_DIM;
+  if (split) {
+    const sdnn_status st = check_workspace(p, N, ws, ws_floats, X, xbytes, C, bias);
+    if (st != SDNN_OK) return st;
+  }
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess) return SDNN_ERR_HIP;
   if (cur != p->device) return SDNN_ERR_DEVICE;
   try {
-    hipError_t e = launch_conv3x3(p, X, C, H, W, NB, bias, (int)epi, (hipStream_t)stream);
+    hipError_t e =
+        split ? launch_conv3x3_split(p, X, C, H, W, NB, bias, (int)epi, ws, (hipStream_t)stream)
+              : launch_conv3x3(p, X, C, H, W, NB, bias, (int)epi, (hipStream_t)stream);
     return e == hipSuccess ? SDNN_OK : SDNN_ERR_HIP;
   } catch (...) {
     return SDNN_ERR_HIP;
   }
+}
+
+sdnn_status sdnn_conv3x3(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
+                         int32_t NB, const float* bias, sdnn_epilogue epi, void* stream) {
+  return conv_entry(p, X, C, H, W, NB, bias, epi, nullptr, 0, false, stream);
+}
+
+sdnn_status sdnn_conv3x3_split(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
+                               int32_t NB, const float* bias, sdnn_epilogue epi, float* workspace,
+                               int64_t workspace_floats, void* stream) {
+  return conv_entry(p, X, C, H, W, NB, bias, epi, workspace, workspace_floats, true, stream);
 }
 
 sdnn_status sdnn_dense_gemm(const float* W, const float* B, float* C, int32_t M, int32_t K,

@@ -27,6 +27,7 @@ constexpr int kTileCols = 256;
 constexpr int kTailGroups = 16;
 // Fields of a group's address words a_0..a_7 (see Packed); L = kGroup - 1.
 constexpr int kRowBits = 8;         // a_j & 0xff: row inside the panel
+constexpr int kSegEndBit = 8;       // a_L: last group of the panel in its K-segment
 constexpr int kEndBit = 9;          // a_L: last group of the panel
 constexpr int kRingRowShift = 10;   // (a_j >> 10) & 0x7f: row of the LDS ring
 constexpr int kSyncBit = 17;        // a_L: publish progress / check readiness first
@@ -54,6 +55,13 @@ static_assert(kRing * kChunk <= 128, "ring rows must fit 7 bits");
 //   whenever c_lo or c_hi differs from the previous group's.  Panels are stored back
 //   to back; panel_start holds each panel's first group (-1: the panel has no
 //   entries).  The stream ends with kTailGroups zero groups.
+//
+//   K-segments (split_chunks = S > 0): chunks [s*S, (s+1)*S) form segment s, no group
+//   holds entries of two segments (an entry of the next segment starts a new group,
+//   like one too far ahead), the first and the last group of each segment a panel has
+//   entries in carry the sync bit, the last one also seg_end (a7 bit 8), and
+//   seg_start[p][s] is the panel's first group in segment s (-1: none).  A launch may
+//   then give each segment to its own workgroup.
 struct Packed {
   int32_t M = 0, K = 0, RW = 0, nchunks = 0, npanels = 0;
   int64_t nnz = 0, stored = 0;     // structural entries, stored entries (with padding)
@@ -63,6 +71,9 @@ struct Packed {
   std::vector<int32_t> panel_order; // [npanels] panels by stored groups, heaviest first
   std::vector<uint32_t> entries;    // [2*(stored + kTailGroups*kGroup)] dwords
   double rho = 1.0;                 // nnz / sum_p |union of the panel's column sets|
+  int32_t split_chunks = 0;         // chunks per K-segment (0: one segment, no table)
+  int32_t nseg = 1;                 // K-segments
+  std::vector<int32_t> seg_start;   // [npanels*nseg] (split_chunks > 0 only)
 };
 
 // Panel heights of the two packings a default plan holds: short panels keep enough
@@ -78,7 +89,7 @@ sdnn_status reorder_bitset(const int32_t* row_ptr, const int32_t* col_idx, int32
                            int32_t* perm_out);
 // Builds the packed stream (inputs already validated, perm is a permutation of 0..M-1).
 sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* values, int32_t M,
-                 int32_t K, int32_t RW, const int32_t* perm, Packed* out);
+                 int32_t K, int32_t RW, const int32_t* perm, int32_t split_chunks, Packed* out);
 
 // A launch shape sdnn_plan_tune measured fastest for one N: which packing, and how many
 // consumer waves per workgroup.
@@ -95,6 +106,8 @@ struct DevPacking {
   const int32_t* panel_start = nullptr;   // [npanels] (in groups, -1: empty panel)
   const int32_t* panel_rows = nullptr;    // [npanels*RW]
   const int32_t* panel_pos = nullptr;     // [npanels] panel index of each slot
+  const int32_t* seg_start = nullptr;     // [npanels*nseg] in slot order (split plans)
+  int32_t nseg = 1;                       // K-segments
   // (panel_start and panel_rows are uploaded in slot order: slot j holds panel
   // panel_pos[j], the j-th heaviest; workgroups take consecutive slots)
 };
@@ -112,6 +125,8 @@ struct sdnn_plan_s {
   int npack = 0;               // 1 (explicit panel height) or 2 (short, tall)
   int32_t out_permuted = 0;    // C rows stored in the permuted order
   int32_t in_permuted = 0;     // W's columns renamed to a caller-given order of B's rows
+  int32_t split_chunks = 0;    // chunks per K-segment (0: the packings have one segment)
+  const int32_t* d_perm = nullptr;  // [M] perm on the device (K-segmented plans only)
   sdnn::DevPacking pk[2];
   sdnn::TunedShape tuned[sdnn::kTunedSlots];  // filled by sdnn_plan_tune
   int32_t ntuned = 0;
@@ -123,6 +138,13 @@ hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N
                        const float* bias, int epi, hipStream_t stream);
 hipError_t launch_conv3x3(const sdnn_plan_s* p, const float* X, float* C, int32_t H, int32_t W,
                           int32_t NB, const float* bias, int epi, hipStream_t stream);
+// K-split variants: ws holds nseg * M * N floats (nseg = p->pk[0].nseg); with one
+// segment they are the plain launches and ws is not touched.
+hipError_t launch_spmm_split(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
+                             const float* bias, int epi, float* ws, hipStream_t stream);
+hipError_t launch_conv3x3_split(const sdnn_plan_s* p, const float* X, float* C, int32_t H,
+                                int32_t W, int32_t NB, const float* bias, int epi, float* ws,
+                                hipStream_t stream);
 // Times every candidate launch shape of the plan at N on the given buffers (blocking)
 // and records the fastest in p->tuned.
 hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStream_t stream,

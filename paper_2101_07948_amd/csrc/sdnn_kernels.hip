@@ -54,9 +54,11 @@ struct ConsumerArgs {
   uint32_t ready_addr;     // LDS address of the ready word
   uint32_t poll_budget;    // failed readiness checks the wave may poll through in total
   uint32_t overrun_addr;   // LDS address of the workgroup's overrun word
+  uint32_t end_mask;       // a7 bit that ends the wave's groups: panel end, or K-segment end
 };
 struct ProducerArgs {
-  int32_t nchunks, K;
+  int32_t nchunks, K;      // nchunks: one past the last chunk to stage
+  int32_t first_chunk;     // first chunk to stage
   uint32_t row_bytes;      // N * 4
   uint32_t bbase_lo, bbase_hi;  // address of B[0][n0]
   int32_t ncol;            // N - n0 (columns of the tile that exist)
@@ -119,6 +121,10 @@ struct SpmmArgs {
   int32_t out_permuted;  // store permuted row i at row i instead of at its source row
   int32_t H, W, NB;      // image geometry of a 3x3 convolution (B is then the input X)
   uint32_t poll_budget;  // failed readiness / ring-limit checks a wave may poll through
+  // split-K: nsplit > 1 gives K-segment s (chunks [s, s+1) * split_chunks) of each tile
+  // and row-block its own workgroup, which writes its partial product, without bias or
+  // activation, to C + s * M * N (C is then the workspace)
+  int32_t M, nsplit, nseg, split_chunks;
 };
 
 // Producer kinds: 4-byte staging (any N), 16-byte staging (N % 4 == 0, aligned), the
@@ -131,8 +137,8 @@ template <int RW, int STAGE>
 __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     const uint32_t* __restrict__ entries, const int32_t* __restrict__ panel_start,
     const int32_t* __restrict__ panel_rows, const int32_t* __restrict__ panel_pos,
-    const float* __restrict__ B, float* __restrict__ C, const float* __restrict__ bias,
-    SpmmArgs a) {
+    const int32_t* __restrict__ seg_start, const float* __restrict__ B, float* __restrict__ C,
+    const float* __restrict__ bias, SpmmArgs a) {
   // the ring ([0, kRingBytes)) and the control words; the ring must start at LDS 0
   // (the loops form LDS addresses from the ring-row field alone), which holds because
   // this is the kernel's only LDS object
@@ -141,15 +147,23 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
   const int bid = blockIdx.x;
   const int lin = (bid & 7) * a.per_xcd + (bid >> 3);
   if (lin >= a.total_wg) return;  // whole workgroup leaves before the barrier
-  const int tile = lin / a.n_rb;
-  const int rb = lin - tile * a.n_rb;
+  // workgroups of one tile and K-segment are consecutive (they share the staged rows)
+  const int per_tile = a.nsplit * a.n_rb;
+  const int tile = lin / per_tile;
+  const int split = (lin - tile * per_tile) / a.n_rb;
+  const int rb = lin - tile * per_tile - split * a.n_rb;
+  const bool splitk = a.nsplit > 1;
+  const int c0 = splitk ? split * a.split_chunks : 0;
+  const int c1 = splitk ? min(c0 + a.split_chunks, a.nchunks) : a.nchunks;
   const int nc = (blockDim.x >> 6) - kProducers;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int n0 = tile * kTileCols;
   const int prod = wave - nc;  // >= 0: producer index
   const int panel = rb * nc + wave;
-  const int gstart = (prod < 0 && panel < a.npanels) ? panel_start[panel] : -1;
+  const int gstart = (prod < 0 && panel < a.npanels)
+                         ? (splitk ? seg_start[(size_t)panel * a.nseg + split] : panel_start[panel])
+                         : -1;
 
   const uint32_t lds_base = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) uint32_t*)lds);
   if (lds_base != 0) return;  // never taken: see above
@@ -158,17 +172,18 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
   const uint32_t overrun_addr = ready_addr + 128;
   uint32_t* ctl = lds + kRingBytes / 4;
   if (prod >= 0) {
-    if (lane == 0) ctl[prod] = 0u;                                           // nothing landed
+    if (lane == 0) ctl[prod] = (uint32_t)c0;                                 // nothing landed
     if (prod == 0 && lane == 0) ctl[32] = 0u;                                // no overrun
     if (prod == 0 && lane >= nc && lane < 16) ctl[16 + lane] = kProgressDone;  // absent consumers
   } else if (lane == 0) {
-    ctl[16 + wave] = gstart >= 0 ? 0u : kProgressDone;
+    ctl[16 + wave] = gstart >= 0 ? (uint32_t)c0 : kProgressDone;
   }
   __syncthreads();
 
   if (prod >= 0) {
     ProducerArgs pa;
-    pa.nchunks = a.nchunks;
+    pa.nchunks = c1;
+    pa.first_chunk = c0;
     pa.K = a.K;
     pa.row_bytes = (uint32_t)a.N * 4u;
     const uint64_t bb = (uint64_t)(uintptr_t)(B + n0);
@@ -218,6 +233,7 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     ca.ready_addr = ready_addr;
     ca.poll_budget = a.poll_budget;
     ca.overrun_addr = overrun_addr;
+    ca.end_mask = splitk ? 1u << kSegEndBit : 1u << kEndBit;
     if constexpr (RW == 4) consume_rw4(p0, p1, p2, p3, ca);
     if constexpr (RW == 8) consume_rw8(p0, p1, p2, p3, ca);
     if constexpr (RW == 12) consume_rw12(p0, p1, p2, p3, ca);
@@ -229,9 +245,21 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
   for (int r = 0; r < RW; ++r) {
     const int orig = panel_rows[panel * RW + r];
     if (orig < 0) continue;
-    const float bb = bias ? bias[orig] : 0.0f;
-    float* crow = C + (size_t)(a.out_permuted ? panel_pos[panel] * RW + r : orig) * a.N;
+    const int row = a.out_permuted ? panel_pos[panel] * RW + r : orig;
     const float v[4] = {p0[r], p1[r], p2[r], p3[r]};
+    if (splitk) {  // raw partial sums; the reduction adds the bias and applies epi
+      float* prow = C + ((size_t)split * a.M + row) * a.N;
+      if (STAGE != kStageDword && ncol + 4 <= a.N) {
+        *reinterpret_cast<float4*>(prow + ncol) = make_float4(v[0], v[1], v[2], v[3]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (ncol + i < a.N) prow[ncol + i] = v[i];
+      }
+      continue;
+    }
+    const float bb = bias ? bias[orig] : 0.0f;
+    float* crow = C + (size_t)row * a.N;
     if (STAGE != kStageDword && ncol + 4 <= a.N) {
       *reinterpret_cast<float4*>(crow + ncol) =
           make_float4(activation(v[0] + bb, a.epi), activation(v[1] + bb, a.epi),
@@ -249,6 +277,7 @@ struct SpmmPtrs {
   const int32_t* panel_start;
   const int32_t* panel_rows;
   const int32_t* panel_pos;
+  const int32_t* seg_start;
   const float* B;
   float* C;
   const float* bias;
@@ -258,8 +287,8 @@ template <int RW, int STAGE>
 hipError_t launch_variant(const SpmmPtrs& p, const SpmmArgs& args, int waves, int grid,
                           hipStream_t stream) {
   hipLaunchKernelGGL((spmm_panel_kernel<RW, STAGE>), dim3(grid), dim3(64 * (waves + kProducers)), 0, stream,
-                     p.entries, p.panel_start, p.panel_rows, p.panel_pos, p.B, p.C, p.bias,
-                     args);
+                     p.entries, p.panel_start, p.panel_rows, p.panel_pos, p.seg_start, p.B, p.C,
+                     p.bias, args);
   return hipGetLastError();
 }
 
@@ -302,7 +331,7 @@ int64_t rounds_of(int64_t n_tiles, int npanels, int waves, int target) {
 // Consumer waves per workgroup: the fewest rounds that the register-limited consumer
 // count allows, and within that many rounds the smallest workgroups (fewest panels
 // each, so the most workgroups share the work).  SDNN_FORCE_WAVES fixes the count.
-LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N) {
+LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N, int nseg = 1) {
   const int target = num_cus > 0 ? num_cus : 256;
   int cap = max_consumers(pk.RW);
   if (cap > pk.npanels) cap = pk.npanels;
@@ -310,13 +339,14 @@ LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N) {
   const int forceW = env_int("SDNN_FORCE_WAVES", 0);
   LaunchCfg c;
   c.n_tiles = (N + kTileCols - 1) / kTileCols;
+  const int64_t units = (int64_t)c.n_tiles * nseg;  // (tile, K-segment) pairs
   if (forceW > 0) {
     c.waves = forceW < cap ? forceW : cap;
   } else {
-    const int64_t fewest = rounds_of(c.n_tiles, pk.npanels, cap, target);
+    const int64_t fewest = rounds_of(units, pk.npanels, cap, target);
     c.waves = cap;
     for (int w = 1; w < cap; ++w)
-      if (rounds_of(c.n_tiles, pk.npanels, w, target) == fewest) {
+      if (rounds_of(units, pk.npanels, w, target) == fewest) {
         c.waves = w;
         break;
       }
@@ -329,15 +359,16 @@ LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N) {
 // at least a full workgroup of tall panels per CU, else the first.  A convolution,
 // whose workgroups are bound by staging its shifted input rows rather than by their
 // panels: the packing that needs fewer rounds, the first on a tie.
-const DevPacking& choose_packing(const sdnn_plan_s* p, int N, bool conv) {
+// A K-split launch, whose workgroups stage a segment each, is chosen like a convolution.
+const DevPacking& choose_packing(const sdnn_plan_s* p, int N, bool conv, int nseg = 1) {
   if (p->npack < 2) return p->pk[0];
   const DevPacking& tall = p->pk[1];
   const int64_t n_tiles = (N + kTileCols - 1) / kTileCols;
   const int cus = p->num_cus > 0 ? p->num_cus : 256;
-  if (conv) {
-    const LaunchCfg s = choose_cfg(p->pk[0], cus, N), t = choose_cfg(tall, cus, N);
-    return rounds_of(n_tiles, tall.npanels, t.waves, cus) <
-                   rounds_of(n_tiles, p->pk[0].npanels, s.waves, cus)
+  if (conv || nseg > 1) {
+    const LaunchCfg s = choose_cfg(p->pk[0], cus, N, nseg), t = choose_cfg(tall, cus, N, nseg);
+    return rounds_of(n_tiles * nseg, tall.npanels, t.waves, cus) <
+                   rounds_of(n_tiles * nseg, p->pk[0].npanels, s.waves, cus)
                ? tall
                : p->pk[0];
   }
@@ -348,29 +379,93 @@ const DevPacking& choose_packing(const sdnn_plan_s* p, int N, bool conv) {
 }  // namespace
 
 namespace {
+// Split-K reduction: C[i][n] = act(sum_s ws[s][i][n] + bias[rowmap[i]]) over the nseg
+// partial products of an M x N output (rowmap: NULL for the identity).  Each thread
+// takes four consecutive columns of one row; vec: N % 4 == 0 and 16-byte aligned
+// buffers, so the four are one float4.
+template <bool VEC>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ ws,
+                                                            float* __restrict__ C,
+                                                            const float* __restrict__ bias,
+                                                            const int32_t* __restrict__ rowmap,
+                                                            int32_t M, int32_t N, int32_t nseg,
+                                                            int32_t epi) {
+  const int64_t nq = (N + 3) / 4, total = (int64_t)M * nq, plane = (int64_t)M * N;
+  for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < total;
+       q += (int64_t)gridDim.x * 256) {
+    const int32_t i = (int32_t)(q / nq);
+    const int32_t n = (int32_t)(q - (int64_t)i * nq) * 4;
+    const int64_t at = (int64_t)i * N + n;
+    const float bb = bias ? bias[rowmap ? rowmap[i] : i] : 0.0f;
+    if (VEC) {
+      float4 acc = *reinterpret_cast<const float4*>(ws + at);
+      for (int s = 1; s < nseg; ++s) {
+        const float4 v = *reinterpret_cast<const float4*>(ws + s * plane + at);
+        acc.x += v.x;
+        acc.y += v.y;
+        acc.z += v.z;
+        acc.w += v.w;
+      }
+      *reinterpret_cast<float4*>(C + at) =
+          make_float4(activation(acc.x + bb, epi), activation(acc.y + bb, epi),
+                      activation(acc.z + bb, epi), activation(acc.w + bb, epi));
+    } else {
+      for (int c = 0; c < 4 && n + c < N; ++c) {
+        float acc = ws[at + c];
+        for (int s = 1; s < nseg; ++s) acc += ws[s * plane + at + c];
+        C[at + c] = activation(acc + bb, epi);
+      }
+    }
+  }
+}
+
+hipError_t launch_reduce(const float* ws, float* C, const float* bias, const int32_t* rowmap,
+                         int32_t M, int32_t N, int32_t nseg, int epi, hipStream_t stream) {
+  const int64_t total = (int64_t)M * ((N + 3) / 4);
+  const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8 * 1024);
+  const bool vec = N % 4 == 0 && ((uintptr_t)ws & 15) == 0 && ((uintptr_t)C & 15) == 0;
+  if (vec)
+    hipLaunchKernelGGL(splitk_reduce_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       ws, C, bias, rowmap, M, N, nseg, epi);
+  else
+    hipLaunchKernelGGL(splitk_reduce_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       ws, C, bias, rowmap, M, N, nseg, epi);
+  return hipGetLastError();
+}
+
 // `shape` (packing index and consumer waves) overrides the plan's tuned or heuristic
-// choice when non-null.  Tuned shapes were timed on products, so a convolution, whose
-// staging differs, keeps the heuristic.
+// choice when non-null.  Tuned shapes were timed on unsplit products, so a convolution,
+// whose staging differs, and a K-split launch keep the heuristic.  ws non-null (a plan
+// with more than one K-segment): every (tile, segment, row-block) is a workgroup that
+// writes its partial product to ws, and a reduction kernel forms C.
 hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                          const float* bias, int epi, const int32_t* conv_hwn,
-                         const TunedShape* shape, hipStream_t stream) {
-  if (!shape && !conv_hwn)
+                         const TunedShape* shape, float* ws, hipStream_t stream) {
+  const int nseg = ws ? p->pk[0].nseg : 1;
+  if (!shape && !conv_hwn && nseg == 1)
     for (int i = 0; i < p->ntuned; ++i)
       if (p->tuned[i].N == N) shape = &p->tuned[i];
-  const DevPacking& pk = shape ? p->pk[shape->pack] : choose_packing(p, N, conv_hwn != nullptr);
-  LaunchCfg cfg = choose_cfg(pk, p->num_cus, N);
+  const DevPacking& pk =
+      shape ? p->pk[shape->pack] : choose_packing(p, N, conv_hwn != nullptr, nseg);
+  LaunchCfg cfg = choose_cfg(pk, p->num_cus, N, nseg);
   if (shape) {
     cfg.waves = shape->waves;
     cfg.n_rb = (pk.npanels + cfg.waves - 1) / cfg.waves;
   }
-  const SpmmPtrs ptrs{pk.entries, pk.panel_start, pk.panel_rows, pk.panel_pos, B, C, bias};
+  float* out = nseg > 1 ? ws : C;
+  const SpmmPtrs ptrs{pk.entries, pk.panel_start, pk.panel_rows, pk.panel_pos, pk.seg_start, B,
+                      out, bias};
   SpmmArgs args;
   args.K = p->K;
   args.N = N;
   args.nchunks = p->nchunks;
   args.npanels = pk.npanels;
   args.n_rb = cfg.n_rb;
-  const int64_t total = (int64_t)cfg.n_tiles * cfg.n_rb;
+  args.M = p->M;
+  args.nsplit = nseg;
+  args.nseg = pk.nseg;
+  args.split_chunks = nseg > 1 ? p->split_chunks : 0;
+  const int64_t total = (int64_t)cfg.n_tiles * nseg * cfg.n_rb;
   if (total > (int64_t)1 << 30) return hipErrorInvalidValue;
   const int64_t grid = (total + 7) / 8 * 8;
   args.total_wg = (int32_t)total;
@@ -384,19 +479,31 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
     const int budget = env_int("SDNN_POLL_BUDGET", kPollBudget);
     args.poll_budget = budget > 0 ? (uint32_t)budget : 0u;
   }
-  if (conv_hwn) return launch_rw<kStageConv>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
-  // the 16-byte producer addresses a chunk's rows with 32-bit per-lane offsets
-  // 16 * lane + r * 4N (r < kChunk / kProducers)
-  const bool vec = (N % 4 == 0) && (((uintptr_t)B & 15) == 0) && (((uintptr_t)C & 15) == 0) &&
-                   (uint64_t)N * 4u * (kChunk / kProducers) < ((uint64_t)1 << 31);
-  return vec ? launch_rw<kStageVec>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream)
-             : launch_rw<kStageDword>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
+  hipError_t err;
+  if (conv_hwn) {
+    err = launch_rw<kStageConv>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
+  } else {
+    // the 16-byte producer addresses a chunk's rows with 32-bit per-lane offsets
+    // 16 * lane + r * 4N (r < kChunk / kProducers)
+    const bool vec = (N % 4 == 0) && (((uintptr_t)B & 15) == 0) && (((uintptr_t)out & 15) == 0) &&
+                     (uint64_t)N * 4u * (kChunk / kProducers) < ((uint64_t)1 << 31);
+    err = vec ? launch_rw<kStageVec>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream)
+              : launch_rw<kStageDword>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
+  }
+  if (err != hipSuccess || nseg == 1) return err;
+  return launch_reduce(ws, C, bias, p->out_permuted ? p->d_perm : nullptr, p->M, N, nseg, epi,
+                       stream);
 }
 }  // namespace
 
 hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                        const float* bias, int epi, hipStream_t stream) {
-  return launch_panels(p, B, C, N, bias, epi, nullptr, nullptr, stream);
+  return launch_panels(p, B, C, N, bias, epi, nullptr, nullptr, nullptr, stream);
+}
+
+hipError_t launch_spmm_split(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
+                             const float* bias, int epi, float* ws, hipStream_t stream) {
+  return launch_panels(p, B, C, N, bias, epi, nullptr, nullptr, ws, stream);
 }
 
 hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStream_t stream,
@@ -420,10 +527,10 @@ hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStr
   float best = -1.0f;
   for (size_t i = 0; i < cands.size() && err == hipSuccess; ++i) {
     for (int r = 0; r < 2 && err == hipSuccess; ++r)   // warm-up
-      err = launch_panels(p, B, C, N, nullptr, 0, nullptr, &cands[i], stream);
+      err = launch_panels(p, B, C, N, nullptr, 0, nullptr, &cands[i], nullptr, stream);
     if (err == hipSuccess) err = hipEventRecord(e0, stream);
     for (int r = 0; r < 5 && err == hipSuccess; ++r)
-      err = launch_panels(p, B, C, N, nullptr, 0, nullptr, &cands[i], stream);
+      err = launch_panels(p, B, C, N, nullptr, 0, nullptr, &cands[i], nullptr, stream);
     if (err == hipSuccess) err = hipEventRecord(e1, stream);
     if (err == hipSuccess) err = hipEventSynchronize(e1);
     float ms = 0.0f;
@@ -447,7 +554,14 @@ hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStr
 hipError_t launch_conv3x3(const sdnn_plan_s* p, const float* X, float* C, int32_t H, int32_t W,
                           int32_t NB, const float* bias, int epi, hipStream_t stream) {
   const int32_t hwn[3] = {H, W, NB};
-  return launch_panels(p, X, C, H * W * NB, bias, epi, hwn, nullptr, stream);
+  return launch_panels(p, X, C, H * W * NB, bias, epi, hwn, nullptr, nullptr, stream);
+}
+
+hipError_t launch_conv3x3_split(const sdnn_plan_s* p, const float* X, float* C, int32_t H,
+                                int32_t W, int32_t NB, const float* bias, int epi, float* ws,
+                                hipStream_t stream) {
+  const int32_t hwn[3] = {H, W, NB};
+  return launch_panels(p, X, C, H * W * NB, bias, epi, hwn, nullptr, ws, stream);
 }
 
 // ---------------------------------------------------------------------------------
