@@ -164,28 +164,47 @@ def plan_check_host(row_ptr, col_idx, values, M: int, K: int, panel_rows: int = 
     return info.as_dict()
 
 
-def _stream_handle(stream) -> Optional[int]:
-    import torch
+_torch = None
+
+
+def _torch_mod():
+    global _torch
+    if _torch is None:
+        import torch
+        _torch = torch
+    return _torch
+
+
+def _stream_handle(stream) -> int:
+    """The raw hipStream_t of `stream` (default: the current stream) as an integer.  The
+    current stream is read through torch's raw-handle accessor, which skips building a
+    Stream object (a few microseconds per call, as much as a small kernel takes)."""
     if stream is None:
-        stream = torch.cuda.current_stream()
-    return ctypes.c_void_p(stream.cuda_stream)
+        torch = _torch_mod()
+        return torch._C._cuda_getCurrentRawStream(torch.cuda.current_device())
+    return stream.cuda_stream
 
 
 def _dev_ptr(t, name: str, shape, allow_none=False):
-    import torch
+    """Device address of a contiguous float32 GPU tensor of the given shape (checked on a
+    fast path; the slow path only builds the error message)."""
     if t is None:
         if allow_none:
             return None
         raise ValueError(f"{name} is required")
+    torch = _torch_mod()
+    try:
+        if t.is_cuda and t.dtype is torch.float32 and t.shape == shape and t.is_contiguous():
+            return t.data_ptr()
+    except AttributeError:
+        pass
     if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
         raise TypeError(f"{name} must be a CUDA/HIP torch tensor")
     if t.dtype != torch.float32:
         raise TypeError(f"{name} must be float32")
     if tuple(t.shape) != tuple(shape):
         raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
-    if not t.is_contiguous():
-        raise ValueError(f"{name} must be contiguous (row-major)")
-    return ctypes.c_void_p(t.data_ptr())
+    raise ValueError(f"{name} must be contiguous (row-major)")
 
 
 class Plan:
@@ -312,8 +331,10 @@ class Plan:
         pb = _dev_ptr(B, "B", (self.K, N))
         pc = _dev_ptr(C, "C", (self.M, N))
         pbias = _dev_ptr(bias, "bias", (self.M,), allow_none=True)
-        _check(self._lib.sdnn_spmm(self.handle, pb, pc, N, pbias, EPI[epi],
-                                   _stream_handle(stream)), "sdnn_spmm")
+        code = self._lib.sdnn_spmm(self._h, pb, pc, N, pbias, EPI[epi], _stream_handle(stream))
+        if code:
+            self.handle  # a closed plan raises here
+            raise SdnnError(code, "sdnn_spmm")
         return C
 
     def close(self):
