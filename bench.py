@@ -402,59 +402,61 @@ def run_suite(out_path):
             print(lines[-1], flush=True)
             del Xs, Cs, Bd, Wd, Cd
 
-    # K-split calls on the grids that leave CUs idle: every K-segment of a tile gets its
-    # own workgroup (plans with split_chunks), and a reduction kernel forms C
+    # K-split calls on the grids that leave CUs idle: runs of a tile's K-segments get
+    # their own workgroups (plans with split_chunks), and a reduction kernel forms C
+    counts = (2, 4, 8)
     lines += ["", "## K-split calls (sdnn_spmm_split / sdnn_conv3x3_split) on small grids", "",
-              "Unsplit: the plain call.  Split: the same problem on plans with split_chunks = "
-              "S (segments of S * 32 rows of B), each timed (cold mean of 50 launches, "
-              "reduction included); the best S is shown with its segment count.", "",
-              "| problem | column tiles x panels | unsplit us | " +
-              " | ".join(f"{k} segments" for k in (2, 4, 6, 8)) + " | best speedup |",
-              "|---|---|---|---|---|---|---|---|"]
+              "Unsplit: the plain call on a plain plan.  Split: a plan with about 16-24 "
+              "K-segments (split_chunks = S chunks of 32 rows each), called with the "
+              "library's choice of workgroups along K (auto) and with forced counts; "
+              "cold means of 50 launches, reduction included.", "",
+              "| problem | column tiles x panels | unsplit us | S | auto us | " +
+              " | ".join(f"{k} along K us" for k in counts) + " | auto speedup |",
+              "|---|---|---|---|---|" + "---|" * len(counts) + "---|"]
     split_cases = [("W0 768x3072 90% N=1024", inputs.workload("w0", N=4).layers[0].W, 1024, None),
+                   ("W0 768x3072 90% N=4096", inputs.workload("w0", N=4).layers[0].W, 4096, None),
+                   ("C2 768x768 90% N=1024", inputs.workload("c2", N=4).layers[0].W, 1024, None),
                    ("S 2048 90% N=256", inputs.s_layer(2048, 2048, 0.9).W, 256, None),
+                   ("S 2048 70% N=128", inputs.s_layer(2048, 2048, 0.7).W, 128, None),
                    ("S 1024 90% N=256", inputs.s_layer(1024, 1024, 0.9).W, 256, None),
                    ("conv 256 x 256, 14x14", None, 14, 256),
+                   ("conv 256 x 256, 7x7", None, 7, 256),
                    ("conv 512 x 512, 7x7", None, 7, 512)]
     for label, W, n_or_hw, ch in split_cases:
         if ch is None:
             N = n_or_hw
             B = torch.randn(W.K, N, device=dev)
             C = torch.empty(W.M, N, device=dev)
-            call = lambda p, ws: (lambda i: p.spmm(B, C) if ws is None else
-                                  p.spmm_split(B, C, workspace=ws))
+            call = lambda p, ws, k: (lambda i: p.spmm(B, C) if ws is None else
+                                     p.spmm_split(B, C, workspace=ws, splits=k))
         else:
             HW = n_or_hw
             L = inputs.conv_layer(ch, ch, HW, HW, 16, 0.9, layer=ch + HW)
             W, N = L.F, HW * HW * 16
             X = torch.from_numpy(L.X).to(dev)
             C = torch.empty(ch, HW, HW, 16, device=dev)
-            call = lambda p, ws: (lambda i: p.conv3x3(X, C) if ws is None else
-                                  p.conv3x3_split(X, C, workspace=ws))
+            call = lambda p, ws, k: (lambda i: p.conv3x3(X, C) if ws is None else
+                                     p.conv3x3_split(X, C, workspace=ws, splits=k))
         nch = -(-W.K // 32)
-        def timed_mean(p, ws):
-            fn = call(p, ws)
-            for i in range(10):
-                fn(i)
-            torch.cuda.synchronize()
+        S = max(1, -(-nch // 24)) if nch >= 48 else max(1, nch // 16)
+        def timed_mean(p, ws, k=0):
+            fn = call(p, ws, k)
+            _settle(fn, 30)
             return _launch_times(fn, 50)[1]
         with sd.Plan.from_csr(W) as plan:
             base = timed_mean(plan, None)
             info = plan.info
         rw, _ = _packing_used(info, W.M, N, cus)
         grid = f"{-(-N // 256)} x {-(-W.M // rw)} ({rw}-row)"
-        cells, best = [], base
-        for nseg in (2, 4, 6, 8):
-            sc = -(-nch // nseg)
-            with sd.Plan.from_csr(W, split_chunks=sc) as plan:
-                ws = torch.empty(max(plan.workspace_floats(N), 1), device=dev)
-                t_ = timed_mean(plan, ws)
-                segs = plan.info["splits"]
-            best = min(best, t_)
-            cells.append(f"{t_*1e3:.1f} (S={sc}, {segs} seg)")
-        lines.append(f"| {label} | {grid} | {base*1e3:.1f} | " + " | ".join(cells) +
-                     f" | {base/best:.2f}x |")
+        with sd.Plan.from_csr(W, split_chunks=S) as plan:
+            ws = torch.empty(max(plan.workspace_floats(N), 1), device=dev)
+            auto = timed_mean(plan, ws, 0)
+            forced = [timed_mean(plan, ws, k) for k in counts]
+            segs = plan.info["splits"]
+        lines.append(f"| {label} | {grid} | {base*1e3:.1f} | {S} ({segs} seg) | {auto*1e3:.1f} | " +
+                     " | ".join(f"{t_*1e3:.1f}" for t_ in forced) + f" | {base/auto:.2f}x |")
         print(lines[-1], flush=True)
+        del C
 
     # the paper's kernel problems (Sec. 4.1): square M = K from 256 to 2048, 70-95 %
     # sparse by magnitude threshold of a Gaussian matrix, three batch widths

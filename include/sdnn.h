@@ -81,9 +81,10 @@ typedef enum {
  *                 The bias is always given in the original row order.
  *   split_chunks: 0 (default) = no K-segments.  S > 0 cuts K into segments of S chunks
  *                 (S * k_chunk rows of B; nseg = ceil(ceil(K / k_chunk) / S) segments)
- *                 so that sdnn_spmm_split / sdnn_conv3x3_split can give each segment
- *                 of a tile its own workgroup (the split-K tiling of Sec. 3.2.2
- *                 extended across workgroups).  Such plans also serve sdnn_spmm and
+ *                 so that sdnn_spmm_split / sdnn_conv3x3_split can give each run of
+ *                 consecutive segments of a tile its own workgroup (the split-K tiling
+ *                 of Sec. 3.2.2 extended across workgroups); small S leaves the call
+ *                 more choice, at the cost of more stored groups.  Such plans also serve sdnn_spmm and
  *                 sdnn_conv3x3, unsplit.  Negative: SDNN_ERR_DIM.
  *   in_perm:      NULL (default) = B row c is input feature c; otherwise K int32 (host,
  *                 read during the call only), a permutation of 0..K-1 giving the order
@@ -179,24 +180,30 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out);
 sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
                       sdnn_epilogue epi, void* stream);
 
-/* K-split execution (Sec. 3.2.2 splits K into tiles that a block walks in turn; here the
- * K-segments of a tile also go to different workgroups, which fills the device when
+/* K-split execution (Sec. 3.2.2 splits K into tiles that a block walks in turn; here runs
+ * of a tile's K-segments also go to different workgroups, which fills the device when
  * M * ceil(N / 256) alone gives too few workgroups).  Same result contract, layouts and
  * stream semantics as sdnn_spmm; the plan must have been created with split_chunks > 0.
- * Each workgroup writes its segment's partial product (no bias, no epilogue) to
- * workspace[s][row][n]; a second kernel on the same stream sums the segments in order
- * s = 0, 1, ..., adds the bias and applies epi into C.  Results can differ from
- * sdnn_spmm in rounding only (another summation order).
- *   workspace:        device, at least splits * M * N fp32 (sdnn_plan_info), 16-byte
- *                     aligned, clear of B, C and bias; scratch of this call only (its
- *                     contents afterwards are unspecified).  Not touched, and may be NULL,
- *                     when the plan has one K-segment: the call is then sdnn_spmm.
+ *   splits:           workgroups along K.  0 = the library's choice for this N (a cost
+ *                     model of staging rounds against the reduction's traffic); k > 0 =
+ *                     runs of ceil(nseg / k) consecutive segments each (at most nseg
+ *                     runs, nseg = sdnn_plan_info's `splits`).  Negative: SDNN_ERR_DIM.
+ * With R runs (R > 1), each workgroup writes its run's partial product (no bias, no
+ * epilogue) to workspace[r][row][n]; a second kernel on the same stream sums the runs in
+ * order r = 0, 1, ..., adds the bias and applies epi into C.  Results can differ from
+ * sdnn_spmm in rounding only (another summation order); they depend on nothing but
+ * W, B, bias, epi and the run boundaries (R and split_chunks).
+ *   workspace:        device, at least nseg * M * N fp32, 16-byte aligned, clear of B, C
+ *                     and bias; scratch of this call only (its contents afterwards are
+ *                     unspecified).  Not touched, and may be NULL, when R = 1: the call
+ *                     is then sdnn_spmm.
  *   workspace_floats: its size in floats.
- * Errors: as sdnn_spmm, plus SDNN_ERR_DIM (plan without split_chunks, workspace too
- * small, misaligned or overlapping) and SDNN_ERR_NULL (workspace NULL with splits > 1). */
+ * Errors: as sdnn_spmm, plus SDNN_ERR_DIM (plan without split_chunks, splits < 0,
+ * workspace too small, misaligned or overlapping) and SDNN_ERR_NULL (workspace NULL
+ * when the plan has more than one segment). */
 sdnn_status sdnn_spmm_split(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
-                            sdnn_epilogue epi, float* workspace, int64_t workspace_floats,
-                            void* stream);
+                            sdnn_epilogue epi, int32_t splits, float* workspace,
+                            int64_t workspace_floats, void* stream);
 
 /* Per-plan variant selection by timing (the paper's preparation stage chooses the best
  * kernel implementation per operator, Sec. 3.1): times sdnn_spmm at this N for every
@@ -235,8 +242,8 @@ sdnn_status sdnn_conv3x3(sdnn_plan p, const float* X, float* C, int32_t H, int32
 /* K-split variant of sdnn_conv3x3 (N = H * W * NB columns), with the workspace
  * contract of sdnn_spmm_split.  Errors: as sdnn_conv3x3 and sdnn_spmm_split. */
 sdnn_status sdnn_conv3x3_split(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
-                               int32_t NB, const float* bias, sdnn_epilogue epi, float* workspace,
-                               int64_t workspace_floats, void* stream);
+                               int32_t NB, const float* bias, sdnn_epilogue epi, int32_t splits,
+                               float* workspace, int64_t workspace_floats, void* stream);
 
 /* Frees the plan and its device memory.  NULL is a no-op. */
 void sdnn_plan_destroy(sdnn_plan p);

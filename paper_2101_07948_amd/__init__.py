@@ -79,8 +79,8 @@ def lib() -> ctypes.CDLL:
         L.sdnn_conv3x3.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
         L.sdnn_plan_tune.argtypes = [p, p, p, i32, p, p, p]
         i64 = ctypes.c_int64
-        L.sdnn_spmm_split.argtypes = [p, p, p, i32, p, ctypes.c_int, p, i64, p]
-        L.sdnn_conv3x3_split.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p, i64, p]
+        L.sdnn_spmm_split.argtypes = [p, p, p, i32, p, ctypes.c_int, i32, p, i64, p]
+        L.sdnn_conv3x3_split.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, i32, p, i64, p]
         for fn in ("sdnn_reorder_rows", "sdnn_row_order", "sdnn_plan_check_host", "sdnn_plan_create",
                    "sdnn_plan_get_perm", "sdnn_plan_info", "sdnn_spmm", "sdnn_dense_gemm",
                    "sdnn_conv3x3", "sdnn_plan_tune", "sdnn_spmm_split", "sdnn_conv3x3_split"):
@@ -284,7 +284,8 @@ class Plan:
         return C
 
     def workspace_floats(self, N: int) -> int:
-        """Floats of the workspace a K-split call at N columns needs (splits * M * N)."""
+        """Floats of the workspace a K-split call at N columns needs (nseg * M * N, nseg =
+        info["splits"], the plan's K-segments)."""
         return int(self.info["splits"]) * self.M * int(N)
 
     def _workspace(self, ws, N: int):
@@ -297,20 +298,23 @@ class Plan:
             raise TypeError("workspace must be a contiguous float32 CUDA/HIP tensor")
         return ctypes.c_void_p(ws.data_ptr()), int(ws.numel())
 
-    def spmm_split(self, B, C, bias=None, epi: str = "none", workspace=None, stream=None):
-        """spmm with each K-segment of a tile in its own workgroup (plans created with
-        split_chunks > 0); workspace: a float32 device tensor of at least
-        workspace_floats(N) elements (allocated here when None)."""
+    def spmm_split(self, B, C, bias=None, epi: str = "none", workspace=None, splits: int = 0,
+                   stream=None):
+        """spmm with runs of a tile's K-segments in separate workgroups (plans created
+        with split_chunks > 0); splits: workgroups along K (0: the library's choice);
+        workspace: a float32 device tensor of at least workspace_floats(N) elements
+        (allocated here when None)."""
         N = int(B.shape[1]) if B is not None and B.dim() == 2 else int(C.shape[1])
         pb = _dev_ptr(B, "B", (self.K, N))
         pc = _dev_ptr(C, "C", (self.M, N))
         pbias = _dev_ptr(bias, "bias", (self.M,), allow_none=True)
         pw, nw = self._workspace(workspace, N)
-        _check(self._lib.sdnn_spmm_split(self.handle, pb, pc, N, pbias, EPI[epi], pw, nw,
-                                         _stream_handle(stream)), "sdnn_spmm_split")
+        _check(self._lib.sdnn_spmm_split(self.handle, pb, pc, N, pbias, EPI[epi], int(splits),
+                                         pw, nw, _stream_handle(stream)), "sdnn_spmm_split")
         return C
 
-    def conv3x3_split(self, X, C, bias=None, epi: str = "none", workspace=None, stream=None):
+    def conv3x3_split(self, X, C, bias=None, epi: str = "none", workspace=None, splits: int = 0,
+                      stream=None):
         """conv3x3 with K-segments in separate workgroups (see spmm_split)."""
         if X.dim() != 4 or C.dim() != 4:
             raise ValueError("X and C must be 4-d (channels, H, W, images)")
@@ -321,8 +325,9 @@ class Plan:
         pc = _dev_ptr(C, "C", (self.M, H, W, NB))
         pbias = _dev_ptr(bias, "bias", (self.M,), allow_none=True)
         pw, nw = self._workspace(workspace, H * W * NB)
-        _check(self._lib.sdnn_conv3x3_split(self.handle, px, pc, H, W, NB, pbias, EPI[epi], pw,
-                                            nw, _stream_handle(stream)), "sdnn_conv3x3_split")
+        _check(self._lib.sdnn_conv3x3_split(self.handle, px, pc, H, W, NB, pbias, EPI[epi],
+                                            int(splits), pw, nw, _stream_handle(stream)),
+               "sdnn_conv3x3_split")
         return C
 
     def spmm(self, B, C, bias=None, epi: str = "none", stream=None):

@@ -178,7 +178,9 @@ def sync(slot, tag):
     return L
 
 
-def consumer(rw):
+def consumer(rw, limit=False):
+    """The FMA loop for RW-row panels.  limit: stop before a sync group whose c_lo reaches
+    the chunk limit (K-split launches; the plain loop leaves that test out)."""
     L = [
         f"s_mov_b32 s{M0S}, m0",
         f"v_mov_b32 v31, {hex(RING_MASK)}",
@@ -198,7 +200,7 @@ def consumer(rw):
     ]
     L += sync(E[0], "e")   # a panel's first group always carries the sync bit
     L += address_phase(E[0], VB[0])
-    L += [f"s_and_b32 s{STMP}, s{E[0] + HIW}, %[em]", "s_cbranch_scc0 .L%=_iter0",
+    L += [f"s_bitcmp1_b32 s{E[0] + HIW}, {END_BIT}", "s_cbranch_scc0 .L%=_iter0",
           "s_waitcnt lgkmcnt(0)"]   # the panel is one group
     L += fmas(E[0], VB[0], rw)
     L.append("s_branch .L%=_finish")
@@ -220,13 +222,22 @@ def consumer(rw):
         cur, nxt = E[i % NSLOT], E[(i + 1) % NSLOT]
         vbc, vbn = VB[i % 2], VB[(i + 1) % 2]
         L.append(f".L%=_sync{i}:")
+        if limit:
+            # a group starting at or past the chunk limit belongs to the next workgroup's
+            # K-segments: finish with the current group
+            L += [f"s_lshr_b32 s{STMP}, s{nxt + LOW}, {LO_SHIFT}",
+                  f"s_cmp_ge_u32 s{STMP}, %[climit]", f"s_cbranch_scc1 .L%=_stop{i}"]
         L += sync(nxt, i)
-        L += [f"s_and_b32 s{STMP}, s{nxt + HIW}, %[em]", f"s_cbranch_scc0 .L%=_ret{i}"]
+        L += [f"s_bitcmp1_b32 s{nxt + HIW}, {END_BIT}", f"s_cbranch_scc0 .L%=_ret{i}"]
         L += address_phase(nxt, vbn)       # group g+1 ends the panel
         L += fmas(cur, vbc, rw)
         L.append("s_waitcnt lgkmcnt(0)")
         L += fmas(nxt, vbn, rw)
         L.append("s_branch .L%=_finish")
+        if limit:
+            L.append(f".L%=_stop{i}:")       # the current group's reads have landed
+            L += fmas(cur, vbc, rw)
+            L.append("s_branch .L%=_finish")
     # a wave that went on without waiting, or whose chunks a producer may have
     # overwritten, leaves NaN instead of unchecked values
     L += [".L%=_finish:",
@@ -244,15 +255,18 @@ def consumer(rw):
     sregs = [f"s{x}" for x in range(E[0], (95 if PROFILE else SREADY1) + 1)]
     vregs = [f"v{x}" for x in range(24, ACC)]
     clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["scc"])
-    return f"""// Consumer, RW = {rw}: accumulator planes p0..p3
-__device__ __forceinline__ void consume_rw{rw}(acc_plane_t<{rw}>& p0, acc_plane_t<{rw}>& p1,
+    name = f"consume_rw{rw}" + ("_limit" if limit else "")
+    operands = ('[sp] "s"(a.stream), [vl] "v"(a.vlane), [pa] "v"(a.prog_addr), '
+                '[ra] "v"(a.ready_addr),\n        [budget] "s"(a.poll_budget), '
+                '[ov] "v"(a.overrun_addr)' + (', [climit] "s"(a.chunk_limit)' if limit else ''))
+    return f"""// Consumer, RW = {rw}{', stopping at the chunk limit' if limit else ''}: accumulator planes p0..p3
+__device__ __forceinline__ void {name}(acc_plane_t<{rw}>& p0, acc_plane_t<{rw}>& p1,
                                          acc_plane_t<{rw}>& p2, acc_plane_t<{rw}>& p3,
                                          {'' if PROFILE else 'const '}ConsumerArgs& a) {{
   asm volatile(
 {body}
       : {planes}{', [twait] "=&s"(a.twait)' if PROFILE else ''}
-      : [sp] "s"(a.stream), [vl] "v"(a.vlane), [pa] "v"(a.prog_addr), [ra] "v"(a.ready_addr),
-        [budget] "s"(a.poll_budget), [ov] "v"(a.overrun_addr), [em] "s"(a.end_mask)
+      : {operands}
       : {clob});
 }}
 """
@@ -598,6 +612,7 @@ def generate() -> str:
              ""]
     for rw in RW_VARIANTS:
         parts.append(consumer(rw))
+        parts.append(consumer(rw, limit=True))
     for kind in ("vec", "dword", "conv"):
         parts.append(producer(kind))
     return "\n".join(parts)

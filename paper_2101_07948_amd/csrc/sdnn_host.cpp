@@ -100,18 +100,16 @@ struct Entry {
 
 // Writes one group (n <= kGroup real entries from e) with its fields.
 void emit_group(std::vector<uint32_t>& out, const Entry* e, int n, bool first, bool last,
-                bool seg_end, int32_t* prev_lo, int32_t* prev_hi) {
+                int32_t* prev_lo, int32_t* prev_hi) {
   uint32_t w[kGroup], a[kGroup];
   for (int j = 0; j < kGroup; ++j) {
     w[j] = j < n ? e[j].w : 0u;            // zero-weight copies of the first entry
     a[j] = j < n ? e[j].a : e[0].a;
   }
   const int32_t lo = e[0].chunk, hi = e[n - 1].chunk;
-  // the consumer looks for the end bits only on groups that carry the sync bit
-  const bool sync = first || last || seg_end || lo != *prev_lo || hi != *prev_hi;
+  const bool sync = first || last || lo != *prev_lo || hi != *prev_hi;
   a[kLoWord] |= (uint32_t)lo << kLoShift;
-  a[kHiWord] |= (uint32_t)hi << kHiShift | (uint32_t)sync << kSyncBit | (uint32_t)last << kEndBit |
-                (uint32_t)seg_end << kSegEndBit;
+  a[kHiWord] |= (uint32_t)hi << kHiShift | (uint32_t)sync << kSyncBit | (uint32_t)last << kEndBit;
   *prev_lo = lo;
   *prev_hi = hi;
   for (int j = 0; j < kGroup; ++j) out.push_back(w[j]);
@@ -189,12 +187,12 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
                seg_of(ent[i + n].chunk) == seg)
           ++n;
         const bool last = i + n == ent.size();
+        // a segment's first group differs from the group before it in c_lo, so it
+        // carries the sync bit, where a workgroup ending at that segment stops
         const bool seg_first = first || seg_of(ent[i - 1].chunk) != seg;
-        const bool seg_end = last || seg_of(ent[i + n].chunk) != seg;
         if (split_chunks > 0 && seg_first)
           P.seg_start[(size_t)p * P.nseg + seg] = (int32_t)(P.entries.size() / (2 * kGroup));
-        emit_group(P.entries, &ent[i], n, first || (split_chunks > 0 && seg_first), last,
-                   split_chunks > 0 && seg_end, &prev_lo, &prev_hi);
+        emit_group(P.entries, &ent[i], n, first, last, &prev_lo, &prev_hi);
         first = false;
         i += n;
       }
@@ -273,19 +271,21 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
       const uint32_t* a = w + kGroup;
       const int32_t lo = (int32_t)(a[kLoWord] >> kLoShift), hi = (int32_t)(a[kHiWord] >> kHiShift);
       const bool sync = (a[kHiWord] >> kSyncBit) & 1u, last = (a[kHiWord] >> kEndBit) & 1u;
-      const bool seg_end = (a[kHiWord] >> kSegEndBit) & 1u;
       if (lo > hi || hi - lo >= kRing || hi >= P.nchunks || lo < prev_lo) return false;
       if (seg_of(hi) != seg_of(lo)) return false;
       const bool first = g == P.panel_start[p];
-      if (sync != (first || last || seg_end || lo != prev_lo || hi != prev_hi)) return false;
-      if (split && seg_first[seg_of(lo)] < 0) seg_first[seg_of(lo)] = g;
+      if (sync != (first || last || lo != prev_lo || hi != prev_hi)) return false;
+      if (split && seg_first[seg_of(lo)] < 0) {
+        if (!sync) return false;  // a workgroup's run of segments stops at this group
+        seg_first[seg_of(lo)] = g;
+      }
       prev_lo = lo;
       prev_hi = hi;
       int nreal = 0;
       int32_t max_chunk = -1;
       for (int j = 0; j < kGroup; ++j) {
         uint32_t fields = a[j] & ((1u << kLoShift) - 1);
-        if (j == kHiWord) fields &= ~(1u << kEndBit | 1u << kSegEndBit);
+        if (j == kHiWord) fields &= ~(1u << kEndBit);
         if ((fields >> kRowBits) & ((1u << (kRingRowShift - kRowBits)) - 1)) return false;
         if (j < kLoWord && (a[j] >> kLoShift) != 0u) return false;
         const uint32_t row = fields & ((1u << kRowBits) - 1);
@@ -318,7 +318,6 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
       const int32_t next_chunk = last ? -1 : col_idx[want[k]] / kChunk;
       if (nreal < kGroup && !last && next_chunk - lo < kRing && seg_of(next_chunk) == seg_of(lo))
         return false;
-      if (seg_end != (split && (last || seg_of(next_chunk) != seg_of(lo)))) return false;
       if (last) {
         expect_group = g + 1;
         break;
@@ -938,12 +937,12 @@ static sdnn_status check_workspace(const sdnn_plan_s* p, int64_t N, const float*
 }
 
 static sdnn_status spmm_entry(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
-                              sdnn_epilogue epi, float* ws, int64_t ws_floats, bool split,
-                              void* stream) {
+                              sdnn_epilogue epi, int32_t splits, float* ws, int64_t ws_floats,
+                              bool split, void* stream) {
   if (!p) return SDNN_ERR_NULL;
   if (N < 0) return SDNN_ERR_DIM;
   if (epi != SDNN_EPI_NONE && epi != SDNN_EPI_RELU && epi != SDNN_EPI_GELU) return SDNN_ERR_DIM;
-  if (split && p->split_chunks <= 0) return SDNN_ERR_DIM;
+  if (split && (p->split_chunks <= 0 || splits < 0)) return SDNN_ERR_DIM;
   if (p->M == 0 || N == 0) return SDNN_OK;
   if (!C) return SDNN_ERR_NULL;
   if (p->K > 0 && !B) return SDNN_ERR_NULL;
@@ -958,7 +957,8 @@ static sdnn_status spmm_entry(sdnn_plan p, const float* B, float* C, int32_t N, 
   if (hipGetDevice(&cur) != hipSuccess) return SDNN_ERR_HIP;
   if (cur != p->device) return SDNN_ERR_DEVICE;
   try {
-    hipError_t e = split ? launch_spmm_split(p, B, C, N, bias, (int)epi, ws, (hipStream_t)stream)
+    hipError_t e = split ? launch_spmm_split(p, B, C, N, bias, (int)epi, splits, ws,
+                                             (hipStream_t)stream)
                          : launch_spmm(p, B, C, N, bias, (int)epi, (hipStream_t)stream);
     return e == hipSuccess ? SDNN_OK : SDNN_ERR_HIP;
   } catch (...) {
@@ -968,13 +968,13 @@ static sdnn_status spmm_entry(sdnn_plan p, const float* B, float* C, int32_t N, 
 
 sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
                       sdnn_epilogue epi, void* stream) {
-  return spmm_entry(p, B, C, N, bias, epi, nullptr, 0, false, stream);
+  return spmm_entry(p, B, C, N, bias, epi, 0, nullptr, 0, false, stream);
 }
 
 sdnn_status sdnn_spmm_split(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
-                            sdnn_epilogue epi, float* workspace, int64_t workspace_floats,
-                            void* stream) {
-  return spmm_entry(p, B, C, N, bias, epi, workspace, workspace_floats, true, stream);
+                            sdnn_epilogue epi, int32_t splits, float* workspace,
+                            int64_t workspace_floats, void* stream) {
+  return spmm_entry(p, B, C, N, bias, epi, splits, workspace, workspace_floats, true, stream);
 }
 
 sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, void* stream,
@@ -1000,14 +1000,14 @@ sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, voi
 }
 
 static sdnn_status conv_entry(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
-                              int32_t NB, const float* bias, sdnn_epilogue epi, float* ws,
-                              int64_t ws_floats, bool split, void* stream) {
+                              int32_t NB, const float* bias, sdnn_epilogue epi, int32_t splits,
+                              float* ws, int64_t ws_floats, bool split, void* stream) {
   if (!p) return SDNN_ERR_NULL;
   if (H < 0 || W < 0 || NB < 0) return SDNN_ERR_DIM;
   if (epi != SDNN_EPI_NONE && epi != SDNN_EPI_RELU && epi != SDNN_EPI_GELU) return SDNN_ERR_DIM;
   if (p->K % 9 != 0 || p->K == 0 || p->in_permuted) return SDNN_ERR_DIM;
   if (NB % 4 != 0) return SDNN_ERR_DIM;
-  if (split && p->split_chunks <= 0) return SDNN_ERR_DIM;
+  if (split && (p->split_chunks <= 0 || splits < 0)) return SDNN_ERR_DIM;
   const int64_t N = (int64_t)H * W * NB;
   if (p->M == 0 || N == 0) return SDNN_OK;
   // 32-bit column and channel-plane byte offsets in the staging loop
@@ -1027,7 +1027,8 @@ static sdnn_status conv_entry(sdnn_plan p, const float* X, float* C, int32_t H, 
   if (cur != p->device) return SDNN_ERR_DEVICE;
   try {
     hipError_t e =
-        split ? launch_conv3x3_split(p, X, C, H, W, NB, bias, (int)epi, ws, (hipStream_t)stream)
+        split ? launch_conv3x3_split(p, X, C, H, W, NB, bias, (int)epi, splits, ws,
+                                     (hipStream_t)stream)
               : launch_conv3x3(p, X, C, H, W, NB, bias, (int)epi, (hipStream_t)stream);
     return e == hipSuccess ? SDNN_OK : SDNN_ERR_HIP;
   } catch (...) {
@@ -1037,13 +1038,14 @@ static sdnn_status conv_entry(sdnn_plan p, const float* X, float* C, int32_t H, 
 
 sdnn_status sdnn_conv3x3(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
                          int32_t NB, const float* bias, sdnn_epilogue epi, void* stream) {
-  return conv_entry(p, X, C, H, W, NB, bias, epi, nullptr, 0, false, stream);
+  return conv_entry(p, X, C, H, W, NB, bias, epi, 0, nullptr, 0, false, stream);
 }
 
 sdnn_status sdnn_conv3x3_split(sdnn_plan p, const float* X, float* C, int32_t H, int32_t W,
-                               int32_t NB, const float* bias, sdnn_epilogue epi, float* workspace,
-                               int64_t workspace_floats, void* stream) {
-  return conv_entry(p, X, C, H, W, NB, bias, epi, workspace, workspace_floats, true, stream);
+                               int32_t NB, const float* bias, sdnn_epilogue epi, int32_t splits,
+                               float* workspace, int64_t workspace_floats, void* stream) {
+  return conv_entry(p, X, C, H, W, NB, bias, epi, splits, workspace, workspace_floats, true,
+                    stream);
 }
 
 sdnn_status sdnn_dense_gemm(const float* W, const float* B, float* C, int32_t M, int32_t K,

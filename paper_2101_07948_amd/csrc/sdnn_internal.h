@@ -27,7 +27,6 @@ constexpr int kTileCols = 256;
 constexpr int kTailGroups = 16;
 // Fields of a group's address words a_0..a_7 (see Packed); L = kGroup - 1.
 constexpr int kRowBits = 8;         // a_j & 0xff: row inside the panel
-constexpr int kSegEndBit = 8;       // a_L: last group of the panel in its K-segment
 constexpr int kEndBit = 9;          // a_L: last group of the panel
 constexpr int kRingRowShift = 10;   // (a_j >> 10) & 0x7f: row of the LDS ring
 constexpr int kSyncBit = 17;        // a_L: publish progress / check readiness first
@@ -58,10 +57,11 @@ static_assert(kRing * kChunk <= 128, "ring rows must fit 7 bits");
 //
 //   K-segments (split_chunks = S > 0): chunks [s*S, (s+1)*S) form segment s, no group
 //   holds entries of two segments (an entry of the next segment starts a new group,
-//   like one too far ahead), the first and the last group of each segment a panel has
-//   entries in carry the sync bit, the last one also seg_end (a7 bit 8), and
-//   seg_start[p][s] is the panel's first group in segment s (-1: none).  A launch may
-//   then give each segment to its own workgroup.
+//   like one too far ahead), so each segment's first group carries the sync bit (its
+//   c_lo differs from the previous group's), and seg_start[p][s] is the panel's first
+//   group in segment s (-1: none).  A launch may then give each run of consecutive
+//   segments to its own workgroup, which starts at the run's first group and stops at
+//   the first sync group whose c_lo lies past the run.
 struct Packed {
   int32_t M = 0, K = 0, RW = 0, nchunks = 0, npanels = 0;
   int64_t nnz = 0, stored = 0;     // structural entries, stored entries (with padding)
@@ -138,13 +138,15 @@ hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N
                        const float* bias, int epi, hipStream_t stream);
 hipError_t launch_conv3x3(const sdnn_plan_s* p, const float* X, float* C, int32_t H, int32_t W,
                           int32_t NB, const float* bias, int epi, hipStream_t stream);
-// K-split variants: ws holds nseg * M * N floats (nseg = p->pk[0].nseg); with one
-// segment they are the plain launches and ws is not touched.
+// K-split variants: `splits` workgroups along K (0: the library's choice; clamped to
+// 1..nseg, nseg = p->pk[0].nseg), ws holds at least nseg * M * N floats; with one
+// workgroup along K they are the plain launches and ws is not touched.
 hipError_t launch_spmm_split(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
-                             const float* bias, int epi, float* ws, hipStream_t stream);
+                             const float* bias, int epi, int splits, float* ws,
+                             hipStream_t stream);
 hipError_t launch_conv3x3_split(const sdnn_plan_s* p, const float* X, float* C, int32_t H,
-                                int32_t W, int32_t NB, const float* bias, int epi, float* ws,
-                                hipStream_t stream);
+                                int32_t W, int32_t NB, const float* bias, int epi, int splits,
+                                float* ws, hipStream_t stream);
 // Times every candidate launch shape of the plan at N on the given buffers (blocking)
 // and records the fastest in p->tuned.
 hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStream_t stream,

@@ -54,7 +54,7 @@ struct ConsumerArgs {
   uint32_t ready_addr;     // LDS address of the ready word
   uint32_t poll_budget;    // failed readiness checks the wave may poll through in total
   uint32_t overrun_addr;   // LDS address of the workgroup's overrun word
-  uint32_t end_mask;       // a7 bit that ends the wave's groups: panel end, or K-segment end
+  uint32_t chunk_limit;    // the wave stops before a sync group whose c_lo reaches this chunk
 };
 struct ProducerArgs {
   int32_t nchunks, K;      // nchunks: one past the last chunk to stage
@@ -121,10 +121,11 @@ struct SpmmArgs {
   int32_t out_permuted;  // store permuted row i at row i instead of at its source row
   int32_t H, W, NB;      // image geometry of a 3x3 convolution (B is then the input X)
   uint32_t poll_budget;  // failed readiness / ring-limit checks a wave may poll through
-  // split-K: nsplit > 1 gives K-segment s (chunks [s, s+1) * split_chunks) of each tile
-  // and row-block its own workgroup, which writes its partial product, without bias or
-  // activation, to C + s * M * N (C is then the workspace)
-  int32_t M, nsplit, nseg, split_chunks;
+  // split-K: nsplit > 1 gives each run of seg_per_split consecutive K-segments (of
+  // split_chunks chunks each; nseg in all) of each tile and row-block its own workgroup,
+  // which writes its partial product, without bias or activation, to C + run * M * N
+  // (C is then the workspace)
+  int32_t M, nsplit, seg_per_split, nseg, split_chunks;
 };
 
 // Producer kinds: 4-byte staging (any N), 16-byte staging (N % 4 == 0, aligned), the
@@ -153,17 +154,23 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
   const int split = (lin - tile * per_tile) / a.n_rb;
   const int rb = lin - tile * per_tile - split * a.n_rb;
   const bool splitk = a.nsplit > 1;
-  const int c0 = splitk ? split * a.split_chunks : 0;
-  const int c1 = splitk ? min(c0 + a.split_chunks, a.nchunks) : a.nchunks;
+  const int s0 = split * a.seg_per_split, s1 = min(s0 + a.seg_per_split, a.nseg);
+  const int c0 = splitk ? s0 * a.split_chunks : 0;
+  const int c1 = splitk ? min(s1 * a.split_chunks, a.nchunks) : a.nchunks;
   const int nc = (blockDim.x >> 6) - kProducers;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int n0 = tile * kTileCols;
   const int prod = wave - nc;  // >= 0: producer index
   const int panel = rb * nc + wave;
-  const int gstart = (prod < 0 && panel < a.npanels)
-                         ? (splitk ? seg_start[(size_t)panel * a.nseg + split] : panel_start[panel])
-                         : -1;
+  int gstart = -1;  // the wave's first group: the first of its panel in the run
+  if (prod < 0 && panel < a.npanels) {
+    if (!splitk) {
+      gstart = panel_start[panel];
+    } else {
+      for (int sg = s0; sg < s1 && gstart < 0; ++sg) gstart = seg_start[(size_t)panel * a.nseg + sg];
+    }
+  }
 
   const uint32_t lds_base = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) uint32_t*)lds);
   if (lds_base != 0) return;  // never taken: see above
@@ -233,11 +240,18 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     ca.ready_addr = ready_addr;
     ca.poll_budget = a.poll_budget;
     ca.overrun_addr = overrun_addr;
-    ca.end_mask = splitk ? 1u << kSegEndBit : 1u << kEndBit;
-    if constexpr (RW == 4) consume_rw4(p0, p1, p2, p3, ca);
-    if constexpr (RW == 8) consume_rw8(p0, p1, p2, p3, ca);
-    if constexpr (RW == 12) consume_rw12(p0, p1, p2, p3, ca);
-    if constexpr (RW == 16) consume_rw16(p0, p1, p2, p3, ca);
+    ca.chunk_limit = (uint32_t)c1;
+    if (splitk) {  // runs of K-segments: the loop also stops at the run's last chunk
+      if constexpr (RW == 4) consume_rw4_limit(p0, p1, p2, p3, ca);
+      if constexpr (RW == 8) consume_rw8_limit(p0, p1, p2, p3, ca);
+      if constexpr (RW == 12) consume_rw12_limit(p0, p1, p2, p3, ca);
+      if constexpr (RW == 16) consume_rw16_limit(p0, p1, p2, p3, ca);
+    } else {
+      if constexpr (RW == 4) consume_rw4(p0, p1, p2, p3, ca);
+      if constexpr (RW == 8) consume_rw8(p0, p1, p2, p3, ca);
+      if constexpr (RW == 12) consume_rw12(p0, p1, p2, p3, ca);
+      if constexpr (RW == 16) consume_rw16(p0, p1, p2, p3, ca);
+    }
   }
 
   const int ncol = n0 + lane * 4;
@@ -379,6 +393,46 @@ const DevPacking& choose_packing(const sdnn_plan_s* p, int N, bool conv, int nse
 }  // namespace
 
 namespace {
+// Workgroups along K for a K-split call that leaves the choice to the library: the
+// count that minimises a small cost model, in microseconds,
+//     rounds * chunks_per_workgroup * t_chunk                  (staging of B)
+//   + (splits > 1) * (t_launch + (splits + 1) * 4 M N / bw)    (reduction kernel)
+// where rounds counts full waves of workgroups on the CUs at the launch shape the call
+// would use, and a chunk costs a workgroup the longer of the staging latency (0.45 us;
+// 0.75 us for the convolution's staging) and its consumers' LDS reads of that chunk
+// (waves * RW * 32 rows * density / fill entries of 1 KB at 434 KB/us, the measured
+// ds_read_b128 rate of one CU).  t_launch = 4 us, bw = 4 TB/s (the partials mostly sit
+// in the Infinity Cache); all measured on MI355X.  A count is tried only if runs of
+// ceil(nseg / count) segments give exactly it, and replaces a smaller one only if it
+// costs at least 10 % less (the model's error on MI355X is about that size).
+int choose_splits(const sdnn_plan_s* p, int N, bool conv) {
+  const int total_seg = p->pk[0].nseg;
+  const int cus = p->num_cus > 0 ? p->num_cus : 256;
+  const int64_t n_tiles = (N + kTileCols - 1) / kTileCols;
+  const double t_lat = conv ? 0.75 : 0.45, t_launch = 4.0, bw = 4.0e6;  // bytes per us
+  const double lds_per_us = 434.0e3;
+  const double density = (double)p->nnz / ((double)p->M * (double)p->K);
+  int best = 1;
+  double best_cost = 0.0;
+  for (int splits = 1; splits <= total_seg; ++splits) {
+    const int per = (total_seg + splits - 1) / splits;
+    if ((total_seg + per - 1) / per != splits) continue;
+    const DevPacking& pk = choose_packing(p, N, conv, splits);
+    const LaunchCfg cfg = choose_cfg(pk, cus, N, splits);
+    const int64_t rounds = rounds_of(n_tiles * splits, pk.npanels, cfg.waves, cus);
+    const int64_t chunks = std::min<int64_t>((int64_t)per * p->split_chunks, p->nchunks);
+    const double reads = (double)cfg.waves * pk.RW * kChunk * density / std::max(pk.fill, 0.05);
+    const double t_chunk = std::max(t_lat, reads * 1024.0 / lds_per_us);
+    double cost = (double)rounds * (double)chunks * t_chunk;
+    if (splits > 1) cost += t_launch + (splits + 1) * 4.0 * (double)p->M * (double)N / bw;
+    if (splits == 1 || cost < 0.9 * best_cost) {  // a larger count must win clearly
+      best_cost = cost;
+      best = splits;
+    }
+  }
+  return best;
+}
+
 // Split-K reduction: C[i][n] = act(sum_s ws[s][i][n] + bias[rowmap[i]]) over the nseg
 // partial products of an M x N output (rowmap: NULL for the identity).  Each thread
 // takes four consecutive columns of one row; vec: N % 4 == 0 and 16-byte aligned
@@ -436,23 +490,32 @@ hipError_t launch_reduce(const float* ws, float* C, const float* bias, const int
 // `shape` (packing index and consumer waves) overrides the plan's tuned or heuristic
 // choice when non-null.  Tuned shapes were timed on unsplit products, so a convolution,
 // whose staging differs, and a K-split launch keep the heuristic.  ws non-null (a plan
-// with more than one K-segment): every (tile, segment, row-block) is a workgroup that
-// writes its partial product to ws, and a reduction kernel forms C.
+// with K-segments): `splits` workgroups along K (0: choose_splits), so every (tile, run
+// of segments, row-block) is a workgroup that writes its partial product to ws, and a
+// reduction kernel forms C.
 hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                          const float* bias, int epi, const int32_t* conv_hwn,
-                         const TunedShape* shape, float* ws, hipStream_t stream) {
-  const int nseg = ws ? p->pk[0].nseg : 1;
-  if (!shape && !conv_hwn && nseg == 1)
+                         const TunedShape* shape, float* ws, int splits, hipStream_t stream) {
+  // nk: workgroups along K, each taking a run of seg_per_split consecutive segments
+  int seg_per_split = 1, nk = 1;
+  if (ws) {
+    const int total_seg = p->pk[0].nseg;
+    if (splits <= 0) splits = choose_splits(p, N, conv_hwn != nullptr);
+    splits = std::min(std::max(splits, 1), total_seg);
+    seg_per_split = (total_seg + splits - 1) / splits;
+    nk = (total_seg + seg_per_split - 1) / seg_per_split;
+  }
+  if (!shape && !conv_hwn && nk == 1)
     for (int i = 0; i < p->ntuned; ++i)
       if (p->tuned[i].N == N) shape = &p->tuned[i];
   const DevPacking& pk =
-      shape ? p->pk[shape->pack] : choose_packing(p, N, conv_hwn != nullptr, nseg);
-  LaunchCfg cfg = choose_cfg(pk, p->num_cus, N, nseg);
+      shape ? p->pk[shape->pack] : choose_packing(p, N, conv_hwn != nullptr, nk);
+  LaunchCfg cfg = choose_cfg(pk, p->num_cus, N, nk);
   if (shape) {
     cfg.waves = shape->waves;
     cfg.n_rb = (pk.npanels + cfg.waves - 1) / cfg.waves;
   }
-  float* out = nseg > 1 ? ws : C;
+  float* out = nk > 1 ? ws : C;
   const SpmmPtrs ptrs{pk.entries, pk.panel_start, pk.panel_rows, pk.panel_pos, pk.seg_start, B,
                       out, bias};
   SpmmArgs args;
@@ -462,10 +525,11 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
   args.npanels = pk.npanels;
   args.n_rb = cfg.n_rb;
   args.M = p->M;
-  args.nsplit = nseg;
+  args.nsplit = nk;
+  args.seg_per_split = seg_per_split;
   args.nseg = pk.nseg;
-  args.split_chunks = nseg > 1 ? p->split_chunks : 0;
-  const int64_t total = (int64_t)cfg.n_tiles * nseg * cfg.n_rb;
+  args.split_chunks = nk > 1 ? p->split_chunks : 0;
+  const int64_t total = (int64_t)cfg.n_tiles * nk * cfg.n_rb;
   if (total > (int64_t)1 << 30) return hipErrorInvalidValue;
   const int64_t grid = (total + 7) / 8 * 8;
   args.total_wg = (int32_t)total;
@@ -490,20 +554,21 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
     err = vec ? launch_rw<kStageVec>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream)
               : launch_rw<kStageDword>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
   }
-  if (err != hipSuccess || nseg == 1) return err;
-  return launch_reduce(ws, C, bias, p->out_permuted ? p->d_perm : nullptr, p->M, N, nseg, epi,
+  if (err != hipSuccess || nk == 1) return err;
+  return launch_reduce(ws, C, bias, p->out_permuted ? p->d_perm : nullptr, p->M, N, nk, epi,
                        stream);
 }
 }  // namespace
 
 hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                        const float* bias, int epi, hipStream_t stream) {
-  return launch_panels(p, B, C, N, bias, epi, nullptr, nullptr, nullptr, stream);
+  return launch_panels(p, B, C, N, bias, epi, nullptr, nullptr, nullptr, 0, stream);
 }
 
 hipError_t launch_spmm_split(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
-                             const float* bias, int epi, float* ws, hipStream_t stream) {
-  return launch_panels(p, B, C, N, bias, epi, nullptr, nullptr, ws, stream);
+                             const float* bias, int epi, int splits, float* ws,
+                             hipStream_t stream) {
+  return launch_panels(p, B, C, N, bias, epi, nullptr, nullptr, ws, splits, stream);
 }
 
 hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStream_t stream,
@@ -527,10 +592,10 @@ hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStr
   float best = -1.0f;
   for (size_t i = 0; i < cands.size() && err == hipSuccess; ++i) {
     for (int r = 0; r < 2 && err == hipSuccess; ++r)   // warm-up
-      err = launch_panels(p, B, C, N, nullptr, 0, nullptr, &cands[i], nullptr, stream);
+      err = launch_panels(p, B, C, N, nullptr, 0, nullptr, &cands[i], nullptr, 0, stream);
     if (err == hipSuccess) err = hipEventRecord(e0, stream);
     for (int r = 0; r < 5 && err == hipSuccess; ++r)
-      err = launch_panels(p, B, C, N, nullptr, 0, nullptr, &cands[i], nullptr, stream);
+      err = launch_panels(p, B, C, N, nullptr, 0, nullptr, &cands[i], nullptr, 0, stream);
     if (err == hipSuccess) err = hipEventRecord(e1, stream);
     if (err == hipSuccess) err = hipEventSynchronize(e1);
     float ms = 0.0f;
@@ -554,14 +619,14 @@ hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStr
 hipError_t launch_conv3x3(const sdnn_plan_s* p, const float* X, float* C, int32_t H, int32_t W,
                           int32_t NB, const float* bias, int epi, hipStream_t stream) {
   const int32_t hwn[3] = {H, W, NB};
-  return launch_panels(p, X, C, H * W * NB, bias, epi, hwn, nullptr, nullptr, stream);
+  return launch_panels(p, X, C, H * W * NB, bias, epi, hwn, nullptr, nullptr, 0, stream);
 }
 
 hipError_t launch_conv3x3_split(const sdnn_plan_s* p, const float* X, float* C, int32_t H,
-                                int32_t W, int32_t NB, const float* bias, int epi, float* ws,
-                                hipStream_t stream) {
+                                int32_t W, int32_t NB, const float* bias, int epi, int splits,
+                                float* ws, hipStream_t stream) {
   const int32_t hwn[3] = {H, W, NB};
-  return launch_panels(p, X, C, H * W * NB, bias, epi, hwn, nullptr, ws, stream);
+  return launch_panels(p, X, C, H * W * NB, bias, epi, hwn, nullptr, ws, splits, stream);
 }
 
 // ---------------------------------------------------------------------------------

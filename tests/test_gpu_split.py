@@ -33,21 +33,21 @@ def assert_close(got, ref, bound, epi, label):
                            f"worst err/tol {np.nanmax(err / tol):.3g}")
 
 
-def split_spmm(plan, B, bias, epi, workspace=None):
+def split_spmm(plan, B, bias, epi, workspace=None, splits=0):
     Bt = torch.from_numpy(np.ascontiguousarray(B)).to(DEV)
     bt = None if bias is None else torch.from_numpy(np.ascontiguousarray(bias)).to(DEV)
     C = torch.full((plan.M, B.shape[1]), float("nan"), device=DEV)
     if workspace is None:  # a poisoned workspace: every partial must be written
         workspace = torch.full((max(plan.workspace_floats(B.shape[1]), 1),), float("nan"),
                                device=DEV)
-    plan.spmm_split(Bt, C, bt, epi, workspace=workspace)
+    plan.spmm_split(Bt, C, bt, epi, workspace=workspace, splits=splits)
     torch.cuda.synchronize()
     return C.cpu().numpy()
 
 
-def check_split(W, B, bias, epi, split_chunks, label="", **kw):
+def check_split(W, B, bias, epi, split_chunks, label="", splits=0, **kw):
     with sd.Plan.from_csr(W, split_chunks=split_chunks, **kw) as plan:
-        got = split_spmm(plan, B, bias, epi)
+        got = split_spmm(plan, B, bias, epi, splits=splits)
         perm, splits = plan.perm, plan.info["splits"]
     nchunks = -(-W.K // 32)
     assert splits == max(1, -(-nchunks // split_chunks)), label
@@ -70,6 +70,33 @@ def test_split_parity_ragged(split_chunks, N):
     W = inputs.pattern_uniform(200, 300, 0.15, inputs.CFG_TEST, 500 + split_chunks, 0.05)
     bias = np.random.default_rng([5, N]).standard_normal(200).astype(np.float32) * 0.02
     check_split(W, rand_B(300, N, N), bias, "relu", split_chunks, f"sc={split_chunks} N={N}")
+
+
+@pytest.mark.parametrize("splits", [0, 1, 2, 3, 4, 6, 10, 99])
+@pytest.mark.parametrize("N", [129, 512])
+def test_split_runs_of_segments(splits, N):
+    """Ten one-chunk segments (K = 300, the last chunk ragged) in runs of
+    ceil(10 / splits): every run count, the library's choice (0) and a count above the
+    segments (clamped to 10).  One run is the unsplit call, bit for bit."""
+    W = inputs.pattern_uniform(200, 300, 0.15, inputs.CFG_TEST, 600, 0.05)
+    bias = np.random.default_rng([6, N]).standard_normal(200).astype(np.float32) * 0.02
+    B = rand_B(300, N, 600 + N)
+    got = check_split(W, B, bias, "gelu", 1, f"splits={splits} N={N}", splits=splits)
+    if splits == 1:
+        with sd.Plan.from_csr(W) as plain:
+            Bt = torch.from_numpy(B).to(DEV)
+            C = torch.empty(200, N, device=DEV)
+            plain.spmm(Bt, C, torch.from_numpy(bias).to(DEV), "gelu")
+            torch.cuda.synchronize()
+            assert np.array_equal(C.cpu().numpy(), got)
+
+
+@pytest.mark.parametrize("splits", [0, 3, 4, 8, 24])
+def test_split_runs_w0(splits):
+    """W0 at N = 1024 on 24 segments of four chunks, in runs."""
+    w = inputs.workload("w0", N=1024)
+    L = w.layers[0]
+    check_split(L.W, w.B, L.bias, L.epi, 4, f"w0 splits={splits}", splits=splits)
 
 
 @pytest.mark.parametrize("epi", ["none", "relu", "gelu"])
@@ -122,7 +149,7 @@ def test_split_matches_unsplit_and_one_segment_plan():
         split.spmm(Bt, C1, bt, "relu")
         ws = torch.full((16,), 7.0, device=DEV)
         assert one._lib.sdnn_spmm_split(one.handle, Bt.data_ptr(), C2.data_ptr(), 640,
-                                        bt.data_ptr(), 1, ws.data_ptr(), 16, None) == 0
+                                        bt.data_ptr(), 1, 0, ws.data_ptr(), 16, None) == 0
         torch.cuda.synchronize()
         assert torch.equal(C0, C1) and torch.equal(C0, C2)
         assert torch.all(ws == 7.0)
@@ -138,14 +165,15 @@ def test_split_rejects_bad_workspace():
         assert plan.info["splits"] == 4 and need == 4 * 256 * 64
         ws = torch.empty(need + 4, device=DEV)
         h, pb, pc = plan.handle, Bt.data_ptr(), C.data_ptr()
-        assert lib.sdnn_spmm_split(h, pb, pc, 64, None, 0, ws.data_ptr(), need - 1, None) == 2
-        assert lib.sdnn_spmm_split(h, pb, pc, 64, None, 0, ws.data_ptr() + 4, need, None) == 2
-        assert lib.sdnn_spmm_split(h, pb, pc, 64, None, 0, None, need, None) == 1
-        assert lib.sdnn_spmm_split(h, pb, pc, 64, None, 0, pc, need, None) == 2       # C
-        assert lib.sdnn_spmm_split(plain.handle, pb, pc, 64, None, 0, ws.data_ptr(), need,
+        assert lib.sdnn_spmm_split(h, pb, pc, 64, None, 0, 0, ws.data_ptr(), need - 1, None) == 2
+        assert lib.sdnn_spmm_split(h, pb, pc, 64, None, 0, 0, ws.data_ptr() + 4, need, None) == 2
+        assert lib.sdnn_spmm_split(h, pb, pc, 64, None, 0, 0, None, need, None) == 1
+        assert lib.sdnn_spmm_split(h, pb, pc, 64, None, 0, 0, pc, need, None) == 2       # C
+        assert lib.sdnn_spmm_split(plain.handle, pb, pc, 64, None, 0, 0, ws.data_ptr(), need,
                                    None) == 2                                          # unsplit plan
-        assert lib.sdnn_spmm_split(h, pb, pc, 0, None, 0, None, 0, None) == 0            # N = 0
-        assert lib.sdnn_spmm_split(h, pb, pc, 64, None, 0, ws.data_ptr(), need, None) == 0
+        assert lib.sdnn_spmm_split(h, pb, pc, 0, None, 0, 0, None, 0, None) == 0            # N = 0
+        assert lib.sdnn_spmm_split(h, pb, pc, 64, None, 0, -1, ws.data_ptr(), need, None) == 2
+        assert lib.sdnn_spmm_split(h, pb, pc, 64, None, 0, 0, ws.data_ptr(), need, None) == 0
         torch.cuda.synchronize()
 
 
@@ -175,28 +203,30 @@ def test_split_graph_capture_replays():
             assert torch.equal(C, eager)
 
 
-def split_conv(plan, X, bias, epi):
+def split_conv(plan, X, bias, epi, splits=0):
     Xt = torch.from_numpy(np.ascontiguousarray(X)).to(DEV)
     IC, H, W, NB = X.shape
     C = torch.full((plan.M, H, W, NB), float("nan"), device=DEV)
     ws = torch.full((max(plan.workspace_floats(H * W * NB), 1),), float("nan"), device=DEV)
     bt = None if bias is None else torch.from_numpy(bias).to(DEV)
-    plan.conv3x3_split(Xt, C, bt, epi, workspace=ws)
+    plan.conv3x3_split(Xt, C, bt, epi, workspace=ws, splits=splits)
     torch.cuda.synchronize()
     return C.cpu().numpy()
 
 
-@pytest.mark.parametrize("OC,IC,H,W,NB,sparsity,epi,sc", [
-    (5, 3, 5, 7, 4, 0.5, "none", 1),        # K = 27: one segment
-    (40, 16, 7, 7, 12, 0.9, "gelu", 1),     # K = 144 over five segments, ragged tile
-    (64, 64, 28, 28, 4, 0.95, "relu", 4),   # 18 chunks in segments of 4 (last ragged)
-    (128, 128, 14, 14, 16, 0.9, "none", 9),
-    (256, 256, 7, 7, 16, 0.9, "relu", 12),
+@pytest.mark.parametrize("OC,IC,H,W,NB,sparsity,epi,sc,splits", [
+    (5, 3, 5, 7, 4, 0.5, "none", 1, 0),        # K = 27: one segment
+    (40, 16, 7, 7, 12, 0.9, "gelu", 1, 0),     # K = 144 over five segments, ragged tile
+    (40, 16, 7, 7, 12, 0.9, "gelu", 1, 2),     # runs of three and two segments
+    (64, 64, 28, 28, 4, 0.95, "relu", 4, 0),   # 18 chunks in segments of 4 (last ragged)
+    (128, 128, 14, 14, 16, 0.9, "none", 9, 0),
+    (256, 256, 7, 7, 16, 0.9, "relu", 12, 0),
+    (256, 256, 7, 7, 16, 0.9, "relu", 4, 5),   # 18 segments in runs of four
 ])
-def test_conv_split_parity(OC, IC, H, W, NB, sparsity, epi, sc):
+def test_conv_split_parity(OC, IC, H, W, NB, sparsity, epi, sc, splits):
     L = inputs.conv_layer(OC, IC, H, W, NB, sparsity, layer=OC + IC + H + 1, epi=epi)
     with sd.Plan.from_csr(L.F, split_chunks=sc) as plan:
-        got = split_conv(plan, L.X, L.bias, epi)
+        got = split_conv(plan, L.X, L.bias, epi, splits)
     ref, bound = oracle.conv3x3_f64(L.F.row_ptr, L.F.col_idx, L.F.values, L.X, L.bias, epi)
     assert_close(got, ref, bound, epi, f"conv {OC}x{IC} {H}x{W}x{NB} sc={sc}")
 

@@ -1,7 +1,7 @@
 """CPU tests of K-segmented packing (plan option split_chunks), through the host-only
 self-check: the packer's stream, re-walked, must hold every entry once, with no group
-spanning two K-segments, seg_end on each segment's last group and a segment table that
-names each segment's first group.  No GPU is touched."""
+spanning two K-segments, the sync bit on each segment's first group and a segment table
+that names each segment's first group.  No GPU is touched."""
 import numpy as np
 import pytest
 
@@ -49,5 +49,5 @@ def test_split_option_rejects_negative():
 def test_split_entry_points_check_plan_before_gpu():
     """A NULL plan is reported before any device work (no GPU is needed for that)."""
     L = sd.lib()
-    assert L.sdnn_spmm_split(None, None, None, 4, None, 0, None, 0, None) == 1
-    assert L.sdnn_conv3x3_split(None, None, None, 2, 2, 4, None, 0, None, 0, None) == 1
+    assert L.sdnn_spmm_split(None, None, None, 4, None, 0, 0, None, 0, None) == 1
+    assert L.sdnn_conv3x3_split(None, None, None, 2, 2, 4, None, 0, 0, None, 0, None) == 1
