@@ -148,7 +148,7 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
   const int bid = blockIdx.x;
   const int lin = (bid & 7) * a.per_xcd + (bid >> 3);
   if (lin >= a.total_wg) return;  // whole workgroup leaves before the barrier
-  // workgroups of one tile and K-segment are consecutive (they share the staged rows)
+  // workgroups of one tile and run of K-segments are consecutive (they stage the same rows)
   const int per_tile = a.nsplit * a.n_rb;
   const int tile = lin / per_tile;
   const int split = (lin - tile * per_tile) / a.n_rb;
@@ -405,6 +405,8 @@ namespace {
 // in the Infinity Cache); all measured on MI355X.  A count is tried only if runs of
 // ceil(nseg / count) segments give exactly it, and replaces a smaller one only if it
 // costs at least 10 % less (the model's error on MI355X is about that size).
+constexpr int kMaxAutoSplits = 32;  // more runs than this never paid for their partials
+
 int choose_splits(const sdnn_plan_s* p, int N, bool conv) {
   const int total_seg = p->pk[0].nseg;
   const int cus = p->num_cus > 0 ? p->num_cus : 256;
@@ -414,7 +416,7 @@ int choose_splits(const sdnn_plan_s* p, int N, bool conv) {
   const double density = (double)p->nnz / ((double)p->M * (double)p->K);
   int best = 1;
   double best_cost = 0.0;
-  for (int splits = 1; splits <= total_seg; ++splits) {
+  for (int splits = 1; splits <= std::min(total_seg, kMaxAutoSplits); ++splits) {
     const int per = (total_seg + splits - 1) / splits;
     if ((total_seg + per - 1) / per != splits) continue;
     const DevPacking& pk = choose_packing(p, N, conv, splits);

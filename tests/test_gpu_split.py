@@ -242,3 +242,33 @@ def test_split_ragged_small_patterns():
     B = rand_B(K, 130, 9)
     for sc in (1, 2, 3):
         check_split(W, B, None, "none", sc, f"small sc={sc}", panel_rows=4)
+
+
+def test_split_random_configurations():
+    """Seeded random problems over every option the split call combines: shape, density,
+    segment length, runs along K (0 = the library's choice), panel height, row order,
+    output order, epilogue and bias."""
+    rng = np.random.default_rng([2101, 7948, 4242])
+    for case in range(40):
+        M = int(rng.integers(1, 300))
+        K = int(rng.integers(1, 700))
+        N = int(rng.integers(1, 700))
+        d = float(rng.choice([0.0, 0.02, 0.1, 0.3, 0.7]))
+        W = inputs.pattern_uniform(M, K, d, inputs.CFG_TEST, 7000 + case, 0.05)
+        sc = int(rng.integers(1, 6))
+        kw = dict(panel_rows=int(rng.choice([0, 4, 8, 12, 16])),
+                  permute=int(rng.integers(0, 6)), out_permuted=bool(rng.integers(0, 2)))
+        epi = str(rng.choice(["none", "relu", "gelu"]))
+        bias = None if rng.random() < 0.3 else \
+            (rng.standard_normal(M) * 0.05).astype(np.float32)
+        splits = int(rng.choice([0, 1, 2, 3, 5, 64]))
+        label = (f"case {case}: M={M} K={K} N={N} d={d} sc={sc} splits={splits} {kw} {epi} "
+                 f"bias={bias is not None}")
+        with sd.Plan.from_csr(W, split_chunks=sc, **kw) as plan:
+            got = split_spmm(plan, rand_B(K, N, 7000 + case), bias, epi, splits=splits)
+            perm = plan.perm
+        ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, K, rand_B(K, N, 7000 + case),
+                                     bias, epi)
+        if kw["out_permuted"]:
+            ref, bound = ref[perm], bound[perm]
+        assert_close(got, ref, bound, epi, label)
