@@ -143,7 +143,9 @@ sdnn_status sdnn_row_order(const int32_t* row_ptr, const int32_t* col_idx, int32
  * computes the row permutation, packs W into the kernel's traversal-ordered stream
  * and uploads it to the current HIP device.  The caller keeps ownership of the CSR
  * arrays (they are copied).  The plan owns its device memory and is bound to the
- * device current at creation.  values may be NULL only when nnz = 0.
+ * device current at creation.  values may be NULL only when nnz = 0.  Limits: K at most
+ * 2^19 = 524288 (16384 staging chunks of 32 rows: the stream's chunk fields), and at
+ * most 2^31 - 1 stored stream entries; beyond either, SDNN_ERR_DIM.
  * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM, SDNN_ERR_CSR, SDNN_ERR_ALLOC, SDNN_ERR_HIP. */
 sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx,
                              const float* values, int32_t M, int32_t K,

@@ -272,3 +272,29 @@ def test_split_random_configurations():
         if kw["out_permuted"]:
             ref, bound = ref[perm], bound[perm]
         assert_close(got, ref, bound, epi, label)
+
+
+def test_longest_k_plain_and_split():
+    """K = 2^19, the longest the stream's chunk fields allow: entries up to the last
+    column, through the plain call and the K-split call (24 segments, library's choice
+    and 5 runs)."""
+    K, M, N = 1 << 19, 16, 64
+    rng = np.random.default_rng([2101, 7948, 19])
+    rows = [sorted(set(rng.choice(K, 100, replace=False).tolist()) | {K - 1, K - 33, 0})
+            for _ in range(M)]
+    rp, ci, _ = pattern_to_csr(rows, K)
+    v = rng.standard_normal(ci.size).astype(np.float32)
+    W = inputs.CSR(rp, ci, v, M, K)
+    B = rand_B(K, N, 19)
+    bias = rng.standard_normal(M).astype(np.float32)
+    ref, bound = oracle.spmm_f64(rp, ci, v, K, B, bias, "relu")
+    with sd.Plan.from_csr(W) as plain:
+        Bt = torch.from_numpy(B).to(DEV)
+        C = torch.full((M, N), float("nan"), device=DEV)
+        plain.spmm(Bt, C, torch.from_numpy(bias).to(DEV), "relu")
+        torch.cuda.synchronize()
+        assert_close(C.cpu().numpy(), ref, bound, "relu", "K = 2^19 plain")
+        del Bt
+    for splits in (0, 5):
+        got = check_split(W, B, bias, "relu", 700, f"K = 2^19 split {splits}", splits=splits)
+        assert got.shape == (M, N)

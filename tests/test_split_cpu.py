@@ -51,3 +51,17 @@ def test_split_entry_points_check_plan_before_gpu():
     L = sd.lib()
     assert L.sdnn_spmm_split(None, None, None, 4, None, 0, 0, None, 0, None) == 1
     assert L.sdnn_conv3x3_split(None, None, None, 2, 2, 4, None, 0, 0, None, 0, None) == 1
+
+
+def test_longest_k_packs_and_one_more_chunk_is_rejected():
+    """K = 2^19 (16384 chunks, the stream's chunk fields full) packs, entries in the last
+    chunk included, also in K-segments; one more row of B is SDNN_ERR_DIM."""
+    K = 1 << 19
+    rows = [[0, 5, K - 1], [K // 2, K - 33, K - 32], [], [7, 31, 32, 1000, 400000]]
+    rp, ci, v = pattern_to_csr(rows, K)
+    for sc in (0, 1, 700):
+        info = sd.plan_check_host(rp, ci, v, len(rows), K, panel_rows=4, split_chunks=sc)
+        assert info["splits"] == (0 if sc == 0 else -(-16384 // sc))
+    with pytest.raises(sd.SdnnError) as e:
+        sd.plan_check_host(rp, ci, v, len(rows), K + 1, panel_rows=4)
+    assert e.value.code == 2
