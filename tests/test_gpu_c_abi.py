@@ -1,0 +1,42 @@
+"""The C ABI driven from a plain C99 program (tests/c_abi/sdnn_c_check.c, built by the
+repository's build step) in a child process: plan creation, sdnn_spmm and
+sdnn_spmm_split with a GELU epilogue, results checked here against the CPU oracle with
+the parity bar (|err| <= 1.13 * (1e-5 * sum |w||b| + 1e-6) + 4 ulp for GELU) and the
+permutation against the oracle's Algorithm 1 bit for bit."""
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from conftest import ROOT
+from paper_2101_07948_amd import inputs
+
+pytestmark = pytest.mark.gpu
+EXE = os.path.join(ROOT, "tests", "c_abi", "sdnn_c_check")
+
+
+def test_c_caller_matches_oracle(tmp_path):
+    assert os.path.exists(EXE), f"{EXE} is missing: run __graft_entry__.build() first"
+    M, K, N = 70, 333, 130
+    W = inputs.pattern_uniform(M, K, 0.1, inputs.CFG_TEST, 8100, 0.05)
+    B = inputs.dense_B(K, N, inputs.CFG_TEST, 8100)
+    bias = inputs.bias_normal(M, inputs.CFG_TEST, 8100, 0.02)
+    for name, arr in (("row_ptr.i32", W.row_ptr.astype(np.int32)),
+                      ("col_idx.i32", W.col_idx.astype(np.int32)),
+                      ("values.f32", W.values.astype(np.float32)),
+                      ("B.f32", B.astype(np.float32)), ("bias.f32", bias.astype(np.float32))):
+        arr.tofile(tmp_path / name)
+    print(f"c_abi: M={M} K={K} N={N}", flush=True)
+    r = subprocess.run([EXE, str(tmp_path), str(M), str(K), str(N)], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, K, B, bias, "gelu")
+    tol = (1e-5 * bound + 1e-6) * 1.13 + 4 * 2.0 ** -24 * np.abs(ref)
+    for name in ("C_plain.f32", "C_split.f32"):
+        got = np.fromfile(tmp_path / name, dtype=np.float32).reshape(M, N).astype(np.float64)
+        bad = ~(np.abs(got - ref) <= tol)
+        assert not bad.any(), f"{name}: {int(bad.sum())} of {bad.size} out of tolerance"
+    perm = np.fromfile(tmp_path / "perm.i32", dtype=np.int32)
+    assert np.array_equal(perm, oracle.reorder(W.row_ptr, W.col_idx, K))
