@@ -288,11 +288,16 @@ class Plan:
         info["splits"], the plan's K-segments)."""
         return int(self.info["splits"]) * self.M * int(N)
 
-    def _workspace(self, ws, N: int):
+    def _workspace(self, ws, N: int, stream):
+        """(pointer, floats) of the caller's workspace, or of one allocated here from torch's
+        caching allocator; such a block is tied to `stream` so that it is not handed out
+        again before the call's kernels on that stream have run."""
         import torch
-        need = self.workspace_floats(N) if int(self.info["splits"]) > 1 else 0
         if ws is None:
+            need = self.workspace_floats(N) if int(self.info["splits"]) > 1 else 0
             ws = torch.empty(max(need, 1), device="cuda")
+            if stream is not None:
+                ws.record_stream(stream)
         if not isinstance(ws, torch.Tensor) or ws.device.type != "cuda" or \
                 ws.dtype != torch.float32 or not ws.is_contiguous():
             raise TypeError("workspace must be a contiguous float32 CUDA/HIP tensor")
@@ -308,7 +313,7 @@ class Plan:
         pb = _dev_ptr(B, "B", (self.K, N))
         pc = _dev_ptr(C, "C", (self.M, N))
         pbias = _dev_ptr(bias, "bias", (self.M,), allow_none=True)
-        pw, nw = self._workspace(workspace, N)
+        pw, nw = self._workspace(workspace, N, stream)
         _check(self._lib.sdnn_spmm_split(self.handle, pb, pc, N, pbias, EPI[epi], int(splits),
                                          pw, nw, _stream_handle(stream)), "sdnn_spmm_split")
         return C
@@ -324,7 +329,7 @@ class Plan:
         px = _dev_ptr(X, "X", (IC, H, W, NB))
         pc = _dev_ptr(C, "C", (self.M, H, W, NB))
         pbias = _dev_ptr(bias, "bias", (self.M,), allow_none=True)
-        pw, nw = self._workspace(workspace, H * W * NB)
+        pw, nw = self._workspace(workspace, H * W * NB, stream)
         _check(self._lib.sdnn_conv3x3_split(self.handle, px, pc, H, W, NB, pbias, EPI[epi],
                                             int(splits), pw, nw, _stream_handle(stream)),
                "sdnn_conv3x3_split")

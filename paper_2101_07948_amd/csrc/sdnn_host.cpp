@@ -753,6 +753,7 @@ sdnn_status sdnn_plan_check_host(const int32_t* row_ptr, const int32_t* col_idx,
       if (!check_packed(csr.row_ptr, csr.col_idx, csr.values, P)) return SDNN_ERR_INTERNAL;
       bytes += packing_bytes(P);
     }
+    if (o.split_chunks > 0) bytes += align256((int64_t)M * 4);  // the device copy of perm
     if (info) fill_info(packs, bytes, o, info);
     return SDNN_OK;
   } catch (...) {

@@ -298,3 +298,17 @@ def test_longest_k_plain_and_split():
     for splits in (0, 5):
         got = check_split(W, B, bias, "relu", 700, f"K = 2^19 split {splits}", splits=splits)
         assert got.shape == (M, N)
+
+
+def test_plan_info_matches_host_check():
+    """The device plan reports the statistics and byte count the host-only check computes,
+    the K-segment table and the device perm of split plans included."""
+    W = inputs.workload("c2", N=4).layers[0].W
+    for kw in ({}, {"split_chunks": 3}, {"split_chunks": 1, "panel_rows": 8},
+               {"split_chunks": 5, "out_permuted": True}):
+        host = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, **kw)
+        with sd.Plan.from_csr(W, **kw) as plan:
+            dev = plan.info
+        for key in ("panels", "packed_bytes", "splits", "panel_rows", "tall_panel_rows", "nnz"):
+            assert dev[key] == host[key], (kw, key, dev[key], host[key])
+        assert dev["rho"] == pytest.approx(host["rho"]) and dev["fill"] == pytest.approx(host["fill"])
