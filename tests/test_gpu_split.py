@@ -312,3 +312,25 @@ def test_plan_info_matches_host_check():
         for key in ("panels", "packed_bytes", "splits", "panel_rows", "tall_panel_rows", "nnz"):
             assert dev[key] == host[key], (kw, key, dev[key], host[key])
         assert dev["rho"] == pytest.approx(host["rho"]) and dev["fill"] == pytest.approx(host["fill"])
+
+
+@pytest.mark.parametrize("splits", [2, 3, 8])
+def test_split_row_permutation_equivariance_bitexact(splits):
+    """A row's partial sums follow its entries in column order inside each run and the
+    runs are added in order, whatever panel the row lands in: permuting W's rows
+    permutes the K-split call's C rows bit for bit (a fixed run count, so that both
+    calls cut K at the same chunks)."""
+    W = inputs.pattern_uniform(300, 500, 0.1, inputs.CFG_TEST, 17, 0.05)
+    B = inputs.dense_B(500, 384, inputs.CFG_TEST, 17)
+    bias = inputs.bias_normal(300, inputs.CFG_TEST, 17, 0.02)
+    pi = np.random.default_rng(18).permutation(300)
+    Wd = W.to_dense()
+    Wp = Wd[pi]
+    rp = np.concatenate([[0], np.cumsum((Wp != 0).sum(axis=1))]).astype(np.int32)
+    ci = np.nonzero(Wp)[1].astype(np.int32)
+    v = Wp[Wp != 0].astype(np.float32)
+    W2 = inputs.CSR(rp, ci, v, 300, 500)
+    with sd.Plan.from_csr(W, split_chunks=2) as p1, sd.Plan.from_csr(W2, split_chunks=2) as p2:
+        C1 = split_spmm(p1, B, bias, "gelu", splits=splits)
+        C2 = split_spmm(p2, B, bias[pi], "gelu", splits=splits)
+    assert np.array_equal(C2, C1[pi])
