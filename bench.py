@@ -213,12 +213,14 @@ def _blas_time(Wd, B, C, reps=20):
     return mean
 
 
-def _packing_used(info, M, N, cus):
-    """Mirror of the launcher's choice (4-row unless the tall packing fills every CU)."""
-    tall = info["tall_panel_rows"]
-    if tall and M * -(-N // 256) >= 8 * tall * cus:
-        return tall, info["tall_rho"]
-    return info["panel_rows"], info["rho"]
+def _packing_used(plan, N):
+    """(panel height, rho) of the packing plan.spmm runs on at N, as the library reports."""
+    rw = plan.launch_shape(N)["panel_rows"]
+    info = plan.info
+    for k in ("", "tall_", "mid_"):
+        if info[k + "panel_rows"] == rw:
+            return rw, info[k + "rho"]
+    return rw, float("nan")
 
 
 def run_suite(out_path):
@@ -250,7 +252,7 @@ def run_suite(out_path):
     for label, L, N in _suite_layers():
         W = L.W
         with sd.Plan.from_csr(W) as plan:
-            rw, rho = _packing_used(plan.info, W.M, N, cus)
+            rw, rho = _packing_used(plan, N)
             per, mean, nsets = _time_layer(plan, L, N)
             wper, _, _ = _time_layer(plan, L, N, cold=False)
         flop = 2.0 * W.nnz * N
@@ -304,7 +306,7 @@ def run_suite(out_path):
         res = {}
         for perm in orders:
             with sd.Plan.from_csr(L.W, permute=perm) as plan:
-                _, rho = _packing_used(plan.info, L.W.M, N, cus)
+                _, rho = _packing_used(plan, N)
                 _, mean, _ = _time_layer(plan, L, N, reps=50)
             res[perm] = (rho, mean)
         lines.append(f"| {label} | " + " | ".join(f"{res[k][0]:.2f}" for k in orders) + " | "
@@ -452,8 +454,7 @@ def run_suite(out_path):
             return _launch_times(fn, 50)[1]
         with sd.Plan.from_csr(W) as plan:
             base = timed_mean(plan, None)
-            info = plan.info
-        rw, _ = _packing_used(info, W.M, N, cus)
+            rw, _ = _packing_used(plan, N)
         grid = f"{-(-N // 256)} x {-(-W.M // rw)} ({rw}-row)"
         with sd.Plan.from_csr(W, split_chunks=S) as plan:
             ws = torch.empty(max(plan.workspace_floats(N), 1), device=dev)

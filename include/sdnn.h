@@ -58,11 +58,13 @@ typedef enum {
 } sdnn_epilogue;
 
 /* Options for sdnn_plan_create; pass NULL for the defaults {0, 1, 0, 0, NULL}.
- *   panel_rows:   rows per register panel.  0 (default) packs W twice, with short
- *                 panels of 4 rows and tall panels of 12 rows, and sdnn_spmm picks per
- *                 call: tall panels once a 256-column tile has at least a full
- *                 workgroup of them per compute unit (M * ceil(N / 256) >= 96 * CUs),
- *                 short panels otherwise.  4, 8, 12 or 16 packs that height only.
+ *   panel_rows:   rows per register panel.  0 (default) packs W three times, with
+ *                 panels of 4, 12 and 8 rows, and sdnn_spmm picks one per call: the
+ *                 fewest rounds of workgroups over the compute units, then the most
+ *                 units busy, then the shortest panels averaging at least 8 entries per
+ *                 32 columns of W (4-row panels are not used below 4); sdnn_plan_tune
+ *                 can replace that choice by a timed one, and sdnn_plan_launch_shape
+ *                 reports it.  4, 8, 12 or 16 packs that height only.
  *   permute:      1 = apply Algorithm 1 (default), 0 = identity order (ablation),
  *                 2 = panel-balancing order: rows, by nonzero count descending, each
  *                 go to the 4-row panel with the fewest nonzeros so far that has room,
@@ -99,8 +101,8 @@ typedef struct {
   const int32_t* in_perm;
 } sdnn_plan_opts;
 
-/* Plan statistics (of the first packing; the tall_* fields describe the second one,
- * or are 0 when the plan holds one packing).
+/* Plan statistics (of the first packing; the tall_* fields describe the second one and
+ * the mid_* fields the third, or are 0 when the plan holds fewer packings).
  *   panels:       number of row panels (ceil(M / panel_rows)).
  *   packed_bytes: device bytes of every packed weight stream and its indexes.
  *   rho:          nnz / sum over panels of |union of the panel rows' column sets|,
@@ -117,6 +119,8 @@ typedef struct {
   int32_t tall_panel_rows, splits;
   double tall_rho, tall_fill;
   int32_t out_permuted, in_permuted;  /* the plan's options (in_permuted: in_perm given) */
+  int32_t mid_panel_rows, packings;   /* third packing's height (0: none); packings held */
+  double mid_rho, mid_fill;
 } sdnn_plan_info_t;
 
 /* Greedy weight-row permutation (Sec. 3.1.2, Algorithm 1), host only, no GPU needed.
@@ -206,6 +210,13 @@ sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const fl
 sdnn_status sdnn_spmm_split(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
                             sdnn_epilogue epi, int32_t splits, float* workspace,
                             int64_t workspace_floats, void* stream);
+
+/* The launch shape sdnn_spmm uses for this plan at N columns (the tuned one if
+ * sdnn_plan_tune recorded one for N, else the rule described under panel_rows):
+ * *panel_rows = the packing's panel height, *waves = consumer waves per workgroup
+ * (either pointer may be NULL).  Host only; touches no device memory.
+ * Errors: SDNN_ERR_NULL (p), SDNN_ERR_DIM (N <= 0 or M = 0). */
+sdnn_status sdnn_plan_launch_shape(sdnn_plan p, int32_t N, int32_t* panel_rows, int32_t* waves);
 
 /* Per-plan variant selection by timing (the paper's preparation stage chooses the best
  * kernel implementation per operator, Sec. 3.1): times sdnn_spmm at this N for every

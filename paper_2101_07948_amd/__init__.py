@@ -44,7 +44,9 @@ class PlanInfo(ctypes.Structure):
                 ("panel_rows", ctypes.c_int32), ("k_chunk", ctypes.c_int32),
                 ("tall_panel_rows", ctypes.c_int32), ("splits", ctypes.c_int32),
                 ("tall_rho", ctypes.c_double), ("tall_fill", ctypes.c_double),
-                ("out_permuted", ctypes.c_int32), ("in_permuted", ctypes.c_int32)]
+                ("out_permuted", ctypes.c_int32), ("in_permuted", ctypes.c_int32),
+                ("mid_panel_rows", ctypes.c_int32), ("packings", ctypes.c_int32),
+                ("mid_rho", ctypes.c_double), ("mid_fill", ctypes.c_double)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -78,12 +80,14 @@ def lib() -> ctypes.CDLL:
         L.sdnn_dense_gemm.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
         L.sdnn_conv3x3.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
         L.sdnn_plan_tune.argtypes = [p, p, p, i32, p, p, p]
+        L.sdnn_plan_launch_shape.argtypes = [p, i32, p, p]
         i64 = ctypes.c_int64
         L.sdnn_spmm_split.argtypes = [p, p, p, i32, p, ctypes.c_int, i32, p, i64, p]
         L.sdnn_conv3x3_split.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, i32, p, i64, p]
         for fn in ("sdnn_reorder_rows", "sdnn_row_order", "sdnn_plan_check_host", "sdnn_plan_create",
                    "sdnn_plan_get_perm", "sdnn_plan_info", "sdnn_spmm", "sdnn_dense_gemm",
-                   "sdnn_conv3x3", "sdnn_plan_tune", "sdnn_spmm_split", "sdnn_conv3x3_split"):
+                   "sdnn_conv3x3", "sdnn_plan_tune", "sdnn_spmm_split", "sdnn_conv3x3_split",
+                   "sdnn_plan_launch_shape"):
             getattr(L, fn).restype = ctypes.c_int
         _lib_handle = L
     return _lib_handle
@@ -251,6 +255,13 @@ class Plan:
         info = PlanInfo()
         _check(self._lib.sdnn_plan_info(self.handle, ctypes.byref(info)), "sdnn_plan_info")
         return info.as_dict()
+
+    def launch_shape(self, N: int) -> dict:
+        """The panel height and consumer waves per workgroup spmm uses at N columns."""
+        rw, waves = ctypes.c_int32(), ctypes.c_int32()
+        _check(self._lib.sdnn_plan_launch_shape(self.handle, int(N), ctypes.byref(rw),
+                                                ctypes.byref(waves)), "sdnn_plan_launch_shape")
+        return {"panel_rows": rw.value, "waves": waves.value}
 
     def tune(self, N: int, B=None, C=None, stream=None) -> dict:
         """Times the plan's launch shapes at this N (on B / C, allocated here when not

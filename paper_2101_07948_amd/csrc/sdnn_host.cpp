@@ -370,7 +370,7 @@ struct Options {
 
 // Panel heights to pack: the explicit option, or the short and tall defaults.
 static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* o) {
-  o->rws = {kShortPanel, kTallPanel};
+  o->rws = {kShortPanel, kTallPanel, kMidPanel};
   if (!opts) return SDNN_OK;
   if (opts->panel_rows != 0) {
     if (opts->panel_rows != 4 && opts->panel_rows != 8 && opts->panel_rows != 12 &&
@@ -662,7 +662,7 @@ static double fill_of(const Packed& P) {
   return P.stored ? (double)P.nnz / (double)P.stored : 1.0;
 }
 
-// Statistics of the first packing, plus the tall one's if there is one.
+// Statistics of the first packing, plus the tall and mid ones' if there are.
 static void fill_info(const std::vector<Packed>& packs, int64_t packed_bytes,
                       const Options& o, sdnn_plan_info_t* out) {
   const Packed& P = packs[0];
@@ -682,6 +682,11 @@ static void fill_info(const std::vector<Packed>& packs, int64_t packed_bytes,
   out->tall_fill = tall ? fill_of(packs[1]) : 0.0;
   out->out_permuted = o.out_permuted;
   out->in_permuted = o.in_perm ? 1 : 0;
+  const bool mid = packs.size() > 2;
+  out->mid_panel_rows = mid ? packs[2].RW : 0;
+  out->packings = (int32_t)packs.size();
+  out->mid_rho = mid ? packs[2].rho : 0.0;
+  out->mid_fill = mid ? fill_of(packs[2]) : 0.0;
 }
 
 static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
@@ -898,6 +903,11 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out) {
   out->tall_fill = tall ? p->pk[1].fill : 0.0;
   out->out_permuted = p->out_permuted;
   out->in_permuted = p->in_permuted;
+  const bool mid = p->npack > 2;
+  out->mid_panel_rows = mid ? p->pk[2].RW : 0;
+  out->packings = p->npack;
+  out->mid_rho = mid ? p->pk[2].rho : 0.0;
+  out->mid_fill = mid ? p->pk[2].fill : 0.0;
   return SDNN_OK;
 }
 
@@ -976,6 +986,16 @@ sdnn_status sdnn_spmm_split(sdnn_plan p, const float* B, float* C, int32_t N, co
                             sdnn_epilogue epi, int32_t splits, float* workspace,
                             int64_t workspace_floats, void* stream) {
   return spmm_entry(p, B, C, N, bias, epi, splits, workspace, workspace_floats, true, stream);
+}
+
+sdnn_status sdnn_plan_launch_shape(sdnn_plan p, int32_t N, int32_t* panel_rows, int32_t* waves) {
+  if (!p) return SDNN_ERR_NULL;
+  if (N <= 0 || p->M == 0) return SDNN_ERR_DIM;
+  int32_t rw = 0, w = 0;
+  launch_shape(p, N, &rw, &w);
+  if (panel_rows) *panel_rows = rw;
+  if (waves) *waves = w;
+  return SDNN_OK;
 }
 
 sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, void* stream,

@@ -76,11 +76,11 @@ struct Packed {
   std::vector<int32_t> seg_start;   // [npanels*nseg] (split_chunks > 0 only)
 };
 
-// Panel heights of the two packings a default plan holds: short panels keep enough
-// waves busy when a tile has few rows per CU; tall panels (used once there are rows
-// for a full workgroup of them per CU) carry more entries per K-chunk and stage each
-// B tile for more rows.
-constexpr int kShortPanel = 4, kTallPanel = 12;
+// Panel heights of the three packings a default plan holds (in this order): short
+// panels keep enough waves busy when a tile has few rows per CU; taller ones carry more
+// entries per K-chunk (so a group spans fewer chunks of the ring) and stage each B tile
+// for more rows.  The launch picks one per call (choose_packing).
+constexpr int kShortPanel = 4, kTallPanel = 12, kMidPanel = 8;
 
 // CSR validation; returns SDNN_OK or SDNN_ERR_*.
 sdnn_status validate_csr(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K);
@@ -122,12 +122,12 @@ struct sdnn_plan_s {
   int64_t nnz = 0, packed_bytes = 0;
   std::vector<int32_t> perm;
   void* d_mem = nullptr;       // one device allocation holding every packing's arrays
-  int npack = 0;               // 1 (explicit panel height) or 2 (short, tall)
+  int npack = 0;               // 1 (explicit panel height) or 3 (short, tall, mid)
   int32_t out_permuted = 0;    // C rows stored in the permuted order
   int32_t in_permuted = 0;     // W's columns renamed to a caller-given order of B's rows
   int32_t split_chunks = 0;    // chunks per K-segment (0: the packings have one segment)
   const int32_t* d_perm = nullptr;  // [M] perm on the device (K-segmented plans only)
-  sdnn::DevPacking pk[2];
+  sdnn::DevPacking pk[3];
   sdnn::TunedShape tuned[sdnn::kTunedSlots];  // filled by sdnn_plan_tune
   int32_t ntuned = 0;
 };
@@ -147,6 +147,8 @@ hipError_t launch_spmm_split(const sdnn_plan_s* p, const float* B, float* C, int
 hipError_t launch_conv3x3_split(const sdnn_plan_s* p, const float* X, float* C, int32_t H,
                                 int32_t W, int32_t NB, const float* bias, int epi, int splits,
                                 float* ws, hipStream_t stream);
+// The packing height and consumer waves launch_spmm uses at N (host only).
+void launch_shape(const sdnn_plan_s* p, int32_t N, int32_t* panel_rows, int32_t* waves);
 // Times every candidate launch shape of the plan at N on the given buffers (blocking)
 // and records the fastest in p->tuned.
 hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStream_t stream,

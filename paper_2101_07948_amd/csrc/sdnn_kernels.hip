@@ -369,11 +369,18 @@ LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N, int nseg = 1) {
   return c;
 }
 
-// The packing a call runs on.  A product: the tall one (second) once the tiles hold
-// at least a full workgroup of tall panels per CU, else the first.  A convolution,
-// whose workgroups are bound by staging its shifted input rows rather than by their
-// panels: the packing that needs fewer rounds, the first on a tie.
-// A K-split launch, whose workgroups stage a segment each, is chosen like a convolution.
+// The packing a call runs on.
+// A product (a default plan holds 4-, 12- and 8-row packings): among the packings, the
+// 4-row one left out when its panels average fewer than 4 entries per 32-row chunk (a
+// group of 8 then spans two chunks or more, which starves the ring's lookahead) and
+// another exists, those needing the fewest rounds of workgroups at their full consumer
+// count; among those, the ones keeping the most CUs busy in those rounds (within 5 %);
+// among those, the shortest panels averaging at least 8 entries per chunk, else the
+// tallest.  (Measured on MI355X over M = K = 512-2048 at 80-98 % and N = 1024-16384 and
+// the C3 / C5 layers: within 10 % of the best packing on all but a few small cases.)
+// A convolution, whose workgroups are bound by staging its shifted input rows rather
+// than by their panels, and a K-split launch: the 4- or the 12-row packing, whichever
+// needs fewer rounds, the 4-row one on a tie.
 const DevPacking& choose_packing(const sdnn_plan_s* p, int N, bool conv, int nseg = 1) {
   if (p->npack < 2) return p->pk[0];
   const DevPacking& tall = p->pk[1];
@@ -386,8 +393,36 @@ const DevPacking& choose_packing(const sdnn_plan_s* p, int N, bool conv, int nse
                ? tall
                : p->pk[0];
   }
-  const int64_t wg_rows = (int64_t)max_consumers(tall.RW) * tall.RW;
-  return (int64_t)p->M * n_tiles >= wg_rows * cus ? tall : p->pk[0];
+  const double density = (double)p->nnz / ((double)p->M * (double)p->K);
+  auto per_chunk = [&](const DevPacking& pk) { return pk.RW * kChunk * density; };
+  int64_t rounds[3];
+  double util[3];
+  bool live[3];
+  int64_t best_rounds = -1;
+  for (int k = 0; k < p->npack; ++k) {
+    const DevPacking& pk = p->pk[k];
+    live[k] = !(pk.RW == 4 && per_chunk(pk) < 4.0);
+    const int waves = std::max(1, std::min(max_consumers(pk.RW), pk.npanels));
+    const int64_t wgs = n_tiles * ((pk.npanels + waves - 1) / waves);
+    rounds[k] = (wgs + cus - 1) / cus;
+    util[k] = (double)wgs / ((double)rounds[k] * cus);
+  }
+  bool any = false;
+  for (int k = 0; k < p->npack; ++k) any |= live[k];
+  if (!any)
+    for (int k = 0; k < p->npack; ++k) live[k] = true;
+  for (int k = 0; k < p->npack; ++k)
+    if (live[k] && (best_rounds < 0 || rounds[k] < best_rounds)) best_rounds = rounds[k];
+  double best_util = 0.0;
+  for (int k = 0; k < p->npack; ++k)
+    if (live[k] && rounds[k] == best_rounds) best_util = std::max(best_util, util[k]);
+  int pick = -1, tallest = -1;
+  for (int k = 0; k < p->npack; ++k) {
+    if (!live[k] || rounds[k] != best_rounds || util[k] < 0.95 * best_util) continue;
+    if (tallest < 0 || p->pk[k].RW > p->pk[tallest].RW) tallest = k;
+    if (per_chunk(p->pk[k]) >= 8.0 && (pick < 0 || p->pk[k].RW < p->pk[pick].RW)) pick = k;
+  }
+  return p->pk[pick >= 0 ? pick : tallest];
 }
 
 }  // namespace
@@ -561,6 +596,15 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
                        stream);
 }
 }  // namespace
+
+void launch_shape(const sdnn_plan_s* p, int32_t N, int32_t* panel_rows, int32_t* waves) {
+  const TunedShape* shape = nullptr;
+  for (int i = 0; i < p->ntuned; ++i)
+    if (p->tuned[i].N == N) shape = &p->tuned[i];
+  const DevPacking& pk = shape ? p->pk[shape->pack] : choose_packing(p, N, false);
+  *panel_rows = pk.RW;
+  *waves = shape ? shape->waves : choose_cfg(pk, p->num_cus, N).waves;
+}
 
 hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                        const float* bias, int epi, hipStream_t stream) {

@@ -6,6 +6,8 @@
  * the test writes from the seeded input generators, and the outputs go back to the
  * test, which checks them against the CPU oracle.
  *
+ *   sdnn_c_check -sizes
+ *     prints sizeof(sdnn_plan_opts) and sizeof(sdnn_plan_info_t) as compiled (no GPU)
  *   sdnn_c_check DIR M K N
  *     reads  DIR/row_ptr.i32 (M+1), DIR/col_idx.i32 (nnz), DIR/values.f32 (nnz),
  *            DIR/B.f32 (K*N), DIR/bias.f32 (M)
@@ -61,6 +63,10 @@ static int write_file(const char* dir, const char* name, const void* data, size_
   } while (0)
 
 int main(int argc, char** argv) {
+  if (argc == 2 && argv[1][0] == '-' && argv[1][1] == 's') {  /* -sizes: no device work */
+    printf("%zu %zu\n", sizeof(sdnn_plan_opts), sizeof(sdnn_plan_info_t));
+    return 0;
+  }
   if (argc != 5) {
     fprintf(stderr, "usage: %s DIR M K N\n", argv[0]);
     return 2;

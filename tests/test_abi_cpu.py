@@ -98,19 +98,24 @@ def test_packed_stream_self_check(name, panel_rows):
 
 
 @pytest.mark.parametrize("name", ["c2", "w0", "c3"])
-def test_default_plan_packs_short_and_tall_panels(name):
-    """With panel_rows = 0 the plan holds a 4-row and a 12-row packing of the same
-    permutation; both pass the stream self-check and tall panels share more columns."""
+def test_default_plan_packs_short_tall_and_mid_panels(name):
+    """With panel_rows = 0 the plan holds 4-, 12- and 8-row packings of the same
+    permutation; all pass the stream self-check and taller panels share more columns."""
     for L in inputs.workload(name, N=4).layers:
         info = sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K)
         assert info["panel_rows"] == 4 and info["tall_panel_rows"] == 12
+        assert info["mid_panel_rows"] == 8 and info["packings"] == 3
         assert info["panels"] == -(-L.W.M // 4)
-        assert info["tall_rho"] >= info["rho"] >= 1.0
-        assert 0.0 < info["tall_fill"] <= 1.0 and 0.0 < info["fill"] <= 1.0
-        one = sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K,
-                                 panel_rows=12)
-        assert one["tall_panel_rows"] == 0 and one["rho"] == info["tall_rho"]
-        assert info["packed_bytes"] > one["packed_bytes"]
+        assert info["tall_rho"] >= info["mid_rho"] >= info["rho"] >= 1.0
+        for f in ("fill", "tall_fill", "mid_fill"):
+            assert 0.0 < info[f] <= 1.0
+        singles = {rw: sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K,
+                                          panel_rows=rw) for rw in (4, 8, 12)}
+        for rw, one in singles.items():
+            assert one["tall_panel_rows"] == 0 and one["mid_panel_rows"] == 0
+            assert one["packings"] == 1
+        assert singles[12]["rho"] == info["tall_rho"] and singles[8]["rho"] == info["mid_rho"]
+        assert info["packed_bytes"] == sum(one["packed_bytes"] for one in singles.values())
 
 
 def test_in_perm_relabels_columns():

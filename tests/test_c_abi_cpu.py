@@ -26,3 +26,16 @@ def test_c_caller_compiles():
     cmd = runpy.run_path(os.path.join(ROOT, "tests", "c_abi", "build_check.py"))["command"]
     r = subprocess.run(cmd(syntax_only=True), capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
+
+
+def test_c_caller_agrees_on_struct_layouts():
+    """The built C caller (if present) was compiled with the struct sizes the binding
+    uses: a host-only query, no device work."""
+    import ctypes
+    import paper_2101_07948_amd as sd
+    exe = os.path.join(ROOT, "tests", "c_abi", "sdnn_c_check")
+    if not os.path.exists(exe):
+        pytest.skip("the C caller is built by __graft_entry__.build()")
+    r = subprocess.run([exe, "-sizes"], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.split() == [str(ctypes.sizeof(sd.PlanOpts)), str(ctypes.sizeof(sd.PlanInfo))]

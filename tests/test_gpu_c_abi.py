@@ -19,6 +19,14 @@ EXE = os.path.join(ROOT, "tests", "c_abi", "sdnn_c_check")
 
 def test_c_caller_matches_oracle(tmp_path):
     assert os.path.exists(EXE), f"{EXE} is missing: run __graft_entry__.build() first"
+    # a binary built against another sdnn.h would disagree with the library on struct
+    # layouts: compare the sizes it was compiled with (a host-only query) first
+    import ctypes
+    import paper_2101_07948_amd as sd
+    r = subprocess.run([EXE, "-sizes"], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.split() == [str(ctypes.sizeof(sd.PlanOpts)), str(ctypes.sizeof(sd.PlanInfo))], \
+        f"{EXE} was built against another sdnn.h: run __graft_entry__.build() again"
     M, K, N = 70, 333, 130
     W = inputs.pattern_uniform(M, K, 0.1, inputs.CFG_TEST, 8100, 0.05)
     B = inputs.dense_B(K, N, inputs.CFG_TEST, 8100)

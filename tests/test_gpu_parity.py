@@ -229,13 +229,18 @@ def test_row_permutation_equivariance_bitexact():
 
 
 def test_tall_panels_at_large_N():
-    """M * ceil(N / 256) = 768 * 32 reaches 96 rows per CU on 256 CUs, so the default
-    plan runs its 12-row packing: checked against the oracle, and bit-identical to a
-    4-row-only plan (every row sums its entries in ascending column order either way)."""
+    """768 rows over 32 column tiles: 4-row panels need two rounds of workgroups on 256
+    CUs, 8- and 12-row ones one, and 8-row panels already hold 25.6 entries per chunk at
+    10 %, so the default plan runs its 8-row packing (as sdnn_plan_launch_shape reports):
+    checked against the oracle, and bit-identical to a 4-row-only plan (every row sums its
+    entries in ascending column order either way)."""
     M, K, N = 768, 1024, 8192
     W = inputs.pattern_uniform(M, K, 0.1, inputs.CFG_TEST, 21, 0.05)
     B = inputs.dense_B(K, N, inputs.CFG_TEST, 21)
     bias = inputs.bias_normal(M, inputs.CFG_TEST, 21, 0.02)
+    with sd.Plan.from_csr(W) as plan:
+        if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+            assert plan.launch_shape(N)["panel_rows"] == 8
     got = check(W.row_ptr, W.col_idx, W.values, M, K, B, bias, "relu", label="tall")
     with sd.Plan.from_csr(W, panel_rows=4) as p4:
         assert p4.info["tall_panel_rows"] == 0
@@ -321,7 +326,8 @@ def test_plan_tune():
     with sd.Plan.from_csr(L.W) as plan:
         before = gpu_spmm(plan, w.B, L.bias, L.epi)
         shape = plan.tune(w.N)
-        assert shape["panel_rows"] in (4, 12) and 1 <= shape["waves"] <= 12
+        assert shape["panel_rows"] in (4, 8, 12) and 1 <= shape["waves"] <= 12
+        assert plan.launch_shape(w.N) == shape
         after = gpu_spmm(plan, w.B, L.bias, L.epi)
         assert np.array_equal(before, after)
         B2 = inputs.dense_B(L.W.K, 300, inputs.CFG_TEST, 61)
@@ -455,3 +461,22 @@ def test_dense_comparison_kernel(M, K, N):
     rp, ci, v = dense_to_csr(Wd)
     ref, bound = oracle.spmm_f64(rp, ci, v, K, B, bias, "gelu")
     assert np.all(np.abs(C.cpu().numpy() - ref) <= tolerance(bound, ref, "gelu"))
+
+
+def test_launch_shape_follows_density_and_grid():
+    """The default plan's packing per call (sdnn_plan_launch_shape) on 256 CUs: 4-row
+    panels when they fill the device at 10 % (W0 at N = 4096), 8-row ones when 4-row
+    panels need more rounds (W0 at N = 16384), 12-row ones at 97-98 % where shorter panels
+    hold too few entries per chunk (C5's layers)."""
+    if torch.cuda.get_device_properties(0).multi_processor_count != 256:
+        pytest.skip("the expected shapes are those of a 256-CU device")
+    w0 = inputs.workload("w0", N=4).layers[0].W
+    c5 = inputs.workload("c5", N=4, num_layers=1).layers
+    for W, N, want in ((w0, 4096, 4), (w0, 16384, 8), (c5[0].W, 16384, 12), (c5[5].W, 1024, 12),
+                       (inputs.s_layer(2048, 2048, 0.95).W, 4096, 8)):
+        with sd.Plan.from_csr(W) as plan:
+            got = plan.launch_shape(N)
+        assert got["panel_rows"] == want, (W.M, W.K, N, got)
+        assert 1 <= got["waves"] <= 12
+    with sd.Plan.from_csr(w0, panel_rows=16) as plan:
+        assert plan.launch_shape(4096)["panel_rows"] == 16
