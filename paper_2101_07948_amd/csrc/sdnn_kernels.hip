@@ -369,30 +369,20 @@ LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N, int nseg = 1) {
   return c;
 }
 
-// The packing a call runs on.
-// A product (a default plan holds 4-, 12- and 8-row packings): among the packings, the
-// 4-row one left out when its panels average fewer than 7 entries per 32-row chunk (a
-// group of 8 then spans more than a chunk, which starves the ring's lookahead) and
-// another exists, those needing the fewest rounds of workgroups at their full consumer
-// count; among those, the ones keeping the most CUs busy in those rounds (within 5 %);
-// among those, the shortest panels averaging at least 8 entries per chunk, else the
-// tallest.  (Measured on MI355X over M = K = 512-2048 at 80-98 % and N = 1024-16384 and
-// the C3 / C5 layers: within 10 % of the best packing on all but a few small cases.)
-// A convolution, whose workgroups are bound by staging its shifted input rows rather
-// than by their panels, and a K-split launch: the 4- or the 12-row packing, whichever
-// needs fewer rounds, the 4-row one on a tie.
-const DevPacking& choose_packing(const sdnn_plan_s* p, int N, bool conv, int nseg = 1) {
+// The packing a call runs on (a default plan holds 4-, 12- and 8-row packings): among
+// the packings, the 4-row one left out when its panels average fewer than 7 entries per
+// 32-row chunk (a group of 8 then spans more than a chunk, which starves the ring's
+// lookahead) and another exists, those needing the fewest rounds of workgroups over the
+// tiles (times the K-runs of a split launch) at their full consumer count; among those,
+// the ones keeping the most CUs busy in those rounds (within 5 %); among those, the
+// shortest panels averaging at least 8 entries per chunk, else the tallest.  Measured on
+// MI355X for products (M = K = 512-2048 at 80-98 %, N = 1024-16384, the W0 and C2-C5
+// layers) and for the 3x3 convolutions of the benchmark, whose staging differs but
+// follows the same trade.
+const DevPacking& choose_packing(const sdnn_plan_s* p, int N, int nseg = 1) {
   if (p->npack < 2) return p->pk[0];
-  const DevPacking& tall = p->pk[1];
-  const int64_t n_tiles = (N + kTileCols - 1) / kTileCols;
+  const int64_t n_tiles = (int64_t)((N + kTileCols - 1) / kTileCols) * nseg;
   const int cus = p->num_cus > 0 ? p->num_cus : 256;
-  if (conv || nseg > 1) {
-    const LaunchCfg s = choose_cfg(p->pk[0], cus, N, nseg), t = choose_cfg(tall, cus, N, nseg);
-    return rounds_of(n_tiles * nseg, tall.npanels, t.waves, cus) <
-                   rounds_of(n_tiles * nseg, p->pk[0].npanels, s.waves, cus)
-               ? tall
-               : p->pk[0];
-  }
   const double density = (double)p->nnz / ((double)p->M * (double)p->K);
   auto per_chunk = [&](const DevPacking& pk) { return pk.RW * kChunk * density; };
   int64_t rounds[3];
@@ -454,7 +444,7 @@ int choose_splits(const sdnn_plan_s* p, int N, bool conv) {
   for (int splits = 1; splits <= std::min(total_seg, kMaxAutoSplits); ++splits) {
     const int per = (total_seg + splits - 1) / splits;
     if ((total_seg + per - 1) / per != splits) continue;
-    const DevPacking& pk = choose_packing(p, N, conv, splits);
+    const DevPacking& pk = choose_packing(p, N, splits);
     const LaunchCfg cfg = choose_cfg(pk, cus, N, splits);
     const int64_t rounds = rounds_of(n_tiles * splits, pk.npanels, cfg.waves, cus);
     const int64_t chunks = std::min<int64_t>((int64_t)per * p->split_chunks, p->nchunks);
@@ -546,7 +536,7 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
     for (int i = 0; i < p->ntuned; ++i)
       if (p->tuned[i].N == N) shape = &p->tuned[i];
   const DevPacking& pk =
-      shape ? p->pk[shape->pack] : choose_packing(p, N, conv_hwn != nullptr, nk);
+      shape ? p->pk[shape->pack] : choose_packing(p, N, nk);
   LaunchCfg cfg = choose_cfg(pk, p->num_cus, N, nk);
   if (shape) {
     cfg.waves = shape->waves;
@@ -601,7 +591,7 @@ void launch_shape(const sdnn_plan_s* p, int32_t N, int32_t* panel_rows, int32_t*
   const TunedShape* shape = nullptr;
   for (int i = 0; i < p->ntuned; ++i)
     if (p->tuned[i].N == N) shape = &p->tuned[i];
-  const DevPacking& pk = shape ? p->pk[shape->pack] : choose_packing(p, N, false);
+  const DevPacking& pk = shape ? p->pk[shape->pack] : choose_packing(p, N);
   *panel_rows = pk.RW;
   *waves = shape ? shape->waves : choose_cfg(pk, p->num_cus, N).waves;
 }
