@@ -174,7 +174,9 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out);
 /* Execution stage (Sec. 3.2.2): C = act(W * B + bias), enqueued on `stream`.
  *   B:    device, K x N row-major fp32, read only.
  *   C:    device, M x N row-major fp32, written once, in the ORIGINAL row order.
- *   N:    columns of B and C, any N >= 0 (N = 0 or M = 0 is a no-op).
+ *   N:    columns of B and C, 0 <= N < 2^29 (N = 0 or M = 0 is a no-op); larger N gives
+ *         SDNN_ERR_DIM, since the kernels address a row of B or C with 32-bit byte
+ *         offsets.
  *   bias: device, M fp32 in original row order, or NULL (treated as zeros).
  *   With out_permuted plans, C row i is output row perm[i] (see sdnn_plan_opts); with
  *   in_perm plans, B's rows are in that order.
@@ -226,7 +228,7 @@ sdnn_status sdnn_plan_launch_shape(sdnn_plan p, int32_t N, int32_t* panel_rows, 
  * values are kept).  Blocking (synchronises `stream`).  Must not run concurrently with
  * any other call on the same plan.  Results of sdnn_spmm do not depend on the shape.
  * On success *panel_rows and *waves (either may be NULL) hold the chosen shape.
- * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM (N <= 0, M = 0, B overlapping C),
+ * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM (N <= 0, N >= 2^29, M = 0, B overlapping C),
  * SDNN_ERR_DEVICE, SDNN_ERR_HIP. */
 sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, void* stream,
                            int32_t* panel_rows, int32_t* waves);

@@ -951,7 +951,8 @@ static sdnn_status spmm_entry(sdnn_plan p, const float* B, float* C, int32_t N, 
                               sdnn_epilogue epi, int32_t splits, float* ws, int64_t ws_floats,
                               bool split, void* stream) {
   if (!p) return SDNN_ERR_NULL;
-  if (N < 0) return SDNN_ERR_DIM;
+  // the kernels address one row of B or C with 32-bit byte offsets
+  if (N < 0 || (int64_t)N * 4 >= kMaxRowBytes) return SDNN_ERR_DIM;
   if (epi != SDNN_EPI_NONE && epi != SDNN_EPI_RELU && epi != SDNN_EPI_GELU) return SDNN_ERR_DIM;
   if (split && (p->split_chunks <= 0 || splits < 0)) return SDNN_ERR_DIM;
   if (p->M == 0 || N == 0) return SDNN_OK;
@@ -1001,7 +1002,7 @@ sdnn_status sdnn_plan_launch_shape(sdnn_plan p, int32_t N, int32_t* panel_rows, 
 sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, void* stream,
                            int32_t* panel_rows, int32_t* waves) {
   if (!p) return SDNN_ERR_NULL;
-  if (N <= 0) return SDNN_ERR_DIM;
+  if (N <= 0 || (int64_t)N * 4 >= kMaxRowBytes) return SDNN_ERR_DIM;
   if (p->M == 0) return SDNN_ERR_DIM;
   if (!C || (p->K > 0 && !B)) return SDNN_ERR_NULL;
   const int64_t bbytes = (int64_t)p->K * N * 4, cbytes = (int64_t)p->M * N * 4;
@@ -1032,7 +1033,7 @@ static sdnn_status conv_entry(sdnn_plan p, const float* X, float* C, int32_t H, 
   const int64_t N = (int64_t)H * W * NB;
   if (p->M == 0 || N == 0) return SDNN_OK;
   // 32-bit column and channel-plane byte offsets in the staging loop
-  if (N * 4 >= ((int64_t)1 << 31) || (int64_t)(p->K / 9) * N * 4 >= ((int64_t)1 << 40))
+  if (N * 4 >= kMaxRowBytes || (int64_t)(p->K / 9) * N * 4 >= ((int64_t)1 << 40))
     return SDNN_ERR_DIM;
   if (!X || !C) return SDNN_ERR_NULL;
   if ((((uintptr_t)X | (uintptr_t)C) & 15) != 0) return SDNN_ERR_DIM;

@@ -34,6 +34,9 @@ constexpr int kLoShift = 17;        // a_{L-1} >> 17: lowest chunk the group rea
 constexpr int kHiShift = 18;        // a_L >> 18: highest chunk the group reads
 constexpr int kLoWord = kGroup - 2, kHiWord = kGroup - 1;
 constexpr int kMaxChunks = 1 << 14; // chunk numbers must fit a3's high bits
+// A row of B or C must stay below 2^31 bytes (N < 2^29): the staging and the stores
+// address within a row with 32-bit byte offsets.
+constexpr int64_t kMaxRowBytes = (int64_t)1 << 31;
 static_assert(kRing * kChunk <= 128, "ring rows must fit 7 bits");
 
 // Host-side packed form of W in the kernel's traversal order (Sec. 3.2.2: each

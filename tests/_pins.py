@@ -133,6 +133,51 @@ def check_invariants(lib=None):
     return fails
 
 
+def check_bias_linearity(lib=None):
+    """With no activation the bias enters linearly and per output row:
+    C(b) - C(0) = b broadcast along N, and C(b1 + b2) - C(0) = (C(b1) - C(0)) + (C(b2) - C(0)),
+    both to double rounding."""
+    fails = []
+    rng = np.random.default_rng(17)
+    for trial in range(6):
+        M, K, N = 19, 27, 11
+        row_ptr, col_idx, vals, _ = random_csr(rng, M, K, 0.3)
+        B = rng.standard_normal((K, N)).astype(np.float32)
+        b1 = rng.standard_normal(M).astype(np.float32)
+        b2 = rng.standard_normal(M).astype(np.float32)
+        C0, _ = oracle.spmm_f64(row_ptr, col_idx, vals, K, B, None, "none", lib=lib)
+        C1, _ = oracle.spmm_f64(row_ptr, col_idx, vals, K, B, b1, "none", lib=lib)
+        C2, _ = oracle.spmm_f64(row_ptr, col_idx, vals, K, B, b2, "none", lib=lib)
+        C12, _ = oracle.spmm_f64(row_ptr, col_idx, vals, K, B, b1 + b2, "none", lib=lib)
+        scale = np.abs(C0) + np.abs(b1)[:, None] + np.abs(b2)[:, None] + 1.0
+        if not np.all(np.abs((C1 - C0) - b1.astype(np.float64)[:, None]) <= 1e-13 * scale):
+            fails.append("C(b) - C(0) != b (bias not added once per row)")
+        want = (C1 - C0) + (C2 - C0)
+        got = C12 - C0
+        # b1 + b2 is formed in float32 above: compare against that rounded sum
+        exact = (b1 + b2).astype(np.float64)[:, None]
+        if not np.all(np.abs(got - exact) <= 1e-13 * scale) or \
+                not np.all(np.abs(want - (b1.astype(np.float64) + b2.astype(np.float64))[:, None])
+                           <= 1e-13 * scale):
+            fails.append("bias is not linear")
+    return fails
+
+
+def check_gelu_odd_part(lib=None):
+    """GELU(x) - GELU(-x) = x * (Phi(x) + Phi(-x)) = x: an identity of the exact erf form
+    that holds at every x, checked on a grid through a one-entry product (w = 1)."""
+    fails = []
+    rp, ci, v = dense_to_csr(np.ones((1, 1), np.float32))
+    xs = np.linspace(-6.0, 6.0, 97).astype(np.float32)
+    for x in xs:
+        Cp, _ = oracle.spmm_f64(rp, ci, v, 1, np.array([[x]], np.float32), None, "gelu", lib=lib)
+        Cm, _ = oracle.spmm_f64(rp, ci, v, 1, np.array([[-x]], np.float32), None, "gelu", lib=lib)
+        if abs((Cp[0, 0] - Cm[0, 0]) - float(x)) > 1e-14 * max(1.0, abs(float(x))):
+            fails.append(f"GELU({x}) - GELU({-x}) = {Cp[0, 0] - Cm[0, 0]!r}, not {float(x)!r}")
+            break
+    return fails
+
+
 def _reorder_properties(row_ptr, col_idx, K, perm):
     """Tie-break-free properties of Algorithm 1: bijection, first = a densest row,
     every later pick attains the maximum overlap with its predecessor."""
@@ -283,8 +328,8 @@ def check_conv(lib=None):
     return fails
 
 
-ALL_CHECKS = [check_bruteforce, check_special_cases, check_gelu_table, check_invariants,
-              check_reorder, check_conv]
+ALL_CHECKS = [check_bruteforce, check_special_cases, check_gelu_table, check_gelu_odd_part,
+              check_invariants, check_bias_linearity, check_reorder, check_conv]
 
 
 def run_all(lib=None):

@@ -13,10 +13,18 @@ def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
 
 
-def tol_fp32(bound):
+# GELU's derivative x*phi(x) + Phi(x) peaks at 1.1289 (x = sqrt(2)): an input error e
+# moves GELU by at most 1.13 e.
+GELU_LIPSCHITZ = 1.13
+
+
+def tol_fp32(bound, epi="none"):
     """Parity tolerance for an fp32 result against the double-precision reference:
-    |err| <= 1e-5 * sum_p |w_p| |B[c_p, n]| + 1e-6, per element."""
-    return 1e-5 * bound + 1e-6
+    |err| <= 1e-5 * sum_p |w_p| |B[c_p, n]| + 1e-6, per element; after GELU the same
+    bound times GELU's Lipschitz constant (the activation's own float rounding, a few ulp
+    of |C|, stays far inside the 1e-6 floor for the |C| <= ~10 these workloads reach)."""
+    tol = 1e-5 * bound + 1e-6
+    return tol * GELU_LIPSCHITZ if epi == "gelu" else tol
 
 
 def random_csr(rng, M, K, density):

@@ -43,6 +43,15 @@ MUTANTS = [
      "if (yy < 0 || yy >= H || xx < 0 || xx >= W) { yy = yy < 0 ? 0 : (yy >= H ? H - 1 : yy); xx = xx < 0 ? 0 : (xx >= W ? W - 1 : xx); }"),
     ("conv_bias_dropped", "C_out[at] = act_f64(acc + bo, epi);", "C_out[at] = act_f64(acc, epi);"),
     ("conv_first_image", "X[i * plane + ((size_t)yy * W + xx) * NB + b]", "X[i * plane + ((size_t)yy * W + xx) * NB]"),
+    # mistakes each of which a named pin must reject on its own
+    ("bias_halved", "const double bi = bias ? (double)bias[i] : 0.0;",
+     "const double bi = bias ? 0.5 * (double)bias[i] : 0.0;", "check_bias_linearity"),
+    ("bias_squared", "const double bi = bias ? (double)bias[i] : 0.0;",
+     "const double bi = bias ? (double)bias[i] * fabs((double)bias[i]) : 0.0;", "check_bias_linearity"),
+    ("gelu_even_erf", "return 0.5 * x * (1.0 + erf(x / sqrt(2.0)));",
+     "return 0.5 * x * (1.0 + erf(fabs(x) / sqrt(2.0)));", "check_gelu_odd_part"),
+    ("gelu_cdf_not_one", "return 0.5 * x * (1.0 + erf(x / sqrt(2.0)));",
+     "return 0.5 * x * (1.000001 + erf(x / sqrt(2.0)));", "check_gelu_odd_part"),
 ]
 
 
@@ -53,8 +62,9 @@ def workdir():
     shutil.rmtree(d, ignore_errors=True)
 
 
-@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_pins_reject_mutant(workdir, name, old, new):
+@pytest.mark.parametrize("mutant", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_reject_mutant(workdir, mutant):
+    name, old, new = mutant[:3]
     src = open(SRC).read()
     assert src.count(old) == 1, f"mutation anchor for {name} not unique"
     path = os.path.join(workdir, f"{name}.c")
@@ -65,3 +75,5 @@ def test_pins_reject_mutant(workdir, name, old, new):
     lib = oracle.load(so)
     fails = _pins.run_all(lib)
     assert fails, f"no pin rejects the planted mistake {name}"
+    if len(mutant) > 3:  # this pin alone must see the mistake
+        assert getattr(_pins, mutant[3])(lib), f"{mutant[3]} does not reject {name}"
