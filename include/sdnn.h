@@ -213,6 +213,25 @@ sdnn_status sdnn_spmm_split(sdnn_plan p, const float* B, float* C, int32_t N, co
                             sdnn_epilogue epi, int32_t splits, float* workspace,
                             int64_t workspace_floats, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): sdnn_spmm_split with the partial
+ * products kept in a fixed scratch array that the library holds on every device it runs
+ * on (16 Mi floats = 64 MiB per device, reserved when the library is loaded and held
+ * until the process ends), so the call itself allocates nothing.  Same arguments,
+ * result contract, run counts and kernels as sdnn_spmm_split without the workspace.
+ *   Limit: R runs need R * M * N floats of scratch; beyond 16 Mi floats the call returns
+ *   SDNN_ERR_DIM (use sdnn_spmm_split with a caller workspace instead).  With R = 1 it
+ *   is sdnn_spmm and touches no scratch.
+ * Every call on one device shares that device's scratch array: two such calls that
+ * overlap in time on one device (different streams, or different host threads without
+ * ordering) race and give unspecified results; calls ordered on one stream are safe.
+ * The first call on a device looks the array's address up (no allocation); a caller
+ * about to capture a graph should make one call on that device before capturing.
+ * Errors: as sdnn_spmm_split, with SDNN_ERR_DIM for a scratch need above the limit. */
+sdnn_status sdnn_spmm_split_noalloc(sdnn_plan p, const float* B, float* C, int32_t N,
+                                    const float* bias, sdnn_epilogue epi, int32_t splits,
+                                    void* stream);
+
 /* The launch shape sdnn_spmm uses for this plan at N columns (the tuned one if
  * sdnn_plan_tune recorded one for N, else the rule described under panel_rows):
  * *panel_rows = the packing's panel height, *waves = consumer waves per workgroup

@@ -83,11 +83,12 @@ def lib() -> ctypes.CDLL:
         L.sdnn_plan_launch_shape.argtypes = [p, i32, p, p]
         i64 = ctypes.c_int64
         L.sdnn_spmm_split.argtypes = [p, p, p, i32, p, ctypes.c_int, i32, p, i64, p]
+        L.sdnn_spmm_split_noalloc.argtypes = [p, p, p, i32, p, ctypes.c_int, i32, p]
         L.sdnn_conv3x3_split.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, i32, p, i64, p]
         for fn in ("sdnn_reorder_rows", "sdnn_row_order", "sdnn_plan_check_host", "sdnn_plan_create",
                    "sdnn_plan_get_perm", "sdnn_plan_info", "sdnn_spmm", "sdnn_dense_gemm",
                    "sdnn_conv3x3", "sdnn_plan_tune", "sdnn_spmm_split", "sdnn_conv3x3_split",
-                   "sdnn_plan_launch_shape"):
+                   "sdnn_plan_launch_shape", "sdnn_spmm_split_noalloc"):
             getattr(L, fn).restype = ctypes.c_int
         _lib_handle = L
     return _lib_handle
@@ -327,6 +328,18 @@ class Plan:
         pw, nw = self._workspace(workspace, N, stream)
         _check(self._lib.sdnn_spmm_split(self.handle, pb, pc, N, pbias, EPI[epi], int(splits),
                                          pw, nw, _stream_handle(stream)), "sdnn_spmm_split")
+        return C
+
+    def spmm_split_noalloc(self, B, C, bias=None, epi: str = "none", splits: int = 0, stream=None):
+        """spmm_split with the partial products in the library's fixed per-device scratch
+        (sdnn_spmm_split_noalloc): no workspace, no allocation."""
+        N = int(B.shape[1]) if B is not None and B.dim() == 2 else int(C.shape[1])
+        pb = _dev_ptr(B, "B", (self.K, N))
+        pc = _dev_ptr(C, "C", (self.M, N))
+        pbias = _dev_ptr(bias, "bias", (self.M,), allow_none=True)
+        _check(self._lib.sdnn_spmm_split_noalloc(self.handle, pb, pc, N, pbias, EPI[epi],
+                                                 int(splits), _stream_handle(stream)),
+               "sdnn_spmm_split_noalloc")
         return C
 
     def conv3x3_split(self, X, C, bias=None, epi: str = "none", workspace=None, splits: int = 0,

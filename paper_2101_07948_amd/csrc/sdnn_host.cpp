@@ -947,9 +947,11 @@ static sdnn_status check_workspace(const sdnn_plan_s* p, int64_t N, const float*
   return SDNN_OK;
 }
 
+// noalloc: a K-split call whose partial products go to the library's fixed scratch array
+// (ws must then be NULL).
 static sdnn_status spmm_entry(sdnn_plan p, const float* B, float* C, int32_t N, const float* bias,
                               sdnn_epilogue epi, int32_t splits, float* ws, int64_t ws_floats,
-                              bool split, void* stream) {
+                              bool split, void* stream, bool noalloc = false) {
   if (!p) return SDNN_ERR_NULL;
   // the kernels address one row of B or C with 32-bit byte offsets
   if (N < 0 || (int64_t)N * 4 >= kMaxRowBytes) return SDNN_ERR_DIM;
@@ -961,13 +963,20 @@ static sdnn_status spmm_entry(sdnn_plan p, const float* B, float* C, int32_t N, 
   const int64_t bbytes = (int64_t)p->K * N * 4, cbytes = (int64_t)p->M * N * 4;
   if (ranges_overlap(B, bbytes, C, cbytes)) return SDNN_ERR_DIM;
   if (ranges_overlap(bias, (int64_t)p->M * 4, C, cbytes)) return SDNN_ERR_DIM;
-  if (split) {
+  if (split && !noalloc) {
     const sdnn_status st = check_workspace(p, N, ws, ws_floats, B, bbytes, C, bias);
     if (st != SDNN_OK) return st;
   }
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess) return SDNN_ERR_HIP;
   if (cur != p->device) return SDNN_ERR_DEVICE;
+  if (noalloc) {
+    const int64_t runs = split_runs(p, N, splits);
+    if (runs > 1) {
+      if (runs * p->M * (int64_t)N > kScratchFloats) return SDNN_ERR_DIM;
+      if (scratch_address(cur, &ws) != hipSuccess) return SDNN_ERR_HIP;
+    }
+  }
   try {
     hipError_t e = split ? launch_spmm_split(p, B, C, N, bias, (int)epi, splits, ws,
                                              (hipStream_t)stream)
@@ -987,6 +996,12 @@ sdnn_status sdnn_spmm_split(sdnn_plan p, const float* B, float* C, int32_t N, co
                             sdnn_epilogue epi, int32_t splits, float* workspace,
                             int64_t workspace_floats, void* stream) {
   return spmm_entry(p, B, C, N, bias, epi, splits, workspace, workspace_floats, true, stream);
+}
+
+sdnn_status sdnn_spmm_split_noalloc(sdnn_plan p, const float* B, float* C, int32_t N,
+                                    const float* bias, sdnn_epilogue epi, int32_t splits,
+                                    void* stream) {
+  return spmm_entry(p, B, C, N, bias, epi, splits, nullptr, 0, true, stream, true);
 }
 
 sdnn_status sdnn_plan_launch_shape(sdnn_plan p, int32_t N, int32_t* panel_rows, int32_t* waves) {

@@ -150,6 +150,15 @@ hipError_t launch_spmm_split(const sdnn_plan_s* p, const float* B, float* C, int
 hipError_t launch_conv3x3_split(const sdnn_plan_s* p, const float* X, float* C, int32_t H,
                                 int32_t W, int32_t NB, const float* bias, int epi, int splits,
                                 float* ws, hipStream_t stream);
+// Workgroups along K that launch_spmm_split runs for `splits` (0: the library's
+// choice) at N; 1 for a plan without K-segments (host only).
+int split_runs(const sdnn_plan_s* p, int32_t N, int32_t splits);
+// The non-allocating K-split call keeps its partial products in a fixed device array of
+// kScratchFloats floats per device; scratch_address gives its address on `device`,
+// which must be the current device (looked up once per device, then cached).
+constexpr int64_t kScratchFloats = (int64_t)16 << 20;  // 64 MiB
+constexpr int kMaxScratchDevices = 64;
+hipError_t scratch_address(int device, float** out);
 // The packing height and consumer waves launch_spmm uses at N (host only).
 void launch_shape(const sdnn_plan_s* p, int32_t N, int32_t* panel_rows, int32_t* waves);
 // Times every candidate launch shape of the plan at N on the given buffers (blocking)

@@ -36,6 +36,7 @@
 #include <stdlib.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "sdnn_internal.h"
@@ -520,18 +521,23 @@ hipError_t launch_reduce(const float* ws, float* C, const float* bias, const int
 // with K-segments): `splits` workgroups along K (0: choose_splits), so every (tile, run
 // of segments, row-block) is a workgroup that writes its partial product to ws, and a
 // reduction kernel forms C.
+// Workgroups along K of a K-split launch (each taking a run of *seg_per_split
+// consecutive segments) for a requested count (0: choose_splits).
+int split_runs_of(const sdnn_plan_s* p, int32_t N, int splits, bool conv, int* seg_per_split) {
+  const int total_seg = p->pk[0].nseg;
+  if (splits <= 0) splits = choose_splits(p, N, conv);
+  splits = std::min(std::max(splits, 1), total_seg);
+  const int per = (total_seg + splits - 1) / splits;
+  if (seg_per_split) *seg_per_split = per;
+  return (total_seg + per - 1) / per;
+}
+
 hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                          const float* bias, int epi, const int32_t* conv_hwn,
                          const TunedShape* shape, float* ws, int splits, hipStream_t stream) {
   // nk: workgroups along K, each taking a run of seg_per_split consecutive segments
   int seg_per_split = 1, nk = 1;
-  if (ws) {
-    const int total_seg = p->pk[0].nseg;
-    if (splits <= 0) splits = choose_splits(p, N, conv_hwn != nullptr);
-    splits = std::min(std::max(splits, 1), total_seg);
-    seg_per_split = (total_seg + splits - 1) / splits;
-    nk = (total_seg + seg_per_split - 1) / seg_per_split;
-  }
+  if (ws) nk = split_runs_of(p, N, splits, conv_hwn != nullptr, &seg_per_split);
   if (!shape && !conv_hwn && nk == 1)
     for (int i = 0; i < p->ntuned; ++i)
       if (p->tuned[i].N == N) shape = &p->tuned[i];
@@ -656,6 +662,36 @@ hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStr
     if (p->tuned[i].N == N) slot = i;
   if (slot < 0) slot = p->ntuned < kTunedSlots ? p->ntuned++ : (int)(N % kTunedSlots);
   p->tuned[slot] = *chosen;
+  return hipSuccess;
+}
+
+int split_runs(const sdnn_plan_s* p, int32_t N, int32_t splits) {
+  return p->split_chunks > 0 ? split_runs_of(p, N, splits, false, nullptr) : 1;
+}
+
+// Partial products of the non-allocating K-split call (sdnn_spmm_split_noalloc): a
+// file-scope device array, so each GPU the library runs on holds its own copy at its own
+// address until the process ends.  In host code `scratch` names a host-side stand-in,
+// never the device memory: host code uses only the address hipGetSymbolAddress returns
+// for the current device, kept per device below.
+static __device__ __align__(256) float scratch[kScratchFloats];
+
+namespace {
+std::mutex g_scratch_mu;
+float* g_scratch_at[kMaxScratchDevices] = {};
+}  // namespace
+
+hipError_t scratch_address(int device, float** out) {
+  if (device < 0 || device >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_at[device]) {
+    void* at = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&at, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!at) return hipErrorInvalidSymbol;
+    g_scratch_at[device] = static_cast<float*>(at);
+  }
+  *out = g_scratch_at[device];
   return hipSuccess;
 }
 
