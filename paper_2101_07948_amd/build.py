@@ -45,5 +45,31 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+HOST_SANITIZED_SOURCES = [os.path.join(HERE, "csrc", "sdnn_host.cpp"),
+                          os.path.join(HERE, "csrc", "sdnn_launch_stubs.cpp")]
+
+
+def build_host_sanitized(out: str) -> str:
+    """The host code alone (CSR validation, row orders, packing and its self-check, the
+    C ABI's argument checks) built for the CPU under AddressSanitizer and
+    UndefinedBehaviorSanitizer, with the kernel launchers replaced by stubs that fail
+    (sdnn_launch_stubs.cpp).  It serves the host-only entry points; load it in a process
+    started with the sanitizer runtime preloaded (tests/test_host_sanitized.py)."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fPIC", "-shared", "-fno-omit-frame-pointer",
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           "-D__HIP_PLATFORM_AMD__", "-I" + os.path.join(rocm, "include"), "-o", out]
+    cmd += HOST_SANITIZED_SOURCES
+    cmd += ["-L" + os.path.join(rocm, "lib"), "-lamdhip64", "-Wl,-rpath," + os.path.join(rocm, "lib")]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError("g++ failed building the sanitizer build of the host code")
+    return out
+
+
 if __name__ == "__main__":
-    print(build(verbose=True))
+    if "--host-sanitized" in sys.argv:
+        print(build_host_sanitized(os.path.join(HERE, "libsdnn_host_asan.so")))
+    else:
+        print(build(verbose=True))
