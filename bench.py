@@ -699,7 +699,22 @@ def main():
         torch.cuda.synchronize()
         dms = e0.elapsed_time(e1) / reps
         dense = {"ms": round(dms, 4), "tflops": round(2.0 * M * K * N / (dms * 1e-3) / 1e12, 2),
+                 "frac_of_fp32_peak": round(2.0 * M * K * N / (dms * 1e-3) / 1e12 / ALU_PEAK_TFLOPS, 4),
                  "sparse_speedup": round(dms / ms, 2)}
+        # the vendor BLAS on the same dense product (torch.mm in FP32, TF32 off): context
+        # next to the library's own dense kernel, not the comparison the target names
+        torch.backends.cuda.matmul.allow_tf32 = False
+        torch.mm(Wd, Bs[0], out=Cd)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            torch.mm(Wd, Bs[0], out=Cd)
+        e1.record()
+        torch.cuda.synchronize()
+        bms = e0.elapsed_time(e1) / reps
+        dense["vendor_blas"] = {"ms": round(bms, 4),
+                                "tflops": round(2.0 * M * K * N / (bms * 1e-3) / 1e12, 2),
+                                "sparse_speedup": round(bms / ms, 2)}
         del Wd, Cd
 
     cpu = None

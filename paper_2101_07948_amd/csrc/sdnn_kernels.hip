@@ -709,66 +709,215 @@ hipError_t launch_conv3x3_split(const sdnn_plan_s* p, const float* X, float* C, 
 }
 
 // ---------------------------------------------------------------------------------
-// Dense FP32 comparison GEMM: C = act(W B + bias), W M x K, B K x N, row-major.
-// 64 x 64 output tile per 256-thread workgroup, 4 x 4 per thread, K tiled by 16
-// through LDS.  A measurement aid only.
+// Dense FP32 comparison GEMM: C = act(W B + bias), W M x K, B K x N, row-major.  A
+// measurement aid in the role of the paper's dense comparators (Sec. 3.2.1: outer-product
+// microkernel, register blocking, cache tiling), written for the FP32 matrix cores:
+//   * workgroup tile BM x 128 of C (BM = 64, 96 or 128), 8 waves (two per SIMD), each
+//     owning a BM x 16 column strip as BM/16 tiles of v_mfma_f32_16x16x4_f32 (a 16 x 16
+//     accumulator tile in 4 VGPRs per lane; one 16 x 4 slice of W times one 4 x 16 slice
+//     of B per issue), so each B slice a wave reads serves BM/16 products;
+//   * K is walked in stages of 32 through double-buffered LDS: the next stage's W and B
+//     tiles are loaded into registers while the current one is multiplied;
+//   * W's stage is stored as [k % 4][m][k / 4] so that a lane's eight values of its row
+//     over the stage's eight MFMA steps are 32 contiguous bytes (two ds_read_b128), and
+//     B's as [k][n] so that a lane's value of each step is one conflict-free ds_read_b32;
+//   * the same fused bias + activation epilogue and a single store of C.
+// Operand layouts of v_mfma_f32_16x16x4_f32 (lane l): A[i = l % 16][k = l / 16],
+// B[k = l / 16][j = l % 16]; accumulator register r holds D[4 (l / 16) + r][l % 16].
 namespace {
-constexpr int DT = 64, DK = 16;
+constexpr int kDenseBK = 32, kDenseWaves = 8;
+constexpr int kDenseThreads = 64 * kDenseWaves;
+typedef float float4_t __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(256) void dense_gemm_kernel(const float* __restrict__ W,
-                                                         const float* __restrict__ B,
-                                                         float* __restrict__ C, int M, int K,
-                                                         int N, const float* __restrict__ bias,
-                                                         int epi) {
-  __shared__ float As[DK][DT + 4];
-  __shared__ float Bs[DK][DT + 4];
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  const int m0 = blockIdx.y * DT, n0 = blockIdx.x * DT;
-  float acc[4][4] = {};
-  for (int k0 = 0; k0 < K; k0 += DK) {
-    for (int i = threadIdx.x; i < DT * DK; i += 256) {
-      const int mm = i / DK, kk = i % DK;
-      const int gm = m0 + mm, gk = k0 + kk;
-      As[kk][mm] = (gm < M && gk < K) ? W[(size_t)gm * K + gk] : 0.0f;
-      const int kb = i / DT, nn = i % DT;
-      const int gkb = k0 + kb, gn = n0 + nn;
-      Bs[kb][nn] = (gkb < K && gn < N) ? B[(size_t)gkb * N + gn] : 0.0f;
+template <int BM, int BN>
+__global__ __launch_bounds__(kDenseThreads) void dense_gemm_kernel(
+    const float* __restrict__ W, const float* __restrict__ B, float* __restrict__ C, int M, int K,
+    int N, const float* __restrict__ bias, int epi) {
+  constexpr int WC = BN / 16, WR = kDenseWaves / WC;  // waves along N and along M
+  constexpr int TM = BM / (16 * WR);          // 16-row MFMA tiles per wave
+  static_assert(WC * WR == kDenseWaves && TM * 16 * WR == BM, "tile shape");
+  constexpr int S = kDenseBK / 4;             // MFMA steps (4 k each) per stage
+  constexpr int A_F4 = BM * kDenseBK / 4;     // float4 loads of one W stage
+  constexpr int B_F4 = kDenseBK * BN / 4;
+  constexpr int A_PER = (A_F4 + kDenseThreads - 1) / kDenseThreads;
+  constexpr int B_PER = (B_F4 + kDenseThreads - 1) / kDenseThreads;
+  // rows padded so that the four k-groups of lanes (l / 16) read distinct LDS banks
+  __shared__ __attribute__((aligned(16))) float As[2][4][BM + 2][S];
+  __shared__ __attribute__((aligned(16))) float Bs[2][kDenseBK][BN + 16];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wc = wave % WC, wr = wave / WC;   // this wave's 16-column strip and row band
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int li = lane & 15, lk = lane >> 4;
+
+  float4 ra[A_PER], rb[B_PER];
+  // interior tiles (every row, column and k of the stage in range, rows 16-byte aligned)
+  // take unconditional float4 loads; edge tiles check each element
+  const bool rows_in = m0 + BM <= M && n0 + BN <= N && (K & 3) == 0 && (N & 3) == 0 &&
+                       (((uintptr_t)W | (uintptr_t)B) & 15) == 0;
+  auto load_stage = [&](int k0) {
+    if (rows_in && k0 + kDenseBK <= K) {
+#pragma unroll
+      for (int t = 0; t < A_PER; ++t) {
+        const int idx = tid + kDenseThreads * t;
+        const int m = idx / (kDenseBK / 4), q = idx % (kDenseBK / 4);
+        if (A_F4 % kDenseThreads == 0 || idx < A_F4)
+          ra[t] = *reinterpret_cast<const float4*>(W + (size_t)(m0 + m) * K + k0 + 4 * q);
+      }
+#pragma unroll
+      for (int t = 0; t < B_PER; ++t) {
+        const int idx = tid + kDenseThreads * t;
+        const int kr = idx / (BN / 4), c = idx % (BN / 4);
+        if (B_F4 % kDenseThreads == 0 || idx < B_F4)
+          rb[t] = *reinterpret_cast<const float4*>(B + (size_t)(k0 + kr) * N + n0 + 4 * c);
+      }
+      return;
     }
-    __syncthreads();
 #pragma unroll
-    for (int kk = 0; kk < DK; ++kk) {
-      float a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    for (int t = 0; t < A_PER; ++t) {
+      const int idx = tid + kDenseThreads * t;
+      const int m = idx / (kDenseBK / 4), q = idx % (kDenseBK / 4);
+      const int gm = m0 + m, gk = k0 + 4 * q;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (idx < A_F4 && gm < M) {
+        const float* src = W + (size_t)gm * K + gk;
+        if (gk + 0 < K) v.x = src[0];
+        if (gk + 1 < K) v.y = src[1];
+        if (gk + 2 < K) v.z = src[2];
+        if (gk + 3 < K) v.w = src[3];
+      }
+      ra[t] = v;
     }
+#pragma unroll
+    for (int t = 0; t < B_PER; ++t) {
+      const int idx = tid + kDenseThreads * t;
+      const int kr = idx / (BN / 4), c = idx % (BN / 4);
+      const int gk = k0 + kr, gn = n0 + 4 * c;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (idx < B_F4 && gk < K) {
+        const float* src = B + (size_t)gk * N + gn;
+        if (gn + 0 < N) v.x = src[0];
+        if (gn + 1 < N) v.y = src[1];
+        if (gn + 2 < N) v.z = src[2];
+        if (gn + 3 < N) v.w = src[3];
+      }
+      rb[t] = v;
+    }
+  };
+  auto store_stage = [&](int buf) {
+#pragma unroll
+    for (int t = 0; t < A_PER; ++t) {
+      const int idx = tid + kDenseThreads * t;
+      if (idx < A_F4) {
+        // k = 4q + c goes to (k % 4, k / 4) = (c, q)
+        const int m = idx / (kDenseBK / 4), q = idx % (kDenseBK / 4);
+        As[buf][0][m][q] = ra[t].x;
+        As[buf][1][m][q] = ra[t].y;
+        As[buf][2][m][q] = ra[t].z;
+        As[buf][3][m][q] = ra[t].w;
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < B_PER; ++t) {
+      const int idx = tid + kDenseThreads * t;
+      if (idx < B_F4) {
+        const int kr = idx / (BN / 4), c = idx % (BN / 4);
+        *reinterpret_cast<float4*>(&Bs[buf][kr][4 * c]) = rb[t];
+      }
+    }
+  };
+
+  float4_t acc[TM];
+#pragma unroll
+  for (int t = 0; t < TM; ++t) acc[t] = float4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int nstages = (K + kDenseBK - 1) / kDenseBK;
+  if (nstages > 0) {
+    load_stage(0);
+    store_stage(0);
+  }
+  __syncthreads();
+  for (int st = 0; st < nstages; ++st) {
+    const int buf = st & 1;
+    if (st + 1 < nstages) load_stage((st + 1) * kDenseBK);
+    // this wave's B column (wave * 16 + li) at k = 4 s + lk, and each tile's W row
+    float fb[S];
+#pragma unroll
+    for (int s2 = 0; s2 < S; ++s2) fb[s2] = Bs[buf][4 * s2 + lk][wc * 16 + li];
+    float fa[TM][S];
+#pragma unroll
+    for (int t = 0; t < TM; ++t)
+#pragma unroll
+      for (int q = 0; q < S / 4; ++q) {
+        const float4 v =
+            *reinterpret_cast<const float4*>(&As[buf][lk][(wr * TM + t) * 16 + li][4 * q]);
+        fa[t][4 * q] = v.x;
+        fa[t][4 * q + 1] = v.y;
+        fa[t][4 * q + 2] = v.z;
+        fa[t][4 * q + 3] = v.w;
+      }
+#pragma unroll
+    for (int s2 = 0; s2 < S; ++s2)
+#pragma unroll
+      for (int t = 0; t < TM; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[t][s2], fb[s2], acc[t], 0, 0, 0);
+    if (st + 1 < nstages) store_stage(buf ^ 1);
     __syncthreads();
   }
+
+  const int j = n0 + wc * 16 + li;
+  if (j >= N) return;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int gm = m0 + ty * 4 + i;
-    if (gm >= M) continue;
-    const float bb = bias ? bias[gm] : 0.0f;
+  for (int t = 0; t < TM; ++t) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int gn = n0 + tx * 4 + j;
-      if (gn < N) C[(size_t)gm * N + gn] = activation(acc[i][j] + bb, epi);
+    for (int r = 0; r < 4; ++r) {
+      const int i = m0 + (wr * TM + t) * 16 + 4 * lk + r;
+      if (i < M) C[(size_t)i * N + j] = activation(acc[t][r] + (bias ? bias[i] : 0.0f), epi);
     }
   }
 }
+
+template <int BM, int BN>
+hipError_t launch_dense_tile(const float* W, const float* B, float* C, int32_t M, int32_t K,
+                             int32_t N, const float* bias, int epi, hipStream_t stream) {
+  const dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
+  if (grid.y > 65535) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((dense_gemm_kernel<BM, BN>), grid, dim3(kDenseThreads), 0, stream, W, B, C, M,
+                     K, N, bias, epi);
+  return hipGetLastError();
+}
 }  // namespace
 
+// The workgroup tile: the one that minimises rounds of workgroups on the CUs times the
+// work of one workgroup; among equals, first one that gives every CU at least two
+// workgroups (the second hides the first one's load and barrier latency), then the
+// largest tile (less operand traffic per product).
 hipError_t launch_dense(const float* W, const float* B, float* C, int32_t M, int32_t K, int32_t N,
                         const float* bias, int epi, hipStream_t stream) {
-  dim3 grid((N + DT - 1) / DT, (M + DT - 1) / DT);
-  if (grid.y > 65535) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(dense_gemm_kernel, grid, dim3(256), 0, stream, W, B, C, M, K, N, bias, epi);
-  return hipGetLastError();
+  int cus = 256, dev = 0;
+  if (hipGetDevice(&dev) == hipSuccess)
+    (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  struct Tile { int bm, bn; };
+  const Tile tiles[] = {{128, 128}, {96, 128}, {96, 64}, {64, 64}};
+  int best = 0;
+  int64_t best_cost = -1;
+  bool best_two = false;
+  for (int c = 0; c < 4; ++c) {
+    const int64_t wgs = (int64_t)((N + tiles[c].bn - 1) / tiles[c].bn) * ((M + tiles[c].bm - 1) / tiles[c].bm);
+    const int64_t cost = (wgs + cus - 1) / cus * tiles[c].bm * tiles[c].bn;
+    const bool two = wgs >= 2 * (int64_t)cus;
+    if (best_cost < 0 || cost < best_cost || (cost == best_cost && two && !best_two)) {
+      best_cost = cost;
+      best = c;
+      best_two = two;
+    }
+  }
+  switch (best) {
+    case 0: return launch_dense_tile<128, 128>(W, B, C, M, K, N, bias, epi, stream);
+    case 1: return launch_dense_tile<96, 128>(W, B, C, M, K, N, bias, epi, stream);
+    case 2: return launch_dense_tile<96, 64>(W, B, C, M, K, N, bias, epi, stream);
+    default: return launch_dense_tile<64, 64>(W, B, C, M, K, N, bias, epi, stream);
+  }
 }
 
 }  // namespace sdnn

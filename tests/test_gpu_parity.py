@@ -445,7 +445,8 @@ def test_overlapping_buffers_rejected():
         assert ei.value.code == 2
 
 
-@pytest.mark.parametrize("M,K,N", [(64, 64, 64), (130, 97, 75), (768, 768, 512)])
+@pytest.mark.parametrize("M,K,N", [(64, 64, 64), (130, 97, 75), (768, 768, 512), (100, 1001, 257),
+                                   (200, 33, 129)])
 def test_dense_comparison_kernel(M, K, N):
     rng = np.random.default_rng(M + K + N)
     Wd = rng.standard_normal((M, K)).astype(np.float32) * 0.05
@@ -547,3 +548,36 @@ def test_c5_encoder_layer_end_to_end_propagated_bound():
     w = inputs.workload("c5", N=16384, num_layers=1)
     cols = np.sort(np.random.default_rng(74).choice(w.N, 64, replace=False))
     _chain_end_to_end(w, cols, "c5")
+
+
+def test_dense_comparison_kernel_full_size_and_offsets():
+    """The dense comparison GEMM on the W0 shape (768 x 3072 times 3072 x 4096, the tile
+    shape the benchmark times) on 64 sampled columns, and on operands that start 4 bytes
+    into their allocations (the element-wise edge path)."""
+    rng = np.random.default_rng(4242)
+    M, K, N = 768, 3072, 4096
+    Wd = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    B = rng.standard_normal((K, N)).astype(np.float32)
+    bias = (rng.standard_normal(M) * 0.02).astype(np.float32)
+    C = torch.full((M, N), float("nan"), device=DEV)
+    sd.dense_gemm(torch.from_numpy(Wd).to(DEV), torch.from_numpy(B).to(DEV), C,
+                  torch.from_numpy(bias).to(DEV), "relu")
+    torch.cuda.synchronize()
+    cols = np.sort(rng.choice(N, 64, replace=False))
+    rp, ci, v = dense_to_csr(Wd)
+    ref, bound = oracle.spmm_f64(rp, ci, v, K, B[:, cols], bias, "relu")
+    assert np.all(np.abs(C[:, cols].cpu().numpy() - ref) <= tolerance(bound, ref, "relu"))
+    # operands offset by one float: not 16-byte aligned
+    M, K, N = 96, 300, 128
+    Wd = (rng.standard_normal((M, K)) * 0.05).astype(np.float32)
+    B = rng.standard_normal((K, N)).astype(np.float32)
+    wbuf = torch.zeros(M * K + 1, device=DEV)
+    bbuf = torch.zeros(K * N + 1, device=DEV)
+    wbuf[1:] = torch.from_numpy(Wd.ravel()).to(DEV)
+    bbuf[1:] = torch.from_numpy(B.ravel()).to(DEV)
+    C = torch.full((M, N), float("nan"), device=DEV)
+    sd.dense_gemm(wbuf[1:].view(M, K), bbuf[1:].view(K, N), C, None, "none")
+    torch.cuda.synchronize()
+    rp, ci, v = dense_to_csr(Wd)
+    ref, bound = oracle.spmm_f64(rp, ci, v, K, B, None, "none")
+    assert np.all(np.abs(C.cpu().numpy() - ref) <= tolerance(bound, ref, "none"))
