@@ -44,7 +44,8 @@ ALU_PEAK_TFLOPS = 256 * 128 * 2 * 2.4e9 / 1e12
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2101_07948_amd", "csrc", f)
                   for f in ("sdnn_kernels.hip", "sdnn_host.cpp", "sdnn_internal.h",
                             "gen_spmm_asm.py", "spmm_asm_gen.h")]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_spmm_w0.json")
+def traffic_file(layer: str = "w0") -> str:
+    return os.path.join(ROOT, "profiles", f"traffic_spmm_{layer}.json")
 
 
 def kernel_hash() -> str:
@@ -54,10 +55,10 @@ def kernel_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
+def measured_traffic(layer: str = "w0"):
     """HBM bytes per launch from committed rocprofv3 counters, if taken on this kernel."""
     try:
-        t = json.load(open(TRAFFIC_FILE))
+        t = json.load(open(traffic_file(layer)))
     except (OSError, ValueError):
         return None
     return t.get("bytes_per_launch") if t.get("kernel_hash") == kernel_hash() else None
@@ -72,13 +73,12 @@ def _pmc_rows(path, counter):
     return sorted(rows)
 
 
-def summarize_pmc(fetch_csv, write_csv, N):
+def summarize_pmc(fetch_csv, write_csv, K, N, layer="w0"):
     """Per-launch HBM traffic of the sparse kernel from FETCH_SIZE / WRITE_SIZE (KiB per
     dispatch), each scaled by what the same counter reads for the calibration copy (an
     elementwise negation that reads and writes exactly K*N*4 bytes).  Only the sparse
     launches before the copy count: those are the warm-up and timed steps, each on a
     buffer set not touched since it was created."""
-    K = 3072
     copy_bytes = 4.0 * K * N
     out = {"kernel_hash": kernel_hash(), "copy_bytes_each_way": copy_bytes}
     for name, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
@@ -96,8 +96,9 @@ def summarize_pmc(fetch_csv, write_csv, N):
         out[name + "_calibration_factor"] = factor
         out[name + "_bytes_per_launch"] = sum(spmm) / len(spmm) * 1024.0 * factor
     out["bytes_per_launch"] = out["fetch_bytes_per_launch"] + out["write_bytes_per_launch"]
-    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
-    json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
+    out["layer"] = layer
+    os.makedirs(os.path.dirname(traffic_file(layer)), exist_ok=True)
+    json.dump(out, open(traffic_file(layer), "w"), indent=1)
     print(json.dumps(out))
 
 
@@ -580,6 +581,9 @@ def main():
     ap.add_argument("--settle-ms", type=float, default=300.0,
                     help="untimed run of the step before the warm-up steps, in ms of wall time")
     ap.add_argument("--N", type=int, default=4096)
+    ap.add_argument("--layer", default="w0",
+                    help="workload layer to time: w0 (the measured layer; default), c2, c3_w1, "
+                         "c3_w2, c4, c5_proj, c5_ffn1, c5_ffn2 (counter passes on other layers)")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="seconds of CPU-oracle timing (0 = skip the cpu_baseline leg)")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense comparison kernel")
@@ -590,7 +594,7 @@ def main():
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, "
                          "WRITE_SIZE) of a --calib-copy run into per-launch HBM bytes and write "
-                         f"{os.path.relpath(TRAFFIC_FILE, ROOT)}")
+                         "profiles/traffic_spmm_<layer>.json")
     ap.add_argument("--suite", metavar="OUT_MD",
                     help="time every configuration, the dense comparison, the row-order "
                          "ablation, the chained C5 stack, the convolutions, the paper-shaped "
@@ -601,7 +605,12 @@ def main():
         run_suite(args.suite)
         return
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc, N=args.N)
+        Ks = {"w0": 3072, "c2": 768, "c3_w1": 768, "c3_w2": 3072, "c4": 512, "c5_proj": 768,
+              "c5_ffn1": 768, "c5_ffn2": 3072}
+        Ns = {"c2": 1024, "c3_w1": 4096, "c3_w2": 4096, "c4": 3136, "c5_proj": 16384,
+              "c5_ffn1": 16384, "c5_ffn2": 16384}
+        summarize_pmc(*args.summarize_pmc, K=Ks[args.layer], N=Ns.get(args.layer, args.N),
+                      layer=args.layer)
         return
 
     if args.gpus != 1:
@@ -617,8 +626,16 @@ def main():
     from paper_2101_07948_amd import inputs
 
     dev = torch.device("cuda:0")
-    w = inputs.workload("w0", N=args.N)
-    L = w.layers[0]
+    layer_of = {"w0": ("w0", 0, {}), "c2": ("c2", 0, {}), "c3_w1": ("c3", 0, {}),
+                "c3_w2": ("c3", 1, {}), "c4": ("c4", 0, {}), "c5_proj": ("c5", 0, {"num_layers": 1}),
+                "c5_ffn1": ("c5", 4, {"num_layers": 1}), "c5_ffn2": ("c5", 5, {"num_layers": 1})}
+    if args.layer not in layer_of:
+        sys.exit(f"unknown --layer {args.layer}")
+    wname, li, kw = layer_of[args.layer]
+    w = inputs.workload(wname, N=None if args.layer != "w0" else args.N, **kw)
+    L = w.layers[li]
+    if li > 0:  # a later layer of a chain: a synthetic input of its own shape
+        w.B = inputs.dense_B(L.W.K, w.N, inputs.CFG_TEST, 4242)
     W, N, M, K = L.W, w.N, L.W.M, L.W.K
     plan = sd.Plan.from_csr(W)
     info = plan.info
@@ -629,19 +646,20 @@ def main():
     for _ in range(nsets - 1):
         Bs.append(Bs[0].clone())
     Cs = [torch.empty((M, N), device=dev) for _ in range(nsets)]
-    bias = torch.from_numpy(L.bias).to(dev)
+    bias = None if L.bias is None else torch.from_numpy(L.bias).to(dev)
     torch.cuda.synchronize()
 
-    _settle(lambda i: plan.spmm(Bs[i % nsets], Cs[i % nsets], bias), args.settle_ms)
+    epi = L.epi
+    _settle(lambda i: plan.spmm(Bs[i % nsets], Cs[i % nsets], bias, epi), args.settle_ms)
     for i in range(args.warmup):
-        plan.spmm(Bs[i % nsets], Cs[i % nsets], bias)
+        plan.spmm(Bs[i % nsets], Cs[i % nsets], bias, epi)
     torch.cuda.synchronize()
 
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record()
     for i in range(args.steps):
-        plan.spmm(Bs[i % nsets], Cs[i % nsets], bias)
+        plan.spmm(Bs[i % nsets], Cs[i % nsets], bias, epi)
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
@@ -660,7 +678,7 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(gbs / HBM_PEAK_GBS, 4)}
-    traffic = measured_traffic()
+    traffic = measured_traffic(args.layer)
     roof["traffic"] = traffic
     roof["hbm_frac"] = round(gbs / HBM_PEAK_GBS, 4)
     roof["alg_bytes"] = int(alg_bytes)
@@ -676,11 +694,11 @@ def main():
     warm_ms = None
     if not args.warm:
         for _ in range(5):
-            plan.spmm(Bs[0], Cs[0], bias)
+            plan.spmm(Bs[0], Cs[0], bias, epi)
         torch.cuda.synchronize()
         e0.record()
         for _ in range(50):
-            plan.spmm(Bs[0], Cs[0], bias)
+            plan.spmm(Bs[0], Cs[0], bias, epi)
         e1.record()
         torch.cuda.synchronize()
         warm_ms = e0.elapsed_time(e1) / 50
@@ -735,8 +753,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "w0: W 768x3072 fp32, 90% uniform-random sparsity, "
-                               f"B 3072x{N} fp32, bias, no activation",
+        "config": {"workload": ("w0: W 768x3072 fp32, 90% uniform-random sparsity, "
+                                f"B 3072x{N} fp32, bias, no activation") if args.layer == "w0"
+                   else f"{args.layer}: W {M}x{K} fp32 (nnz {W.nnz}), B {K}x{N} fp32, bias, {L.epi}",
                    "M": M, "K": K, "N": N, "nnz": W.nnz, "panel_rows": info["panel_rows"],
                    "rho": round(info["rho"], 4), "buffer_sets": nsets},
         "alg_GBps": round(gbs, 1),

@@ -149,9 +149,10 @@ def sync(slot, tag):
     landed (c_hi < min of the producers' ready words), polling while the budget
     lasts."""
     width, _, rng = ready_regs()
-    L = [f"s_lshr_b32 s{STMP}, s{slot + LOW}, {LO_SHIFT}", f"v_mov_b32 v30, s{STMP}"]
+    L = [f"s_lshr_b32 s{STMP}, s{slot + LOW}, {LO_SHIFT}",
+         f"s_add_u32 s{STMP}, s{STMP}, %[cbase]", f"v_mov_b32 v30, s{STMP}"]
     L += lane0_write("%[pa]", "v30")
-    L += [f"s_lshr_b32 s{STMP}, s{slot + HIW}, {HI_SHIFT}"]
+    L += [f"s_lshr_b32 s{STMP}, s{slot + HIW}, {HI_SHIFT}", f"s_add_u32 s{STMP}, s{STMP}, %[cbase]"]
     if PROFILE:
         L += [f"s_memtime s[{SEXEC}:{SEXEC + 1}]", "s_waitcnt lgkmcnt(0)"]
     L += [
@@ -247,7 +248,7 @@ def consumer(rw, limit=False):
           f"s_cmp_eq_u32 s{STMP}, 0", "s_cbranch_scc1 .L%=_clean",
           ".L%=_poison:"]
     L += [f"v_mov_b32 v{ACC + x}, 0x7fc00000" for x in range(4 * rw)]
-    L += [".L%=_clean:", f"v_mov_b32 v30, {hex(INF)}"]
+    L += [".L%=_clean:", "v_mov_b32 v30, %[next]"]
     L += lane0_write("%[pa]", "v30")
     L += ["s_waitcnt vmcnt(0) lgkmcnt(0)", f"s_mov_b32 m0, s{M0S}"]
     body = "\n".join('      "' + x + '\\n\\t"' for x in L)
@@ -258,7 +259,8 @@ def consumer(rw, limit=False):
     name = f"consume_rw{rw}" + ("_limit" if limit else "")
     operands = ('[sp] "s"(a.stream), [vl] "v"(a.vlane), [pa] "v"(a.prog_addr), '
                 '[ra] "v"(a.ready_addr),\n        [budget] "s"(a.poll_budget), '
-                '[ov] "v"(a.overrun_addr)' + (', [climit] "s"(a.chunk_limit)' if limit else ''))
+                '[ov] "v"(a.overrun_addr), [cbase] "s"(a.chunk_base), [next] "s"(a.next_progress)'
+                + (', [climit] "s"(a.chunk_limit)' if limit else ''))
     return f"""// Consumer, RW = {rw}{', stopping at the chunk limit' if limit else ''}: accumulator planes p0..p3
 __device__ __forceinline__ void {name}(acc_plane_t<{rw}>& p0, acc_plane_t<{rw}>& p1,
                                          acc_plane_t<{rw}>& p2, acc_plane_t<{rw}>& p3,
@@ -277,6 +279,7 @@ PISS, PSIG, PINF, PLIM, PTMP, PPOLL, PROW, PM0 = 40, 41, 42, 43, 44, 45, 46, 47
 PADDR, PEX, PBASE, PCS = 48, 50, 52, 54       # 64-bit each
 PCM = 56                                       # column masks (1 or 4 pairs)
 PKM1, PLAST = 64, 65
+PCI, PB0 = 78, 80                              # chunk within the item; the item's first chunk address
 # producer VGPRs: row offsets of the fast path, progress words, min tree
 VO, VP, VMIN = 32, 40, 56
 
@@ -457,6 +460,8 @@ def producer(kind):
         f"s_addc_u32 s{PBASE + 1}, s{PBASE + 1}, %[bb_hi]",
         f"s_lshl_b32 s{PCS}, %[rs], {lg_chunk}",
         f"s_lshr_b32 s{PCS + 1}, %[rs], {32 - lg_chunk}",
+        f"s_mov_b64 s[{PB0}:{PB0 + 1}], s[{PBASE}:{PBASE + 1}]",
+        f"s_mov_b32 s{PCI}, %[fc]",
     ]
     if kind == "vec":  # PLAST = K / CHUNK: chunks below it hold CHUNK rows of B
         L += [f"s_lshr_b32 s{PLAST}, %[K], {lg_chunk}",
@@ -530,7 +535,7 @@ def producer(kind):
     if conv:
         L += issue_rows_conv(half)
     else:
-        L += [f"s_cmp_lt_u32 s{PISS}, s{PLAST}", "s_cbranch_scc0 .L%=_clamped"]
+        L += [f"s_cmp_lt_u32 s{PCI}, s{PLAST}", "s_cbranch_scc0 .L%=_clamped"]
         if vec:
             L.append(f"s_mov_b64 exec, s[{PCM}:{PCM + 1}]")   # also spaces the m0 write from the DMA
             for r in range(half):
@@ -540,7 +545,7 @@ def producer(kind):
                       "s_add_u32 m0, m0, 0x400"]
             L.append("s_branch .L%=_issued")
         L += [".L%=_clamped:",
-              f"s_lshl_b32 s{PROW}, s{PISS}, {lg_chunk}",
+              f"s_lshl_b32 s{PROW}, s{PCI}, {lg_chunk}",
               f"s_add_u32 s{PROW}, s{PROW}, %[prow0]"]
         L += issue_rows_clamped(vec, half)
     L += [
@@ -550,6 +555,12 @@ def producer(kind):
         f"s_addc_u32 s{PBASE + 1}, s{PBASE + 1}, s{PCS + 1}",
         f"s_add_u32 s{PISS}, s{PISS}, 1",
         f"s_add_u32 s{PINF}, s{PINF}, 1",
+        # the next item (the tile's next row-block) restages the same rows from its start
+        f"s_add_u32 s{PCI}, s{PCI}, 1",
+        f"s_cmp_lt_u32 s{PCI}, %[nci]",
+        "s_cbranch_scc1 .L%=_loop",
+        f"s_mov_b32 s{PCI}, 0",
+        f"s_mov_b64 s[{PBASE}:{PBASE + 1}], s[{PB0}:{PB0 + 1}]",
         "s_branch .L%=_loop",
         # wait for the oldest chunk in flight (loads complete in order), publish it
         ".L%=_land:",
@@ -574,7 +585,7 @@ def producer(kind):
         f"s_mov_b32 m0, s{PM0}",
     ]
     body = "\n".join('      "' + x + '\\n\\t"' for x in L)
-    sregs = [f"s{x}" for x in list(range(PISS, PCM + 2 * pieces)) + [PKM1, PLAST]]
+    sregs = [f"s{x}" for x in list(range(PISS, PCM + 2 * pieces)) + [PKM1, PLAST, PCI, PB0, PB0 + 1]]
     if conv:
         sregs += [f"s{x}" for x in range(RB[0], PXB + 2)]
     vregs = ["v27"] + [f"v{x}" for x in range(VO, VMIN + 5)]
@@ -589,7 +600,8 @@ __device__ __forceinline__ void produce_{kind}(const ProducerArgs& a) {{
       : [nch] "s"(a.nchunks), [K] "s"(a.K), [rs] "s"(a.row_bytes), [bb_lo] "s"(a.bbase_lo),
         [bb_hi] "s"(a.bbase_hi), [ncol] "s"(a.ncol), [prow0] "s"(a.first_row),
         [vl] "v"(a.vlane), [pg] "v"(a.prog_addr), [ra] "v"(a.ready_addr),
-        [budget] "s"(a.poll_budget), [ov] "v"(a.overrun_addr), [fc] "s"(a.first_chunk){CONV_OPERANDS if conv else ""}
+        [budget] "s"(a.poll_budget), [ov] "v"(a.overrun_addr), [fc] "s"(a.first_chunk),
+        [nci] "s"(a.item_chunks){CONV_OPERANDS if conv else ""}
       : {clob});
 }}
 """

@@ -56,10 +56,14 @@ struct ConsumerArgs {
   uint32_t poll_budget;    // failed readiness checks the wave may poll through in total
   uint32_t overrun_addr;   // LDS address of the workgroup's overrun word
   uint32_t chunk_limit;    // the wave stops before a sync group whose c_lo reaches this chunk
+  uint32_t chunk_base;     // ring chunk number of the item's chunk 0 (added to c_lo, c_hi)
+  uint32_t next_progress;  // progress word written when the panel is done
 };
 struct ProducerArgs {
-  int32_t nchunks, K;      // nchunks: one past the last chunk to stage
+  int32_t nchunks, K;      // nchunks: one past the last ring chunk to stage
   int32_t first_chunk;     // first chunk to stage
+  int32_t item_chunks;     // chunks per item: ring chunk g stages chunk g % item_chunks of B
+                           // (a persistent workgroup's row-blocks restage the same rows)
   uint32_t row_bytes;      // N * 4
   uint32_t bbase_lo, bbase_hi;  // address of B[0][n0]
   int32_t ncol;            // N - n0 (columns of the tile that exist)
@@ -105,9 +109,29 @@ constexpr int kCtlWords = 256;
 static_assert(512 + 16 * kProducers <= kCtlWords * 4, "filler words outside the control area");
 static_assert(kProducers <= 16, "ready words overlap the progress words");
 
+// GELU(x) = x Phi(x) = 0.5 x (1 + erf(x / sqrt 2)) (the exact erf form).  erf(z) for
+// z >= 0 comes from Abramowitz & Stegun 7.1.26 (Hastings' approximation, absolute error
+// at most 1.5e-7): erf(z) = 1 - q, q = t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) e^(-z^2),
+// t = 1 / (1 + p z); with erf(-z) = -erf(z), GELU(x) = 0.5 x (2 - q) for x >= 0 and
+// 0.5 x q for x < 0 (no cancellation on the negative side).  The reciprocal and the
+// exponential are the hardware's (v_rcp_f32, v_exp_f32, about 1 ulp); the result is within
+// 0.5 |x| * 4e-7 of the exact GELU, far inside the 1e-6 floor of the parity bar at the
+// |x| these layers reach, and costs about a third of the library erff's instructions.
+__device__ __forceinline__ float gelu(float x) {
+  const float z = fabsf(x) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, z, 1.0f));
+  float poly = fmaf(t, 1.061405429f, -1.453152027f);
+  poly = fmaf(t, poly, 1.421413741f);
+  poly = fmaf(t, poly, -0.284496736f);
+  poly = fmaf(t, poly, 0.254829592f);
+  poly *= t;
+  const float q = poly * __builtin_amdgcn_exp2f(-z * z * 1.4426950408889634f);
+  return 0.5f * x * (x >= 0.0f ? 2.0f - q : q);
+}
+
 __device__ __forceinline__ float activation(float x, int epi) {
   if (epi == SDNN_EPI_RELU) return fmaxf(x, 0.0f);
-  if (epi == SDNN_EPI_GELU) return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+  if (epi == SDNN_EPI_GELU) return gelu(x);
   return x;
 }
 
@@ -127,6 +151,10 @@ struct SpmmArgs {
   // which writes its partial product, without bias or activation, to C + run * M * N
   // (C is then the workspace)
   int32_t M, nsplit, seg_per_split, nseg, split_chunks;
+  // persistent workgroups (unsplit launches): wg_per_tile workgroups per column tile,
+  // workgroup g of a tile taking row-blocks g, g + wg_per_tile, ... in turn (wg_per_tile =
+  // n_rb: one row-block each)
+  int32_t wg_per_tile;
 };
 
 // Producer kinds: 4-byte staging (any N), 16-byte staging (N % 4 == 0, aligned), the
@@ -150,10 +178,11 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
   const int lin = (bid & 7) * a.per_xcd + (bid >> 3);
   if (lin >= a.total_wg) return;  // whole workgroup leaves before the barrier
   // workgroups of one tile and run of K-segments are consecutive (they stage the same rows)
-  const int per_tile = a.nsplit * a.n_rb;
+  const int per_tile = a.nsplit * a.wg_per_tile;
   const int tile = lin / per_tile;
-  const int split = (lin - tile * per_tile) / a.n_rb;
-  const int rb = lin - tile * per_tile - split * a.n_rb;
+  const int split = (lin - tile * per_tile) / a.wg_per_tile;
+  const int g = lin - tile * per_tile - split * a.wg_per_tile;
+  const int nitems = (a.n_rb - g + a.wg_per_tile - 1) / a.wg_per_tile;  // row-blocks g + i * wg_per_tile
   const bool splitk = a.nsplit > 1;
   const int s0 = split * a.seg_per_split, s1 = min(s0 + a.seg_per_split, a.nseg);
   const int c0 = splitk ? s0 * a.split_chunks : 0;
@@ -163,15 +192,6 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
   const int lane = threadIdx.x & 63;
   const int n0 = tile * kTileCols;
   const int prod = wave - nc;  // >= 0: producer index
-  const int panel = rb * nc + wave;
-  int gstart = -1;  // the wave's first group: the first of its panel in the run
-  if (prod < 0 && panel < a.npanels) {
-    if (!splitk) {
-      gstart = panel_start[panel];
-    } else {
-      for (int sg = s0; sg < s1 && gstart < 0; ++sg) gstart = seg_start[(size_t)panel * a.nseg + sg];
-    }
-  }
 
   const uint32_t lds_base = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) uint32_t*)lds);
   if (lds_base != 0) return;  // never taken: see above
@@ -184,14 +204,16 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     if (prod == 0 && lane == 0) ctl[32] = 0u;                                // no overrun
     if (prod == 0 && lane >= nc && lane < 16) ctl[16 + lane] = kProgressDone;  // absent consumers
   } else if (lane == 0) {
-    ctl[16 + wave] = gstart >= 0 ? (uint32_t)c0 : kProgressDone;
+    ctl[16 + wave] = (uint32_t)c0;  // reads the first item from its first chunk on
   }
   __syncthreads();
 
   if (prod >= 0) {
     ProducerArgs pa;
-    pa.nchunks = c1;
+    // ring chunks: the items' chunk ranges back to back (split runs: one item, [c0, c1))
+    pa.nchunks = splitk ? c1 : nitems * a.nchunks;
     pa.first_chunk = c0;
+    pa.item_chunks = splitk ? c1 : a.nchunks;
     pa.K = a.K;
     pa.row_bytes = (uint32_t)a.N * 4u;
     const uint64_t bb = (uint64_t)(uintptr_t)(B + n0);
@@ -230,59 +252,81 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     }
     return;
   }
-  if (panel >= a.npanels) return;
-
-  acc_plane_t<RW> p0 = {}, p1 = {}, p2 = {}, p3 = {};
-  if (gstart >= 0) {  // a panel without entries only writes epi(bias)
-    ConsumerArgs ca;
-    ca.stream = entries + (size_t)gstart * (2 * kGroup);
-    ca.vlane = (uint32_t)lane * 16u;
-    ca.prog_addr = prog0 + 4u * (uint32_t)wave;
-    ca.ready_addr = ready_addr;
-    ca.poll_budget = a.poll_budget;
-    ca.overrun_addr = overrun_addr;
-    ca.chunk_limit = (uint32_t)c1;
-    if (splitk) {  // runs of K-segments: the loop also stops at the run's last chunk
-      if constexpr (RW == 4) consume_rw4_limit(p0, p1, p2, p3, ca);
-      if constexpr (RW == 8) consume_rw8_limit(p0, p1, p2, p3, ca);
-      if constexpr (RW == 12) consume_rw12_limit(p0, p1, p2, p3, ca);
-      if constexpr (RW == 16) consume_rw16_limit(p0, p1, p2, p3, ca);
-    } else {
-      if constexpr (RW == 4) consume_rw4(p0, p1, p2, p3, ca);
-      if constexpr (RW == 8) consume_rw8(p0, p1, p2, p3, ca);
-      if constexpr (RW == 12) consume_rw12(p0, p1, p2, p3, ca);
-      if constexpr (RW == 16) consume_rw16(p0, p1, p2, p3, ca);
-    }
-  }
 
   const int ncol = n0 + lane * 4;
+  for (int it = 0; it < nitems; ++it) {
+    const int rb = g + it * a.wg_per_tile;
+    const int panel = rb * nc + wave;
+    const uint32_t cbase = splitk ? 0u : (uint32_t)(it * a.nchunks);
+    const uint32_t next = it + 1 < nitems ? (uint32_t)((it + 1) * a.nchunks) : kProgressDone;
+    int gstart = -1;  // the wave's first group: the first of its panel in the run
+    if (panel < a.npanels) {
+      if (!splitk) {
+        gstart = panel_start[panel];
+      } else {
+        for (int sg = s0; sg < s1 && gstart < 0; ++sg) gstart = seg_start[(size_t)panel * a.nseg + sg];
+      }
+    }
+    if (panel >= a.npanels) {  // no panel here, nor in any later row-block
+      if (lane == 0) ctl[16 + wave] = kProgressDone;
+      return;
+    }
+
+    acc_plane_t<RW> p0 = {}, p1 = {}, p2 = {}, p3 = {};
+    if (gstart >= 0) {  // a panel without entries only writes epi(bias)
+      ConsumerArgs ca;
+      ca.stream = entries + (size_t)gstart * (2 * kGroup);
+      ca.vlane = (uint32_t)lane * 16u;
+      ca.prog_addr = prog0 + 4u * (uint32_t)wave;
+      ca.ready_addr = ready_addr;
+      ca.poll_budget = a.poll_budget;
+      ca.overrun_addr = overrun_addr;
+      ca.chunk_limit = (uint32_t)c1;
+      ca.chunk_base = cbase;
+      ca.next_progress = next;
+      if (splitk) {  // runs of K-segments: the loop also stops at the run's last chunk
+        if constexpr (RW == 4) consume_rw4_limit(p0, p1, p2, p3, ca);
+        if constexpr (RW == 8) consume_rw8_limit(p0, p1, p2, p3, ca);
+        if constexpr (RW == 12) consume_rw12_limit(p0, p1, p2, p3, ca);
+        if constexpr (RW == 16) consume_rw16_limit(p0, p1, p2, p3, ca);
+      } else {
+        if constexpr (RW == 4) consume_rw4(p0, p1, p2, p3, ca);
+        if constexpr (RW == 8) consume_rw8(p0, p1, p2, p3, ca);
+        if constexpr (RW == 12) consume_rw12(p0, p1, p2, p3, ca);
+        if constexpr (RW == 16) consume_rw16(p0, p1, p2, p3, ca);
+      }
+    } else if (lane == 0) {
+      ctl[16 + wave] = next;  // nothing to read in this row-block
+    }
+
 #pragma unroll
-  for (int r = 0; r < RW; ++r) {
-    const int orig = panel_rows[panel * RW + r];
-    if (orig < 0) continue;
-    const int row = a.out_permuted ? panel_pos[panel] * RW + r : orig;
-    const float v[4] = {p0[r], p1[r], p2[r], p3[r]};
-    if (splitk) {  // raw partial sums; the reduction adds the bias and applies epi
-      float* prow = C + ((size_t)split * a.M + row) * a.N;
+    for (int r = 0; r < RW; ++r) {
+      const int orig = panel_rows[panel * RW + r];
+      if (orig < 0) continue;
+      const int row = a.out_permuted ? panel_pos[panel] * RW + r : orig;
+      const float v[4] = {p0[r], p1[r], p2[r], p3[r]};
+      if (splitk) {  // raw partial sums; the reduction adds the bias and applies epi
+        float* prow = C + ((size_t)split * a.M + row) * a.N;
+        if (STAGE != kStageDword && ncol + 4 <= a.N) {
+          *reinterpret_cast<float4*>(prow + ncol) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (ncol + i < a.N) prow[ncol + i] = v[i];
+        }
+        continue;
+      }
+      const float bb = bias ? bias[orig] : 0.0f;
+      float* crow = C + (size_t)row * a.N;
       if (STAGE != kStageDword && ncol + 4 <= a.N) {
-        *reinterpret_cast<float4*>(prow + ncol) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4*>(crow + ncol) =
+            make_float4(activation(v[0] + bb, a.epi), activation(v[1] + bb, a.epi),
+                        activation(v[2] + bb, a.epi), activation(v[3] + bb, a.epi));
       } else {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          if (ncol + i < a.N) prow[ncol + i] = v[i];
+          if (ncol + i < a.N) crow[ncol + i] = activation(v[i] + bb, a.epi);
       }
-      continue;
-    }
-    const float bb = bias ? bias[orig] : 0.0f;
-    float* crow = C + (size_t)row * a.N;
-    if (STAGE != kStageDword && ncol + 4 <= a.N) {
-      *reinterpret_cast<float4*>(crow + ncol) =
-          make_float4(activation(v[0] + bb, a.epi), activation(v[1] + bb, a.epi),
-                      activation(v[2] + bb, a.epi), activation(v[3] + bb, a.epi));
-    } else {
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (ncol + i < a.N) crow[ncol + i] = activation(v[i] + bb, a.epi);
     }
   }
 }
@@ -562,7 +606,26 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
   args.seg_per_split = seg_per_split;
   args.nseg = pk.nseg;
   args.split_chunks = nk > 1 ? p->split_chunks : 0;
-  const int64_t total = (int64_t)cfg.n_tiles * nk * cfg.n_rb;
+  // Persistent workgroups: when an unsplit product has more (tile, row-block) items than
+  // CUs, each tile gets wg_per_tile = CUs / tiles workgroups (at least one) that take its
+  // row-blocks in turn; the producers stage the next row-block's chunks into the ring
+  // while the consumers finish the current one, so a workgroup's start-up (first chunks
+  // in flight) and wind-down (epilogue, stores) overlap its neighbours' work instead of
+  // recurring per row-block.  Ring chunk numbers run on across row-blocks, so a
+  // row-block's chunk c sits in ring slot (base + c) % kRing: the row-blocks' chunk
+  // counts must be multiples of kRing, as the stream's ring rows assume c % kRing.
+  const int cus = p->num_cus > 0 ? p->num_cus : 256;
+  int wg_per_tile = cfg.n_rb;
+  if (nk == 1 && !conv_hwn && p->nchunks % kRing == 0 &&
+      (int64_t)cfg.n_tiles * cfg.n_rb > cus)
+    wg_per_tile = std::max(1, std::min(cfg.n_rb, cus / std::max(1, cfg.n_tiles)));
+  {
+    const int forced = env_int("SDNN_FORCE_WG_PER_TILE", 0);
+    if (forced > 0 && nk == 1 && !conv_hwn && p->nchunks % kRing == 0)
+      wg_per_tile = std::min(forced, cfg.n_rb);
+  }
+  args.wg_per_tile = wg_per_tile;
+  const int64_t total = (int64_t)cfg.n_tiles * nk * wg_per_tile;
   if (total > (int64_t)1 << 30) return hipErrorInvalidValue;
   const int64_t grid = (total + 7) / 8 * 8;
   args.total_wg = (int32_t)total;

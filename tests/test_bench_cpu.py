@@ -38,7 +38,7 @@ def test_traffic_calibration(tmp_path, monkeypatch):
     """Each counter is scaled by what it reads for the calibration copy (4*K*N bytes each
     way, K = 3072), and only sparse-kernel dispatches before the copy count."""
     bench = load_bench()
-    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "traffic.json"))
+    monkeypatch.setattr(bench, "traffic_file", lambda layer="w0": str(tmp_path / "traffic.json"))
     N = 4096
     copy_kib = 4 * 3072 * N / 1024            # 49152 KiB each way
     spmm = "void sdnn::spmm_panel_kernel<4, 1>(...)"
@@ -49,7 +49,7 @@ def test_traffic_calibration(tmp_path, monkeypatch):
                                          (4, neg, copy_kib / 2), (5, spmm, 9999.0)])
     write_counters(write, "WRITE_SIZE", [(1, spmm, 300.0), (2, spmm, 300.0), (3, spmm, 300.0),
                                          (4, neg, copy_kib), (5, spmm, 9999.0)])
-    bench.summarize_pmc(str(fetch), str(write), N)
+    bench.summarize_pmc(str(fetch), str(write), 3072, N)
     out = json.load(open(tmp_path / "traffic.json"))
     assert out["kernel_hash"] == bench.kernel_hash()
     assert out["fetch_launches"] == 3 and out["write_launches"] == 3
@@ -63,7 +63,7 @@ def test_traffic_calibration(tmp_path, monkeypatch):
 def test_traffic_is_reported_only_for_the_profiled_sources(tmp_path, monkeypatch):
     bench = load_bench()
     path = tmp_path / "traffic.json"
-    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(path))
+    monkeypatch.setattr(bench, "traffic_file", lambda layer="w0": str(path))
     json.dump({"kernel_hash": "0" * 16, "bytes_per_launch": 123.0}, open(path, "w"))
     assert bench.measured_traffic() is None
     json.dump({"kernel_hash": bench.kernel_hash(), "bytes_per_launch": 123.0}, open(path, "w"))

@@ -581,3 +581,32 @@ def test_dense_comparison_kernel_full_size_and_offsets():
     rp, ci, v = dense_to_csr(Wd)
     ref, bound = oracle.spmm_f64(rp, ci, v, K, B, None, "none")
     assert np.all(np.abs(C.cpu().numpy() - ref) <= tolerance(bound, ref, "none"))
+
+
+@pytest.mark.parametrize("wg_per_tile", [1, 2, 3])
+@pytest.mark.parametrize("N,epi", [(1024, "gelu"), (643, "relu")])
+def test_persistent_workgroups(wg_per_tile, N, epi):
+    """Workgroups that take several row-blocks of their column tile in turn (the ring's
+    chunk numbers running on across row-blocks): forced to 1, 2 or 3 workgroups per tile
+    on a problem with 8 row-blocks, with 16-byte (N = 1024) and 4-byte (N = 643)
+    staging, against the oracle and bit for bit against one row-block per workgroup
+    (each row sums its entries in the same order either way)."""
+    M, K = 384, 512
+    W = inputs.pattern_uniform(M, K, 0.1, inputs.CFG_TEST, 300 + N, 0.05)
+    B = inputs.dense_B(K, N, inputs.CFG_TEST, 300 + N)
+    bias = inputs.bias_normal(M, inputs.CFG_TEST, 300, 0.02)
+    with sd.Plan.from_csr(W, panel_rows=4) as plan:
+        with Forced(waves=12):
+            one = gpu_spmm(plan, B, bias, epi)
+            old = os.environ.get("SDNN_FORCE_WG_PER_TILE")
+            os.environ["SDNN_FORCE_WG_PER_TILE"] = str(wg_per_tile)
+            try:
+                got = gpu_spmm(plan, B, bias, epi)
+            finally:
+                if old is None:
+                    os.environ.pop("SDNN_FORCE_WG_PER_TILE", None)
+                else:
+                    os.environ["SDNN_FORCE_WG_PER_TILE"] = old
+    assert np.array_equal(got, one)
+    ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, K, B, bias, epi)
+    assert np.all(np.abs(got.astype(np.float64) - ref) <= tolerance(bound, ref, epi))
