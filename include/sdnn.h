@@ -57,7 +57,7 @@ typedef enum {
   SDNN_EPI_GELU = 2  /* 0.5 * x * (1 + erf(x / sqrt(2))) */
 } sdnn_epilogue;
 
-/* Options for sdnn_plan_create; pass NULL for the defaults {0, 1, 0, 0, NULL}.
+/* Options for sdnn_plan_create; pass NULL for the defaults {0, 1, 0, 0, NULL, 0}.
  *   panel_rows:   rows per register panel.  0 (default) packs W three times, with
  *                 panels of 4, 12 and 8 rows, and sdnn_spmm picks one per call: the
  *                 fewest rounds of workgroups over the compute units, then the most
@@ -92,13 +92,24 @@ typedef enum {
  *                 read during the call only), a permutation of 0..K-1 giving the order
  *                 of B's rows: B row i holds input feature in_perm[i].  Pass the
  *                 previous layer's perm when that layer used out_permuted = 1.
- *                 Not a permutation: SDNN_ERR_DIM. */
+ *                 Not a permutation: SDNN_ERR_DIM.
+ *   grouping:     which rows share a panel.  The plan's permutation (permute) is what
+ *                 sdnn_plan_get_perm reports and what out_permuted stores by in every
+ *                 case; the panels are either consecutive rows of it (1) or balanced
+ *                 panels (2: the panel-balancing rule of permute = 2 applied to W's
+ *                 rows), each row still summing its entries in ascending column order,
+ *                 so C is bit-identical either way.  0 (default) = by cost: balanced
+ *                 when its heaviest 4-row panel holds at least 15 % fewer nonzeros than
+ *                 the permutation's heaviest (the panels of a workgroup advance
+ *                 together, so the heaviest sets the pace), else the permutation's.
+ *                 Outside 0..2: SDNN_ERR_DIM. */
 typedef struct {
   int32_t panel_rows;
   int32_t permute;
   int32_t out_permuted;
   int32_t split_chunks;
   const int32_t* in_perm;
+  int32_t grouping;
 } sdnn_plan_opts;
 
 /* Plan statistics (of the first packing; the tall_* fields describe the second one and
@@ -121,6 +132,8 @@ typedef struct {
   int32_t out_permuted, in_permuted;  /* the plan's options (in_permuted: in_perm given) */
   int32_t mid_panel_rows, packings;   /* third packing's height (0: none); packings held */
   double mid_rho, mid_fill;
+  int32_t grouping, reserved;         /* panel grouping used: 1 consecutive rows of perm,
+                                         2 balanced panels (see sdnn_plan_opts.grouping) */
 } sdnn_plan_info_t;
 
 /* Greedy weight-row permutation (Sec. 3.1.2, Algorithm 1), host only, no GPU needed.

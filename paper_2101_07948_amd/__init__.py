@@ -34,7 +34,7 @@ class SdnnError(RuntimeError):
 class PlanOpts(ctypes.Structure):
     _fields_ = [("panel_rows", ctypes.c_int32), ("permute", ctypes.c_int32),
                 ("out_permuted", ctypes.c_int32), ("split_chunks", ctypes.c_int32),
-                ("in_perm", ctypes.c_void_p)]
+                ("in_perm", ctypes.c_void_p), ("grouping", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -46,7 +46,8 @@ class PlanInfo(ctypes.Structure):
                 ("tall_rho", ctypes.c_double), ("tall_fill", ctypes.c_double),
                 ("out_permuted", ctypes.c_int32), ("in_permuted", ctypes.c_int32),
                 ("mid_panel_rows", ctypes.c_int32), ("packings", ctypes.c_int32),
-                ("mid_rho", ctypes.c_double), ("mid_fill", ctypes.c_double)]
+                ("mid_rho", ctypes.c_double), ("mid_fill", ctypes.c_double),
+                ("grouping", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -123,15 +124,19 @@ def _order_mode(permute) -> int:
     return (1 if permute else 0) if isinstance(permute, bool) else int(permute)
 
 
+GROUPINGS = {"auto": 0, "order": 1, "balanced": 2}
+
+
 def _opts(K: int, panel_rows: int, permute: bool, out_permuted: bool = False, in_perm=None,
-          split_chunks: int = 0):
+          split_chunks: int = 0, grouping="auto"):
     """PlanOpts plus the in_perm array it points to (kept alive by the caller)."""
     keep = None if in_perm is None else _i32(in_perm)
     if keep is not None and keep.shape != (int(K),):
         raise ValueError(f"in_perm must hold K = {K} entries, got shape {keep.shape}")
     mode = _order_mode(permute)
+    g = GROUPINGS[grouping] if isinstance(grouping, str) else int(grouping)
     o = PlanOpts(int(panel_rows), mode, 1 if out_permuted else 0, int(split_chunks),
-                 None if keep is None else keep.ctypes.data)
+                 None if keep is None else keep.ctypes.data, g)
     return o, keep
 
 
@@ -158,11 +163,11 @@ def row_order(row_ptr, col_idx, K: int, permute="algorithm1") -> np.ndarray:
 
 def plan_check_host(row_ptr, col_idx, values, M: int, K: int, panel_rows: int = 0,
                     permute: bool = True, out_permuted: bool = False, in_perm=None,
-                    split_chunks: int = 0) -> dict:
+                    split_chunks: int = 0, grouping="auto") -> dict:
     """Host-only self-check of the preparation stage; returns the plan statistics."""
     row_ptr, col_idx, values = _i32(row_ptr), _i32(col_idx), _f32(values)
     info = PlanInfo()
-    o, _keep = _opts(K, panel_rows, permute, out_permuted, in_perm, split_chunks)
+    o, _keep = _opts(K, panel_rows, permute, out_permuted, in_perm, split_chunks, grouping)
     _check(lib().sdnn_plan_check_host(_np_ptr(row_ptr), _np_ptr(col_idx), _np_ptr(values), M, K,
                                       ctypes.byref(o), ctypes.byref(info)),
            "sdnn_plan_check_host")
@@ -220,15 +225,17 @@ class Plan:
 
     def __init__(self, row_ptr, col_idx, values, M: int, K: int, panel_rows: int = 0,
                  permute: bool = True, out_permuted: bool = False, in_perm=None,
-                 split_chunks: int = 0):
+                 split_chunks: int = 0, grouping="auto"):
         """out_permuted: write C in the plan's permuted row order (C[i] = output row
         perm[i]); in_perm: the order of B's rows (B[i] = input feature in_perm[i]),
         e.g. the previous layer's perm when that layer used out_permuted; split_chunks:
-        K-segments of that many staging chunks for spmm_split / conv3x3_split."""
+        K-segments of that many staging chunks for spmm_split / conv3x3_split;
+        grouping: "auto", "order" (panels are consecutive rows of perm) or "balanced"."""
         row_ptr, col_idx, values = _i32(row_ptr), _i32(col_idx), _f32(values)
         self.M, self.K = int(M), int(K)
         h = ctypes.c_void_p()
-        o, _keep = _opts(self.K, panel_rows, permute, out_permuted, in_perm, split_chunks)
+        o, _keep = _opts(self.K, panel_rows, permute, out_permuted, in_perm, split_chunks,
+                         grouping)
         self._lib = lib()
         _check(self._lib.sdnn_plan_create(_np_ptr(row_ptr), _np_ptr(col_idx), _np_ptr(values),
                                           self.M, self.K, ctypes.byref(o), ctypes.byref(h)),

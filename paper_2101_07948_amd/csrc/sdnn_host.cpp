@@ -118,7 +118,7 @@ void emit_group(std::vector<uint32_t>& out, const Entry* e, int n, bool first, b
 }  // namespace
 
 sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* values, int32_t M,
-                 int32_t K, int32_t RW, const int32_t* perm, int32_t split_chunks, Packed* out) {
+                 int32_t K, int32_t RW, const int32_t* group, int32_t split_chunks, Packed* out) {
   try {
     Packed& P = *out;
     P.M = M;
@@ -128,9 +128,8 @@ sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* va
     P.nchunks = (K + kChunk - 1) / kChunk;
     if (P.nchunks > kMaxChunks) return SDNN_ERR_DIM;
     P.npanels = (M + RW - 1) / RW;
-    P.perm.assign(perm, perm + M);
     P.panel_rows.assign((size_t)P.npanels * RW, -1);
-    for (int32_t i = 0; i < M; ++i) P.panel_rows[i] = perm[i];
+    for (int32_t i = 0; i < M; ++i) P.panel_rows[i] = group[i];
     P.panel_start.assign((size_t)P.npanels, -1);
     P.split_chunks = split_chunks;
     P.nseg = split_chunks > 0 ? std::max(1, (P.nchunks + split_chunks - 1) / split_chunks) : 1;
@@ -351,11 +350,28 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
   for (size_t d = (size_t)(2 * P.stored); d < P.entries.size(); ++d)
     if (P.entries[d] != 0u) return false;
   std::vector<char> used((size_t)std::max(P.M, 1), 0);
+  std::vector<int32_t> pos((size_t)std::max(P.M, 1), -1);
   for (int32_t i = 0; i < P.M; ++i) {
     const int32_t x = P.perm[i];
     if (x < 0 || x >= P.M || used[x]) return false;
     used[x] = 1;
+    pos[x] = i;
   }
+  // every panel row is stored to its original row, or to its position in perm
+  if (P.panel_out.size() != P.panel_rows.size()) return false;
+  std::fill(used.begin(), used.end(), 0);
+  for (size_t j = 0; j < P.panel_rows.size(); ++j) {
+    const int32_t orig = P.panel_rows[j], out = P.panel_out[j];
+    if (orig < 0) {
+      if (out != -1) return false;
+      continue;
+    }
+    if (orig >= P.M || used[orig]) return false;
+    used[orig] = 1;
+    if (out != (P.out_permuted ? pos[orig] : orig)) return false;
+  }
+  for (int32_t i = 0; i < P.M; ++i)
+    if (!used[i]) return false;
   return true;
 }
 
@@ -363,6 +379,7 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
 struct Options {
   std::vector<int32_t> rws;      // panel heights to pack
   int32_t permute = 1;           // row order: Algorithm 1 (see row_order)
+  int32_t grouping = 0;          // panel grouping: 0 by cost, 1 the row order's, 2 balanced
   int32_t out_permuted = 0;      // store C in the permuted row order
   int32_t split_chunks = 0;      // chunks per K-segment (0: no K-segments)
   const int32_t* in_perm = nullptr;  // order of B's rows (NULL: original)
@@ -381,6 +398,8 @@ static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* 
   if (opts->permute < 0 || opts->permute > 5) return SDNN_ERR_DIM;
   if (opts->out_permuted != 0 && opts->out_permuted != 1) return SDNN_ERR_DIM;
   if (opts->split_chunks < 0) return SDNN_ERR_DIM;
+  if (opts->grouping < 0 || opts->grouping > 2) return SDNN_ERR_DIM;
+  o->grouping = opts->grouping;
   o->split_chunks = opts->split_chunks;
   o->permute = opts->permute;
   o->out_permuted = opts->out_permuted;
@@ -650,10 +669,53 @@ static sdnn_status prepare(const int32_t* row_ptr, const int32_t* col_idx, const
   }
   st = row_order(csr->row_ptr, csr->col_idx, M, K, o->permute, perm.data());
   if (st != SDNN_OK) return st;
+  // the panels: consecutive rows of the order, or balanced ones (the order stays the
+  // plan's reported permutation either way, and fixes the stored row order of
+  // out_permuted plans); by cost, the balanced grouping when its heaviest short panel
+  // carries at least 15 % fewer nonzeros (the panels of a workgroup advance together
+  // through the staged chunks, so the heaviest one sets the pace)
+  std::vector<int32_t> balanced, pos;
+  int32_t grouping = o->grouping;
+  try {
+    if (grouping != 1) {
+      balanced.resize(M);
+      balanced_order(csr->row_ptr, M, balanced.data());
+    }
+    if (grouping == 0) {
+      auto heaviest = [&](const std::vector<int32_t>& ord) {
+        int64_t best = 0;
+        for (int32_t p = 0; p * kShortPanel < M; ++p) {
+          int64_t w = 0;
+          for (int32_t r = p * kShortPanel; r < std::min(M, (p + 1) * kShortPanel); ++r)
+            w += csr->row_ptr[ord[r] + 1] - csr->row_ptr[ord[r]];
+          best = std::max(best, w);
+        }
+        return best;
+      };
+      grouping = (double)heaviest(balanced) <= 0.85 * (double)heaviest(perm) ? 2 : 1;
+    }
+    pos.assign((size_t)std::max(M, 1), 0);
+    for (int32_t i = 0; i < M; ++i) pos[perm[i]] = i;
+  } catch (const std::bad_alloc&) {
+    return SDNN_ERR_ALLOC;
+  }
+  const int32_t* group = grouping == 2 ? balanced.data() : perm.data();
   for (size_t i = 0; i < o->rws.size(); ++i) {
-    st = pack(csr->row_ptr, csr->col_idx, csr->values, M, K, o->rws[i], perm.data(),
-              o->split_chunks, &(*packs)[i]);
+    Packed& P = (*packs)[i];
+    st = pack(csr->row_ptr, csr->col_idx, csr->values, M, K, o->rws[i], group, o->split_chunks, &P);
     if (st != SDNN_OK) return st;
+    try {
+      P.perm = perm;
+      P.grouping = grouping;
+      P.out_permuted = o->out_permuted;
+      P.panel_out.assign(P.panel_rows.size(), -1);
+      for (size_t j = 0; j < P.panel_rows.size(); ++j) {
+        const int32_t orig = P.panel_rows[j];
+        if (orig >= 0) P.panel_out[j] = o->out_permuted ? pos[orig] : orig;
+      }
+    } catch (const std::bad_alloc&) {
+      return SDNN_ERR_ALLOC;
+    }
   }
   return SDNN_OK;
 }
@@ -687,6 +749,8 @@ static void fill_info(const std::vector<Packed>& packs, int64_t packed_bytes,
   out->packings = (int32_t)packs.size();
   out->mid_rho = mid ? packs[2].rho : 0.0;
   out->mid_fill = mid ? fill_of(packs[2]) : 0.0;
+  out->grouping = P.grouping;
+  out->reserved = 0;
 }
 
 static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
@@ -694,7 +758,7 @@ static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 // Device bytes of one packing's three arrays (each 256-byte aligned).
 static int64_t packing_bytes(const Packed& P) {
   return align256((int64_t)P.entries.size() * 4) + align256((int64_t)P.panel_start.size() * 4) +
-         align256((int64_t)P.panel_rows.size() * 4) + align256((int64_t)P.panel_order.size() * 4) +
+         align256((int64_t)P.panel_rows.size() * 4) + align256((int64_t)P.panel_out.size() * 4) +
          align256((int64_t)P.seg_start.size() * 4);
 }
 
@@ -798,6 +862,7 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
     plan->out_permuted = o.out_permuted;
     plan->split_chunks = o.split_chunks;
     plan->in_permuted = o.in_perm ? 1 : 0;
+    plan->grouping = P0.grouping;
 
     int64_t total = 0;
     for (const Packed& P : packs) total += packing_bytes(P);
@@ -827,8 +892,8 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
         d.entries = (const uint32_t*)base;
         d.panel_start = (const int32_t*)(base + b_ent);
         d.panel_rows = (const int32_t*)(base + b_ent + b_seg);
-        d.panel_pos = (const int32_t*)(base + b_ent + b_seg + b_rows);
-        const int64_t b_pos = align256((int64_t)P.panel_order.size() * 4);
+        d.panel_out = (const int32_t*)(base + b_ent + b_seg + b_rows);
+        const int64_t b_pos = align256((int64_t)P.panel_out.size() * 4);
         d.nseg = P.nseg;
         d.seg_start = P.seg_start.empty() ? nullptr
                                           : (const int32_t*)(base + b_ent + b_seg + b_rows + b_pos);
@@ -842,7 +907,7 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
           const int32_t q = P.panel_order[j];
           hs[j] = P.panel_start[q];
           memcpy(hr + (size_t)j * P.RW, P.panel_rows.data() + (size_t)q * P.RW, 4 * (size_t)P.RW);
-          hp[j] = q;
+          memcpy(hp + (size_t)j * P.RW, P.panel_out.data() + (size_t)q * P.RW, 4 * (size_t)P.RW);
           if (!P.seg_start.empty())
             memcpy((int32_t*)(h + b_ent + b_seg + b_rows + b_pos) + (size_t)j * P.nseg,
                    P.seg_start.data() + (size_t)q * P.nseg, 4 * (size_t)P.nseg);
@@ -908,6 +973,8 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out) {
   out->packings = p->npack;
   out->mid_rho = mid ? p->pk[2].rho : 0.0;
   out->mid_fill = mid ? p->pk[2].fill : 0.0;
+  out->grouping = p->grouping;
+  out->reserved = 0;
   return SDNN_OK;
 }
 

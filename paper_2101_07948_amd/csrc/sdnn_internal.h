@@ -68,8 +68,14 @@ static_assert(kRing * kChunk <= 128, "ring rows must fit 7 bits");
 struct Packed {
   int32_t M = 0, K = 0, RW = 0, nchunks = 0, npanels = 0;
   int64_t nnz = 0, stored = 0;     // structural entries, stored entries (with padding)
-  std::vector<int32_t> perm;        // [M]   original row at permuted position
-  std::vector<int32_t> panel_rows;  // [npanels*RW] original row or -1 (padding)
+  std::vector<int32_t> perm;        // [M]   original row at permuted position (reported order)
+  std::vector<int32_t> panel_rows;  // [npanels*RW] original row or -1 (padding), in the
+                                    // grouping order (the row order, or balanced panels)
+  std::vector<int32_t> panel_out;   // [npanels*RW] row of C each panel row is stored to
+                                    // (its original row, or its position in perm for
+                                    // out_permuted plans), -1 for padding
+  int32_t grouping = 1;             // 1: panels are consecutive rows of perm; 2: balanced
+  int32_t out_permuted = 0;         // panel_out holds positions in perm
   std::vector<int32_t> panel_start; // [npanels] first group of the panel, or -1
   std::vector<int32_t> panel_order; // [npanels] panels by stored groups, heaviest first
   std::vector<uint32_t> entries;    // [2*(stored + kTailGroups*kGroup)] dwords
@@ -90,9 +96,11 @@ sdnn_status validate_csr(const int32_t* row_ptr, const int32_t* col_idx, int32_t
 // Algorithm 1 on 64-bit column bitsets (inputs already validated).
 sdnn_status reorder_bitset(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K,
                            int32_t* perm_out);
-// Builds the packed stream (inputs already validated, perm is a permutation of 0..M-1).
+// Builds the packed stream (inputs already validated): panel p holds rows
+// group[p*RW .. p*RW+RW-1] (group is a permutation of 0..M-1; out->perm is left to the
+// caller).
 sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* values, int32_t M,
-                 int32_t K, int32_t RW, const int32_t* perm, int32_t split_chunks, Packed* out);
+                 int32_t K, int32_t RW, const int32_t* group, int32_t split_chunks, Packed* out);
 
 // A launch shape sdnn_plan_tune measured fastest for one N: which packing, and how many
 // consumer waves per workgroup.
@@ -107,12 +115,12 @@ struct DevPacking {
   double rho = 1.0, fill = 1.0;
   const uint32_t* entries = nullptr;      // [2*(stored + kTailGroups*kGroup)] dwords
   const int32_t* panel_start = nullptr;   // [npanels] (in groups, -1: empty panel)
-  const int32_t* panel_rows = nullptr;    // [npanels*RW]
-  const int32_t* panel_pos = nullptr;     // [npanels] panel index of each slot
+  const int32_t* panel_rows = nullptr;    // [npanels*RW] original rows (bias)
+  const int32_t* panel_out = nullptr;     // [npanels*RW] rows of C the panel rows go to
   const int32_t* seg_start = nullptr;     // [npanels*nseg] in slot order (split plans)
   int32_t nseg = 1;                       // K-segments
-  // (panel_start and panel_rows are uploaded in slot order: slot j holds panel
-  // panel_pos[j], the j-th heaviest; workgroups take consecutive slots)
+  // (panel_start, panel_rows and panel_out are uploaded in slot order: slot j holds the
+  // j-th heaviest panel; workgroups take consecutive slots)
 };
 
 }  // namespace sdnn
@@ -129,6 +137,7 @@ struct sdnn_plan_s {
   int32_t out_permuted = 0;    // C rows stored in the permuted order
   int32_t in_permuted = 0;     // W's columns renamed to a caller-given order of B's rows
   int32_t split_chunks = 0;    // chunks per K-segment (0: the packings have one segment)
+  int32_t grouping = 1;        // panel grouping the packings use (1: perm order, 2: balanced)
   const int32_t* d_perm = nullptr;  // [M] perm on the device (K-segmented plans only)
   sdnn::DevPacking pk[3];
   sdnn::TunedShape tuned[sdnn::kTunedSlots];  // filled by sdnn_plan_tune

@@ -166,7 +166,7 @@ enum { kStageDword = 0, kStageVec = 1, kStageConv = 2 };
 template <int RW, int STAGE>
 __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     const uint32_t* __restrict__ entries, const int32_t* __restrict__ panel_start,
-    const int32_t* __restrict__ panel_rows, const int32_t* __restrict__ panel_pos,
+    const int32_t* __restrict__ panel_rows, const int32_t* __restrict__ panel_out,
     const int32_t* __restrict__ seg_start, const float* __restrict__ B, float* __restrict__ C,
     const float* __restrict__ bias, SpmmArgs a) {
   // the ring ([0, kRingBytes)) and the control words; the ring must start at LDS 0
@@ -303,7 +303,7 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     for (int r = 0; r < RW; ++r) {
       const int orig = panel_rows[panel * RW + r];
       if (orig < 0) continue;
-      const int row = a.out_permuted ? panel_pos[panel] * RW + r : orig;
+      const int row = panel_out[panel * RW + r];
       const float v[4] = {p0[r], p1[r], p2[r], p3[r]};
       if (splitk) {  // raw partial sums; the reduction adds the bias and applies epi
         float* prow = C + ((size_t)split * a.M + row) * a.N;
@@ -335,7 +335,7 @@ struct SpmmPtrs {
   const uint32_t* entries;
   const int32_t* panel_start;
   const int32_t* panel_rows;
-  const int32_t* panel_pos;
+  const int32_t* panel_out;
   const int32_t* seg_start;
   const float* B;
   float* C;
@@ -346,7 +346,7 @@ template <int RW, int STAGE>
 hipError_t launch_variant(const SpmmPtrs& p, const SpmmArgs& args, int waves, int grid,
                           hipStream_t stream) {
   hipLaunchKernelGGL((spmm_panel_kernel<RW, STAGE>), dim3(grid), dim3(64 * (waves + kProducers)), 0, stream,
-                     p.entries, p.panel_start, p.panel_rows, p.panel_pos, p.seg_start, p.B, p.C,
+                     p.entries, p.panel_start, p.panel_rows, p.panel_out, p.seg_start, p.B, p.C,
                      p.bias, args);
   return hipGetLastError();
 }
@@ -593,7 +593,7 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
     cfg.n_rb = (pk.npanels + cfg.waves - 1) / cfg.waves;
   }
   float* out = nk > 1 ? ws : C;
-  const SpmmPtrs ptrs{pk.entries, pk.panel_start, pk.panel_rows, pk.panel_pos, pk.seg_start, B,
+  const SpmmPtrs ptrs{pk.entries, pk.panel_start, pk.panel_rows, pk.panel_out, pk.seg_start, B,
                       out, bias};
   SpmmArgs args;
   args.K = p->K;

@@ -83,7 +83,7 @@ int main(int argc, char** argv) {
   if (!col_idx || !values || !B || !bias) return 3;
 
   /* segments of 2 chunks (64 rows of B) so that the split call has several */
-  sdnn_plan_opts opts = {0, 1, 0, 2, NULL};
+  sdnn_plan_opts opts = {0, 1, 0, 2, NULL, 0};
   sdnn_plan plan = NULL;
   CHECK_SDNN(sdnn_plan_create(row_ptr, col_idx, values, M, K, &opts, &plan));
   sdnn_plan_info_t info;

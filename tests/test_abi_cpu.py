@@ -254,3 +254,43 @@ def test_generated_kernel_header_in_sync():
     gen = importlib.util.module_from_spec(spec)
     spec.loader.exec_module(gen)
     assert gen.main(check=True) == 0, "spmm_asm_gen.h is stale: run the package build"
+
+
+@pytest.mark.parametrize("grouping", ["order", "balanced"])
+@pytest.mark.parametrize("out_permuted", [False, True])
+def test_panel_grouping_self_check(grouping, out_permuted):
+    """The panels may group rows differently from the reported permutation (consecutive
+    rows of it, or balanced panels): the host self-check re-walks every packing, checks
+    that each panel row is stored to its original row (or, for out_permuted plans, to its
+    position in perm), and the reported permutation stays Algorithm 1's."""
+    L = inputs.workload("c3", N=4).layers[0]
+    W = L.W
+    info = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, grouping=grouping,
+                              out_permuted=out_permuted)
+    assert info["grouping"] == (1 if grouping == "order" else 2)
+
+
+def test_panel_grouping_by_cost():
+    """By cost, the balanced grouping where Algorithm 1 piles long rows into the same
+    panels (the lognormal C3 layers: its heaviest 4-row panel is far above the
+    balanced one's), the permutation's own panels on uniform W0 and on the block-
+    correlated C5 layers (whose panels then keep their column overlap, rho)."""
+    for name, li, kw, want in (("c3", 0, {}, 2), ("c3", 1, {}, 2), ("w0", 0, {}, 1),
+                               ("c5", 0, {"num_layers": 1}, 1), ("c5", 4, {"num_layers": 1}, 1)):
+        W = inputs.workload(name, N=4, **kw).layers[li].W
+        info = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K)
+        assert info["grouping"] == want, (name, li)
+        nnz = np.diff(W.row_ptr)
+        perm = sd.reorder_rows(W.row_ptr, W.col_idx, W.K)
+        heavy_order = nnz[perm][: W.M // 4 * 4].reshape(-1, 4).sum(1).max()
+        bal = sd.row_order(W.row_ptr, W.col_idx, W.K, "balanced")
+        heavy_bal = nnz[bal][: W.M // 4 * 4].reshape(-1, 4).sum(1).max()
+        assert (heavy_bal <= 0.85 * heavy_order) == (want == 2)
+
+
+def test_bad_grouping_rejected():
+    W = inputs.pattern_uniform(16, 16, 0.2, inputs.CFG_TEST, 1, 0.05)
+    for g in (-1, 3):
+        with pytest.raises(sd.SdnnError) as ei:
+            sd.plan_check_host(W.row_ptr, W.col_idx, W.values, 16, 16, grouping=g)
+        assert ei.value.code == 2

@@ -610,3 +610,25 @@ def test_persistent_workgroups(wg_per_tile, N, epi):
     assert np.array_equal(got, one)
     ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, K, B, bias, epi)
     assert np.all(np.abs(got.astype(np.float64) - ref) <= tolerance(bound, ref, epi))
+
+
+@pytest.mark.parametrize("out_permuted", [False, True])
+def test_panel_grouping_bitexact(out_permuted):
+    """Balanced panels and the permutation's consecutive rows give the same C bit for bit
+    (each row sums its entries in ascending column order in any panel), in the original
+    row order and, for out_permuted plans, in the permutation's order; the reported
+    permutation is Algorithm 1's either way."""
+    L = inputs.workload("c3", N=4).layers[1]
+    W = L.W
+    B = inputs.dense_B(W.K, 1000, inputs.CFG_TEST, 77)
+    with sd.Plan.from_csr(W, grouping="order", out_permuted=out_permuted) as p1, \
+            sd.Plan.from_csr(W, grouping="balanced", out_permuted=out_permuted) as p2:
+        assert p1.info["grouping"] == 1 and p2.info["grouping"] == 2
+        want = oracle.reorder(W.row_ptr, W.col_idx, W.K)
+        assert np.array_equal(p1.perm, want) and np.array_equal(p2.perm, want)
+        C1 = gpu_spmm(p1, B, L.bias, "relu")
+        C2 = gpu_spmm(p2, B, L.bias, "relu")
+    assert np.array_equal(C1, C2)
+    ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, W.K, B, L.bias, "relu")
+    order = want if out_permuted else np.arange(W.M)
+    assert np.all(np.abs(C2.astype(np.float64) - ref[order]) <= tolerance(bound[order], ref[order], "relu"))
