@@ -87,6 +87,7 @@ RW_VARIANTS = (4, 8, 12, 16)
 END_BIT, SYNC_BIT, LO_SHIFT, HI_SHIFT = 9, 17, 17, 18
 RING_MASK = 0x1FC00
 CHUNK, RING = 32, 4
+TILE_BYTES = 1024  # bytes of one B row segment of a 256-column tile (the next tile's start)
 PMAX_VEC, PMAX_DWORD = 2, 1                   # chunks in flight per producer variant
 TOUCH_AHEAD = 512  # bytes of stream pulled into L2 ahead of the scalar ring
 GROUP_BYTES = 8 * G
@@ -279,7 +280,9 @@ PISS, PSIG, PINF, PLIM, PTMP, PPOLL, PROW, PM0 = 40, 41, 42, 43, 44, 45, 46, 47
 PADDR, PEX, PBASE, PCS = 48, 50, 52, 54       # 64-bit each
 PCM = 56                                       # column masks (1 or 4 pairs)
 PKM1, PLAST = 64, 65
-PCI, PB0 = 78, 80                              # chunk within the item; the item's first chunk address
+PCI, PB0, PRB = 78, 80, 79                     # chunk within the item; the item's first chunk
+                                               # address; the item's row-block (tile-major items)
+PTB = 82                                       # the item's tile base, B + n0 (64-bit)
 # producer VGPRs: row offsets of the fast path, progress words, min tree
 VO, VP, VMIN = 32, 40, 56
 
@@ -317,8 +320,8 @@ def issue_rows_clamped(vec, half):
             f"s_min_u32 s{PTMP}, s{PROW}, s{PKM1}",
             f"s_mul_i32 s{PADDR}, s{PTMP}, %[rs]",
             f"s_mul_hi_u32 s{PADDR + 1}, s{PTMP}, %[rs]",
-            f"s_add_u32 s{PADDR}, s{PADDR}, %[bb_lo]",
-            f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, %[bb_hi]",
+            f"s_add_u32 s{PADDR}, s{PADDR}, s{PTB}",
+            f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, s{PTB + 1}",
         ]
         if vec:
             L += [f"global_load_lds_dwordx4 %[vl], s[{PADDR}:{PADDR + 1}]",
@@ -462,6 +465,9 @@ def producer(kind):
         f"s_lshr_b32 s{PCS + 1}, %[rs], {32 - lg_chunk}",
         f"s_mov_b64 s[{PB0}:{PB0 + 1}], s[{PBASE}:{PBASE + 1}]",
         f"s_mov_b32 s{PCI}, %[fc]",
+        f"s_mov_b32 s{PRB}, %[rb0]",
+        f"s_mov_b32 s{PTB}, %[bb_lo]",
+        f"s_mov_b32 s{PTB + 1}, %[bb_hi]",
     ]
     if kind == "vec":  # PLAST = K / CHUNK: chunks below it hold CHUNK rows of B
         L += [f"s_lshr_b32 s{PLAST}, %[K], {lg_chunk}",
@@ -555,11 +561,26 @@ def producer(kind):
         f"s_addc_u32 s{PBASE + 1}, s{PBASE + 1}, s{PCS + 1}",
         f"s_add_u32 s{PISS}, s{PISS}, 1",
         f"s_add_u32 s{PINF}, s{PINF}, 1",
-        # the next item (the tile's next row-block) restages the same rows from its start
+        # the next item restages its tile's rows from the start: the same tile (the
+        # tile's next row-block), or, for tile-major items, dtile tiles on plus one more
+        # when the row-block index wraps past the tile's row-blocks
         f"s_add_u32 s{PCI}, s{PCI}, 1",
         f"s_cmp_lt_u32 s{PCI}, %[nci]",
         "s_cbranch_scc1 .L%=_loop",
         f"s_mov_b32 s{PCI}, 0",
+        f"s_add_u32 s{PRB}, s{PRB}, %[drb]",
+        f"s_cmp_lt_u32 s{PRB}, %[nrb]",
+        "s_cbranch_scc1 .L%=_samerb",
+        f"s_sub_u32 s{PRB}, s{PRB}, %[nrb]",
+        f"s_add_u32 s{PB0}, s{PB0}, {TILE_BYTES}",
+        f"s_addc_u32 s{PB0 + 1}, s{PB0 + 1}, 0",
+        f"s_add_u32 s{PTB}, s{PTB}, {TILE_BYTES}",
+        f"s_addc_u32 s{PTB + 1}, s{PTB + 1}, 0",
+        ".L%=_samerb:",
+        f"s_add_u32 s{PB0}, s{PB0}, %[dtb]",
+        f"s_addc_u32 s{PB0 + 1}, s{PB0 + 1}, 0",
+        f"s_add_u32 s{PTB}, s{PTB}, %[dtb]",
+        f"s_addc_u32 s{PTB + 1}, s{PTB + 1}, 0",
         f"s_mov_b64 s[{PBASE}:{PBASE + 1}], s[{PB0}:{PB0 + 1}]",
         "s_branch .L%=_loop",
         # wait for the oldest chunk in flight (loads complete in order), publish it
@@ -585,7 +606,8 @@ def producer(kind):
         f"s_mov_b32 m0, s{PM0}",
     ]
     body = "\n".join('      "' + x + '\\n\\t"' for x in L)
-    sregs = [f"s{x}" for x in list(range(PISS, PCM + 2 * pieces)) + [PKM1, PLAST, PCI, PB0, PB0 + 1]]
+    sregs = [f"s{x}" for x in list(range(PISS, PCM + 2 * pieces)) + [PKM1, PLAST, PCI, PRB, PB0, PB0 + 1,
+                                                                    PTB, PTB + 1]]
     if conv:
         sregs += [f"s{x}" for x in range(RB[0], PXB + 2)]
     vregs = ["v27"] + [f"v{x}" for x in range(VO, VMIN + 5)]
@@ -601,7 +623,8 @@ __device__ __forceinline__ void produce_{kind}(const ProducerArgs& a) {{
         [bb_hi] "s"(a.bbase_hi), [ncol] "s"(a.ncol), [prow0] "s"(a.first_row),
         [vl] "v"(a.vlane), [pg] "v"(a.prog_addr), [ra] "v"(a.ready_addr),
         [budget] "s"(a.poll_budget), [ov] "v"(a.overrun_addr), [fc] "s"(a.first_chunk),
-        [nci] "s"(a.item_chunks){CONV_OPERANDS if conv else ""}
+        [nci] "s"(a.item_chunks), [rb0] "s"(a.item_rb), [drb] "s"(a.item_drb),
+        [nrb] "s"(a.item_nrb), [dtb] "s"(a.item_dtile_bytes){CONV_OPERANDS if conv else ""}
       : {clob});
 }}
 """
@@ -615,6 +638,7 @@ def generate() -> str:
              f"constexpr int kStreamTailGroups = {NSLOT - 1 + (TOUCH_AHEAD + GROUP_BYTES - 1) // GROUP_BYTES + 1};",
              "// stream and ring layout the loops assume",
              f"constexpr int kAsmChunk = {CHUNK}, kAsmRing = {RING}, kAsmProducers = {NPROD};",
+             f"constexpr int kAsmTileBytes = {TILE_BYTES};",
              f"constexpr int kAsmMaxConsumers = {MAX_CONS};",
              f"constexpr int kAsmGroup = {G}, kAsmAccBase = {ACC};",
              f"constexpr int kAsmEndBit = {END_BIT}, kAsmSyncBit = {SYNC_BIT};",

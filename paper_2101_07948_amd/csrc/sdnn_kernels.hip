@@ -64,6 +64,10 @@ struct ProducerArgs {
   int32_t first_chunk;     // first chunk to stage
   int32_t item_chunks;     // chunks per item: ring chunk g stages chunk g % item_chunks of B
                            // (a persistent workgroup's row-blocks restage the same rows)
+  // the item's tile after each item: item_rb += item_drb, wrapping at item_nrb with one
+  // more tile, and item_dtile_bytes more of B (0, 0: every item is on the same tile)
+  int32_t item_rb, item_drb, item_nrb;
+  uint32_t item_dtile_bytes;
   uint32_t row_bytes;      // N * 4
   uint32_t bbase_lo, bbase_hi;  // address of B[0][n0]
   int32_t ncol;            // N - n0 (columns of the tile that exist)
@@ -86,6 +90,7 @@ struct ProducerArgs {
 static_assert(kStreamTailGroups <= kTailGroups, "stream tail shorter than the prefetch");
 static_assert(kAsmChunk == kChunk && kAsmRing == kRing, "ring layout mismatch");
 static_assert(kAsmGroup == kGroup, "group size mismatch");
+static_assert(kAsmTileBytes == kTileCols * 4, "tile width mismatch");
 constexpr int kProducers = kAsmProducers;
 static_assert(kAsmEndBit == kEndBit && kAsmSyncBit == kSyncBit && kAsmLoShift == kLoShift &&
                   kAsmHiShift == kHiShift,
@@ -153,8 +158,10 @@ struct SpmmArgs {
   int32_t M, nsplit, seg_per_split, nseg, split_chunks;
   // persistent workgroups (unsplit launches): wg_per_tile workgroups per column tile,
   // workgroup g of a tile taking row-blocks g, g + wg_per_tile, ... in turn (wg_per_tile =
-  // n_rb: one row-block each)
-  int32_t wg_per_tile;
+  // n_rb: one row-block each); or, tile_major, workgroup w taking the items (tile, row-
+  // block) numbered w, w + total_wg, ... in tile-major order, so that at any time the
+  // workgroups of one XCD (consecutive w) work on consecutive items, mostly of one tile
+  int32_t wg_per_tile, tile_major, n_tiles;
 };
 
 // Producer kinds: 4-byte staging (any N), 16-byte staging (N % 4 == 0, aligned), the
@@ -179,10 +186,13 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
   if (lin >= a.total_wg) return;  // whole workgroup leaves before the barrier
   // workgroups of one tile and run of K-segments are consecutive (they stage the same rows)
   const int per_tile = a.nsplit * a.wg_per_tile;
-  const int tile = lin / per_tile;
-  const int split = (lin - tile * per_tile) / a.wg_per_tile;
-  const int g = lin - tile * per_tile - split * a.wg_per_tile;
-  const int nitems = (a.n_rb - g + a.wg_per_tile - 1) / a.wg_per_tile;  // row-blocks g + i * wg_per_tile
+  const int tile0 = a.tile_major ? lin / a.n_rb : lin / per_tile;
+  const int split = a.tile_major ? 0 : (lin - tile0 * per_tile) / a.wg_per_tile;
+  const int g = a.tile_major ? lin - tile0 * a.n_rb : lin - tile0 * per_tile - split * a.wg_per_tile;
+  // items: row-blocks g + i * wg_per_tile of tile0, or (tile-major) items lin + i * total_wg
+  const int nitems = a.tile_major
+                         ? (a.n_tiles * a.n_rb - lin + a.total_wg - 1) / a.total_wg
+                         : (a.n_rb - g + a.wg_per_tile - 1) / a.wg_per_tile;
   const bool splitk = a.nsplit > 1;
   const int s0 = split * a.seg_per_split, s1 = min(s0 + a.seg_per_split, a.nseg);
   const int c0 = splitk ? s0 * a.split_chunks : 0;
@@ -190,7 +200,6 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
   const int nc = (blockDim.x >> 6) - kProducers;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int n0 = tile * kTileCols;
   const int prod = wave - nc;  // >= 0: producer index
 
   const uint32_t lds_base = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) uint32_t*)lds);
@@ -214,6 +223,11 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     pa.nchunks = splitk ? c1 : nitems * a.nchunks;
     pa.first_chunk = c0;
     pa.item_chunks = splitk ? c1 : a.nchunks;
+    pa.item_rb = a.tile_major ? g : 0;
+    pa.item_drb = a.tile_major ? a.total_wg % a.n_rb : 0;
+    pa.item_nrb = a.tile_major ? a.n_rb : 1;
+    pa.item_dtile_bytes = a.tile_major ? (uint32_t)(a.total_wg / a.n_rb) * (kTileCols * 4u) : 0u;
+    const int n0 = tile0 * kTileCols;
     pa.K = a.K;
     pa.row_bytes = (uint32_t)a.N * 4u;
     const uint64_t bb = (uint64_t)(uintptr_t)(B + n0);
@@ -253,9 +267,14 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     return;
   }
 
-  const int ncol = n0 + lane * 4;
   for (int it = 0; it < nitems; ++it) {
-    const int rb = g + it * a.wg_per_tile;
+    int tile = tile0, rb = g + it * a.wg_per_tile;
+    if (a.tile_major) {
+      const int k = lin + it * a.total_wg;
+      tile = k / a.n_rb;
+      rb = k - tile * a.n_rb;
+    }
+    const int ncol = tile * kTileCols + lane * 4;
     const int panel = rb * nc + wave;
     const uint32_t cbase = splitk ? 0u : (uint32_t)(it * a.nchunks);
     const uint32_t next = it + 1 < nitems ? (uint32_t)((it + 1) * a.nchunks) : kProgressDone;
@@ -267,9 +286,9 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
         for (int sg = s0; sg < s1 && gstart < 0; ++sg) gstart = seg_start[(size_t)panel * a.nseg + sg];
       }
     }
-    if (panel >= a.npanels) {  // no panel here, nor in any later row-block
-      if (lane == 0) ctl[16 + wave] = kProgressDone;
-      return;
+    if (panel >= a.npanels) {  // no panel in this row-block (tile-major: maybe in later ones)
+      if (lane == 0) ctl[16 + wave] = next;
+      continue;
     }
 
     acc_plane_t<RW> p0 = {}, p1 = {}, p2 = {}, p3 = {};
@@ -614,18 +633,42 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
   // recurring per row-block.  Ring chunk numbers run on across row-blocks, so a
   // row-block's chunk c sits in ring slot (base + c) % kRing: the row-blocks' chunk
   // counts must be multiples of kRing, as the stream's ring rows assume c % kRing.
+  // When every tile is full (N a multiple of the tile width) the items go to the
+  // workgroups in tile-major order instead (workgroup w takes items w, w + CUs, ...):
+  // the consecutive workgroups of one XCD then share one or a few tiles at a time, whose
+  // B rows stay in that XCD's L2 across the row-blocks, where CUs / tiles workgroups per
+  // tile would spread each XCD over many tiles (C5's 3072 x 768 layer: 8 tiles of 768 KB
+  // per XCD against a 4 MB L2).
   const int cus = p->num_cus > 0 ? p->num_cus : 256;
-  int wg_per_tile = cfg.n_rb;
-  if (nk == 1 && !conv_hwn && p->nchunks % kRing == 0 &&
-      (int64_t)cfg.n_tiles * cfg.n_rb > cus)
-    wg_per_tile = std::max(1, std::min(cfg.n_rb, cus / std::max(1, cfg.n_tiles)));
-  {
+  const int64_t items = (int64_t)cfg.n_tiles * cfg.n_rb;
+  const bool can_persist = nk == 1 && !conv_hwn && p->nchunks % kRing == 0;
+  int wg_per_tile = cfg.n_rb, tile_major = 0;
+  int64_t total = (int64_t)cfg.n_tiles * nk * cfg.n_rb;
+  if (can_persist && items > cus) {
+    if (N % kTileCols == 0) {
+      tile_major = 1;
+      total = cus;
+    } else {
+      wg_per_tile = std::max(1, std::min(cfg.n_rb, cus / std::max(1, cfg.n_tiles)));
+      total = (int64_t)cfg.n_tiles * wg_per_tile;
+    }
+  }
+  if (can_persist) {  // forced shapes (tests)
     const int forced = env_int("SDNN_FORCE_WG_PER_TILE", 0);
-    if (forced > 0 && nk == 1 && !conv_hwn && p->nchunks % kRing == 0)
+    const int forced_tm = env_int("SDNN_FORCE_TILE_MAJOR_WGS", 0);
+    if (forced > 0) {
+      tile_major = 0;
       wg_per_tile = std::min(forced, cfg.n_rb);
+      total = (int64_t)cfg.n_tiles * wg_per_tile;
+    } else if (forced_tm > 0 && N % kTileCols == 0) {
+      tile_major = 1;
+      wg_per_tile = cfg.n_rb;
+      total = std::min<int64_t>(forced_tm, items);
+    }
   }
   args.wg_per_tile = wg_per_tile;
-  const int64_t total = (int64_t)cfg.n_tiles * nk * wg_per_tile;
+  args.tile_major = tile_major;
+  args.n_tiles = cfg.n_tiles;
   if (total > (int64_t)1 << 30) return hipErrorInvalidValue;
   const int64_t grid = (total + 7) / 8 * 8;
   args.total_wg = (int32_t)total;

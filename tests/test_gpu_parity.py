@@ -632,3 +632,65 @@ def test_panel_grouping_bitexact(out_permuted):
     ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, W.K, B, L.bias, "relu")
     order = want if out_permuted else np.arange(W.M)
     assert np.all(np.abs(C2.astype(np.float64) - ref[order]) <= tolerance(bound[order], ref[order], "relu"))
+
+
+@pytest.mark.parametrize("wgs", [5, 8, 13])
+def test_persistent_workgroups_tile_major(wgs):
+    """Persistent workgroups taking (tile, row-block) items in tile-major order (each
+    workgroup's items on changing tiles, the producers moving to the next item's tile):
+    forced to 5, 8 or 13 workgroups over 4 tiles x 8 row-blocks, against the oracle and
+    bit for bit against one item per workgroup."""
+    M, K, N = 384, 640, 1024
+    W = inputs.pattern_uniform(M, K, 0.1, inputs.CFG_TEST, 400 + wgs, 0.05)
+    B = inputs.dense_B(K, N, inputs.CFG_TEST, 400 + wgs)
+    bias = inputs.bias_normal(M, inputs.CFG_TEST, 400, 0.02)
+    with sd.Plan.from_csr(W, panel_rows=4) as plan:
+        with Forced(waves=12):
+            one = gpu_spmm(plan, B, bias, "gelu")
+            old = os.environ.get("SDNN_FORCE_TILE_MAJOR_WGS")
+            os.environ["SDNN_FORCE_TILE_MAJOR_WGS"] = str(wgs)
+            try:
+                got = gpu_spmm(plan, B, bias, "gelu")
+            finally:
+                if old is None:
+                    os.environ.pop("SDNN_FORCE_TILE_MAJOR_WGS", None)
+                else:
+                    os.environ["SDNN_FORCE_TILE_MAJOR_WGS"] = old
+    assert np.array_equal(got, one)
+    ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, K, B, bias, "gelu")
+    assert np.all(np.abs(got.astype(np.float64) - ref) <= tolerance(bound, ref, "gelu"))
+
+
+@pytest.mark.parametrize("unaligned", [False, True])
+def test_persistent_tile_major_ragged_k(unaligned):
+    """Tile-major persistent items with K = 760 (a last staging chunk of 24 rows, staged by
+    the clamped path) and, unaligned, a B that starts 4 bytes into its allocation (4-byte
+    staging): each item's chunks come from its own tile."""
+    M, K, N = 384, 760, 1024
+    W = inputs.pattern_uniform(M, K, 0.1, inputs.CFG_TEST, 500, 0.05)
+    Bn = inputs.dense_B(K, N, inputs.CFG_TEST, 500)
+    bias = inputs.bias_normal(M, inputs.CFG_TEST, 500, 0.02)
+    buf = torch.zeros(K * N + 1, device=DEV)
+    off = 1 if unaligned else 0
+    buf[off:off + K * N] = torch.from_numpy(Bn.ravel()).to(DEV)
+    Bt = buf[off:off + K * N].view(K, N)
+    outs = []
+    with sd.Plan.from_csr(W, panel_rows=4) as plan:
+        for wgs in (0, 7):
+            old = os.environ.get("SDNN_FORCE_TILE_MAJOR_WGS")
+            if wgs:
+                os.environ["SDNN_FORCE_TILE_MAJOR_WGS"] = str(wgs)
+            try:
+                with Forced(waves=12):
+                    C = torch.full((M, N), float("nan"), device=DEV)
+                    plan.spmm(Bt, C, torch.from_numpy(bias).to(DEV), "relu")
+                    torch.cuda.synchronize()
+                    outs.append(C.cpu().numpy())
+            finally:
+                if old is None:
+                    os.environ.pop("SDNN_FORCE_TILE_MAJOR_WGS", None)
+                else:
+                    os.environ["SDNN_FORCE_TILE_MAJOR_WGS"] = old
+    assert np.array_equal(outs[0], outs[1])
+    ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, K, Bn, bias, "relu")
+    assert np.all(np.abs(outs[1].astype(np.float64) - ref) <= tolerance(bound, ref, "relu"))
