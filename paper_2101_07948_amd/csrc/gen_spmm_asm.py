@@ -256,7 +256,7 @@ def consumer(rw, limit=False):
     planes = ", ".join(f'"+{{v[{ACC + k * rw}:{ACC + k * rw + rw - 1}]}}"(p{k})' for k in range(4))
     sregs = [f"s{x}" for x in range(E[0], (95 if PROFILE else SREADY1) + 1)]
     vregs = [f"v{x}" for x in range(24, ACC)]
-    clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["scc"])
+    clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["scc", "memory"])
     name = f"consume_rw{rw}" + ("_limit" if limit else "")
     operands = ('[sp] "s"(a.stream), [vl] "v"(a.vlane), [pa] "v"(a.prog_addr), '
                 '[ra] "v"(a.ready_addr),\n        [budget] "s"(a.poll_budget), '
@@ -611,7 +611,7 @@ def producer(kind):
     if conv:
         sregs += [f"s{x}" for x in range(RB[0], PXB + 2)]
     vregs = ["v27"] + [f"v{x}" for x in range(VO, VMIN + 5)]
-    clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["vcc", "scc"])
+    clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["vcc", "scc", "memory"])
     title = {"vec": "16-byte staging", "dword": "4-byte staging",
              "conv": "the virtual B of a 3x3 convolution"}[kind]
     return f"""// Producer, {title}
