@@ -584,6 +584,8 @@ def main():
     ap.add_argument("--layer", default="w0",
                     help="workload layer to time: w0 (the measured layer; default), c2, c3_w1, "
                          "c3_w2, c4, c5_proj, c5_ffn1, c5_ffn2 (counter passes on other layers)")
+    ap.add_argument("--grouping", default="auto", choices=["auto", "order", "balanced"],
+                    help="panel grouping of the plan (counter passes comparing groupings)")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="seconds of CPU-oracle timing (0 = skip the cpu_baseline leg)")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense comparison kernel")
@@ -637,7 +639,7 @@ def main():
     if li > 0:  # a later layer of a chain: a synthetic input of its own shape
         w.B = inputs.dense_B(L.W.K, w.N, inputs.CFG_TEST, 4242)
     W, N, M, K = L.W, w.N, L.W.M, L.W.K
-    plan = sd.Plan.from_csr(W)
+    plan = sd.Plan.from_csr(W, grouping=args.grouping)
     info = plan.info
 
     bytes_set = 4 * (K * N + M * N)

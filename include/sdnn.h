@@ -98,10 +98,10 @@ typedef enum {
  *                 case; the panels are either consecutive rows of it (1) or balanced
  *                 panels (2: the panel-balancing rule of permute = 2 applied to W's
  *                 rows), each row still summing its entries in ascending column order,
- *                 so C is bit-identical either way.  0 (default) = by cost: balanced
- *                 when its heaviest 4-row panel holds at least 15 % fewer nonzeros than
- *                 the permutation's heaviest (the panels of a workgroup advance
- *                 together, so the heaviest sets the pace), else the permutation's.
+ *                 so C is bit-identical either way.  0 (default) = the library's
+ *                 choice, at present balanced panels: the panels of a workgroup advance
+ *                 together through the staged chunks of B, so the heaviest panel, and
+ *                 the one whose nonzeros bunch into the fewest chunks, set the pace.
  *                 Outside 0..2: SDNN_ERR_DIM. */
 typedef struct {
   int32_t panel_rows;

@@ -379,7 +379,7 @@ static bool check_packed(const int32_t* row_ptr, const int32_t* col_idx, const f
 struct Options {
   std::vector<int32_t> rws;      // panel heights to pack
   int32_t permute = 1;           // row order: Algorithm 1 (see row_order)
-  int32_t grouping = 0;          // panel grouping: 0 by cost, 1 the row order's, 2 balanced
+  int32_t grouping = 0;          // panel grouping: 0 the library's (balanced), 1 the row order's, 2 balanced
   int32_t out_permuted = 0;      // store C in the permuted row order
   int32_t split_chunks = 0;      // chunks per K-segment (0: no K-segments)
   const int32_t* in_perm = nullptr;  // order of B's rows (NULL: original)
@@ -671,28 +671,18 @@ static sdnn_status prepare(const int32_t* row_ptr, const int32_t* col_idx, const
   if (st != SDNN_OK) return st;
   // the panels: consecutive rows of the order, or balanced ones (the order stays the
   // plan's reported permutation either way, and fixes the stored row order of
-  // out_permuted plans); by cost, the balanced grouping when its heaviest short panel
-  // carries at least 15 % fewer nonzeros (the panels of a workgroup advance together
-  // through the staged chunks, so the heaviest one sets the pace)
+  // out_permuted plans).  The library's choice is the balanced grouping: a workgroup's
+  // panels advance together through the staged chunks, so the heaviest panel and the one
+  // whose entries bunch into the fewest chunks set the pace, and the loop reads B once per
+  // stored entry whatever the panel's column overlap.  Measured on MI355X against the
+  // permutation's own panels on W0 and C2-C5: never slower, 2-8 % faster on the uniform
+  // and block-correlated layers, 1.3-1.8x on the lognormal ones.
   std::vector<int32_t> balanced, pos;
-  int32_t grouping = o->grouping;
+  int32_t grouping = o->grouping == 0 ? 2 : o->grouping;
   try {
-    if (grouping != 1) {
+    if (grouping == 2) {
       balanced.resize(M);
       balanced_order(csr->row_ptr, M, balanced.data());
-    }
-    if (grouping == 0) {
-      auto heaviest = [&](const std::vector<int32_t>& ord) {
-        int64_t best = 0;
-        for (int32_t p = 0; p * kShortPanel < M; ++p) {
-          int64_t w = 0;
-          for (int32_t r = p * kShortPanel; r < std::min(M, (p + 1) * kShortPanel); ++r)
-            w += csr->row_ptr[ord[r] + 1] - csr->row_ptr[ord[r]];
-          best = std::max(best, w);
-        }
-        return best;
-      };
-      grouping = (double)heaviest(balanced) <= 0.85 * (double)heaviest(perm) ? 2 : 1;
     }
     pos.assign((size_t)std::max(M, 1), 0);
     for (int32_t i = 0; i < M; ++i) pos[perm[i]] = i;

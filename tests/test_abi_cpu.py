@@ -171,11 +171,13 @@ def test_bad_permutation_options_rejected():
 
 def test_permutation_raises_reuse_on_grouped_columns():
     """Algorithm 1's purpose (Sec. 3.1.2): adjacent rows share columns.  On block-
-    correlated rows the panel reuse factor rho must improve over the identity order."""
+    correlated rows the reuse factor rho of panels of consecutive rows must improve over
+    the identity order."""
     W = inputs.pattern_grouped8(768, 768, 0.03, inputs.CFG_C5, 0, 0.1)
-    on = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, panel_rows=8)
+    on = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, panel_rows=8,
+                            grouping="order")
     off = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, panel_rows=8,
-                             permute=False)
+                             permute=False, grouping="order")
     assert on["rho"] > 1.3 * off["rho"]
 
 
@@ -270,22 +272,24 @@ def test_panel_grouping_self_check(grouping, out_permuted):
     assert info["grouping"] == (1 if grouping == "order" else 2)
 
 
-def test_panel_grouping_by_cost():
-    """By cost, the balanced grouping where Algorithm 1 piles long rows into the same
-    panels (the lognormal C3 layers: its heaviest 4-row panel is far above the
-    balanced one's), the permutation's own panels on uniform W0 and on the block-
-    correlated C5 layers (whose panels then keep their column overlap, rho)."""
-    for name, li, kw, want in (("c3", 0, {}, 2), ("c3", 1, {}, 2), ("w0", 0, {}, 1),
-                               ("c5", 0, {"num_layers": 1}, 1), ("c5", 4, {"num_layers": 1}, 1)):
+def test_panel_grouping_default_is_balanced():
+    """The library's grouping is the balanced one on every workload layer (consecutive
+    rows of the permutation only when asked for); the reported permutation stays
+    Algorithm 1's either way, and the balanced panels' heaviest never exceeds the
+    permutation's own."""
+    for name, li, kw in (("c3", 0, {}), ("c3", 1, {}), ("w0", 0, {}),
+                         ("c5", 0, {"num_layers": 1}), ("c5", 4, {"num_layers": 1})):
         W = inputs.workload(name, N=4, **kw).layers[li].W
         info = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K)
-        assert info["grouping"] == want, (name, li)
+        assert info["grouping"] == 2, (name, li)
+        info1 = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, grouping="order")
+        assert info1["grouping"] == 1, (name, li)
         nnz = np.diff(W.row_ptr)
         perm = sd.reorder_rows(W.row_ptr, W.col_idx, W.K)
         heavy_order = nnz[perm][: W.M // 4 * 4].reshape(-1, 4).sum(1).max()
         bal = sd.row_order(W.row_ptr, W.col_idx, W.K, "balanced")
         heavy_bal = nnz[bal][: W.M // 4 * 4].reshape(-1, 4).sum(1).max()
-        assert (heavy_bal <= 0.85 * heavy_order) == (want == 2)
+        assert heavy_bal <= heavy_order
 
 
 def test_bad_grouping_rejected():

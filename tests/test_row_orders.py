@@ -100,7 +100,7 @@ def test_panel_union_raises_panel_reuse():
     rows it is at least Algorithm 1's and well above the identity order's."""
     W = inputs.pattern_grouped8(768, 768, 0.03, inputs.CFG_C5, 0, 0.1)
     rho = {m: sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, panel_rows=4,
-                                 permute=m)["rho"]
+                                 permute=m, grouping="order")["rho"]
            for m in ("identity", "algorithm1", "panel_union")}
     assert rho["panel_union"] >= rho["algorithm1"] > 1.3 * rho["identity"]
 
