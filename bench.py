@@ -709,29 +709,26 @@ def main():
     if not args.no_dense:
         Wd = torch.from_numpy(W.to_dense()).to(dev)
         Cd = torch.empty((M, N), device=dev)
-        sd.dense_gemm(Wd, Bs[0], Cd, bias)
-        torch.cuda.synchronize()
-        reps = 10
-        e0.record()
-        for _ in range(reps):
-            sd.dense_gemm(Wd, Bs[0], Cd, bias)
-        e1.record()
-        torch.cuda.synchronize()
-        dms = e0.elapsed_time(e1) / reps
+        reps = 20
+
+        def timed(fn):  # 100 ms settle, then the mean of `reps` back-to-back calls
+            _settle(lambda i: fn(), 100.0)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / reps
+
+        dms = timed(lambda: sd.dense_gemm(Wd, Bs[0], Cd, bias))
         dense = {"ms": round(dms, 4), "tflops": round(2.0 * M * K * N / (dms * 1e-3) / 1e12, 2),
                  "frac_of_fp32_peak": round(2.0 * M * K * N / (dms * 1e-3) / 1e12 / ALU_PEAK_TFLOPS, 4),
                  "sparse_speedup": round(dms / ms, 2)}
         # the vendor BLAS on the same dense product (torch.mm in FP32, TF32 off): context
         # next to the library's own dense kernel, not the comparison the target names
         torch.backends.cuda.matmul.allow_tf32 = False
-        torch.mm(Wd, Bs[0], out=Cd)
-        torch.cuda.synchronize()
-        e0.record()
-        for _ in range(reps):
-            torch.mm(Wd, Bs[0], out=Cd)
-        e1.record()
-        torch.cuda.synchronize()
-        bms = e0.elapsed_time(e1) / reps
+        bms = timed(lambda: torch.mm(Wd, Bs[0], out=Cd))
         dense["vendor_blas"] = {"ms": round(bms, 4),
                                 "tflops": round(2.0 * M * K * N / (bms * 1e-3) / 1e12, 2),
                                 "sparse_speedup": round(bms / ms, 2)}

@@ -827,10 +827,12 @@ hipError_t launch_conv3x3_split(const sdnn_plan_s* p, const float* X, float* C, 
 // Dense FP32 comparison GEMM: C = act(W B + bias), W M x K, B K x N, row-major.  A
 // measurement aid in the role of the paper's dense comparators (Sec. 3.2.1: outer-product
 // microkernel, register blocking, cache tiling), written for the FP32 matrix cores:
-//   * workgroup tile BM x 128 of C (BM = 64, 96 or 128), 8 waves (two per SIMD), each
-//     owning a BM x 16 column strip as BM/16 tiles of v_mfma_f32_16x16x4_f32 (a 16 x 16
-//     accumulator tile in 4 VGPRs per lane; one 16 x 4 slice of W times one 4 x 16 slice
-//     of B per issue), so each B slice a wave reads serves BM/16 products;
+//   * workgroup tile BM x BN of C (128 x 128, 96 x 128, 96 x 64 or 64 x 64, the one that
+//     needs the fewest tile-rounds over the CUs), 8 waves (two per SIMD) arranged as
+//     (8 / (BN / 16)) row bands x (BN / 16) column strips of 16, each wave owning its band
+//     of its strip as tiles of v_mfma_f32_16x16x4_f32 (a 16 x 16 accumulator tile in 4
+//     VGPRs per lane; one 16 x 4 slice of W times one 4 x 16 slice of B per issue), so each
+//     B slice a wave reads serves all of its band's tiles;
 //   * K is walked in stages of 32 through double-buffered LDS: the next stage's W and B
 //     tiles are loaded into registers while the current one is multiplied;
 //   * W's stage is stored as [k % 4][m][k / 4] so that a lane's eight values of its row
