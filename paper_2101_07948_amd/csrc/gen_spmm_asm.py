@@ -148,9 +148,12 @@ def fold_ready():
 def sync(slot, tag):
     """Publish progress = c_lo of the group in `slot`, then wait until its c_hi has
     landed (c_hi < min of the producers' ready words), polling while the budget
-    lasts."""
+    lasts.  Wave priority: a consumer enters each sync point at priority 1 and drops to
+    0 when it has to poll, until its next sync point.  The ring lets no wave run more than
+    four chunks ahead of the slowest, so a wave that waits is ahead of its workgroup, and
+    the SIMD's issue then favours the waves that hold the ring back."""
     width, _, rng = ready_regs()
-    L = [f"s_lshr_b32 s{STMP}, s{slot + LOW}, {LO_SHIFT}",
+    L = ["s_setprio 1", f"s_lshr_b32 s{STMP}, s{slot + LOW}, {LO_SHIFT}",
          f"s_add_u32 s{STMP}, s{STMP}, %[cbase]", f"v_mov_b32 v30, s{STMP}"]
     L += lane0_write("%[pa]", "v30")
     L += [f"s_lshr_b32 s{STMP}, s{slot + HIW}, {HI_SHIFT}", f"s_add_u32 s{STMP}, s{STMP}, %[cbase]"]
@@ -163,6 +166,7 @@ def sync(slot, tag):
         f"s_cmp_eq_u32 s{SPOLL}, 0",
         f"s_cbranch_scc1 .L%=_ready{tag}",
         f"s_sub_u32 s{SPOLL}, s{SPOLL}, 1",
+        "s_setprio 0",
         f"ds_read_{width} {rng}, %[ra]",
         "s_waitcnt lgkmcnt(0)",
     ]
