@@ -365,7 +365,7 @@ def run_suite(out_path):
               f"order, the next plan built with in_perm): {pmean:.2f} ms per forward "
               f"= {flop/(pmean*1e-3)/1e12:.1f} TFLOP/s.",
               f"* Preparation of the {len(w.layers)} plans (validation, Algorithm 1, panel grouping, "
-              f"three packings, upload): {prep_s:.2f} s on the host."]
+              f"four packings, upload): {prep_s:.2f} s on the host."]
     print("\n".join(lines[-4:]), flush=True)
 
     # sparse 3x3 convolutions shaped like the paper's benchmark (Sec. 4.1): IC, OC in

@@ -58,8 +58,8 @@ typedef enum {
 } sdnn_epilogue;
 
 /* Options for sdnn_plan_create; pass NULL for the defaults {0, 1, 0, 0, NULL, 0}.
- *   panel_rows:   rows per register panel.  0 (default) packs W three times, with
- *                 panels of 4, 12 and 8 rows, and sdnn_spmm picks one per call: the
+ *   panel_rows:   rows per register panel.  0 (default) packs W four times, with
+ *                 panels of 4, 12, 8 and 16 rows, and sdnn_spmm picks one per call: the
  *                 fewest rounds of workgroups over the compute units, then the most
  *                 units busy, then the shortest panels averaging at least 8 entries per
  *                 32 columns of W (4-row panels are not used below 7); sdnn_plan_tune
@@ -112,8 +112,9 @@ typedef struct {
   int32_t grouping;
 } sdnn_plan_opts;
 
-/* Plan statistics (of the first packing; the tall_* fields describe the second one and
- * the mid_* fields the third, or are 0 when the plan holds fewer packings).
+/* Plan statistics (of the first packing; the tall_* fields describe the second one, the
+ * mid_* fields the third and the tallest_* fields the fourth, or are 0 when the plan
+ * holds fewer packings).
  *   panels:       number of row panels (ceil(M / panel_rows)).
  *   packed_bytes: device bytes of every packed weight stream and its indexes.
  *   rho:          nnz / sum over panels of |union of the panel rows' column sets|,
@@ -134,6 +135,8 @@ typedef struct {
   double mid_rho, mid_fill;
   int32_t grouping, reserved;         /* panel grouping used: 1 consecutive rows of perm,
                                          2 balanced panels (see sdnn_plan_opts.grouping) */
+  int32_t tallest_panel_rows, reserved2;  /* fourth packing's height (0: none) */
+  double tallest_rho, tallest_fill;
 } sdnn_plan_info_t;
 
 /* Greedy weight-row permutation (Sec. 3.1.2, Algorithm 1), host only, no GPU needed.

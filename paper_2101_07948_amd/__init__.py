@@ -47,7 +47,9 @@ class PlanInfo(ctypes.Structure):
                 ("out_permuted", ctypes.c_int32), ("in_permuted", ctypes.c_int32),
                 ("mid_panel_rows", ctypes.c_int32), ("packings", ctypes.c_int32),
                 ("mid_rho", ctypes.c_double), ("mid_fill", ctypes.c_double),
-                ("grouping", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("grouping", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("tallest_panel_rows", ctypes.c_int32), ("reserved2", ctypes.c_int32),
+                ("tallest_rho", ctypes.c_double), ("tallest_fill", ctypes.c_double)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -236,6 +238,9 @@ class Plan:
         h = ctypes.c_void_p()
         o, _keep = _opts(self.K, panel_rows, permute, out_permuted, in_perm, split_chunks,
                          grouping)
+        # torch first: its HIP runtime is then the one the process (and libsdnn) uses; a
+        # plan created before torch's first load would leave torch without a GPU
+        _torch_mod()
         self._lib = lib()
         _check(self._lib.sdnn_plan_create(_np_ptr(row_ptr), _np_ptr(col_idx), _np_ptr(values),
                                           self.M, self.K, ctypes.byref(o), ctypes.byref(h)),

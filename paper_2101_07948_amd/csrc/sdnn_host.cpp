@@ -387,7 +387,7 @@ struct Options {
 
 // Panel heights to pack: the explicit option, or the short and tall defaults.
 static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* o) {
-  o->rws = {kShortPanel, kTallPanel, kMidPanel};
+  o->rws = {kShortPanel, kTallPanel, kMidPanel, kTallestPanel};
   if (!opts) return SDNN_OK;
   if (opts->panel_rows != 0) {
     if (opts->panel_rows != 4 && opts->panel_rows != 8 && opts->panel_rows != 12 &&
@@ -739,6 +739,11 @@ static void fill_info(const std::vector<Packed>& packs, int64_t packed_bytes,
   out->packings = (int32_t)packs.size();
   out->mid_rho = mid ? packs[2].rho : 0.0;
   out->mid_fill = mid ? fill_of(packs[2]) : 0.0;
+  const bool tallest = packs.size() > 3;
+  out->tallest_panel_rows = tallest ? packs[3].RW : 0;
+  out->reserved2 = 0;
+  out->tallest_rho = tallest ? packs[3].rho : 0.0;
+  out->tallest_fill = tallest ? fill_of(packs[3]) : 0.0;
   out->grouping = P.grouping;
   out->reserved = 0;
 }
@@ -965,6 +970,11 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out) {
   out->mid_fill = mid ? p->pk[2].fill : 0.0;
   out->grouping = p->grouping;
   out->reserved = 0;
+  const bool tallest = p->npack > 3;
+  out->tallest_panel_rows = tallest ? p->pk[3].RW : 0;
+  out->reserved2 = 0;
+  out->tallest_rho = tallest ? p->pk[3].rho : 0.0;
+  out->tallest_fill = tallest ? p->pk[3].fill : 0.0;
   return SDNN_OK;
 }
 

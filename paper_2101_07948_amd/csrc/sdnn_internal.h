@@ -85,11 +85,12 @@ struct Packed {
   std::vector<int32_t> seg_start;   // [npanels*nseg] (split_chunks > 0 only)
 };
 
-// Panel heights of the three packings a default plan holds (in this order): short
+// Panel heights of the four packings a default plan holds (in this order): short
 // panels keep enough waves busy when a tile has few rows per CU; taller ones carry more
 // entries per K-chunk (so a group spans fewer chunks of the ring) and stage each B tile
 // for more rows.  The launch picks one per call (choose_packing).
-constexpr int kShortPanel = 4, kTallPanel = 12, kMidPanel = 8;
+constexpr int kShortPanel = 4, kTallPanel = 12, kMidPanel = 8, kTallestPanel = 16;
+constexpr int kMaxPackings = 4;
 
 // CSR validation; returns SDNN_OK or SDNN_ERR_*.
 sdnn_status validate_csr(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K);
@@ -133,13 +134,13 @@ struct sdnn_plan_s {
   int64_t nnz = 0, packed_bytes = 0;
   std::vector<int32_t> perm;
   void* d_mem = nullptr;       // one device allocation holding every packing's arrays
-  int npack = 0;               // 1 (explicit panel height) or 3 (short, tall, mid)
+  int npack = 0;               // 1 (explicit panel height) or 4 (short, tall, mid, tallest)
   int32_t out_permuted = 0;    // C rows stored in the permuted order
   int32_t in_permuted = 0;     // W's columns renamed to a caller-given order of B's rows
   int32_t split_chunks = 0;    // chunks per K-segment (0: the packings have one segment)
   int32_t grouping = 1;        // panel grouping the packings use (1: perm order, 2: balanced)
   const int32_t* d_perm = nullptr;  // [M] perm on the device (K-segmented plans only)
-  sdnn::DevPacking pk[3];
+  sdnn::DevPacking pk[sdnn::kMaxPackings];
   sdnn::TunedShape tuned[sdnn::kTunedSlots];  // filled by sdnn_plan_tune
   int32_t ntuned = 0;
 };

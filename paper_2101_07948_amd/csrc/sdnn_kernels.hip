@@ -443,7 +443,7 @@ LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N, int nseg = 1) {
   return c;
 }
 
-// The packing a call runs on (a default plan holds 4-, 12- and 8-row packings): among
+// The packing a call runs on (a default plan holds 4-, 12-, 8- and 16-row packings): among
 // the packings, the 4-row one left out when its panels average fewer than 7 entries per
 // 32-row chunk (a group of 8 then spans more than a chunk, which starves the ring's
 // lookahead) and another exists, those needing the fewest rounds of workgroups over the
@@ -459,9 +459,9 @@ const DevPacking& choose_packing(const sdnn_plan_s* p, int N, int nseg = 1) {
   const int cus = p->num_cus > 0 ? p->num_cus : 256;
   const double density = (double)p->nnz / ((double)p->M * (double)p->K);
   auto per_chunk = [&](const DevPacking& pk) { return pk.RW * kChunk * density; };
-  int64_t rounds[3];
-  double util[3];
-  bool live[3];
+  int64_t rounds[kMaxPackings];
+  double util[kMaxPackings];
+  bool live[kMaxPackings];
   int64_t best_rounds = -1;
   for (int k = 0; k < p->npack; ++k) {
     const DevPacking& pk = p->pk[k];

@@ -98,23 +98,26 @@ def test_packed_stream_self_check(name, panel_rows):
 
 
 @pytest.mark.parametrize("name", ["c2", "w0", "c3"])
-def test_default_plan_packs_short_tall_and_mid_panels(name):
-    """With panel_rows = 0 the plan holds 4-, 12- and 8-row packings of the same
-    permutation; all pass the stream self-check and taller panels share more columns."""
+def test_default_plan_packs_four_panel_heights(name):
+    """With panel_rows = 0 the plan holds 4-, 12-, 8- and 16-row packings of the same
+    grouping; all pass the stream self-check, taller panels share more columns, and each
+    packing equals the plan with that height alone."""
     for L in inputs.workload(name, N=4).layers:
         info = sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K)
         assert info["panel_rows"] == 4 and info["tall_panel_rows"] == 12
-        assert info["mid_panel_rows"] == 8 and info["packings"] == 3
+        assert info["mid_panel_rows"] == 8 and info["tallest_panel_rows"] == 16
+        assert info["packings"] == 4
         assert info["panels"] == -(-L.W.M // 4)
-        assert info["tall_rho"] >= info["mid_rho"] >= info["rho"] >= 1.0
-        for f in ("fill", "tall_fill", "mid_fill"):
+        assert info["tallest_rho"] >= info["tall_rho"] >= info["mid_rho"] >= info["rho"] >= 1.0
+        for f in ("fill", "tall_fill", "mid_fill", "tallest_fill"):
             assert 0.0 < info[f] <= 1.0
         singles = {rw: sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K,
-                                          panel_rows=rw) for rw in (4, 8, 12)}
+                                          panel_rows=rw) for rw in (4, 8, 12, 16)}
         for rw, one in singles.items():
             assert one["tall_panel_rows"] == 0 and one["mid_panel_rows"] == 0
-            assert one["packings"] == 1
+            assert one["tallest_panel_rows"] == 0 and one["packings"] == 1
         assert singles[12]["rho"] == info["tall_rho"] and singles[8]["rho"] == info["mid_rho"]
+        assert singles[16]["rho"] == info["tallest_rho"]
         assert info["packed_bytes"] == sum(one["packed_bytes"] for one in singles.values())
 
 
