@@ -62,7 +62,7 @@ typedef enum {
  *                 panels of 4, 12, 8 and 16 rows, and sdnn_spmm picks one per call: the
  *                 fewest rounds of workgroups over the compute units, then the most
  *                 units busy, then the shortest panels averaging at least 8 entries per
- *                 32 columns of W (4-row panels are not used below 7); sdnn_plan_tune
+ *                 32 columns of W (4-row panels are not used below 8); sdnn_plan_tune
  *                 can replace that choice by a timed one, and sdnn_plan_launch_shape
  *                 reports it.  4, 8, 12 or 16 packs that height only.
  *   permute:      1 = apply Algorithm 1 (default), 0 = identity order (ablation),

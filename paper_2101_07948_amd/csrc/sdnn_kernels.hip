@@ -444,9 +444,10 @@ LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N, int nseg = 1) {
 }
 
 // The packing a call runs on (a default plan holds 4-, 12-, 8- and 16-row packings): among
-// the packings, the 4-row one left out when its panels average fewer than 7 entries per
-// 32-row chunk (a group of 8 then spans more than a chunk, which starves the ring's
-// lookahead) and another exists, those needing the fewest rounds of workgroups over the
+// the packings, the 4-row one left out when its panels average fewer than 8 entries per
+// 32-row chunk (a group of 8 then spans a chunk or more, which starves the ring's
+// lookahead, and the workgroups' staging chains outweigh their arithmetic) and another
+// exists, those needing the fewest rounds of workgroups over the
 // tiles (times the K-runs of a split launch) at their full consumer count; among those,
 // the ones keeping the most CUs busy in those rounds (within 5 %); among those, the
 // shortest panels averaging at least 8 entries per chunk, else the tallest.  Measured on
@@ -465,7 +466,7 @@ const DevPacking& choose_packing(const sdnn_plan_s* p, int N, int nseg = 1) {
   int64_t best_rounds = -1;
   for (int k = 0; k < p->npack; ++k) {
     const DevPacking& pk = p->pk[k];
-    live[k] = !(pk.RW == 4 && per_chunk(pk) < 7.0);
+    live[k] = !(pk.RW == 4 && per_chunk(pk) < 8.0);
     const int waves = std::max(1, std::min(max_consumers(pk.RW), pk.npanels));
     const int64_t wgs = n_tiles * ((pk.npanels + waves - 1) / waves);
     rounds[k] = (wgs + cus - 1) / cus;
