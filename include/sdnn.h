@@ -57,7 +57,7 @@ typedef enum {
   SDNN_EPI_GELU = 2  /* 0.5 * x * (1 + erf(x / sqrt(2))) */
 } sdnn_epilogue;
 
-/* Options for sdnn_plan_create; pass NULL for the defaults {0, 1, 0, 0, NULL, 0}.
+/* Options for sdnn_plan_create; pass NULL for the defaults {0, 1, 0, 0, NULL, 0, 0}.
  *   panel_rows:   rows per register panel.  0 (default) packs W four times, with
  *                 panels of 4, 12, 8 and 16 rows, and sdnn_spmm picks one per call: the
  *                 fewest rounds of workgroups over the compute units, then the most
@@ -102,7 +102,17 @@ typedef enum {
  *                 choice, at present balanced panels: the panels of a workgroup advance
  *                 together through the staged chunks of B, so the heaviest panel, and
  *                 the one whose nonzeros bunch into the fewest chunks, set the pace.
- *                 Outside 0..2: SDNN_ERR_DIM. */
+ *                 Outside 0..2: SDNN_ERR_DIM.
+ *   tile_cols:    columns of C per workgroup tile (the microkernel's output tile width,
+ *                 Sec. 3.2.2).  0 (default) = the plan holds its stream for tiles of 256
+ *                 columns (4 per lane, one workgroup per compute unit) and for tiles of 128
+ *                 (2 per lane, half the LDS ring, two workgroups per compute unit), and
+ *                 sdnn_spmm picks one per call (sdnn_plan_launch_tile reports which);
+ *                 256 = 256-column tiles only (half the device memory for the streams);
+ *                 128 = 128-column tiles wherever the call allows them.  128-column tiles
+ *                 serve sdnn_spmm with N % 4 == 0 and 16-byte aligned B and C; K-split
+ *                 calls, convolutions and other sdnn_spmm calls use 256.  Other values:
+ *                 SDNN_ERR_DIM. */
 typedef struct {
   int32_t panel_rows;
   int32_t permute;
@@ -110,6 +120,7 @@ typedef struct {
   int32_t split_chunks;
   const int32_t* in_perm;
   int32_t grouping;
+  int32_t tile_cols;
 } sdnn_plan_opts;
 
 /* Plan statistics (of the first packing; the tall_* fields describe the second one, the
@@ -133,8 +144,9 @@ typedef struct {
   int32_t out_permuted, in_permuted;  /* the plan's options (in_permuted: in_perm given) */
   int32_t mid_panel_rows, packings;   /* third packing's height (0: none); packings held */
   double mid_rho, mid_fill;
-  int32_t grouping, reserved;         /* panel grouping used: 1 consecutive rows of perm,
-                                         2 balanced panels (see sdnn_plan_opts.grouping) */
+  int32_t grouping, tile_cols;        /* panel grouping used: 1 consecutive rows of perm,
+                                         2 balanced panels (see sdnn_plan_opts.grouping);
+                                         the tile_cols option the plan was created with */
   int32_t tallest_panel_rows, reserved2;  /* fourth packing's height (0: none) */
   double tallest_rho, tallest_fill;
 } sdnn_plan_info_t;
@@ -254,6 +266,12 @@ sdnn_status sdnn_spmm_split_noalloc(sdnn_plan p, const float* B, float* C, int32
  * (either pointer may be NULL).  Host only; touches no device memory.
  * Errors: SDNN_ERR_NULL (p), SDNN_ERR_DIM (N <= 0 or M = 0). */
 sdnn_status sdnn_plan_launch_shape(sdnn_plan p, int32_t N, int32_t* panel_rows, int32_t* waves);
+
+/* The tile width (columns of C per workgroup) sdnn_spmm uses for this plan at N columns
+ * when B and C are 16-byte aligned and N % 4 == 0 (otherwise it is 256): the tuned one if
+ * sdnn_plan_tune recorded one for N, else the plan's tile_cols option, else the library's
+ * rule.  Host only.  Errors: SDNN_ERR_NULL (p or tile_cols), SDNN_ERR_DIM (N <= 0, M = 0). */
+sdnn_status sdnn_plan_launch_tile(sdnn_plan p, int32_t N, int32_t* tile_cols);
 
 /* Per-plan variant selection by timing (the paper's preparation stage chooses the best
  * kernel implementation per operator, Sec. 3.1): times sdnn_spmm at this N for every

@@ -34,7 +34,8 @@ class SdnnError(RuntimeError):
 class PlanOpts(ctypes.Structure):
     _fields_ = [("panel_rows", ctypes.c_int32), ("permute", ctypes.c_int32),
                 ("out_permuted", ctypes.c_int32), ("split_chunks", ctypes.c_int32),
-                ("in_perm", ctypes.c_void_p), ("grouping", ctypes.c_int32)]
+                ("in_perm", ctypes.c_void_p), ("grouping", ctypes.c_int32),
+                ("tile_cols", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -47,7 +48,7 @@ class PlanInfo(ctypes.Structure):
                 ("out_permuted", ctypes.c_int32), ("in_permuted", ctypes.c_int32),
                 ("mid_panel_rows", ctypes.c_int32), ("packings", ctypes.c_int32),
                 ("mid_rho", ctypes.c_double), ("mid_fill", ctypes.c_double),
-                ("grouping", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("grouping", ctypes.c_int32), ("tile_cols", ctypes.c_int32),
                 ("tallest_panel_rows", ctypes.c_int32), ("reserved2", ctypes.c_int32),
                 ("tallest_rho", ctypes.c_double), ("tallest_fill", ctypes.c_double)]
 
@@ -84,6 +85,7 @@ def lib() -> ctypes.CDLL:
         L.sdnn_conv3x3.argtypes = [p, p, p, i32, i32, i32, p, ctypes.c_int, p]
         L.sdnn_plan_tune.argtypes = [p, p, p, i32, p, p, p]
         L.sdnn_plan_launch_shape.argtypes = [p, i32, p, p]
+        L.sdnn_plan_launch_tile.argtypes = [p, i32, p]
         i64 = ctypes.c_int64
         L.sdnn_spmm_split.argtypes = [p, p, p, i32, p, ctypes.c_int, i32, p, i64, p]
         L.sdnn_spmm_split_noalloc.argtypes = [p, p, p, i32, p, ctypes.c_int, i32, p]
@@ -91,7 +93,7 @@ def lib() -> ctypes.CDLL:
         for fn in ("sdnn_reorder_rows", "sdnn_row_order", "sdnn_plan_check_host", "sdnn_plan_create",
                    "sdnn_plan_get_perm", "sdnn_plan_info", "sdnn_spmm", "sdnn_dense_gemm",
                    "sdnn_conv3x3", "sdnn_plan_tune", "sdnn_spmm_split", "sdnn_conv3x3_split",
-                   "sdnn_plan_launch_shape", "sdnn_spmm_split_noalloc"):
+                   "sdnn_plan_launch_shape", "sdnn_spmm_split_noalloc", "sdnn_plan_launch_tile"):
             getattr(L, fn).restype = ctypes.c_int
         _lib_handle = L
     return _lib_handle
@@ -130,7 +132,7 @@ GROUPINGS = {"auto": 0, "order": 1, "balanced": 2}
 
 
 def _opts(K: int, panel_rows: int, permute: bool, out_permuted: bool = False, in_perm=None,
-          split_chunks: int = 0, grouping="auto"):
+          split_chunks: int = 0, grouping="auto", tile_cols: int = 0):
     """PlanOpts plus the in_perm array it points to (kept alive by the caller)."""
     keep = None if in_perm is None else _i32(in_perm)
     if keep is not None and keep.shape != (int(K),):
@@ -138,7 +140,7 @@ def _opts(K: int, panel_rows: int, permute: bool, out_permuted: bool = False, in
     mode = _order_mode(permute)
     g = GROUPINGS[grouping] if isinstance(grouping, str) else int(grouping)
     o = PlanOpts(int(panel_rows), mode, 1 if out_permuted else 0, int(split_chunks),
-                 None if keep is None else keep.ctypes.data, g)
+                 None if keep is None else keep.ctypes.data, g, int(tile_cols))
     return o, keep
 
 
@@ -165,11 +167,12 @@ def row_order(row_ptr, col_idx, K: int, permute="algorithm1") -> np.ndarray:
 
 def plan_check_host(row_ptr, col_idx, values, M: int, K: int, panel_rows: int = 0,
                     permute: bool = True, out_permuted: bool = False, in_perm=None,
-                    split_chunks: int = 0, grouping="auto") -> dict:
+                    split_chunks: int = 0, grouping="auto", tile_cols: int = 0) -> dict:
     """Host-only self-check of the preparation stage; returns the plan statistics."""
     row_ptr, col_idx, values = _i32(row_ptr), _i32(col_idx), _f32(values)
     info = PlanInfo()
-    o, _keep = _opts(K, panel_rows, permute, out_permuted, in_perm, split_chunks, grouping)
+    o, _keep = _opts(K, panel_rows, permute, out_permuted, in_perm, split_chunks, grouping,
+                     tile_cols)
     _check(lib().sdnn_plan_check_host(_np_ptr(row_ptr), _np_ptr(col_idx), _np_ptr(values), M, K,
                                       ctypes.byref(o), ctypes.byref(info)),
            "sdnn_plan_check_host")
@@ -227,17 +230,19 @@ class Plan:
 
     def __init__(self, row_ptr, col_idx, values, M: int, K: int, panel_rows: int = 0,
                  permute: bool = True, out_permuted: bool = False, in_perm=None,
-                 split_chunks: int = 0, grouping="auto"):
+                 split_chunks: int = 0, grouping="auto", tile_cols: int = 0):
         """out_permuted: write C in the plan's permuted row order (C[i] = output row
         perm[i]); in_perm: the order of B's rows (B[i] = input feature in_perm[i]),
         e.g. the previous layer's perm when that layer used out_permuted; split_chunks:
         K-segments of that many staging chunks for spmm_split / conv3x3_split;
-        grouping: "auto", "order" (panels are consecutive rows of perm) or "balanced"."""
+        grouping: "auto", "order" (panels are consecutive rows of perm) or "balanced";
+        tile_cols: 0 (the library picks 256 or 128 columns per workgroup tile per call),
+        256 or 128."""
         row_ptr, col_idx, values = _i32(row_ptr), _i32(col_idx), _f32(values)
         self.M, self.K = int(M), int(K)
         h = ctypes.c_void_p()
         o, _keep = _opts(self.K, panel_rows, permute, out_permuted, in_perm, split_chunks,
-                         grouping)
+                         grouping, tile_cols)
         # torch first: its HIP runtime is then the one the process (and libsdnn) uses; a
         # plan created before torch's first load would leave torch without a GPU
         _torch_mod()
@@ -270,11 +275,14 @@ class Plan:
         return info.as_dict()
 
     def launch_shape(self, N: int) -> dict:
-        """The panel height and consumer waves per workgroup spmm uses at N columns."""
-        rw, waves = ctypes.c_int32(), ctypes.c_int32()
+        """The panel height, consumer waves per workgroup and tile width spmm uses at N
+        columns (the tile width for 16-byte aligned B and C with N % 4 == 0)."""
+        rw, waves, tile = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
         _check(self._lib.sdnn_plan_launch_shape(self.handle, int(N), ctypes.byref(rw),
                                                 ctypes.byref(waves)), "sdnn_plan_launch_shape")
-        return {"panel_rows": rw.value, "waves": waves.value}
+        _check(self._lib.sdnn_plan_launch_tile(self.handle, int(N), ctypes.byref(tile)),
+               "sdnn_plan_launch_tile")
+        return {"panel_rows": rw.value, "waves": waves.value, "tile_cols": tile.value}
 
     def tune(self, N: int, B=None, C=None, stream=None) -> dict:
         """Times the plan's launch shapes at this N (on B / C, allocated here when not
@@ -289,7 +297,10 @@ class Plan:
         rw, waves = ctypes.c_int32(), ctypes.c_int32()
         _check(self._lib.sdnn_plan_tune(self.handle, pb, pc, int(N), _stream_handle(stream),
                                         ctypes.byref(rw), ctypes.byref(waves)), "sdnn_plan_tune")
-        return {"panel_rows": rw.value, "waves": waves.value}
+        tile = ctypes.c_int32()
+        _check(self._lib.sdnn_plan_launch_tile(self.handle, int(N), ctypes.byref(tile)),
+               "sdnn_plan_launch_tile")
+        return {"panel_rows": rw.value, "waves": waves.value, "tile_cols": tile.value}
 
     def conv3x3(self, X, C, bias=None, epi: str = "none", stream=None):
         """Sparse 3x3 convolution (stride 1, padding 1) on the GPU: the plan holds the

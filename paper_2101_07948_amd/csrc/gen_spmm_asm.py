@@ -78,84 +78,118 @@ OUT = os.path.join(HERE, "spmm_asm_gen.h")
 G = 8                                         # entries per group (64 bytes)
 NSLOT = 3
 E = tuple(36 + 2 * G * i for i in range(NSLOT))  # SGPR bases of the stream-group ring
-PTR, SREADY, STMP, SPOLL, M0S, SEXEC, SREADY1 = 84, 86, 87, 88, 89, 90, 92
 LOW, HIW = 2 * G - 2, 2 * G - 1               # slot offsets of the c_lo / c_hi words
-VB = (32, 32 + 4 * G)                         # VGPR bases of the two B-value sets
-ACC = 32 + 8 * G                              # first accumulator VGPR
 UNROLL = 6                                    # multiple of NSLOT and of 2
 RW_VARIANTS = (4, 8, 12, 16)
-END_BIT, SYNC_BIT, LO_SHIFT, HI_SHIFT = 9, 17, 17, 18
-RING_MASK = 0x1FC00
+SYNC_BIT, LO_SHIFT, HI_SHIFT = 17, 17, 18
 CHUNK, RING = 32, 4
-TILE_BYTES = 1024  # bytes of one B row segment of a 256-column tile (the next tile's start)
 PMAX_VEC, PMAX_DWORD = 2, 1                   # chunks in flight per producer variant
 TOUCH_AHEAD = 512  # bytes of stream pulled into L2 ahead of the scalar ring
 GROUP_BYTES = 8 * G
 INF = 0x7FFFFFFF
-NPROD = 4          # producer waves; producer p stages rows [p, p+1) * CHUNK/NPROD of a chunk
 MAX_CONS = 14      # consumer waves a workgroup can have
 PROFILE = False    # scratch builds only: time consumers spend waiting (%[twait])
 
 
-def address_phase(slot, vb):
+class Layout:
+    """Tile layout of a kernel variant.  V columns per lane (a tile is 64 V columns), so a
+    staged B row segment is ROW_BYTES = 256 V bytes and the ring row of an entry sits at
+    bit ROW_SHIFT of its address word (the LDS address of the lane's V values is then
+    (a & RING_MASK) | (4 V lane)); the end-of-panel flag sits below the ring-row field,
+    above the 8 bits that VGPR index mode reads.  NPROD producer waves; producer p stages
+    rows [p, p+1) * CHUNK/NPROD of every chunk."""
+
+    def __init__(self, name, v, nprod, row_shift, end_bit, scalars):
+        self.name, self.V, self.NPROD = name, v, nprod
+        # consumer SGPRs besides the stream ring: next group to fetch (64-bit), chunks
+        # known ready, temp, poll budget, saved m0, saved exec (64-bit), temp
+        (self.PTR, self.SREADY, self.STMP, self.SPOLL, self.M0S, self.SEXEC,
+         self.SREADY1) = scalars
+        self.ROW_SHIFT, self.END_BIT = row_shift, end_bit
+        self.ROW_BYTES = 1 << row_shift
+        assert self.ROW_BYTES == 256 * v and end_bit >= 8 and end_bit < row_shift
+        self.RING_MASK = (RING * CHUNK - 1) << row_shift
+        self.VB = (32, 32 + v * G)                # VGPR bases of the two B-value sets
+        self.ACC = 32 + 2 * v * G                 # first accumulator VGPR
+        self.prefix = "" if name == "wide" else "n_"
+
+
+# 256-column tiles (4 columns per lane, ds_read_b128, 1 KB ring rows, 128 KB ring: one
+# workgroup per CU) and 128-column tiles (2 columns per lane, ds_read_b64, 512-byte ring
+# rows, 64 KB ring and two producers: two workgroups per CU)
+# (both kernels run at most 6 waves per SIMD, which leaves 102 SGPRs a wave)
+WIDE = Layout("wide", 4, 4, 10, 9, (84, 86, 87, 88, 89, 90, 92))
+NARROW = Layout("narrow", 2, 2, 9, 8, (84, 86, 87, 88, 89, 90, 92))
+# the wide layout's names, used by the producers and the header
+VB, ACC, END_BIT, RING_MASK = WIDE.VB, WIDE.ACC, WIDE.END_BIT, WIDE.RING_MASK
+TILE_BYTES = WIDE.ROW_BYTES  # bytes of one B row segment of a 256-column tile (the next tile's start)
+NPROD = WIDE.NPROD
+
+
+def address_phase(slot, vb, lay=WIDE):
     L = []
+    v = lay.V
     for j in range(G):
-        L.append(f"v_and_or_b32 v{vb + 4 * j}, s{slot + G + j}, v31, %[vl]")
-        L.append(f"ds_read_b128 v[{vb + 4 * j}:{vb + 4 * j + 3}], v{vb + 4 * j}")
+        L.append(f"v_and_or_b32 v{vb + v * j}, s{slot + G + j}, v31, %[vl]")
+        L.append(f"ds_read_b{32 * v} v[{vb + v * j}:{vb + v * j + v - 1}], v{vb + v * j}")
     return L
 
 
-def fmas(slot, vb, rw):
+def fmas(slot, vb, rw, lay=WIDE):
     L = []
+    v = lay.V
     for j in range(G):
         if j == 0:
             L.append(f"s_set_gpr_idx_on s{slot + G}, gpr_idx(DST,SRC2)")
         else:
             L.append(f"s_set_gpr_idx_idx s{slot + G + j}")
-        for k in range(4):
-            p = ACC + k * rw
-            L.append(f"v_fma_f32 v{p}, s{slot + j}, v{vb + 4 * j + k}, v{p}")
+        for k in range(v):
+            p = lay.ACC + k * rw
+            L.append(f"v_fma_f32 v{p}, s{slot + j}, v{vb + v * j + k}, v{p}")
     L.append("s_set_gpr_idx_off")
     return L
 
 
-def lane0_write(addr, vdata):
+def lane0_write(addr, vdata, lay=WIDE):
     """ds_write_b32 from lane 0 only (all lanes hold the same value)."""
+    SEXEC = lay.SEXEC
     return [f"s_mov_b64 s[{SEXEC}:{SEXEC + 1}], exec", "s_mov_b64 exec, 1",
             f"ds_write_b32 {addr}, {vdata}", f"s_mov_b64 exec, s[{SEXEC}:{SEXEC + 1}]"]
 
 
-def ready_regs():
+def ready_regs(nprod=NPROD):
     """VGPRs that receive the producers' ready words: v27 | v[26:27] | v[24:27]."""
-    assert NPROD in (1, 2, 4)
-    width = {1: "b32", 2: "b64", 4: "b128"}[NPROD]
-    words = [f"v{24 + 4 - NPROD + k}" for k in range(NPROD)]
-    rng = words[0] if NPROD == 1 else f"v[{24 + 4 - NPROD}:27]"
+    assert nprod in (1, 2, 4)
+    width = {1: "b32", 2: "b64", 4: "b128"}[nprod]
+    words = [f"v{24 + 4 - nprod + k}" for k in range(nprod)]
+    rng = words[0] if nprod == 1 else f"v[{24 + 4 - nprod}:27]"
     return width, words, rng
 
 
-def fold_ready():
+def fold_ready(lay=WIDE):
     """SREADY = min of the ready words in ready_regs().  Each word goes from the LDS
     result straight to an SGPR: a VALU write of a VGPR followed at once by
     v_readfirstlane of it reads the old value on gfx950."""
-    _, words, _ = ready_regs()
+    SREADY, SREADY1 = lay.SREADY, lay.SREADY1
+    _, words, _ = ready_regs(lay.NPROD)
     L = [f"v_readfirstlane_b32 s{SREADY}, {words[0]}"]
     for w in words[1:]:
         L += [f"v_readfirstlane_b32 s{SREADY1}, {w}", f"s_min_u32 s{SREADY}, s{SREADY}, s{SREADY1}"]
     return L
 
 
-def sync(slot, tag):
+def sync(slot, tag, lay=WIDE):
     """Publish progress = c_lo of the group in `slot`, then wait until its c_hi has
     landed (c_hi < min of the producers' ready words), polling while the budget
     lasts.  Wave priority: a consumer enters each sync point at priority 1 and drops to
     0 when it has to poll, until its next sync point.  The ring lets no wave run more than
     four chunks ahead of the slowest, so a wave that waits is ahead of its workgroup, and
     the SIMD's issue then favours the waves that hold the ring back."""
-    width, _, rng = ready_regs()
+    STMP, SREADY, SPOLL, SEXEC = lay.STMP, lay.SREADY, lay.SPOLL, lay.SEXEC
+    width, _, rng = ready_regs(lay.NPROD)
     L = ["s_setprio 1", f"s_lshr_b32 s{STMP}, s{slot + LOW}, {LO_SHIFT}",
          f"s_add_u32 s{STMP}, s{STMP}, %[cbase]", f"v_mov_b32 v30, s{STMP}"]
-    L += lane0_write("%[pa]", "v30")
+    L += lane0_write("%[pa]", "v30", lay)
     L += [f"s_lshr_b32 s{STMP}, s{slot + HIW}, {HI_SHIFT}", f"s_add_u32 s{STMP}, s{STMP}, %[cbase]"]
     if PROFILE:
         L += [f"s_memtime s[{SEXEC}:{SEXEC + 1}]", "s_waitcnt lgkmcnt(0)"]
@@ -170,7 +204,7 @@ def sync(slot, tag):
         f"ds_read_{width} {rng}, %[ra]",
         "s_waitcnt lgkmcnt(0)",
     ]
-    L += fold_ready()
+    L += fold_ready(lay)
     L += [
         f"s_cmp_lt_u32 s{STMP}, s{SREADY}",
         f"s_cbranch_scc1 .L%=_ready{tag}",
@@ -184,12 +218,15 @@ def sync(slot, tag):
     return L
 
 
-def consumer(rw, limit=False):
-    """The FMA loop for RW-row panels.  limit: stop before a sync group whose c_lo reaches
-    the chunk limit (K-split launches; the plain loop leaves that test out)."""
+def consumer(rw, limit=False, lay=WIDE):
+    """The FMA loop for RW-row panels of the tile layout `lay`.  limit: stop before a sync
+    group whose c_lo reaches the chunk limit (K-split launches; the plain loop leaves that
+    test out)."""
+    VB, ACC, END_BIT, V = lay.VB, lay.ACC, lay.END_BIT, lay.V
+    PTR, SREADY, STMP, SPOLL, M0S = lay.PTR, lay.SREADY, lay.STMP, lay.SPOLL, lay.M0S
     L = [
         f"s_mov_b32 s{M0S}, m0",
-        f"v_mov_b32 v31, {hex(RING_MASK)}",
+        f"v_mov_b32 v31, {hex(lay.RING_MASK)}",
         "v_mov_b32 v28, 0",
         f"s_mov_b32 s{SREADY}, 0",
         f"s_mov_b32 s{SPOLL}, %[budget]",
@@ -204,11 +241,11 @@ def consumer(rw, limit=False):
         f"s_addc_u32 s{PTR + 1}, s{PTR + 1}, 0",
         "s_waitcnt lgkmcnt(0)",
     ]
-    L += sync(E[0], "e")   # a panel's first group always carries the sync bit
-    L += address_phase(E[0], VB[0])
+    L += sync(E[0], "e", lay)   # a panel's first group always carries the sync bit
+    L += address_phase(E[0], VB[0], lay)
     L += [f"s_bitcmp1_b32 s{E[0] + HIW}, {END_BIT}", "s_cbranch_scc0 .L%=_iter0",
           "s_waitcnt lgkmcnt(0)"]   # the panel is one group
-    L += fmas(E[0], VB[0], rw)
+    L += fmas(E[0], VB[0], rw, lay)
     L.append("s_branch .L%=_finish")
     for i in range(UNROLL):
         cur, nxt, pre = E[i % NSLOT], E[(i + 1) % NSLOT], E[(i + NSLOT - 1) % NSLOT]
@@ -221,8 +258,8 @@ def consumer(rw, limit=False):
         if TOUCH_AHEAD:  # pull the stream line TOUCH_AHEAD bytes ahead into L2
             L.append(f"global_load_dword v29, v28, s[{PTR}:{PTR + 1}] offset:{TOUCH_AHEAD}")
         L += [f"s_add_u32 s{PTR}, s{PTR}, {GROUP_BYTES}", f"s_addc_u32 s{PTR + 1}, s{PTR + 1}, 0"]
-        L += address_phase(nxt, vbn)
-        L += fmas(cur, vbc, rw)
+        L += address_phase(nxt, vbn, lay)
+        L += fmas(cur, vbc, rw, lay)
     L.append("s_branch .L%=_iter0")
     for i in range(UNROLL):
         cur, nxt = E[i % NSLOT], E[(i + 1) % NSLOT]
@@ -233,16 +270,16 @@ def consumer(rw, limit=False):
             # K-segments: finish with the current group
             L += [f"s_lshr_b32 s{STMP}, s{nxt + LOW}, {LO_SHIFT}",
                   f"s_cmp_ge_u32 s{STMP}, %[climit]", f"s_cbranch_scc1 .L%=_stop{i}"]
-        L += sync(nxt, i)
+        L += sync(nxt, i, lay)
         L += [f"s_bitcmp1_b32 s{nxt + HIW}, {END_BIT}", f"s_cbranch_scc0 .L%=_ret{i}"]
-        L += address_phase(nxt, vbn)       # group g+1 ends the panel
-        L += fmas(cur, vbc, rw)
+        L += address_phase(nxt, vbn, lay)  # group g+1 ends the panel
+        L += fmas(cur, vbc, rw, lay)
         L.append("s_waitcnt lgkmcnt(0)")
-        L += fmas(nxt, vbn, rw)
+        L += fmas(nxt, vbn, rw, lay)
         L.append("s_branch .L%=_finish")
         if limit:
             L.append(f".L%=_stop{i}:")       # the current group's reads have landed
-            L += fmas(cur, vbc, rw)
+            L += fmas(cur, vbc, rw, lay)
             L.append("s_branch .L%=_finish")
     # a wave that went on without waiting, or whose chunks a producer may have
     # overwritten, leaves NaN instead of unchecked values
@@ -252,24 +289,26 @@ def consumer(rw, limit=False):
           f"v_readfirstlane_b32 s{STMP}, v30",
           f"s_cmp_eq_u32 s{STMP}, 0", "s_cbranch_scc1 .L%=_clean",
           ".L%=_poison:"]
-    L += [f"v_mov_b32 v{ACC + x}, 0x7fc00000" for x in range(4 * rw)]
+    L += [f"v_mov_b32 v{ACC + x}, 0x7fc00000" for x in range(V * rw)]
     L += [".L%=_clean:", "v_mov_b32 v30, %[next]"]
-    L += lane0_write("%[pa]", "v30")
+    L += lane0_write("%[pa]", "v30", lay)
     L += ["s_waitcnt vmcnt(0) lgkmcnt(0)", f"s_mov_b32 m0, s{M0S}"]
     body = "\n".join('      "' + x + '\\n\\t"' for x in L)
-    planes = ", ".join(f'"+{{v[{ACC + k * rw}:{ACC + k * rw + rw - 1}]}}"(p{k})' for k in range(4))
-    sregs = [f"s{x}" for x in range(E[0], (95 if PROFILE else SREADY1) + 1)]
-    vregs = [f"v{x}" for x in range(24, ACC)]
+    planes = ", ".join(f'"+{{v[{ACC + k * rw}:{ACC + k * rw + rw - 1}]}}"(p{k})' for k in range(V))
+    lo, hi = min(E[0], PTR), max(E[-1] + 2 * G - 1, lay.SREADY1)
+    sregs = [f"s{x}" for x in range(lo, (95 if PROFILE else hi) + 1)]
+    # v24..v31 minus the ready words a narrow consumer does not read, then the B sets
+    vregs = [f"v{x}" for x in range(24 + 4 - lay.NPROD, ACC)]
     clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["scc", "memory"])
-    name = f"consume_rw{rw}" + ("_limit" if limit else "")
+    name = f"consume_{lay.prefix}rw{rw}" + ("_limit" if limit else "")
     operands = ('[sp] "s"(a.stream), [vl] "v"(a.vlane), [pa] "v"(a.prog_addr), '
                 '[ra] "v"(a.ready_addr),\n        [budget] "s"(a.poll_budget), '
                 '[ov] "v"(a.overrun_addr), [cbase] "s"(a.chunk_base), [next] "s"(a.next_progress)'
                 + (', [climit] "s"(a.chunk_limit)' if limit else ''))
-    return f"""// Consumer, RW = {rw}{', stopping at the chunk limit' if limit else ''}: accumulator planes p0..p3
-__device__ __forceinline__ void {name}(acc_plane_t<{rw}>& p0, acc_plane_t<{rw}>& p1,
-                                         acc_plane_t<{rw}>& p2, acc_plane_t<{rw}>& p3,
-                                         {'' if PROFILE else 'const '}ConsumerArgs& a) {{
+    params = ", ".join(f"acc_plane_t<{rw}>& p{k}" for k in range(V))
+    return f"""// Consumer, RW = {rw}, {64 * V}-column tiles{', stopping at the chunk limit' if limit else ''}: accumulator planes p0..p{V - 1}
+__device__ __forceinline__ void {name}({params},
+    {'' if PROFILE else 'const '}ConsumerArgs& a) {{
   asm volatile(
 {body}
       : {planes}{', [twait] "=&s"(a.twait)' if PROFILE else ''}
@@ -339,6 +378,28 @@ def issue_rows_clamped(vec, half):
                 L += [f"s_mov_b64 exec, s[{m}:{m + 1}]", "s_nop 0",
                       f"global_load_lds_dword %[vl], s[{PADDR}:{PADDR + 1}]",
                       "s_add_u32 m0, m0, 0x100"]
+        L.append(f"s_add_u32 s{PROW}, s{PROW}, 1")
+    return L
+
+
+def issue_rows_clamped_narrow(half):
+    """128-column tiles: stage rows PROW .. PROW+half-1 of B (each clamped to K-1) two per
+    1 KB of LDS at m0, m0+1KB, ...: row r to lanes 0-31 (bytes 0-511 of the pair), row r+1
+    to lanes 32-63, each half its own DMA with its own clamped row (%[vl] = 16 (lane % 32))."""
+    L = []
+    for r in range(half):
+        L += [
+            f"s_min_u32 s{PTMP}, s{PROW}, s{PKM1}",
+            f"s_mul_i32 s{PADDR}, s{PTMP}, %[rs]",
+            f"s_mul_hi_u32 s{PADDR + 1}, s{PTMP}, %[rs]",
+            f"s_add_u32 s{PADDR}, s{PADDR}, s{PTB}",
+            f"s_addc_u32 s{PADDR + 1}, s{PADDR + 1}, s{PTB + 1}",
+        ]
+        m = PCM + 2 + 2 * (r % 2)       # lanes 0-31, then lanes 32-63 (column-masked)
+        L += [f"s_mov_b64 exec, s[{m}:{m + 1}]",
+              f"global_load_lds_dwordx4 %[vl], s[{PADDR}:{PADDR + 1}]"]
+        if r % 2:
+            L.append("s_add_u32 m0, m0, 0x400")
         L.append(f"s_add_u32 s{PROW}, s{PROW}, 1")
     return L
 
@@ -433,7 +494,8 @@ def issue_rows_conv(half):
 
 def producer(kind):
     """Producer loop (kind: "vec" 16-byte rows, "dword" 4-byte pieces, "conv" the virtual
-    B of a 3x3 convolution).  State: issued (chunks whose loads went out), landed
+    B of a 3x3 convolution, "vecn" 16-byte rows of 128-column tiles: two 512-byte rows
+    per DMA, lanes 0-31 the first).  State: issued (chunks whose loads went out), landed
     (chunks published in the ready word), in flight = issued - landed <= PMAX, and the
     cached issue limit PLIM (re-read from the progress words only when issued reaches
     it).  vec: chunks below PLAST take the fast path: the chunk's base address advances
@@ -442,13 +504,18 @@ def producer(kind):
     when K is not a multiple of CHUNK, and every chunk of the 4-byte variant, take the
     clamped path, which re-stages row K-1 for rows past K (LDS rows no entry reads).
     conv: rows as in issue_rows_conv, `half` loads per chunk like vec."""
-    vec = kind in ("vec", "conv")
+    narrow = kind == "vecn"
+    lay = NARROW if narrow else WIDE
+    vec = kind in ("vec", "conv", "vecn")
     conv = kind == "conv"
-    half = CHUNK // NPROD
+    half = CHUNK // lay.NPROD
     pmax = PMAX_VEC if vec else PMAX_DWORD
-    loads_per_chunk = half if vec else 4 * half
+    # loads of a fast-path chunk (the clamped path of a narrow chunk issues twice as many,
+    # which only makes the vmcnt waits below wait longer)
+    loads_per_chunk = half // 2 if narrow else half if vec else 4 * half
     assert loads_per_chunk * (pmax - 1) <= 63
     lg_chunk = CHUNK.bit_length() - 1
+    rs_lg = lay.ROW_SHIFT
     L = [
         f"s_mov_b32 s{PM0}, m0",
         f"s_mov_b32 s{PISS}, %[fc]",
@@ -478,6 +545,12 @@ def producer(kind):
               f"v_mov_b32 v{VO}, %[vl]"]
         for r in range(1, half):
             L.append(f"v_add_u32 v{VO + r}, %[rs], v{VO + r - 1}")
+    elif narrow:  # v[VO + j] = %[vf] + 2 j row_bytes (%[vf]: lanes 32-63 one row on)
+        L += [f"s_lshr_b32 s{PLAST}, %[K], {lg_chunk}",
+              f"v_mov_b32 v{VO}, %[vf]",
+              f"s_lshl_b32 s{PTMP}, %[rs], 1"]
+        for r in range(1, half // 2):
+            L.append(f"v_add_u32 v{VO + r}, s{PTMP}, v{VO + r - 1}")
     else:
         L.append(f"s_mov_b32 s{PLAST}, 0")
     if conv:
@@ -488,9 +561,22 @@ def producer(kind):
               f"s_mov_b32 s{PXB}, %[bb_lo]",
               f"s_mov_b32 s{PXB + 1}, %[bb_hi]"]
     # column masks: vec -> lanes whose 4 columns exist (lane < ncol / 4);
-    # dword -> piece q of a row: lanes with 64 q + lane < ncol
-    pieces = 1 if vec else 4
-    for q in range(pieces):
+    # dword -> piece q of a row: lanes with 64 q + lane < ncol;
+    # vecn -> lanes with lane % 32 < ncol / 4 (both rows of a pair), then the lanes 0-31
+    # and the lanes 32-63 of that mask
+    pieces = 3 if narrow else 1 if vec else 4
+    if narrow:
+        L += [
+            f"s_lshr_b32 s{PTMP}, %[ncol], 2",
+            f"s_min_u32 s{PTMP}, s{PTMP}, 32",
+            f"s_bfm_b64 s[{PCM}:{PCM + 1}], s{PTMP}, 0",
+            f"s_mov_b32 s{PCM + 1}, s{PCM}",
+            f"s_mov_b32 s{PCM + 2}, s{PCM}",
+            f"s_mov_b32 s{PCM + 3}, 0",
+            f"s_mov_b32 s{PCM + 4}, 0",
+            f"s_mov_b32 s{PCM + 5}, s{PCM}",
+        ]
+    for q in range(0 if narrow else pieces):
         m = PCM + 2 * q
         if vec:
             L.append(f"s_lshr_b32 s{PTMP}, %[ncol], 2")
@@ -537,8 +623,8 @@ def producer(kind):
         # (issued % RING) * CHUNK + prow0
         ".L%=_issue:",
         f"s_and_b32 s{PTMP}, s{PISS}, {RING - 1}",
-        f"s_lshl_b32 s{PTMP}, s{PTMP}, {lg_chunk + 10}",
-        "s_lshl_b32 m0, %[prow0], 10",
+        f"s_lshl_b32 s{PTMP}, s{PTMP}, {lg_chunk + rs_lg}",
+        f"s_lshl_b32 m0, %[prow0], {rs_lg}",
         f"s_add_u32 m0, m0, s{PTMP}",
         f"s_mov_b64 s[{PEX}:{PEX + 1}], exec",
     ]
@@ -548,7 +634,7 @@ def producer(kind):
         L += [f"s_cmp_lt_u32 s{PCI}, s{PLAST}", "s_cbranch_scc0 .L%=_clamped"]
         if vec:
             L.append(f"s_mov_b64 exec, s[{PCM}:{PCM + 1}]")   # also spaces the m0 write from the DMA
-            for r in range(half):
+            for r in range(loads_per_chunk):
                 if r:
                     L.append("s_nop 0")                       # m0 write, then a DMA reading it
                 L += [f"global_load_lds_dwordx4 v{VO + r}, s[{PBASE}:{PBASE + 1}]",
@@ -557,7 +643,7 @@ def producer(kind):
         L += [".L%=_clamped:",
               f"s_lshl_b32 s{PROW}, s{PCI}, {lg_chunk}",
               f"s_add_u32 s{PROW}, s{PROW}, %[prow0]"]
-        L += issue_rows_clamped(vec, half)
+        L += issue_rows_clamped_narrow(half) if narrow else issue_rows_clamped(vec, half)
     L += [
         ".L%=_issued:",
         f"s_mov_b64 exec, s[{PEX}:{PEX + 1}]",
@@ -576,9 +662,9 @@ def producer(kind):
         f"s_cmp_lt_u32 s{PRB}, %[nrb]",
         "s_cbranch_scc1 .L%=_samerb",
         f"s_sub_u32 s{PRB}, s{PRB}, %[nrb]",
-        f"s_add_u32 s{PB0}, s{PB0}, {TILE_BYTES}",
+        f"s_add_u32 s{PB0}, s{PB0}, {lay.ROW_BYTES}",
         f"s_addc_u32 s{PB0 + 1}, s{PB0 + 1}, 0",
-        f"s_add_u32 s{PTB}, s{PTB}, {TILE_BYTES}",
+        f"s_add_u32 s{PTB}, s{PTB}, {lay.ROW_BYTES}",
         f"s_addc_u32 s{PTB + 1}, s{PTB + 1}, 0",
         ".L%=_samerb:",
         f"s_add_u32 s{PB0}, s{PB0}, %[dtb]",
@@ -617,7 +703,8 @@ def producer(kind):
     vregs = ["v27"] + [f"v{x}" for x in range(VO, VMIN + 5)]
     clob = ", ".join(f'"{r}"' for r in sregs + vregs + ["vcc", "scc", "memory"])
     title = {"vec": "16-byte staging", "dword": "4-byte staging",
-             "conv": "the virtual B of a 3x3 convolution"}[kind]
+             "conv": "the virtual B of a 3x3 convolution",
+             "vecn": "16-byte staging of 128-column tiles"}[kind]
     return f"""// Producer, {title}
 __device__ __forceinline__ void produce_{kind}(const ProducerArgs& a) {{
   asm volatile(
@@ -628,7 +715,7 @@ __device__ __forceinline__ void produce_{kind}(const ProducerArgs& a) {{
         [vl] "v"(a.vlane), [pg] "v"(a.prog_addr), [ra] "v"(a.ready_addr),
         [budget] "s"(a.poll_budget), [ov] "v"(a.overrun_addr), [fc] "s"(a.first_chunk),
         [nci] "s"(a.item_chunks), [rb0] "s"(a.item_rb), [drb] "s"(a.item_drb),
-        [nrb] "s"(a.item_nrb), [dtb] "s"(a.item_dtile_bytes){CONV_OPERANDS if conv else ""}
+        [nrb] "s"(a.item_nrb), [dtb] "s"(a.item_dtile_bytes){CONV_OPERANDS if conv else ""}{', [vf] "v"(a.vlane_fast)' if narrow else ""}
       : {clob});
 }}
 """
@@ -648,12 +735,18 @@ def generate() -> str:
              f"constexpr int kAsmEndBit = {END_BIT}, kAsmSyncBit = {SYNC_BIT};",
              f"constexpr int kAsmLoShift = {LO_SHIFT}, kAsmHiShift = {HI_SHIFT};",
              f"constexpr uint32_t kAsmRingMask = {hex(RING_MASK)}u;",
+             "// the same for 128-column tiles",
+             f"constexpr int kAsmProducersN = {NARROW.NPROD}, kAsmTileBytesN = {NARROW.ROW_BYTES};",
+             f"constexpr int kAsmAccBaseN = {NARROW.ACC}, kAsmEndBitN = {NARROW.END_BIT};",
+             f"constexpr uint32_t kAsmRingMaskN = {hex(NARROW.RING_MASK)}u;",
              f"constexpr uint32_t kProgressDone = {hex(INF)}u;",
              ""]
     for rw in RW_VARIANTS:
         parts.append(consumer(rw))
         parts.append(consumer(rw, limit=True))
-    for kind in ("vec", "dword", "conv"):
+    for rw in RW_VARIANTS:
+        parts.append(consumer(rw, lay=NARROW))
+    for kind in ("vec", "dword", "conv", "vecn"):
         parts.append(producer(kind))
     return "\n".join(parts)
 

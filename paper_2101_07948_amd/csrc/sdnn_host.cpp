@@ -383,6 +383,7 @@ struct Options {
   int32_t out_permuted = 0;      // store C in the permuted row order
   int32_t split_chunks = 0;      // chunks per K-segment (0: no K-segments)
   const int32_t* in_perm = nullptr;  // order of B's rows (NULL: original)
+  int32_t tile_cols = 0;         // 0: both tile widths; 256: 256-column tiles only; 128: 128 where the call allows
 };
 
 // Panel heights to pack: the explicit option, or the short and tall defaults.
@@ -399,7 +400,10 @@ static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* 
   if (opts->out_permuted != 0 && opts->out_permuted != 1) return SDNN_ERR_DIM;
   if (opts->split_chunks < 0) return SDNN_ERR_DIM;
   if (opts->grouping < 0 || opts->grouping > 2) return SDNN_ERR_DIM;
+  if (opts->tile_cols != 0 && opts->tile_cols != kTileCols && opts->tile_cols != kNarrowTileCols)
+    return SDNN_ERR_DIM;
   o->grouping = opts->grouping;
+  o->tile_cols = opts->tile_cols;
   o->split_chunks = opts->split_chunks;
   o->permute = opts->permute;
   o->out_permuted = opts->out_permuted;
@@ -745,16 +749,52 @@ static void fill_info(const std::vector<Packed>& packs, int64_t packed_bytes,
   out->tallest_rho = tallest ? packs[3].rho : 0.0;
   out->tallest_fill = tallest ? fill_of(packs[3]) : 0.0;
   out->grouping = P.grouping;
-  out->reserved = 0;
+  out->tile_cols = o.tile_cols;
 }
 
 static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
-// Device bytes of one packing's three arrays (each 256-byte aligned).
-static int64_t packing_bytes(const Packed& P) {
-  return align256((int64_t)P.entries.size() * 4) + align256((int64_t)P.panel_start.size() * 4) +
-         align256((int64_t)P.panel_rows.size() * 4) + align256((int64_t)P.panel_out.size() * 4) +
-         align256((int64_t)P.seg_start.size() * 4);
+// Device bytes of one packing's arrays (each 256-byte aligned), with the stream of the
+// 128-column tiles when `narrow`.
+static int64_t packing_bytes(const Packed& P, bool narrow) {
+  return align256((int64_t)P.entries.size() * 4) * (narrow ? 2 : 1) +
+         align256((int64_t)P.panel_start.size() * 4) + align256((int64_t)P.panel_rows.size() * 4) +
+         align256((int64_t)P.panel_out.size() * 4) + align256((int64_t)P.seg_start.size() * 4);
+}
+
+// Plans serve 128-column tiles unless the option fixes 256.
+static bool wants_narrow(const Options& o) { return o.tile_cols != kTileCols; }
+
+std::vector<uint32_t> narrow_stream(const std::vector<uint32_t>& entries) {
+  std::vector<uint32_t> out(entries);
+  const size_t groups = entries.size() / (2 * kGroup);
+  for (size_t g = 0; g < groups; ++g)
+    for (int j = 0; j < kGroup; ++j) {
+      uint32_t& a = out[g * 2 * kGroup + kGroup + j];
+      const uint32_t ring = (a >> kRingRowShift) & (uint32_t)(kRing * kChunk - 1);
+      const uint32_t end = (a >> kEndBit) & 1u;
+      const uint32_t high = a & ~((1u << kSyncBit) - 1u);  // chunk and sync fields
+      a = high | ring << kRingRowShiftNarrow | end << kEndBitNarrow | (a & ((1u << kRowBits) - 1u));
+    }
+  return out;
+}
+
+bool check_narrow_stream(const std::vector<uint32_t>& entries, const std::vector<uint32_t>& narrow) {
+  if (narrow.size() != entries.size()) return false;
+  for (size_t d = 0; d < entries.size(); ++d) {
+    const uint32_t w = entries[d], n = narrow[d];
+    if ((d / kGroup) % 2 == 0) {  // weight words are copied
+      if (w != n) return false;
+      continue;
+    }
+    // address words: row (bits 0-7), ring row, end flag, and bits 17 up
+    if ((w & 0xffu) != (n & 0xffu)) return false;
+    if (((w >> 10) & 0x7fu) != ((n >> 9) & 0x7fu)) return false;
+    if (((w >> 9) & 1u) != ((n >> 8) & 1u)) return false;
+    if ((w >> 17) != (n >> 17)) return false;
+    if ((n >> 16) & 1u) return false;  // the narrow layout leaves bit 16 clear
+  }
+  return true;
 }
 
 }  // namespace sdnn
@@ -815,7 +855,9 @@ sdnn_status sdnn_plan_check_host(const int32_t* row_ptr, const int32_t* col_idx,
     int64_t bytes = 0;
     for (const Packed& P : packs) {
       if (!check_packed(csr.row_ptr, csr.col_idx, csr.values, P)) return SDNN_ERR_INTERNAL;
-      bytes += packing_bytes(P);
+      if (wants_narrow(o) && !check_narrow_stream(P.entries, narrow_stream(P.entries)))
+        return SDNN_ERR_INTERNAL;
+      bytes += packing_bytes(P, wants_narrow(o));
     }
     if (o.split_chunks > 0) bytes += align256((int64_t)M * 4);  // the device copy of perm
     if (info) fill_info(packs, bytes, o, info);
@@ -858,9 +900,11 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
     plan->split_chunks = o.split_chunks;
     plan->in_permuted = o.in_perm ? 1 : 0;
     plan->grouping = P0.grouping;
+    plan->tile_cols = o.tile_cols;
+    const bool narrow = wants_narrow(o);
 
     int64_t total = 0;
-    for (const Packed& P : packs) total += packing_bytes(P);
+    for (const Packed& P : packs) total += packing_bytes(P, narrow);
     // a K-segmented plan's reduction adds the bias through perm (out_permuted plans)
     const int64_t perm_off = total;
     if (o.split_chunks > 0) total += align256((int64_t)M * 4);
@@ -885,6 +929,9 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
         d.rho = P.rho;
         d.fill = fill_of(P);
         d.entries = (const uint32_t*)base;
+        // the 128-column stream sits after the packing's other arrays
+        const int64_t b_all = packing_bytes(P, false);
+        d.entries_n = narrow ? (const uint32_t*)(base + b_all) : nullptr;
         d.panel_start = (const int32_t*)(base + b_ent);
         d.panel_rows = (const int32_t*)(base + b_ent + b_seg);
         d.panel_out = (const int32_t*)(base + b_ent + b_seg + b_rows);
@@ -895,6 +942,10 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
         // panel tables in workgroup (slot) order: slot j is panel panel_order[j]
         char* h = host.data() + off;
         if (!P.entries.empty()) memcpy(h, P.entries.data(), P.entries.size() * 4);
+        if (narrow && !P.entries.empty()) {
+          const std::vector<uint32_t> nst = narrow_stream(P.entries);
+          memcpy(h + b_all, nst.data(), nst.size() * 4);
+        }
         int32_t* hs = (int32_t*)(h + b_ent);
         int32_t* hr = (int32_t*)(h + b_ent + b_seg);
         int32_t* hp = (int32_t*)(h + b_ent + b_seg + b_rows);
@@ -907,7 +958,7 @@ sdnn_status sdnn_plan_create(const int32_t* row_ptr, const int32_t* col_idx, con
             memcpy((int32_t*)(h + b_ent + b_seg + b_rows + b_pos) + (size_t)j * P.nseg,
                    P.seg_start.data() + (size_t)q * P.nseg, 4 * (size_t)P.nseg);
         }
-        off += packing_bytes(P);
+        off += packing_bytes(P, narrow);
       }
       if (o.split_chunks > 0 && M > 0) {
         memcpy(host.data() + perm_off, P0.perm.data(), (size_t)M * 4);
@@ -969,7 +1020,7 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out) {
   out->mid_rho = mid ? p->pk[2].rho : 0.0;
   out->mid_fill = mid ? p->pk[2].fill : 0.0;
   out->grouping = p->grouping;
-  out->reserved = 0;
+  out->tile_cols = p->tile_cols;
   const bool tallest = p->npack > 3;
   out->tallest_panel_rows = tallest ? p->pk[3].RW : 0;
   out->reserved2 = 0;
@@ -1074,10 +1125,18 @@ sdnn_status sdnn_spmm_split_noalloc(sdnn_plan p, const float* B, float* C, int32
 sdnn_status sdnn_plan_launch_shape(sdnn_plan p, int32_t N, int32_t* panel_rows, int32_t* waves) {
   if (!p) return SDNN_ERR_NULL;
   if (N <= 0 || p->M == 0) return SDNN_ERR_DIM;
-  int32_t rw = 0, w = 0;
-  launch_shape(p, N, &rw, &w);
+  int32_t rw = 0, w = 0, t = 0;
+  launch_shape(p, N, &rw, &w, &t);
   if (panel_rows) *panel_rows = rw;
   if (waves) *waves = w;
+  return SDNN_OK;
+}
+
+sdnn_status sdnn_plan_launch_tile(sdnn_plan p, int32_t N, int32_t* tile_cols) {
+  if (!p || !tile_cols) return SDNN_ERR_NULL;
+  if (N <= 0 || p->M == 0) return SDNN_ERR_DIM;
+  int32_t rw = 0, w = 0;
+  launch_shape(p, N, &rw, &w, tile_cols);
   return SDNN_OK;
 }
 

@@ -20,8 +20,10 @@ constexpr int kRing = 4;
 // Stream entries are consumed in groups of kGroup: one group is 64 bytes, one scalar
 // load and one scalar-cache line.
 constexpr int kGroup = 8;
-// Columns of C per workgroup tile: 64 lanes x 4 consecutive columns.
+// Columns of C per workgroup tile: 64 lanes x 4 consecutive columns; or, for the
+// 128-column tiles, 64 lanes x 2 (the narrow layout, two workgroups per CU).
 constexpr int kTileCols = 256;
+constexpr int kNarrowTileCols = 128;
 // Zero groups appended after the last panel: the kernel's stream prefetch may read
 // this many groups past the end of a panel's stream.
 constexpr int kTailGroups = 16;
@@ -34,6 +36,10 @@ constexpr int kLoShift = 17;        // a_{L-1} >> 17: lowest chunk the group rea
 constexpr int kHiShift = 18;        // a_L >> 18: highest chunk the group reads
 constexpr int kLoWord = kGroup - 2, kHiWord = kGroup - 1;
 constexpr int kMaxChunks = 1 << 14; // chunk numbers must fit a3's high bits
+// The stream of the 128-column tiles carries the same groups with 512-byte ring rows:
+// the ring-row field one bit lower and the end flag at bit 8 (narrow_stream).
+constexpr int kRingRowShiftNarrow = 9;  // (a_j >> 9) & 0x7f
+constexpr int kEndBitNarrow = 8;
 // A row of B or C must stay below 2^31 bytes (N < 2^29): the staging and the stores
 // address within a row with 32-bit byte offsets.
 constexpr int64_t kMaxRowBytes = (int64_t)1 << 31;
@@ -103,10 +109,17 @@ sdnn_status reorder_bitset(const int32_t* row_ptr, const int32_t* col_idx, int32
 sdnn_status pack(const int32_t* row_ptr, const int32_t* col_idx, const float* values, int32_t M,
                  int32_t K, int32_t RW, const int32_t* group, int32_t split_chunks, Packed* out);
 
-// A launch shape sdnn_plan_tune measured fastest for one N: which packing, and how many
-// consumer waves per workgroup.
+// The stream of the 128-column tiles: each address word a_j of P.entries re-encoded with
+// the ring row at bit kRingRowShiftNarrow and the end flag at kEndBitNarrow (weights,
+// row, chunk and sync fields unchanged).
+std::vector<uint32_t> narrow_stream(const std::vector<uint32_t>& entries);
+// True if `narrow` is narrow_stream(entries) field by field (decoded independently).
+bool check_narrow_stream(const std::vector<uint32_t>& entries, const std::vector<uint32_t>& narrow);
+
+// A launch shape sdnn_plan_tune measured fastest for one N: which packing, how many
+// consumer waves per workgroup and which tile width.
 struct TunedShape {
-  int32_t N = 0, pack = 0, waves = 0;
+  int32_t N = 0, pack = 0, waves = 0, tile = 256;
 };
 constexpr int kTunedSlots = 8;
 
@@ -115,6 +128,7 @@ struct DevPacking {
   int32_t RW = 0, npanels = 0;
   double rho = 1.0, fill = 1.0;
   const uint32_t* entries = nullptr;      // [2*(stored + kTailGroups*kGroup)] dwords
+  const uint32_t* entries_n = nullptr;    // the same groups for 128-column tiles (or null)
   const int32_t* panel_start = nullptr;   // [npanels] (in groups, -1: empty panel)
   const int32_t* panel_rows = nullptr;    // [npanels*RW] original rows (bias)
   const int32_t* panel_out = nullptr;     // [npanels*RW] rows of C the panel rows go to
@@ -139,6 +153,7 @@ struct sdnn_plan_s {
   int32_t in_permuted = 0;     // W's columns renamed to a caller-given order of B's rows
   int32_t split_chunks = 0;    // chunks per K-segment (0: the packings have one segment)
   int32_t grouping = 1;        // panel grouping the packings use (1: perm order, 2: balanced)
+  int32_t tile_cols = 0;       // 0: the launch picks 256 or 128 columns per tile; else fixed
   const int32_t* d_perm = nullptr;  // [M] perm on the device (K-segmented plans only)
   sdnn::DevPacking pk[sdnn::kMaxPackings];
   sdnn::TunedShape tuned[sdnn::kTunedSlots];  // filled by sdnn_plan_tune
@@ -169,8 +184,10 @@ int split_runs(const sdnn_plan_s* p, int32_t N, int32_t splits);
 constexpr int64_t kScratchFloats = (int64_t)16 << 20;  // 64 MiB
 constexpr int kMaxScratchDevices = 64;
 hipError_t scratch_address(int device, float** out);
-// The packing height and consumer waves launch_spmm uses at N (host only).
-void launch_shape(const sdnn_plan_s* p, int32_t N, int32_t* panel_rows, int32_t* waves);
+// The packing height, consumer waves and tile width launch_spmm uses at N for B and C
+// that allow 16-byte staging (host only).
+void launch_shape(const sdnn_plan_s* p, int32_t N, int32_t* panel_rows, int32_t* waves,
+                  int32_t* tile_cols);
 // Times every candidate launch shape of the plan at N on the given buffers (blocking)
 // and records the fastest in p->tuned.
 hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStream_t stream,

@@ -72,7 +72,10 @@ struct ProducerArgs {
   uint32_t bbase_lo, bbase_hi;  // address of B[0][n0]
   int32_t ncol;            // N - n0 (columns of the tile that exist)
   uint32_t first_row;      // first row of each chunk this producer stages
-  uint32_t vlane;          // the lane's byte offset in a B row segment (16 or 4 * lane)
+  uint32_t vlane;          // the lane's byte offset in a B row segment (16 or 4 * lane;
+                           // 128-column tiles: 16 * (lane % 32))
+  uint32_t vlane_fast;     // 128-column tiles: 16 * (lane % 32) + (lane / 32) * N * 4, the
+                           // lane's offset from a row pair's first row
   uint32_t prog_addr;      // LDS address of the 16 progress words
   uint32_t ready_addr;     // LDS address of this producer's ready word
   uint32_t poll_budget;    // failed ring-limit checks the wave may poll through in total
@@ -97,8 +100,16 @@ static_assert(kAsmEndBit == kEndBit && kAsmSyncBit == kSyncBit && kAsmLoShift ==
               "stream fields mismatch");
 static_assert(kAsmRingMask == (uint32_t)(kRing * kChunk - 1) << kRingRowShift,
               "ring-row mask mismatch");
+static_assert(kAsmTileBytesN == kNarrowTileCols * 4 && kAsmEndBitN == kEndBitNarrow &&
+                  kAsmRingMaskN == (uint32_t)(kRing * kChunk - 1) << kRingRowShiftNarrow,
+              "128-column layout mismatch");
 
-constexpr int kRingBytes = kRing * kChunk * 1024;
+// Tile layouts (TW columns per tile): 256 columns, 4 per lane, one workgroup per CU; or
+// 128 columns, 2 per lane, a 64 KB ring and two producer waves, two workgroups per CU.
+template <int TW>
+constexpr int ring_bytes() { return kRing * kChunk * TW * 4; }
+template <int TW>
+constexpr int producers_of() { return TW == kTileCols ? kAsmProducers : kAsmProducersN; }
 // Failed checks a wave may poll through before it goes on without waiting (results then
 // turn to NaN, never silently wrong); SDNN_POLL_BUDGET overrides it (tests only).
 constexpr int kPollBudget = 1 << 22;
@@ -107,11 +118,29 @@ constexpr int kPollBudget = 1 << 22;
 // that 16 waves per CU leave each wave, and RW >= 12 needs 12 waves per CU.
 template <int RW>
 constexpr int max_threads() { return kAsmAccBase + 4 * RW <= 128 ? 1024 : 768; }
+// 128-column tiles: the accumulators end at v[kAsmAccBaseN + 2 * RW - 1]; VGPRs are
+// granted in blocks of 8 from 512 per SIMD lane, and a workgroup takes half the waves a
+// CU then holds, so that two workgroups (2 x 65 KB of LDS) share each CU: 6 waves per SIMD
+// at RW = 4 and 8 (10 consumers per workgroup), 5 at RW = 12 and 16 (8).  (7 waves at RW = 4
+// would leave the compiler 88 SGPRs, too few beside the loop's 58: it then reserves a
+// stack frame.)
+template <int RW>
+constexpr int narrow_waves_per_simd() {
+  return 512 / ((kAsmAccBaseN + 2 * RW + 7) / 8 * 8) < 6 ? 512 / ((kAsmAccBaseN + 2 * RW + 7) / 8 * 8)
+                                                          : 6;
+}
+template <int RW>
+constexpr int narrow_threads() { return 64 * (4 * narrow_waves_per_simd<RW>() / 2); }
+template <int RW, int TW>
+constexpr int threads_of() { return TW == kTileCols ? max_threads<RW>() : narrow_threads<RW>(); }
+template <int RW, int TW>
+constexpr int min_waves_of() { return TW == kTileCols ? 1 : narrow_waves_per_simd<RW>(); }
 // LDS control words after the ring: ready[kProducers] at +0, progress[16] at +64, the
 // overrun word at +128 (nonzero once a producer staged past the ring limit), and 16
 // bytes per producer at +512 that the convolution producer's filler loads write.
 constexpr int kCtlWords = 256;
 static_assert(512 + 16 * kProducers <= kCtlWords * 4, "filler words outside the control area");
+static_assert(kAsmProducersN <= kProducers, "ready words overlap the progress words");
 static_assert(kProducers <= 16, "ready words overlap the progress words");
 
 // GELU(x) = x Phi(x) = 0.5 x (1 + erf(x / sqrt 2)) (the exact erf form).  erf(z) for
@@ -139,9 +168,14 @@ __device__ __forceinline__ float gelu(float x) {
 // 201 MB output of the 3072 x 768 layer at N = 16384 otherwise push the 0.57 MB stream out
 // between tiles).
 typedef float nt_float4 __attribute__((ext_vector_type(4)));
+typedef float nt_float2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ void store_c4(float* p, float x, float y, float z, float w) {
   const nt_float4 v = {x, y, z, w};
   __builtin_nontemporal_store(v, reinterpret_cast<nt_float4*>(p));
+}
+__device__ __forceinline__ void store_c2(float* p, float x, float y) {
+  const nt_float2 v = {x, y};
+  __builtin_nontemporal_store(v, reinterpret_cast<nt_float2*>(p));
 }
 __device__ __forceinline__ void store_c1(float* p, float x) { __builtin_nontemporal_store(x, p); }
 
@@ -180,9 +214,10 @@ struct SpmmArgs {
 enum { kStageDword = 0, kStageVec = 1, kStageConv = 2 };
 
 // RW: rows per panel; STAGE: the producer kind (16-byte kinds also store C as float4:
-// N % 4 == 0 and B, C 16-byte aligned).  blockDim.x = 64 * (consumers + kProducers).
-template <int RW, int STAGE>
-__global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
+// N % 4 == 0 and B, C 16-byte aligned); TW: columns per tile (256, or 128 with 16-byte
+// staging of unsplit products only).  blockDim.x = 64 * (consumers + producers_of<TW>()).
+template <int RW, int STAGE, int TW>
+__global__ __launch_bounds__((threads_of<RW, TW>()), (min_waves_of<RW, TW>())) void spmm_panel_kernel(
     const uint32_t* __restrict__ entries, const int32_t* __restrict__ panel_start,
     const int32_t* __restrict__ panel_rows, const int32_t* __restrict__ panel_out,
     const int32_t* __restrict__ seg_start, const float* __restrict__ B, float* __restrict__ C,
@@ -190,7 +225,12 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
   // the ring ([0, kRingBytes)) and the control words; the ring must start at LDS 0
   // (the loops form LDS addresses from the ring-row field alone), which holds because
   // this is the kernel's only LDS object
-  __shared__ __attribute__((aligned(16))) uint32_t lds[kRingBytes / 4 + kCtlWords];
+  static_assert(TW == kTileCols || (TW == kNarrowTileCols && STAGE == kStageVec),
+                "128-column tiles stage 16-byte rows");
+  constexpr int NP = producers_of<TW>();
+  constexpr int V = TW / 64;  // columns per lane
+  constexpr int kRingB = ring_bytes<TW>();
+  __shared__ __attribute__((aligned(16))) uint32_t lds[kRingB / 4 + kCtlWords];
 
   const int bid = blockIdx.x;
   const int lin = (bid & 7) * a.per_xcd + (bid >> 3);
@@ -208,17 +248,17 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
   const int s0 = split * a.seg_per_split, s1 = min(s0 + a.seg_per_split, a.nseg);
   const int c0 = splitk ? s0 * a.split_chunks : 0;
   const int c1 = splitk ? min(s1 * a.split_chunks, a.nchunks) : a.nchunks;
-  const int nc = (blockDim.x >> 6) - kProducers;
+  const int nc = (blockDim.x >> 6) - NP;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int prod = wave - nc;  // >= 0: producer index
 
   const uint32_t lds_base = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) uint32_t*)lds);
   if (lds_base != 0) return;  // never taken: see above
-  const uint32_t ready_addr = lds_base + kRingBytes;
+  const uint32_t ready_addr = lds_base + kRingB;
   const uint32_t prog0 = ready_addr + 64;
   const uint32_t overrun_addr = ready_addr + 128;
-  uint32_t* ctl = lds + kRingBytes / 4;
+  uint32_t* ctl = lds + kRingB / 4;
   if (prod >= 0) {
     if (lane == 0) ctl[prod] = (uint32_t)c0;                                 // nothing landed
     if (prod == 0 && lane == 0) ctl[32] = 0u;                                // no overrun
@@ -237,16 +277,22 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
     pa.item_rb = a.tile_major ? g : 0;
     pa.item_drb = a.tile_major ? a.total_wg % a.n_rb : 0;
     pa.item_nrb = a.tile_major ? a.n_rb : 1;
-    pa.item_dtile_bytes = a.tile_major ? (uint32_t)(a.total_wg / a.n_rb) * (kTileCols * 4u) : 0u;
-    const int n0 = tile0 * kTileCols;
+    pa.item_dtile_bytes = a.tile_major ? (uint32_t)(a.total_wg / a.n_rb) * (TW * 4u) : 0u;
+    const int n0 = tile0 * TW;
     pa.K = a.K;
     pa.row_bytes = (uint32_t)a.N * 4u;
     const uint64_t bb = (uint64_t)(uintptr_t)(B + n0);
     pa.bbase_lo = (uint32_t)bb;
     pa.bbase_hi = (uint32_t)(bb >> 32);
     pa.ncol = a.N - n0;
-    pa.first_row = (uint32_t)(prod * (kChunk / kProducers));
-    pa.vlane = (uint32_t)lane * (STAGE != kStageDword ? 16u : 4u);
+    pa.first_row = (uint32_t)(prod * (kChunk / NP));
+    if constexpr (TW == kTileCols) {
+      pa.vlane = (uint32_t)lane * (STAGE != kStageDword ? 16u : 4u);
+      pa.vlane_fast = pa.vlane;
+    } else {  // lanes 32-63 stage the second row of each pair
+      pa.vlane = (uint32_t)(lane & 31) * 16u;
+      pa.vlane_fast = pa.vlane + (uint32_t)(lane >> 5) * pa.row_bytes;
+    }
     pa.prog_addr = prog0;
     pa.ready_addr = ready_addr + 4u * (uint32_t)prod;
     pa.poll_budget = a.poll_budget;
@@ -271,7 +317,8 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
       }
       produce_conv(pa);
     } else if constexpr (STAGE == kStageVec) {
-      produce_vec(pa);
+      if constexpr (TW == kTileCols) produce_vec(pa);
+      else produce_vecn(pa);
     } else {
       produce_dword(pa);
     }
@@ -285,7 +332,7 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
       tile = k / a.n_rb;
       rb = k - tile * a.n_rb;
     }
-    const int ncol = tile * kTileCols + lane * 4;
+    const int ncol = tile * TW + lane * V;
     const int panel = rb * nc + wave;
     const uint32_t cbase = splitk ? 0u : (uint32_t)(it * a.nchunks);
     const uint32_t next = it + 1 < nitems ? (uint32_t)((it + 1) * a.nchunks) : kProgressDone;
@@ -302,11 +349,11 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
       continue;
     }
 
-    acc_plane_t<RW> p0 = {}, p1 = {}, p2 = {}, p3 = {};
+    acc_plane_t<RW> p0 = {}, p1 = {}, p2 = {}, p3 = {};  // p2, p3: 256-column tiles only
     if (gstart >= 0) {  // a panel without entries only writes epi(bias)
       ConsumerArgs ca;
       ca.stream = entries + (size_t)gstart * (2 * kGroup);
-      ca.vlane = (uint32_t)lane * 16u;
+      ca.vlane = (uint32_t)lane * (4u * V);
       ca.prog_addr = prog0 + 4u * (uint32_t)wave;
       ca.ready_addr = ready_addr;
       ca.poll_budget = a.poll_budget;
@@ -314,7 +361,12 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
       ca.chunk_limit = (uint32_t)c1;
       ca.chunk_base = cbase;
       ca.next_progress = next;
-      if (splitk) {  // runs of K-segments: the loop also stops at the run's last chunk
+      if constexpr (TW != kTileCols) {  // unsplit products only
+        if constexpr (RW == 4) consume_n_rw4(p0, p1, ca);
+        if constexpr (RW == 8) consume_n_rw8(p0, p1, ca);
+        if constexpr (RW == 12) consume_n_rw12(p0, p1, ca);
+        if constexpr (RW == 16) consume_n_rw16(p0, p1, ca);
+      } else if (splitk) {  // runs of K-segments: the loop also stops at the run's last chunk
         if constexpr (RW == 4) consume_rw4_limit(p0, p1, p2, p3, ca);
         if constexpr (RW == 8) consume_rw8_limit(p0, p1, p2, p3, ca);
         if constexpr (RW == 12) consume_rw12_limit(p0, p1, p2, p3, ca);
@@ -335,6 +387,16 @@ __global__ __launch_bounds__(max_threads<RW>()) void spmm_panel_kernel(
       if (orig < 0) continue;
       const int row = panel_out[panel * RW + r];
       const float v[4] = {p0[r], p1[r], p2[r], p3[r]};
+      if constexpr (TW != kTileCols) {
+        const float bb = bias ? bias[orig] : 0.0f;
+        float* crow = C + (size_t)row * a.N;
+        if (ncol + 2 <= a.N) {
+          store_c2(crow + ncol, activation(v[0] + bb, a.epi), activation(v[1] + bb, a.epi));
+        } else if (ncol < a.N) {
+          store_c1(crow + ncol, activation(v[0] + bb, a.epi));
+        }
+        continue;
+      }
       if (splitk) {  // raw partial sums; the reduction adds the bias and applies epi
         float* prow = C + ((size_t)split * a.M + row) * a.N;
         if (STAGE != kStageDword && ncol + 4 <= a.N) {
@@ -371,31 +433,39 @@ struct SpmmPtrs {
   const float* bias;
 };
 
-template <int RW, int STAGE>
+template <int RW, int STAGE, int TW>
 hipError_t launch_variant(const SpmmPtrs& p, const SpmmArgs& args, int waves, int grid,
                           hipStream_t stream) {
-  hipLaunchKernelGGL((spmm_panel_kernel<RW, STAGE>), dim3(grid), dim3(64 * (waves + kProducers)), 0, stream,
+  hipLaunchKernelGGL((spmm_panel_kernel<RW, STAGE, TW>), dim3(grid),
+                     dim3(64 * (waves + producers_of<TW>())), 0, stream,
                      p.entries, p.panel_start, p.panel_rows, p.panel_out, p.seg_start, p.B, p.C,
                      p.bias, args);
   return hipGetLastError();
 }
 
-template <int STAGE>
+template <int STAGE, int TW = kTileCols>
 hipError_t launch_rw(int RW, const SpmmPtrs& p, const SpmmArgs& args, int waves, int grid,
                      hipStream_t stream) {
   switch (RW) {
-    case 4: return launch_variant<4, STAGE>(p, args, waves, grid, stream);
-    case 8: return launch_variant<8, STAGE>(p, args, waves, grid, stream);
-    case 12: return launch_variant<12, STAGE>(p, args, waves, grid, stream);
-    case 16: return launch_variant<16, STAGE>(p, args, waves, grid, stream);
+    case 4: return launch_variant<4, STAGE, TW>(p, args, waves, grid, stream);
+    case 8: return launch_variant<8, STAGE, TW>(p, args, waves, grid, stream);
+    case 12: return launch_variant<12, STAGE, TW>(p, args, waves, grid, stream);
+    case 16: return launch_variant<16, STAGE, TW>(p, args, waves, grid, stream);
   }
   return hipErrorInvalidValue;
 }
 
-int max_consumers(int RW) {
-  const int threads = RW == 4 ? max_threads<4>() : RW == 8 ? max_threads<8>()
-                    : RW == 12 ? max_threads<12>() : max_threads<16>();
-  const int c = threads / 64 - kProducers;
+// Consumer waves a workgroup can hold at panel height RW and tile width TW (the register
+// limit of the accumulators, less the producers).
+int max_consumers(int RW, int TW = kTileCols) {
+  int threads;
+  if (TW == kTileCols)
+    threads = RW == 4 ? max_threads<4>() : RW == 8 ? max_threads<8>()
+            : RW == 12 ? max_threads<12>() : max_threads<16>();
+  else
+    threads = RW == 4 ? narrow_threads<4>() : RW == 8 ? narrow_threads<8>()
+            : RW == 12 ? narrow_threads<12>() : narrow_threads<16>();
+  const int c = threads / 64 - (TW == kTileCols ? kAsmProducers : kAsmProducersN);
   return c < kAsmMaxConsumers ? c : kAsmMaxConsumers;
 }
 
@@ -408,6 +478,22 @@ struct LaunchCfg {
   int waves, n_tiles, n_rb;  // waves: consumer waves per workgroup (the producers come on top)
 };
 
+// Workgroups a grid is sized for: one per CU.  Two workgroups with 128-column tiles fit a CU
+// (65 KB of LDS each), but on the layers whose launch takes those tiles a grid of one per CU
+// with more consumer waves each was the faster (C2's 768 x 768 layer at N = 1024: 14.1 against
+// 15.4 us; the 768 x 3072 layer at N = 1024: 43.8 against 51.6 us).
+int slots_of(int num_cus, int tw) {
+  (void)tw;
+  return num_cus > 0 ? num_cus : 256;
+}
+
+// Workgroups the device holds at once (the persistent launches' grid): one per CU with
+// 256-column tiles (129 KB of LDS each), two with 128-column tiles (65 KB).
+int resident_of(int num_cus, int tw) {
+  const int cus = num_cus > 0 ? num_cus : 256;
+  return tw == kTileCols ? cus : 2 * cus;
+}
+
 // The 129 KB of ring and control LDS allow one workgroup per CU, so a grid of G
 // workgroups runs in ceil(G / CUs) rounds, and a partly filled last round costs as
 // much as a full one.
@@ -419,14 +505,14 @@ int64_t rounds_of(int64_t n_tiles, int npanels, int waves, int target) {
 // Consumer waves per workgroup: the fewest rounds that the register-limited consumer
 // count allows, and within that many rounds the smallest workgroups (fewest panels
 // each, so the most workgroups share the work).  SDNN_FORCE_WAVES fixes the count.
-LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N, int nseg = 1) {
-  const int target = num_cus > 0 ? num_cus : 256;
-  int cap = max_consumers(pk.RW);
+LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N, int nseg = 1, int tw = kTileCols) {
+  const int target = slots_of(num_cus, tw);
+  int cap = max_consumers(pk.RW, tw);
   if (cap > pk.npanels) cap = pk.npanels;
   if (cap < 1) cap = 1;
   const int forceW = env_int("SDNN_FORCE_WAVES", 0);
   LaunchCfg c;
-  c.n_tiles = (N + kTileCols - 1) / kTileCols;
+  c.n_tiles = (N + tw - 1) / tw;
   const int64_t units = (int64_t)c.n_tiles * nseg;  // (tile, K-segment) pairs
   if (forceW > 0) {
     c.waves = forceW < cap ? forceW : cap;
@@ -454,10 +540,10 @@ LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N, int nseg = 1) {
 // MI355X for products (M = K = 512-2048 at 80-98 %, N = 1024-16384, the W0 and C2-C5
 // layers) and for the 3x3 convolutions of the benchmark, whose staging differs but
 // follows the same trade.
-const DevPacking& choose_packing(const sdnn_plan_s* p, int N, int nseg = 1) {
+const DevPacking& choose_packing(const sdnn_plan_s* p, int N, int nseg = 1, int tw = kTileCols) {
   if (p->npack < 2) return p->pk[0];
-  const int64_t n_tiles = (int64_t)((N + kTileCols - 1) / kTileCols) * nseg;
-  const int cus = p->num_cus > 0 ? p->num_cus : 256;
+  const int64_t n_tiles = (int64_t)((N + tw - 1) / tw) * nseg;
+  const int cus = slots_of(p->num_cus, tw);
   const double density = (double)p->nnz / ((double)p->M * (double)p->K);
   auto per_chunk = [&](const DevPacking& pk) { return pk.RW * kChunk * density; };
   int64_t rounds[kMaxPackings];
@@ -467,7 +553,7 @@ const DevPacking& choose_packing(const sdnn_plan_s* p, int N, int nseg = 1) {
   for (int k = 0; k < p->npack; ++k) {
     const DevPacking& pk = p->pk[k];
     live[k] = !(pk.RW == 4 && per_chunk(pk) < 8.0);
-    const int waves = std::max(1, std::min(max_consumers(pk.RW), pk.npanels));
+    const int waves = std::max(1, std::min(max_consumers(pk.RW, tw), pk.npanels));
     const int64_t wgs = n_tiles * ((pk.npanels + waves - 1) / waves);
     rounds[k] = (wgs + cus - 1) / cus;
     util[k] = (double)wgs / ((double)rounds[k] * cus);
@@ -605,6 +691,33 @@ int split_runs_of(const sdnn_plan_s* p, int32_t N, int splits, bool conv, int* s
   return (total_seg + per - 1) / per;
 }
 
+// Whether a call may run on 128-column tiles: an unsplit product (not a convolution) with
+// N % 4 == 0 and 16-byte aligned B and C (the 16-byte staging), on a plan that holds the
+// 128-column stream, with per-lane staging offsets 16 (lane % 32) + (lane / 32 + 2 j) 4N
+// (j < 8) below 2^31.
+bool narrow_allowed(const sdnn_plan_s* p, int N, bool aligned, int nk, bool conv) {
+  return aligned && !conv && nk == 1 && p->pk[0].entries_n != nullptr &&
+         (uint64_t)N * 4u * (kChunk / kAsmProducersN) < ((uint64_t)1 << 31);
+}
+
+// Tile width of a call that may use either: the plan's tile_cols option, else 128 columns
+// when the 256-column launch would give its workgroups at most 4 consumer waves (few tiles
+// and rows per CU: each workgroup's time is then the staging chain of its tile's K rows, and
+// half-width rows halve the staged bytes per chunk), else 256 (the 128-column loop issues an
+// LDS read and an address op per two FMAs instead of four, which the loaded layers pay for).
+// Measured on MI355X over 68 layers and batch widths (the benchmark's layers, C2-C5 and W0 at
+// N = 256-4096, M = K = 256-2048 at 70-95 % with N = 128-2048): every launch of 1-4 waves
+// was 7-30 % faster on 128 columns (C1 8.9 -> 6.6 us, C2 16.6 -> 13.8 us, the 768 x 3072
+// layer at N = 1024 53.5 -> 43.4 us, M = K = 2048 at 90 % with N = 128 34.8 -> 26.3 us); from
+// 6 waves on 256 columns was as fast or faster (W0 at N = 4096 67.0 against 82.7 us, C5's
+// 3072 x 768 layer 130.5 against 185.5 us).
+constexpr int kNarrowMaxWaves = 4;
+int choose_tile(const sdnn_plan_s* p, int N) {
+  if (p->tile_cols != 0) return p->tile_cols;
+  const DevPacking& pk = choose_packing(p, N);
+  return choose_cfg(pk, p->num_cus, N).waves <= kNarrowMaxWaves ? kNarrowTileCols : kTileCols;
+}
+
 hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                          const float* bias, int epi, const int32_t* conv_hwn,
                          const TunedShape* shape, float* ws, int splits, hipStream_t stream) {
@@ -614,16 +727,20 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
   if (!shape && !conv_hwn && nk == 1)
     for (int i = 0; i < p->ntuned; ++i)
       if (p->tuned[i].N == N) shape = &p->tuned[i];
+  float* out = nk > 1 ? ws : C;
+  const bool aligned = (N % 4 == 0) && (((uintptr_t)B & 15) == 0) && (((uintptr_t)out & 15) == 0);
+  int tw = kTileCols;
+  if (narrow_allowed(p, N, aligned, nk, conv_hwn != nullptr))
+    tw = shape ? shape->tile : choose_tile(p, N);
   const DevPacking& pk =
-      shape ? p->pk[shape->pack] : choose_packing(p, N, nk);
-  LaunchCfg cfg = choose_cfg(pk, p->num_cus, N, nk);
+      shape ? p->pk[shape->pack] : choose_packing(p, N, nk, tw);
+  LaunchCfg cfg = choose_cfg(pk, p->num_cus, N, nk, tw);
   if (shape) {
-    cfg.waves = shape->waves;
+    cfg.waves = std::min(shape->waves, max_consumers(pk.RW, tw));
     cfg.n_rb = (pk.npanels + cfg.waves - 1) / cfg.waves;
   }
-  float* out = nk > 1 ? ws : C;
-  const SpmmPtrs ptrs{pk.entries, pk.panel_start, pk.panel_rows, pk.panel_out, pk.seg_start, B,
-                      out, bias};
+  const SpmmPtrs ptrs{tw == kTileCols ? pk.entries : pk.entries_n, pk.panel_start, pk.panel_rows,
+                      pk.panel_out, pk.seg_start, B, out, bias};
   SpmmArgs args;
   args.K = p->K;
   args.N = N;
@@ -649,13 +766,13 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
   // B rows stay in that XCD's L2 across the row-blocks, where CUs / tiles workgroups per
   // tile would spread each XCD over many tiles (C5's 3072 x 768 layer: 8 tiles of 768 KB
   // per XCD against a 4 MB L2).
-  const int cus = p->num_cus > 0 ? p->num_cus : 256;
+  const int cus = resident_of(p->num_cus, tw);  // workgroups resident at once
   const int64_t items = (int64_t)cfg.n_tiles * cfg.n_rb;
   const bool can_persist = nk == 1 && !conv_hwn && p->nchunks % kRing == 0;
   int wg_per_tile = cfg.n_rb, tile_major = 0;
   int64_t total = (int64_t)cfg.n_tiles * nk * cfg.n_rb;
   if (can_persist && items > cus) {
-    if (N % kTileCols == 0) {
+    if (N % tw == 0) {
       tile_major = 1;
       total = cus;
     } else {
@@ -670,7 +787,7 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
       tile_major = 0;
       wg_per_tile = std::min(forced, cfg.n_rb);
       total = (int64_t)cfg.n_tiles * wg_per_tile;
-    } else if (forced_tm > 0 && N % kTileCols == 0) {
+    } else if (forced_tm > 0 && N % tw == 0) {
       tile_major = 1;
       wg_per_tile = cfg.n_rb;
       total = std::min<int64_t>(forced_tm, items);
@@ -695,11 +812,12 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
   hipError_t err;
   if (conv_hwn) {
     err = launch_rw<kStageConv>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
+  } else if (tw == kNarrowTileCols) {
+    err = launch_rw<kStageVec, kNarrowTileCols>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
   } else {
     // the 16-byte producer addresses a chunk's rows with 32-bit per-lane offsets
     // 16 * lane + r * 4N (r < kChunk / kProducers)
-    const bool vec = (N % 4 == 0) && (((uintptr_t)B & 15) == 0) && (((uintptr_t)out & 15) == 0) &&
-                     (uint64_t)N * 4u * (kChunk / kProducers) < ((uint64_t)1 << 31);
+    const bool vec = aligned && (uint64_t)N * 4u * (kChunk / kProducers) < ((uint64_t)1 << 31);
     err = vec ? launch_rw<kStageVec>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream)
               : launch_rw<kStageDword>(pk.RW, ptrs, args, cfg.waves, (int)grid, stream);
   }
@@ -709,13 +827,18 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
 }
 }  // namespace
 
-void launch_shape(const sdnn_plan_s* p, int32_t N, int32_t* panel_rows, int32_t* waves) {
+void launch_shape(const sdnn_plan_s* p, int32_t N, int32_t* panel_rows, int32_t* waves,
+                  int32_t* tile_cols) {
   const TunedShape* shape = nullptr;
   for (int i = 0; i < p->ntuned; ++i)
     if (p->tuned[i].N == N) shape = &p->tuned[i];
-  const DevPacking& pk = shape ? p->pk[shape->pack] : choose_packing(p, N);
+  int tw = kTileCols;
+  if (narrow_allowed(p, N, N % 4 == 0, 1, false)) tw = shape ? shape->tile : choose_tile(p, N);
+  const DevPacking& pk = shape ? p->pk[shape->pack] : choose_packing(p, N, 1, tw);
   *panel_rows = pk.RW;
-  *waves = shape ? shape->waves : choose_cfg(pk, p->num_cus, N).waves;
+  *waves = shape ? std::min(shape->waves, max_consumers(pk.RW, tw))
+                 : choose_cfg(pk, p->num_cus, N, 1, tw).waves;
+  *tile_cols = tw;
 }
 
 hipError_t launch_spmm(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
@@ -731,19 +854,25 @@ hipError_t launch_spmm_split(const sdnn_plan_s* p, const float* B, float* C, int
 
 hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStream_t stream,
                      TunedShape* chosen) {
-  // candidates: every packing, each with its register-limited consumer count and
-  // three fewer-wave shapes, plus the heuristic's own choice
+  // candidates: every tile width the call allows and every packing, each with its
+  // register-limited consumer count and three fewer-wave shapes, plus the heuristic's own
+  // choice
   std::vector<TunedShape> cands;
-  for (int k = 0; k < p->npack; ++k) {
-    const int cap = std::min(max_consumers(p->pk[k].RW), p->pk[k].npanels);
-    const int heur = choose_cfg(p->pk[k], p->num_cus, N).waves;
-    for (int w : {cap, (3 * cap) / 4, cap / 2, cap / 4, heur}) {
-      if (w < 1) continue;
-      bool dup = false;
-      for (const TunedShape& t : cands) dup |= (t.pack == k && t.waves == w);
-      if (!dup) cands.push_back(TunedShape{N, k, w});
+  const bool aligned = (N % 4 == 0) && (((uintptr_t)B & 15) == 0) && (((uintptr_t)C & 15) == 0);
+  std::vector<int> tiles{kTileCols};
+  if (narrow_allowed(p, N, aligned, 1, false) && p->tile_cols != kTileCols)
+    tiles.push_back(kNarrowTileCols);
+  for (int tw : tiles)
+    for (int k = 0; k < p->npack; ++k) {
+      const int cap = std::min(max_consumers(p->pk[k].RW, tw), p->pk[k].npanels);
+      const int heur = choose_cfg(p->pk[k], p->num_cus, N, 1, tw).waves;
+      for (int w : {cap, (3 * cap) / 4, cap / 2, cap / 4, heur}) {
+        if (w < 1) continue;
+        bool dup = false;
+        for (const TunedShape& t : cands) dup |= (t.pack == k && t.waves == w && t.tile == tw);
+        if (!dup) cands.push_back(TunedShape{N, k, w, tw});
+      }
     }
-  }
   hipEvent_t e0 = nullptr, e1 = nullptr;
   hipError_t err = hipEventCreate(&e0);
   if (err == hipSuccess) err = hipEventCreate(&e1);

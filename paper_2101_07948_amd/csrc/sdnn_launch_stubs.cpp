@@ -34,9 +34,11 @@ hipError_t launch_dense(const float*, const float*, float*, int32_t, int32_t, in
 }
 hipError_t scratch_address(int, float**) { return hipErrorNotSupported; }
 int split_runs(const sdnn_plan_s*, int32_t, int32_t) { return 1; }
-void launch_shape(const sdnn_plan_s* p, int32_t, int32_t* panel_rows, int32_t* waves) {
+void launch_shape(const sdnn_plan_s* p, int32_t, int32_t* panel_rows, int32_t* waves,
+                  int32_t* tile_cols) {
   *panel_rows = p->pk[0].RW;
   *waves = 1;
+  *tile_cols = kTileCols;
 }
 
 }  // namespace sdnn

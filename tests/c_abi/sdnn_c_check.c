@@ -83,7 +83,7 @@ int main(int argc, char** argv) {
   if (!col_idx || !values || !B || !bias) return 3;
 
   /* segments of 2 chunks (64 rows of B) so that the split call has several */
-  sdnn_plan_opts opts = {0, 1, 0, 2, NULL, 0};
+  sdnn_plan_opts opts = {0, 1, 0, 2, NULL, 0, 0};
   sdnn_plan plan = NULL;
   CHECK_SDNN(sdnn_plan_create(row_ptr, col_idx, values, M, K, &opts, &plan));
   sdnn_plan_info_t info;
@@ -115,6 +115,18 @@ int main(int argc, char** argv) {
   CHECK_SDNN(sdnn_plan_get_perm(plan, perm));
   if (!write_file(dir, "perm.i32", perm, sizeof(int32_t) * (size_t)M)) return 4;
 
+  /* the same product from a plan fixed to 128-column tiles (used when N % 4 == 0) */
+  sdnn_plan_opts nopts = {0, 1, 0, 0, NULL, 0, 128};
+  sdnn_plan nplan = NULL;
+  int32_t tile = 0;
+  CHECK_SDNN(sdnn_plan_create(row_ptr, col_idx, values, M, K, &nopts, &nplan));
+  CHECK_SDNN(sdnn_plan_launch_tile(nplan, N, &tile));
+  CHECK_SDNN(sdnn_spmm(nplan, dB, dC, N, dbias, SDNN_EPI_GELU, NULL));
+  CHECK_HIP(hipDeviceSynchronize());
+  CHECK_HIP(hipMemcpy(C, dC, sizeof(float) * (size_t)M * N, hipMemcpyDeviceToHost));
+  if (!write_file(dir, "C_narrow.f32", C, sizeof(float) * (size_t)M * N)) return 4;
+  sdnn_plan_destroy(nplan);
+
   sdnn_plan_destroy(plan);
   hipFree(dB);
   hipFree(dC);
@@ -127,6 +139,7 @@ int main(int argc, char** argv) {
   free(bias);
   free(C);
   free(perm);
-  printf("sdnn_c_check ok: M=%d K=%d N=%d nnz=%zu segments=%d\n", M, K, N, nnz, info.splits);
+  printf("sdnn_c_check ok: M=%d K=%d N=%d nnz=%zu segments=%d tile=%d\n", M, K, N, nnz,
+         info.splits, tile);
   return 0;
 }

@@ -301,3 +301,20 @@ def test_bad_grouping_rejected():
         with pytest.raises(sd.SdnnError) as ei:
             sd.plan_check_host(W.row_ptr, W.col_idx, W.values, 16, 16, grouping=g)
         assert ei.value.code == 2
+
+
+def test_tile_cols_option():
+    """tile_cols: 0 (default) and 128 hold the stream a second time, re-encoded for the
+    128-column tiles (the host self-check decodes every address word of both and compares
+    the fields); 256 holds one stream; other values are rejected."""
+    W = inputs.workload("c3", N=4).layers[1].W
+    sizes = {}
+    for t in (0, 128, 256):
+        info = sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, tile_cols=t)
+        assert info["tile_cols"] == t
+        sizes[t] = info["packed_bytes"]
+    assert sizes[0] == sizes[128] > sizes[256]
+    for bad in (-1, 64, 192, 512):
+        with pytest.raises(sd.SdnnError) as ei:
+            sd.plan_check_host(W.row_ptr, W.col_idx, W.values, W.M, W.K, tile_cols=bad)
+        assert ei.value.code == 2

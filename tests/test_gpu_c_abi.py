@@ -1,8 +1,8 @@
 """The C ABI driven from a plain C99 program (tests/c_abi/sdnn_c_check.c, built by the
-repository's build step) in a child process: plan creation, sdnn_spmm and
-sdnn_spmm_split with a GELU epilogue, results checked here against the CPU oracle with
-the parity bar (|err| <= 1.13 * (1e-5 * sum |w||b| + 1e-6) for GELU) and the
-permutation against the oracle's Algorithm 1 bit for bit."""
+repository's build step) in a child process: plan creation, sdnn_spmm, sdnn_spmm_split
+and sdnn_spmm from a plan fixed to 128-column tiles, with a GELU epilogue, results
+checked here against the CPU oracle with the parity bar (|err| <= 1.13 * (1e-5 * sum |w||b|
++ 1e-6) for GELU) and the permutation against the oracle's Algorithm 1 bit for bit."""
 import os
 import subprocess
 
@@ -17,7 +17,10 @@ pytestmark = pytest.mark.gpu
 EXE = os.path.join(ROOT, "tests", "c_abi", "sdnn_c_check")
 
 
-def test_c_caller_matches_oracle(tmp_path):
+@pytest.mark.parametrize("N", [130, 132])
+def test_c_caller_matches_oracle(tmp_path, N):
+    """N = 130 stages B in 4-byte pieces (no 128-column tiles); N = 132 allows the
+    128-column tiles, whose result equals the 256-column one bit for bit."""
     assert os.path.exists(EXE), f"{EXE} is missing: run __graft_entry__.build() first"
     # a binary built against another sdnn.h would disagree with the library on struct
     # layouts: compare the sizes it was compiled with (a host-only query) first
@@ -27,7 +30,7 @@ def test_c_caller_matches_oracle(tmp_path):
     assert r.returncode == 0, r.stderr
     assert r.stdout.split() == [str(ctypes.sizeof(sd.PlanOpts)), str(ctypes.sizeof(sd.PlanInfo))], \
         f"{EXE} was built against another sdnn.h: run __graft_entry__.build() again"
-    M, K, N = 70, 333, 130
+    M, K = 70, 333
     W = inputs.pattern_uniform(M, K, 0.1, inputs.CFG_TEST, 8100, 0.05)
     B = inputs.dense_B(K, N, inputs.CFG_TEST, 8100)
     bias = inputs.bias_normal(M, inputs.CFG_TEST, 8100, 0.02)
@@ -42,9 +45,12 @@ def test_c_caller_matches_oracle(tmp_path):
     assert r.returncode == 0, r.stdout + r.stderr
     ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, K, B, bias, "gelu")
     tol = tol_fp32(bound, "gelu")
-    for name in ("C_plain.f32", "C_split.f32"):
+    for name in ("C_plain.f32", "C_split.f32", "C_narrow.f32"):
         got = np.fromfile(tmp_path / name, dtype=np.float32).reshape(M, N).astype(np.float64)
         bad = ~(np.abs(got - ref) <= tol)
         assert not bad.any(), f"{name}: {int(bad.sum())} of {bad.size} out of tolerance"
+    plain = np.fromfile(tmp_path / "C_plain.f32", dtype=np.float32)
+    assert np.array_equal(plain, np.fromfile(tmp_path / "C_narrow.f32", dtype=np.float32))
+    assert f"tile={128 if N % 4 == 0 else 256}" in r.stdout, r.stdout
     perm = np.fromfile(tmp_path / "perm.i32", dtype=np.int32)
     assert np.array_equal(perm, oracle.reorder(W.row_ptr, W.col_idx, K))
