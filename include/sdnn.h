@@ -110,8 +110,8 @@ typedef enum {
  *                 sdnn_spmm picks one per call (sdnn_plan_launch_tile reports which);
  *                 256 = 256-column tiles only (half the device memory for the streams);
  *                 128 = 128-column tiles wherever the call allows them.  128-column tiles
- *                 serve sdnn_spmm with N % 4 == 0 and 16-byte aligned B and C; K-split
- *                 calls, convolutions and other sdnn_spmm calls use 256.  Other values:
+ *                 serve sdnn_spmm and sdnn_spmm_split with N % 4 == 0 and 16-byte aligned
+ *                 B and C; convolutions and other calls use 256.  Other values:
  *                 SDNN_ERR_DIM. */
 typedef struct {
   int32_t panel_rows;
@@ -220,10 +220,12 @@ sdnn_status sdnn_spmm(sdnn_plan p, const float* B, float* C, int32_t N, const fl
  * of a tile's K-segments also go to different workgroups, which fills the device when
  * M * ceil(N / 256) alone gives too few workgroups).  Same result contract, layouts and
  * stream semantics as sdnn_spmm; the plan must have been created with split_chunks > 0.
- *   splits:           workgroups along K.  0 = the library's choice for this N (a cost
- *                     model of staging rounds against the reduction's traffic); k > 0 =
- *                     runs of ceil(nseg / k) consecutive segments each (at most nseg
- *                     runs, nseg = sdnn_plan_info's `splits`).  Negative: SDNN_ERR_DIM.
+ *   splits:           workgroups along K.  0 = the library's choice for this N (the count
+ *                     sdnn_plan_tune measured fastest at this N, else a cost model of
+ *                     staging rounds against the reduction's traffic); k > 0 = runs of
+ *                     ceil(nseg / k) consecutive segments each (at most nseg runs, nseg =
+ *                     sdnn_plan_info's `splits`); sdnn_plan_split_runs reports the count.
+ *                     Negative: SDNN_ERR_DIM.
  * With R runs (R > 1), each workgroup writes its run's partial product (no bias, no
  * epilogue) to workspace[r][row][n]; a second kernel on the same stream sums the runs in
  * order r = 0, 1, ..., adds the bias and applies epi into C.  Results can differ from
@@ -267,6 +269,12 @@ sdnn_status sdnn_spmm_split_noalloc(sdnn_plan p, const float* B, float* C, int32
  * Errors: SDNN_ERR_NULL (p), SDNN_ERR_DIM (N <= 0 or M = 0). */
 sdnn_status sdnn_plan_launch_shape(sdnn_plan p, int32_t N, int32_t* panel_rows, int32_t* waves);
 
+/* The workgroups along K that sdnn_spmm_split runs for this plan at N columns when asked
+ * for `splits` (0: the library's choice, see sdnn_spmm_split); 1 for a plan without
+ * K-segments.  Host only.  Errors: SDNN_ERR_NULL (p or runs), SDNN_ERR_DIM (N <= 0, M = 0,
+ * splits < 0). */
+sdnn_status sdnn_plan_split_runs(sdnn_plan p, int32_t N, int32_t splits, int32_t* runs);
+
 /* The tile width (columns of C per workgroup) sdnn_spmm uses for this plan at N columns
  * when B and C are 16-byte aligned and N % 4 == 0 (otherwise it is 256): the tuned one if
  * sdnn_plan_tune recorded one for N, else the plan's tile_cols option, else the library's
@@ -274,13 +282,19 @@ sdnn_status sdnn_plan_launch_shape(sdnn_plan p, int32_t N, int32_t* panel_rows, 
 sdnn_status sdnn_plan_launch_tile(sdnn_plan p, int32_t N, int32_t* tile_cols);
 
 /* Per-plan variant selection by timing (the paper's preparation stage chooses the best
- * kernel implementation per operator, Sec. 3.1): times sdnn_spmm at this N for every
- * packing the plan holds with several consumer-wave counts per workgroup, on the
- * caller's B (K x N) and C (M x N, overwritten with unspecified values), and records
- * the fastest in the plan; later sdnn_spmm calls with the same N use it (up to 8 N
- * values are kept).  Blocking (synchronises `stream`).  Must not run concurrently with
- * any other call on the same plan.  Results of sdnn_spmm do not depend on the shape.
- * On success *panel_rows and *waves (either may be NULL) hold the chosen shape.
+ * kernel implementation per operator, Sec. 3.1, and autotunes the microkernel and the
+ * split-K tiling factor per sparse matrix, Sec. 3.2.2): times sdnn_spmm at this N for every
+ * packing the plan holds (panel height) with several consumer-wave counts per workgroup, on
+ * each tile width the call allows (256 and 128 columns, see tile_cols), on the caller's B
+ * (K x N) and C (M x N, overwritten with unspecified values), and records the fastest in
+ * the plan; later sdnn_spmm calls with the same N use it (up to 8 N values are kept).  For
+ * a plan with K-segments it then times sdnn_spmm_split at every workgroup count along K
+ * (up to 32) in a workspace it allocates for the search and frees (skipped if that
+ * allocation fails), and records the fastest, one meaning the unsplit call, for
+ * sdnn_spmm_split calls with splits = 0 at this N.  Blocking (synchronises `stream`).
+ * Must not run concurrently with any other call on the same plan.  Results of sdnn_spmm
+ * do not depend on the shape.  On success *panel_rows and *waves (either may be NULL)
+ * hold the chosen shape (sdnn_plan_launch_tile and sdnn_plan_split_runs report the rest).
  * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM (N <= 0, N >= 2^29, M = 0, B overlapping C),
  * SDNN_ERR_DEVICE, SDNN_ERR_HIP. */
 sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, void* stream,

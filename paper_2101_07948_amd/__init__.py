@@ -86,6 +86,7 @@ def lib() -> ctypes.CDLL:
         L.sdnn_plan_tune.argtypes = [p, p, p, i32, p, p, p]
         L.sdnn_plan_launch_shape.argtypes = [p, i32, p, p]
         L.sdnn_plan_launch_tile.argtypes = [p, i32, p]
+        L.sdnn_plan_split_runs.argtypes = [p, i32, i32, p]
         i64 = ctypes.c_int64
         L.sdnn_spmm_split.argtypes = [p, p, p, i32, p, ctypes.c_int, i32, p, i64, p]
         L.sdnn_spmm_split_noalloc.argtypes = [p, p, p, i32, p, ctypes.c_int, i32, p]
@@ -93,7 +94,8 @@ def lib() -> ctypes.CDLL:
         for fn in ("sdnn_reorder_rows", "sdnn_row_order", "sdnn_plan_check_host", "sdnn_plan_create",
                    "sdnn_plan_get_perm", "sdnn_plan_info", "sdnn_spmm", "sdnn_dense_gemm",
                    "sdnn_conv3x3", "sdnn_plan_tune", "sdnn_spmm_split", "sdnn_conv3x3_split",
-                   "sdnn_plan_launch_shape", "sdnn_spmm_split_noalloc", "sdnn_plan_launch_tile"):
+                   "sdnn_plan_launch_shape", "sdnn_spmm_split_noalloc", "sdnn_plan_launch_tile",
+                   "sdnn_plan_split_runs"):
             getattr(L, fn).restype = ctypes.c_int
         _lib_handle = L
     return _lib_handle
@@ -286,7 +288,8 @@ class Plan:
 
     def tune(self, N: int, B=None, C=None, stream=None) -> dict:
         """Times the plan's launch shapes at this N (on B / C, allocated here when not
-        given) and records the fastest for later spmm calls with the same N."""
+        given) and records the fastest for later spmm calls with the same N; for plans with
+        K-segments also the fastest workgroup count along K of spmm_split (split_runs)."""
         import torch
         if B is None:
             B = torch.randn(self.K, N, device="cuda")
@@ -301,6 +304,14 @@ class Plan:
         _check(self._lib.sdnn_plan_launch_tile(self.handle, int(N), ctypes.byref(tile)),
                "sdnn_plan_launch_tile")
         return {"panel_rows": rw.value, "waves": waves.value, "tile_cols": tile.value}
+
+    def split_runs(self, N: int, splits: int = 0) -> int:
+        """Workgroups along K that spmm_split runs at N for `splits` (0: the library's
+        choice, the tuned count if tune recorded one)."""
+        runs = ctypes.c_int32()
+        _check(self._lib.sdnn_plan_split_runs(self.handle, int(N), int(splits), ctypes.byref(runs)),
+               "sdnn_plan_split_runs")
+        return runs.value
 
     def conv3x3(self, X, C, bias=None, epi: str = "none", stream=None):
         """Sparse 3x3 convolution (stride 1, padding 1) on the GPU: the plan holds the

@@ -746,6 +746,7 @@ def generate() -> str:
         parts.append(consumer(rw, limit=True))
     for rw in RW_VARIANTS:
         parts.append(consumer(rw, lay=NARROW))
+        parts.append(consumer(rw, limit=True, lay=NARROW))
     for kind in ("vec", "dword", "conv", "vecn"):
         parts.append(producer(kind))
     return "\n".join(parts)

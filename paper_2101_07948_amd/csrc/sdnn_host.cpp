@@ -1132,6 +1132,13 @@ sdnn_status sdnn_plan_launch_shape(sdnn_plan p, int32_t N, int32_t* panel_rows, 
   return SDNN_OK;
 }
 
+sdnn_status sdnn_plan_split_runs(sdnn_plan p, int32_t N, int32_t splits, int32_t* runs) {
+  if (!p || !runs) return SDNN_ERR_NULL;
+  if (N <= 0 || p->M == 0 || splits < 0) return SDNN_ERR_DIM;
+  *runs = split_runs(p, N, splits);
+  return SDNN_OK;
+}
+
 sdnn_status sdnn_plan_launch_tile(sdnn_plan p, int32_t N, int32_t* tile_cols) {
   if (!p || !tile_cols) return SDNN_ERR_NULL;
   if (N <= 0 || p->M == 0) return SDNN_ERR_DIM;

@@ -117,9 +117,10 @@ std::vector<uint32_t> narrow_stream(const std::vector<uint32_t>& entries);
 bool check_narrow_stream(const std::vector<uint32_t>& entries, const std::vector<uint32_t>& narrow);
 
 // A launch shape sdnn_plan_tune measured fastest for one N: which packing, how many
-// consumer waves per workgroup and which tile width.
+// consumer waves per workgroup and which tile width; and, for plans with K-segments, the
+// workgroups along K and the tile width of the fastest K-split call (0: not measured).
 struct TunedShape {
-  int32_t N = 0, pack = 0, waves = 0, tile = 256;
+  int32_t N = 0, pack = 0, waves = 0, tile = 256, splits = 0, split_tile = 0;
 };
 constexpr int kTunedSlots = 8;
 

@@ -215,7 +215,7 @@ enum { kStageDword = 0, kStageVec = 1, kStageConv = 2 };
 
 // RW: rows per panel; STAGE: the producer kind (16-byte kinds also store C as float4:
 // N % 4 == 0 and B, C 16-byte aligned); TW: columns per tile (256, or 128 with 16-byte
-// staging of unsplit products only).  blockDim.x = 64 * (consumers + producers_of<TW>()).
+// staging only).  blockDim.x = 64 * (consumers + producers_of<TW>()).
 template <int RW, int STAGE, int TW>
 __global__ __launch_bounds__((threads_of<RW, TW>()), (min_waves_of<RW, TW>())) void spmm_panel_kernel(
     const uint32_t* __restrict__ entries, const int32_t* __restrict__ panel_start,
@@ -361,11 +361,18 @@ __global__ __launch_bounds__((threads_of<RW, TW>()), (min_waves_of<RW, TW>())) v
       ca.chunk_limit = (uint32_t)c1;
       ca.chunk_base = cbase;
       ca.next_progress = next;
-      if constexpr (TW != kTileCols) {  // unsplit products only
-        if constexpr (RW == 4) consume_n_rw4(p0, p1, ca);
-        if constexpr (RW == 8) consume_n_rw8(p0, p1, ca);
-        if constexpr (RW == 12) consume_n_rw12(p0, p1, ca);
-        if constexpr (RW == 16) consume_n_rw16(p0, p1, ca);
+      if constexpr (TW != kTileCols) {
+        if (splitk) {
+          if constexpr (RW == 4) consume_n_rw4_limit(p0, p1, ca);
+          if constexpr (RW == 8) consume_n_rw8_limit(p0, p1, ca);
+          if constexpr (RW == 12) consume_n_rw12_limit(p0, p1, ca);
+          if constexpr (RW == 16) consume_n_rw16_limit(p0, p1, ca);
+        } else {
+          if constexpr (RW == 4) consume_n_rw4(p0, p1, ca);
+          if constexpr (RW == 8) consume_n_rw8(p0, p1, ca);
+          if constexpr (RW == 12) consume_n_rw12(p0, p1, ca);
+          if constexpr (RW == 16) consume_n_rw16(p0, p1, ca);
+        }
       } else if (splitk) {  // runs of K-segments: the loop also stops at the run's last chunk
         if constexpr (RW == 4) consume_rw4_limit(p0, p1, p2, p3, ca);
         if constexpr (RW == 8) consume_rw8_limit(p0, p1, p2, p3, ca);
@@ -388,6 +395,12 @@ __global__ __launch_bounds__((threads_of<RW, TW>()), (min_waves_of<RW, TW>())) v
       const int row = panel_out[panel * RW + r];
       const float v[4] = {p0[r], p1[r], p2[r], p3[r]};
       if constexpr (TW != kTileCols) {
+        if (splitk) {  // raw partial sums (16-byte aligned workspace, N % 4 == 0)
+          float* prow = C + ((size_t)split * a.M + row) * a.N;
+          if (ncol + 2 <= a.N) *reinterpret_cast<float2*>(prow + ncol) = make_float2(v[0], v[1]);
+          else if (ncol < a.N) prow[ncol] = v[0];
+          continue;
+        }
         const float bb = bias ? bias[orig] : 0.0f;
         float* crow = C + (size_t)row * a.N;
         if (ncol + 2 <= a.N) {
@@ -684,6 +697,9 @@ hipError_t launch_reduce(const float* ws, float* C, const float* bias, const int
 // consecutive segments) for a requested count (0: choose_splits).
 int split_runs_of(const sdnn_plan_s* p, int32_t N, int splits, bool conv, int* seg_per_split) {
   const int total_seg = p->pk[0].nseg;
+  if (splits <= 0 && !conv)  // the count sdnn_plan_tune measured fastest at this N
+    for (int i = 0; i < p->ntuned; ++i)
+      if (p->tuned[i].N == N && p->tuned[i].splits > 0) splits = p->tuned[i].splits;
   if (splits <= 0) splits = choose_splits(p, N, conv);
   splits = std::min(std::max(splits, 1), total_seg);
   const int per = (total_seg + splits - 1) / splits;
@@ -691,12 +707,12 @@ int split_runs_of(const sdnn_plan_s* p, int32_t N, int splits, bool conv, int* s
   return (total_seg + per - 1) / per;
 }
 
-// Whether a call may run on 128-column tiles: an unsplit product (not a convolution) with
-// N % 4 == 0 and 16-byte aligned B and C (the 16-byte staging), on a plan that holds the
-// 128-column stream, with per-lane staging offsets 16 (lane % 32) + (lane / 32 + 2 j) 4N
-// (j < 8) below 2^31.
-bool narrow_allowed(const sdnn_plan_s* p, int N, bool aligned, int nk, bool conv) {
-  return aligned && !conv && nk == 1 && p->pk[0].entries_n != nullptr &&
+// Whether a call may run on 128-column tiles: a product (not a convolution) with N % 4 == 0
+// and 16-byte aligned B and output (C, or a K-split call's workspace: the 16-byte staging),
+// on a plan that holds the 128-column stream, with per-lane staging offsets
+// 16 (lane % 32) + (lane / 32 + 2 j) 4N (j < 8) below 2^31.
+bool narrow_allowed(const sdnn_plan_s* p, int N, bool aligned, bool conv) {
+  return aligned && !conv && p->pk[0].entries_n != nullptr &&
          (uint64_t)N * 4u * (kChunk / kAsmProducersN) < ((uint64_t)1 << 31);
 }
 
@@ -711,27 +727,35 @@ bool narrow_allowed(const sdnn_plan_s* p, int N, bool aligned, int nk, bool conv
 // layer at N = 1024 53.5 -> 43.4 us, M = K = 2048 at 90 % with N = 128 34.8 -> 26.3 us); from
 // 6 waves on 256 columns was as fast or faster (W0 at N = 4096 67.0 against 82.7 us, C5's
 // 3072 x 768 layer 130.5 against 185.5 us).
+// A K-split launch of nk workgroups along K follows the same rule on its own grid.
 constexpr int kNarrowMaxWaves = 4;
-int choose_tile(const sdnn_plan_s* p, int N) {
+int choose_tile(const sdnn_plan_s* p, int N, int nk = 1) {
   if (p->tile_cols != 0) return p->tile_cols;
-  const DevPacking& pk = choose_packing(p, N);
-  return choose_cfg(pk, p->num_cus, N).waves <= kNarrowMaxWaves ? kNarrowTileCols : kTileCols;
+  const DevPacking& pk = choose_packing(p, N, nk);
+  return choose_cfg(pk, p->num_cus, N, nk).waves <= kNarrowMaxWaves ? kNarrowTileCols : kTileCols;
 }
 
+// tile: a tile width to use where the call allows it (0: the tuned or the rule's).
 hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t N,
                          const float* bias, int epi, const int32_t* conv_hwn,
-                         const TunedShape* shape, float* ws, int splits, hipStream_t stream) {
+                         const TunedShape* shape, float* ws, int splits, hipStream_t stream,
+                         int tile = 0) {
   // nk: workgroups along K, each taking a run of seg_per_split consecutive segments
   int seg_per_split = 1, nk = 1;
-  if (ws) nk = split_runs_of(p, N, splits, conv_hwn != nullptr, &seg_per_split);
+  if (ws) {
+    nk = split_runs_of(p, N, splits, conv_hwn != nullptr, &seg_per_split);
+    if (splits <= 0 && !tile)  // a tuned count comes with its tile width
+      for (int i = 0; i < p->ntuned; ++i)
+        if (p->tuned[i].N == N && p->tuned[i].splits == nk && nk > 1) tile = p->tuned[i].split_tile;
+  }
   if (!shape && !conv_hwn && nk == 1)
     for (int i = 0; i < p->ntuned; ++i)
       if (p->tuned[i].N == N) shape = &p->tuned[i];
   float* out = nk > 1 ? ws : C;
   const bool aligned = (N % 4 == 0) && (((uintptr_t)B & 15) == 0) && (((uintptr_t)out & 15) == 0);
   int tw = kTileCols;
-  if (narrow_allowed(p, N, aligned, nk, conv_hwn != nullptr))
-    tw = shape ? shape->tile : choose_tile(p, N);
+  if (narrow_allowed(p, N, aligned, conv_hwn != nullptr))
+    tw = shape ? shape->tile : tile ? tile : choose_tile(p, N, nk);
   const DevPacking& pk =
       shape ? p->pk[shape->pack] : choose_packing(p, N, nk, tw);
   LaunchCfg cfg = choose_cfg(pk, p->num_cus, N, nk, tw);
@@ -833,7 +857,7 @@ void launch_shape(const sdnn_plan_s* p, int32_t N, int32_t* panel_rows, int32_t*
   for (int i = 0; i < p->ntuned; ++i)
     if (p->tuned[i].N == N) shape = &p->tuned[i];
   int tw = kTileCols;
-  if (narrow_allowed(p, N, N % 4 == 0, 1, false)) tw = shape ? shape->tile : choose_tile(p, N);
+  if (narrow_allowed(p, N, N % 4 == 0, false)) tw = shape ? shape->tile : choose_tile(p, N);
   const DevPacking& pk = shape ? p->pk[shape->pack] : choose_packing(p, N, 1, tw);
   *panel_rows = pk.RW;
   *waves = shape ? std::min(shape->waves, max_consumers(pk.RW, tw))
@@ -854,14 +878,15 @@ hipError_t launch_spmm_split(const sdnn_plan_s* p, const float* B, float* C, int
 
 hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStream_t stream,
                      TunedShape* chosen) {
-  // candidates: every tile width the call allows and every packing, each with its
-  // register-limited consumer count and three fewer-wave shapes, plus the heuristic's own
-  // choice
+  // candidates: every tile width the call and the plan's tile_cols option allow and every
+  // packing, each with its register-limited consumer count and three fewer-wave shapes,
+  // plus the heuristic's own choice
   std::vector<TunedShape> cands;
   const bool aligned = (N % 4 == 0) && (((uintptr_t)B & 15) == 0) && (((uintptr_t)C & 15) == 0);
-  std::vector<int> tiles{kTileCols};
-  if (narrow_allowed(p, N, aligned, 1, false) && p->tile_cols != kTileCols)
-    tiles.push_back(kNarrowTileCols);
+  std::vector<int> tiles;
+  if (!narrow_allowed(p, N, aligned, false) || p->tile_cols != kNarrowTileCols)
+    tiles.push_back(kTileCols);
+  if (narrow_allowed(p, N, aligned, false)) tiles.push_back(kNarrowTileCols);
   for (int tw : tiles)
     for (int k = 0; k < p->npack; ++k) {
       const int cap = std::min(max_consumers(p->pk[k].RW, tw), p->pk[k].npanels);
@@ -899,15 +924,63 @@ hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStr
       best = ms_best[i];
       *chosen = cands[i];
     }
+  int slot = -1;
+  if (err == hipSuccess) {
+    for (int i = 0; i < p->ntuned; ++i)
+      if (p->tuned[i].N == N) slot = i;
+    if (slot < 0) slot = p->ntuned < kTunedSlots ? p->ntuned++ : (int)(N % kTunedSlots);
+    chosen->splits = 0;
+    p->tuned[slot] = *chosen;
+  }
+  // K-segmented plans: the split-K tiling factor, i.e. the workgroups along K of
+  // sdnn_spmm_split (each count whose runs of ceil(nseg / count) segments give exactly it, up
+  // to kMaxAutoSplits, on each tile width the call allows, at the launch's own packing and
+  // consumer count), timed into a workspace allocated for the search; one workgroup along K
+  // is the unsplit call just tuned
+  const int nseg = p->pk[0].nseg;
+  if (err == hipSuccess && p->split_chunks > 0 && nseg > 1) {
+    float* ws = nullptr;
+    const size_t ws_bytes = (size_t)nseg * (size_t)p->M * (size_t)N * sizeof(float);
+    if (hipMalloc(&ws, ws_bytes) == hipSuccess) {
+      int best_runs = 1, best_tile = 0;
+      float best_ms = best;
+      for (int r = 2; r <= std::min(nseg, kMaxAutoSplits) && err == hipSuccess; ++r) {
+        const int per = (nseg + r - 1) / r;
+        if ((nseg + per - 1) / per != r) continue;
+        for (int tw : tiles) {
+          float ms_r = -1.0f;
+          for (int pass = 0; pass < 2 && err == hipSuccess; ++pass) {
+            for (int w = 0; w < 2 && err == hipSuccess; ++w)
+              err = launch_panels(p, B, C, N, nullptr, 0, nullptr, nullptr, ws, r, stream, tw);
+            if (err == hipSuccess) err = hipEventRecord(e0, stream);
+            for (int w = 0; w < 8 && err == hipSuccess; ++w)
+              err = launch_panels(p, B, C, N, nullptr, 0, nullptr, nullptr, ws, r, stream, tw);
+            if (err == hipSuccess) err = hipEventRecord(e1, stream);
+            if (err == hipSuccess) err = hipEventSynchronize(e1);
+            float ms = 0.0f;
+            if (err == hipSuccess) err = hipEventElapsedTime(&ms, e0, e1);
+            if (err == hipSuccess && (ms_r < 0.0f || ms < ms_r)) ms_r = ms;
+          }
+          if (err == hipSuccess && ms_r < best_ms) {
+            best_ms = ms_r;
+            best_runs = r;
+            best_tile = tw;
+          }
+        }
+      }
+      (void)hipStreamSynchronize(stream);
+      (void)hipFree(ws);
+      if (err == hipSuccess) {
+        p->tuned[slot].splits = best_runs;
+        p->tuned[slot].split_tile = best_tile;
+      }
+    } else {
+      (void)hipGetLastError();  // no room for the search: the cost model keeps deciding
+    }
+  }
   if (e0) (void)hipEventDestroy(e0);
   if (e1) (void)hipEventDestroy(e1);
-  if (err != hipSuccess) return err;
-  int slot = -1;
-  for (int i = 0; i < p->ntuned; ++i)
-    if (p->tuned[i].N == N) slot = i;
-  if (slot < 0) slot = p->ntuned < kTunedSlots ? p->ntuned++ : (int)(N % kTunedSlots);
-  p->tuned[slot] = *chosen;
-  return hipSuccess;
+  return err;
 }
 
 int split_runs(const sdnn_plan_s* p, int32_t N, int32_t splits) {

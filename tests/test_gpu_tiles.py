@@ -3,9 +3,9 @@ a 64 KB staging ring, two workgroups per CU) against the CPU oracle with the par
 and against the 256-column tiles bit for bit (both sum each row's entries in ascending
 column order).  Covers every panel height, ragged N (N % 128 != 0) and ragged K (the
 clamped staging of a partial last chunk), each epilogue, forced consumer counts, the
-persistent launches (tile-major and per-tile), out_permuted plans, the fallback to
-256-column tiles where a call does not allow 128 (N % 4 != 0, a misaligned B, K-split
-calls), the poll budget and tuning over both widths."""
+persistent launches (tile-major and per-tile), out_permuted plans, K-split calls, the
+fallback to 256-column tiles where a call does not allow 128 (N % 4 != 0, a misaligned B),
+the poll budget and tuning over both widths and over the workgroups along K."""
 import os
 
 import numpy as np
@@ -146,11 +146,11 @@ def test_out_permuted():
 
 
 def test_fallbacks_to_256_columns():
-    """Calls that do not allow 128-column tiles run on 256-column ones: N % 4 != 0, a B
-    that is not 16-byte aligned, and K-split calls."""
+    """Calls that do not allow 128-column tiles run on 256-column ones: N % 4 != 0 and a B
+    that is not 16-byte aligned."""
     M, K = 150, 200
     W = inputs.pattern_uniform(M, K, 0.1, inputs.CFG_TEST, 4900, 0.05)
-    with sd.Plan.from_csr(W, tile_cols=128, split_chunks=1) as plan:
+    with sd.Plan.from_csr(W, tile_cols=128) as plan:
         assert plan.launch_shape(130)["tile_cols"] == 256
         B = inputs.dense_B(K, 130, inputs.CFG_TEST, 4901)
         assert_parity(W, B, None, "none", run(plan, B, None, "none"), "N = 130")
@@ -160,10 +160,50 @@ def test_fallbacks_to_256_columns():
         Bt.copy_(torch.from_numpy(B))
         assert Bt.data_ptr() % 16 != 0
         assert_parity(W, B, None, "none", run(plan, B, None, "none", Bt=Bt), "misaligned B")
-        C = torch.full((M, 256), float("nan"), device=DEV)
-        plan.spmm_split(torch.from_numpy(B).to(DEV), C, None, "none", splits=3)
+
+
+@pytest.mark.parametrize("rw", [4, 16])
+@pytest.mark.parametrize("splits", [2, 3, 0])
+def test_k_split_calls(rw, splits):
+    """sdnn_spmm_split on 128-column tiles (K = 1000: 32 chunks, the last one ragged, in
+    segments of 3 chunks; N = 516: a ragged last tile): each run's partial products, the
+    reduction with bias and GELU, against the oracle, and bit for bit against the
+    256-column tiles at the same run boundaries."""
+    M, K, N = 400, 1000, 516
+    W = inputs.pattern_uniform(M, K, 0.1, inputs.CFG_TEST, 5200 + rw, 0.05)
+    B = inputs.dense_B(K, N, inputs.CFG_TEST, 5201)
+    bias = inputs.bias_normal(M, inputs.CFG_TEST, 5202, 0.02)
+    Bt = torch.from_numpy(B).to(DEV)
+    bt = torch.from_numpy(bias).to(DEV)
+    out = {}
+    for tw in (128, 256):
+        with sd.Plan.from_csr(W, tile_cols=tw, panel_rows=rw, split_chunks=3) as plan:
+            runs = plan.split_runs(N, splits)
+            C = torch.full((M, N), float("nan"), device=DEV)
+            plan.spmm_split(Bt, C, bt, "gelu", splits=runs)
+            torch.cuda.synchronize()
+            out[tw] = C.cpu().numpy()
+    print(f"tiles: K-split RW {rw} splits {splits} -> {runs} runs", flush=True)
+    assert_parity(W, B, bias, "gelu", out[128], f"split {runs}")
+    assert np.array_equal(out[128], out[256])
+
+
+def test_tune_records_split_runs():
+    """On a plan with K-segments sdnn_plan_tune also times the workgroup counts along K;
+    spmm_split with splits = 0 then runs the recorded count, against the oracle."""
+    W = inputs.pattern_uniform(768, 3072, 0.1, inputs.CFG_TEST, 5300, 0.02)
+    N = 1024
+    B = inputs.dense_B(3072, N, inputs.CFG_TEST, 5301)
+    Bt = torch.from_numpy(B).to(DEV)
+    with sd.Plan.from_csr(W, split_chunks=4) as plan:
+        plan.tune(N, Bt, torch.empty(768, N, device=DEV))
+        runs = plan.split_runs(N)
+        assert 1 <= runs <= plan.info["splits"]
+        C = torch.full((768, N), float("nan"), device=DEV)
+        plan.spmm_split(Bt, C, None, "none")
         torch.cuda.synchronize()
-        assert_parity(W, B, None, "none", C.cpu().numpy(), "K-split")
+    print(f"tiles: tuned split runs {runs}", flush=True)
+    assert_parity(W, B, None, "none", C.cpu().numpy(), f"tuned {runs} runs")
 
 
 @pytest.mark.parametrize("budget", [0, 2, 64])
