@@ -218,7 +218,7 @@ def _packing_used(plan, N):
     """(panel height, rho) of the packing plan.spmm runs on at N, as the library reports."""
     rw = plan.launch_shape(N)["panel_rows"]
     info = plan.info
-    for k in ("", "tall_", "mid_", "tallest_"):
+    for k in ("", "tall_", "mid_", "tallest_", "deep_"):
         if info[k + "panel_rows"] == rw:
             return rw, info[k + "rho"]
     return rw, float("nan")

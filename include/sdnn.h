@@ -59,12 +59,16 @@ typedef enum {
 
 /* Options for sdnn_plan_create; pass NULL for the defaults {0, 1, 0, 0, NULL, 0, 0}.
  *   panel_rows:   rows per register panel.  0 (default) packs W four times, with
- *                 panels of 4, 12, 8 and 16 rows, and sdnn_spmm picks one per call: the
- *                 fewest rounds of workgroups over the compute units, then the most
- *                 units busy, then the shortest panels averaging at least 8 entries per
- *                 32 columns of W (4-row panels are not used below 8); sdnn_plan_tune
- *                 can replace that choice by a timed one, and sdnn_plan_launch_shape
- *                 reports it.  4, 8, 12 or 16 packs that height only.
+ *                 panels of 4, 12, 8 and 16 rows, and a fifth time with 32-row panels
+ *                 for 128-column tiles unless tile_cols = 256.  sdnn_spmm picks one per
+ *                 call: the 32-row panels (with 12 consumer waves per workgroup) when W
+ *                 holds under 20 entries per 16 rows and 32 columns and their grid fills
+ *                 the compute units; otherwise the fewest rounds of workgroups over the
+ *                 compute units, then the most units busy, then the shortest panels
+ *                 averaging at least 8 entries per 32 columns of W (4-row panels are not
+ *                 used below 8); sdnn_plan_tune can replace that choice by a timed one,
+ *                 and sdnn_plan_launch_shape reports it.  4, 8, 12 or 16 packs that
+ *                 height only; 32 too, with tile_cols = 128 (else SDNN_ERR_DIM).
  *   permute:      1 = apply Algorithm 1 (default), 0 = identity order (ablation),
  *                 2 = panel-balancing order: rows, by nonzero count descending, each
  *                 go to the 4-row panel with the fewest nonzeros so far that has room,
@@ -124,8 +128,8 @@ typedef struct {
 } sdnn_plan_opts;
 
 /* Plan statistics (of the first packing; the tall_* fields describe the second one, the
- * mid_* fields the third and the tallest_* fields the fourth, or are 0 when the plan
- * holds fewer packings).
+ * mid_* fields the third, the tallest_* fields the fourth and the deep_* fields the fifth,
+ * or are 0 when the plan holds fewer packings).
  *   panels:       number of row panels (ceil(M / panel_rows)).
  *   packed_bytes: device bytes of every packed weight stream and its indexes.
  *   rho:          nnz / sum over panels of |union of the panel rows' column sets|,
@@ -149,6 +153,8 @@ typedef struct {
                                          the tile_cols option the plan was created with */
   int32_t tallest_panel_rows, reserved2;  /* fourth packing's height (0: none) */
   double tallest_rho, tallest_fill;
+  int32_t deep_panel_rows, reserved3;     /* fifth packing's height (0: none) */
+  double deep_rho, deep_fill;
 } sdnn_plan_info_t;
 
 /* Greedy weight-row permutation (Sec. 3.1.2, Algorithm 1), host only, no GPU needed.

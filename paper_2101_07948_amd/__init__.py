@@ -50,7 +50,9 @@ class PlanInfo(ctypes.Structure):
                 ("mid_rho", ctypes.c_double), ("mid_fill", ctypes.c_double),
                 ("grouping", ctypes.c_int32), ("tile_cols", ctypes.c_int32),
                 ("tallest_panel_rows", ctypes.c_int32), ("reserved2", ctypes.c_int32),
-                ("tallest_rho", ctypes.c_double), ("tallest_fill", ctypes.c_double)]
+                ("tallest_rho", ctypes.c_double), ("tallest_fill", ctypes.c_double),
+                ("deep_panel_rows", ctypes.c_int32), ("reserved3", ctypes.c_int32),
+                ("deep_rho", ctypes.c_double), ("deep_fill", ctypes.c_double)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}

@@ -81,6 +81,7 @@ E = tuple(36 + 2 * G * i for i in range(NSLOT))  # SGPR bases of the stream-grou
 LOW, HIW = 2 * G - 2, 2 * G - 1               # slot offsets of the c_lo / c_hi words
 UNROLL = 6                                    # multiple of NSLOT and of 2
 RW_VARIANTS = (4, 8, 12, 16)
+RW_VARIANTS_NARROW = (4, 8, 12, 16, 32)  # 32-row panels: 128-column tiles only
 SYNC_BIT, LO_SHIFT, HI_SHIFT = 17, 17, 18
 CHUNK, RING = 32, 4
 PMAX_VEC, PMAX_DWORD = 2, 1                   # chunks in flight per producer variant
@@ -744,7 +745,7 @@ def generate() -> str:
     for rw in RW_VARIANTS:
         parts.append(consumer(rw))
         parts.append(consumer(rw, limit=True))
-    for rw in RW_VARIANTS:
+    for rw in RW_VARIANTS_NARROW:
         parts.append(consumer(rw, lay=NARROW))
         parts.append(consumer(rw, limit=True, lay=NARROW))
     for kind in ("vec", "dword", "conv", "vecn"):

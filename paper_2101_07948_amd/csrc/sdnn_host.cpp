@@ -388,12 +388,14 @@ struct Options {
 
 // Panel heights to pack: the explicit option, or the short and tall defaults.
 static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* o) {
-  o->rws = {kShortPanel, kTallPanel, kMidPanel, kTallestPanel};
+  o->rws = {kShortPanel, kTallPanel, kMidPanel, kTallestPanel, kDeepPanel};
   if (!opts) return SDNN_OK;
   if (opts->panel_rows != 0) {
     if (opts->panel_rows != 4 && opts->panel_rows != 8 && opts->panel_rows != 12 &&
-        opts->panel_rows != 16)
+        opts->panel_rows != 16 && opts->panel_rows != 32)
       return SDNN_ERR_DIM;
+    // 32-row panels exist for 128-column tiles only (their 64 accumulators per lane)
+    if (opts->panel_rows == 32 && opts->tile_cols != kNarrowTileCols) return SDNN_ERR_DIM;
     o->rws = {opts->panel_rows};
   }
   if (opts->permute < 0 || opts->permute > 5) return SDNN_ERR_DIM;
@@ -404,6 +406,8 @@ static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* 
     return SDNN_ERR_DIM;
   o->grouping = opts->grouping;
   o->tile_cols = opts->tile_cols;
+  // the 32-row packing serves 128-column tiles only
+  if (opts->panel_rows == 0 && opts->tile_cols == kTileCols) o->rws.pop_back();
   o->split_chunks = opts->split_chunks;
   o->permute = opts->permute;
   o->out_permuted = opts->out_permuted;
@@ -748,6 +752,11 @@ static void fill_info(const std::vector<Packed>& packs, int64_t packed_bytes,
   out->reserved2 = 0;
   out->tallest_rho = tallest ? packs[3].rho : 0.0;
   out->tallest_fill = tallest ? fill_of(packs[3]) : 0.0;
+  const bool deep = packs.size() > 4;
+  out->deep_panel_rows = deep ? packs[4].RW : 0;
+  out->reserved3 = 0;
+  out->deep_rho = deep ? packs[4].rho : 0.0;
+  out->deep_fill = deep ? fill_of(packs[4]) : 0.0;
   out->grouping = P.grouping;
   out->tile_cols = o.tile_cols;
 }
@@ -1026,6 +1035,11 @@ sdnn_status sdnn_plan_info(sdnn_plan p, sdnn_plan_info_t* out) {
   out->reserved2 = 0;
   out->tallest_rho = tallest ? p->pk[3].rho : 0.0;
   out->tallest_fill = tallest ? p->pk[3].fill : 0.0;
+  const bool deep = p->npack > 4;
+  out->deep_panel_rows = deep ? p->pk[4].RW : 0;
+  out->reserved3 = 0;
+  out->deep_rho = deep ? p->pk[4].rho : 0.0;
+  out->deep_fill = deep ? p->pk[4].fill : 0.0;
   return SDNN_OK;
 }
 
@@ -1088,6 +1102,10 @@ static sdnn_status spmm_entry(sdnn_plan p, const float* B, float* C, int32_t N, 
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess) return SDNN_ERR_HIP;
   if (cur != p->device) return SDNN_ERR_DEVICE;
+  // a plan of 32-row panels alone runs on 128-column tiles only (their 16-byte staging)
+  if (p->npack == 1 && p->pk[0].RW > kTallestPanel &&
+      (N % 4 != 0 || ((uintptr_t)B & 15) != 0 || ((uintptr_t)C & 15) != 0))
+    return SDNN_ERR_DIM;
   if (noalloc) {
     const int64_t runs = split_runs(p, N, splits);
     if (runs > 1) {
@@ -1176,6 +1194,7 @@ static sdnn_status conv_entry(sdnn_plan p, const float* X, float* C, int32_t H, 
   if (H < 0 || W < 0 || NB < 0) return SDNN_ERR_DIM;
   if (epi != SDNN_EPI_NONE && epi != SDNN_EPI_RELU && epi != SDNN_EPI_GELU) return SDNN_ERR_DIM;
   if (p->K % 9 != 0 || p->K == 0 || p->in_permuted) return SDNN_ERR_DIM;
+  if (p->npack == 1 && p->pk[0].RW > kTallestPanel) return SDNN_ERR_DIM;  // 128-column only
   if (NB % 4 != 0) return SDNN_ERR_DIM;
   if (split && (p->split_chunks <= 0 || splits < 0)) return SDNN_ERR_DIM;
   const int64_t N = (int64_t)H * W * NB;

@@ -91,12 +91,15 @@ struct Packed {
   std::vector<int32_t> seg_start;   // [npanels*nseg] (split_chunks > 0 only)
 };
 
-// Panel heights of the four packings a default plan holds (in this order): short
-// panels keep enough waves busy when a tile has few rows per CU; taller ones carry more
-// entries per K-chunk (so a group spans fewer chunks of the ring) and stage each B tile
-// for more rows.  The launch picks one per call (choose_packing).
+// Panel heights of the packings a default plan holds (in this order): short panels keep
+// enough waves busy when a tile has few rows per CU; taller ones carry more entries per
+// K-chunk (so a group spans fewer chunks of the ring) and stage each B tile for more rows.
+// The fifth, 32-row panels, serves 128-column tiles only (a plan holds it when it holds
+// their stream): 14 such panels share each staged B row.  The launch picks one per call
+// (choose_packing).
 constexpr int kShortPanel = 4, kTallPanel = 12, kMidPanel = 8, kTallestPanel = 16;
-constexpr int kMaxPackings = 4;
+constexpr int kDeepPanel = 32;
+constexpr int kMaxPackings = 5;
 
 // CSR validation; returns SDNN_OK or SDNN_ERR_*.
 sdnn_status validate_csr(const int32_t* row_ptr, const int32_t* col_idx, int32_t M, int32_t K);
@@ -149,7 +152,8 @@ struct sdnn_plan_s {
   int64_t nnz = 0, packed_bytes = 0;
   std::vector<int32_t> perm;
   void* d_mem = nullptr;       // one device allocation holding every packing's arrays
-  int npack = 0;               // 1 (explicit panel height) or 4 (short, tall, mid, tallest)
+  int npack = 0;               // 1 (explicit panel height), 4 (short, tall, mid, tallest) or
+                               // 5 (and deep, with the 128-column stream)
   int32_t out_permuted = 0;    // C rows stored in the permuted order
   int32_t in_permuted = 0;     // W's columns renamed to a caller-given order of B's rows
   int32_t split_chunks = 0;    // chunks per K-segment (0: the packings have one segment)

@@ -123,14 +123,17 @@ constexpr int max_threads() { return kAsmAccBase + 4 * RW <= 128 ? 1024 : 768; }
 // CU then holds, so that two workgroups (2 x 65 KB of LDS) share each CU: 6 waves per SIMD
 // at RW = 4 and 8 (10 consumers per workgroup), 5 at RW = 12 and 16 (8).  (7 waves at RW = 4
 // would leave the compiler 88 SGPRs, too few beside the loop's 58: it then reserves a
-// stack frame.)
+// stack frame.)  32-row panels (128 VGPRs, 4 waves per SIMD) take a whole CU: 16 waves, 14
+// consumers, 448 rows sharing each staged 512-byte row of B.
 template <int RW>
 constexpr int narrow_waves_per_simd() {
   return 512 / ((kAsmAccBaseN + 2 * RW + 7) / 8 * 8) < 6 ? 512 / ((kAsmAccBaseN + 2 * RW + 7) / 8 * 8)
                                                           : 6;
 }
 template <int RW>
-constexpr int narrow_threads() { return 64 * (4 * narrow_waves_per_simd<RW>() / 2); }
+constexpr int narrow_threads() {
+  return RW >= 32 ? 64 * 4 * narrow_waves_per_simd<RW>() : 64 * (4 * narrow_waves_per_simd<RW>() / 2);
+}
 template <int RW, int TW>
 constexpr int threads_of() { return TW == kTileCols ? max_threads<RW>() : narrow_threads<RW>(); }
 template <int RW, int TW>
@@ -367,11 +370,13 @@ __global__ __launch_bounds__((threads_of<RW, TW>()), (min_waves_of<RW, TW>())) v
           if constexpr (RW == 8) consume_n_rw8_limit(p0, p1, ca);
           if constexpr (RW == 12) consume_n_rw12_limit(p0, p1, ca);
           if constexpr (RW == 16) consume_n_rw16_limit(p0, p1, ca);
+          if constexpr (RW == 32) consume_n_rw32_limit(p0, p1, ca);
         } else {
           if constexpr (RW == 4) consume_n_rw4(p0, p1, ca);
           if constexpr (RW == 8) consume_n_rw8(p0, p1, ca);
           if constexpr (RW == 12) consume_n_rw12(p0, p1, ca);
           if constexpr (RW == 16) consume_n_rw16(p0, p1, ca);
+          if constexpr (RW == 32) consume_n_rw32(p0, p1, ca);
         }
       } else if (splitk) {  // runs of K-segments: the loop also stops at the run's last chunk
         if constexpr (RW == 4) consume_rw4_limit(p0, p1, p2, p3, ca);
@@ -464,6 +469,9 @@ hipError_t launch_rw(int RW, const SpmmPtrs& p, const SpmmArgs& args, int waves,
     case 8: return launch_variant<8, STAGE, TW>(p, args, waves, grid, stream);
     case 12: return launch_variant<12, STAGE, TW>(p, args, waves, grid, stream);
     case 16: return launch_variant<16, STAGE, TW>(p, args, waves, grid, stream);
+    case 32:
+      if constexpr (TW == kNarrowTileCols) return launch_variant<32, STAGE, TW>(p, args, waves, grid, stream);
+      break;
   }
   return hipErrorInvalidValue;
 }
@@ -477,7 +485,8 @@ int max_consumers(int RW, int TW = kTileCols) {
             : RW == 12 ? max_threads<12>() : max_threads<16>();
   else
     threads = RW == 4 ? narrow_threads<4>() : RW == 8 ? narrow_threads<8>()
-            : RW == 12 ? narrow_threads<12>() : narrow_threads<16>();
+            : RW == 12 ? narrow_threads<12>() : RW == 16 ? narrow_threads<16>()
+            : narrow_threads<32>();
   const int c = threads / 64 - (TW == kTileCols ? kAsmProducers : kAsmProducersN);
   return c < kAsmMaxConsumers ? c : kAsmMaxConsumers;
 }
@@ -500,11 +509,26 @@ int slots_of(int num_cus, int tw) {
   return num_cus > 0 ? num_cus : 256;
 }
 
-// Workgroups the device holds at once (the persistent launches' grid): one per CU with
-// 256-column tiles (129 KB of LDS each), two with 128-column tiles (65 KB).
-int resident_of(int num_cus, int tw) {
+// Waves per SIMD the kernel for panel height RW and tile width tw allows (its VGPRs).
+int waves_per_simd(int RW, int tw) {
+  if (tw == kTileCols) {
+    const int vgprs = (kAsmAccBase + 4 * RW + 7) / 8 * 8;
+    return std::min(8, 512 / vgprs);
+  }
+  return RW == 4 ? narrow_waves_per_simd<4>() : RW == 8 ? narrow_waves_per_simd<8>()
+       : RW == 12 ? narrow_waves_per_simd<12>() : RW == 16 ? narrow_waves_per_simd<16>()
+       : narrow_waves_per_simd<32>();
+}
+
+// Workgroups the device holds at once (the persistent launches' grid): per CU, at most one
+// with 256-column tiles (129 KB of LDS each) and two with 128-column tiles (65 KB), and no
+// more than the CU's waves at the kernel's occupancy allow (a 14-consumer workgroup of
+// 32-row panels takes a whole CU).
+int resident_of(int num_cus, int tw, int RW, int waves) {
   const int cus = num_cus > 0 ? num_cus : 256;
-  return tw == kTileCols ? cus : 2 * cus;
+  const int per_wg = waves + (tw == kTileCols ? kAsmProducers : kAsmProducersN);
+  const int by_waves = std::max(1, 4 * waves_per_simd(RW, tw) / per_wg);
+  return cus * std::min(tw == kTileCols ? 1 : 2, by_waves);
 }
 
 // The 129 KB of ring and control LDS allow one workgroup per CU, so a grid of G
@@ -553,8 +577,28 @@ LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N, int nseg = 1, int
 // MI355X for products (M = K = 512-2048 at 80-98 %, N = 1024-16384, the W0 and C2-C5
 // layers) and for the 3x3 convolutions of the benchmark, whose staging differs but
 // follows the same trade.
+// The 32-row packing with kDeepWaves consumer waves per workgroup (128-column tiles: 384
+// rows share each staged 512-byte B row, against 128 rows per 1 KB row on 256-column tiles
+// with 16-row panels), taken for an unsplit product when W holds under 20 entries per 16
+// rows and 32 columns (so the other packings' workgroups stage many B rows for few entries)
+// and its grid fills the CUs; null otherwise.  Measured on MI355X at 97 % and N = 16384:
+// the 768 x 3072 layer 119.2 -> 87.5 us, the 768 x 768 layer 40.2 -> 32.0 us, the 3072 x 768
+// layer 130.4 -> 122.5 us (at N = 4096 40.2 -> 33.6 us); with fewer items than CUs (the
+// 768-row layers at N = 8192) or at 94 % and denser it was slower.
+constexpr int kDeepWaves = 12;
+const DevPacking* deep_packing(const sdnn_plan_s* p, int N, int nseg) {
+  if (nseg != 1 || p->npack < 5 || p->pk[4].RW != kDeepPanel || !p->pk[4].entries_n) return nullptr;
+  const double density = (double)p->nnz / ((double)p->M * (double)p->K);
+  if (kTallestPanel * kChunk * density >= 20.0) return nullptr;
+  const int64_t tiles = (N + kNarrowTileCols - 1) / kNarrowTileCols;
+  const int64_t rbs = (p->pk[4].npanels + kDeepWaves - 1) / kDeepWaves;
+  return tiles * rbs >= (p->num_cus > 0 ? p->num_cus : 256) ? &p->pk[4] : nullptr;
+}
+
 const DevPacking& choose_packing(const sdnn_plan_s* p, int N, int nseg = 1, int tw = kTileCols) {
   if (p->npack < 2) return p->pk[0];
+  if (tw == kNarrowTileCols)
+    if (const DevPacking* d = deep_packing(p, N, nseg)) return *d;
   const int64_t n_tiles = (int64_t)((N + tw - 1) / tw) * nseg;
   const int cus = slots_of(p->num_cus, tw);
   const double density = (double)p->nnz / ((double)p->M * (double)p->K);
@@ -565,7 +609,7 @@ const DevPacking& choose_packing(const sdnn_plan_s* p, int N, int nseg = 1, int 
   int64_t best_rounds = -1;
   for (int k = 0; k < p->npack; ++k) {
     const DevPacking& pk = p->pk[k];
-    live[k] = !(pk.RW == 4 && per_chunk(pk) < 8.0);
+    live[k] = !(pk.RW == 4 && per_chunk(pk) < 8.0) && pk.RW <= kTallestPanel;
     const int waves = std::max(1, std::min(max_consumers(pk.RW, tw), pk.npanels));
     const int64_t wgs = n_tiles * ((pk.npanels + waves - 1) / waves);
     rounds[k] = (wgs + cus - 1) / cus;
@@ -574,7 +618,7 @@ const DevPacking& choose_packing(const sdnn_plan_s* p, int N, int nseg = 1, int 
   bool any = false;
   for (int k = 0; k < p->npack; ++k) any |= live[k];
   if (!any)
-    for (int k = 0; k < p->npack; ++k) live[k] = true;
+    for (int k = 0; k < p->npack; ++k) live[k] = p->pk[k].RW <= kTallestPanel;
   for (int k = 0; k < p->npack; ++k)
     if (live[k] && (best_rounds < 0 || rounds[k] < best_rounds)) best_rounds = rounds[k];
   double best_util = 0.0;
@@ -731,6 +775,7 @@ bool narrow_allowed(const sdnn_plan_s* p, int N, bool aligned, bool conv) {
 constexpr int kNarrowMaxWaves = 4;
 int choose_tile(const sdnn_plan_s* p, int N, int nk = 1) {
   if (p->tile_cols != 0) return p->tile_cols;
+  if (deep_packing(p, N, nk)) return kNarrowTileCols;
   const DevPacking& pk = choose_packing(p, N, nk);
   return choose_cfg(pk, p->num_cus, N, nk).waves <= kNarrowMaxWaves ? kNarrowTileCols : kTileCols;
 }
@@ -758,6 +803,7 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
     tw = shape ? shape->tile : tile ? tile : choose_tile(p, N, nk);
   const DevPacking& pk =
       shape ? p->pk[shape->pack] : choose_packing(p, N, nk, tw);
+  if (pk.RW > 16 && tw != kNarrowTileCols) return hipErrorInvalidValue;  // 128-column only
   LaunchCfg cfg = choose_cfg(pk, p->num_cus, N, nk, tw);
   if (shape) {
     cfg.waves = std::min(shape->waves, max_consumers(pk.RW, tw));
@@ -790,7 +836,7 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
   // B rows stay in that XCD's L2 across the row-blocks, where CUs / tiles workgroups per
   // tile would spread each XCD over many tiles (C5's 3072 x 768 layer: 8 tiles of 768 KB
   // per XCD against a 4 MB L2).
-  const int cus = resident_of(p->num_cus, tw);  // workgroups resident at once
+  const int cus = resident_of(p->num_cus, tw, pk.RW, cfg.waves);  // workgroups resident at once
   const int64_t items = (int64_t)cfg.n_tiles * cfg.n_rb;
   const bool can_persist = nk == 1 && !conv_hwn && p->nchunks % kRing == 0;
   int wg_per_tile = cfg.n_rb, tile_major = 0;
@@ -889,6 +935,7 @@ hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStr
   if (narrow_allowed(p, N, aligned, false)) tiles.push_back(kNarrowTileCols);
   for (int tw : tiles)
     for (int k = 0; k < p->npack; ++k) {
+      if (p->pk[k].RW > kTallestPanel && tw != kNarrowTileCols) continue;  // 128-column only
       const int cap = std::min(max_consumers(p->pk[k].RW, tw), p->pk[k].npanels);
       const int heur = choose_cfg(p->pk[k], p->num_cus, N, 1, tw).waves;
       for (int w : {cap, (3 * cap) / 4, cap / 2, cap / 4, heur}) {

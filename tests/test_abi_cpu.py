@@ -81,11 +81,11 @@ def test_library_reorder_worked_examples_and_random():
 
 
 @pytest.mark.parametrize("name", ["c1", "c2", "c4", "w0", "c3"])
-@pytest.mark.parametrize("panel_rows", [4, 8, 12, 16])
+@pytest.mark.parametrize("panel_rows", [4, 8, 12, 16, 32])
 def test_packed_stream_self_check(name, panel_rows):
     for L in inputs.workload(name, N=4).layers:
         info = sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K,
-                                  panel_rows=panel_rows)
+                                  panel_rows=panel_rows, tile_cols=128 if panel_rows == 32 else 0)
         assert info["nnz"] == L.W.nnz and info["M"] == L.W.M and info["K"] == L.W.K
         assert info["panels"] == -(-L.W.M // panel_rows)
         # filler closes a panel's last group, or a group whose next entry lies a whole
@@ -98,27 +98,36 @@ def test_packed_stream_self_check(name, panel_rows):
 
 
 @pytest.mark.parametrize("name", ["c2", "w0", "c3"])
-def test_default_plan_packs_four_panel_heights(name):
-    """With panel_rows = 0 the plan holds 4-, 12-, 8- and 16-row packings of the same
-    grouping; all pass the stream self-check, taller panels share more columns, and each
-    packing equals the plan with that height alone."""
+def test_default_plan_packs_five_panel_heights(name):
+    """With panel_rows = 0 the plan holds 4-, 12-, 8-, 16- and 32-row packings of the same
+    grouping (the 32-row one, for 128-column tiles only, is left out with tile_cols = 256);
+    all pass the stream self-check, taller panels share more columns, and each packing
+    equals the plan with that height alone."""
     for L in inputs.workload(name, N=4).layers:
         info = sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K)
         assert info["panel_rows"] == 4 and info["tall_panel_rows"] == 12
         assert info["mid_panel_rows"] == 8 and info["tallest_panel_rows"] == 16
-        assert info["packings"] == 4
+        assert info["deep_panel_rows"] == 32 and info["packings"] == 5
         assert info["panels"] == -(-L.W.M // 4)
-        assert info["tallest_rho"] >= info["tall_rho"] >= info["mid_rho"] >= info["rho"] >= 1.0
-        for f in ("fill", "tall_fill", "mid_fill", "tallest_fill"):
+        assert (info["deep_rho"] >= info["tallest_rho"] >= info["tall_rho"] >= info["mid_rho"]
+                >= info["rho"] >= 1.0)
+        for f in ("fill", "tall_fill", "mid_fill", "tallest_fill", "deep_fill"):
             assert 0.0 < info[f] <= 1.0
         singles = {rw: sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K,
-                                          panel_rows=rw) for rw in (4, 8, 12, 16)}
+                                          panel_rows=rw, tile_cols=128) for rw in (4, 8, 12, 16, 32)}
         for rw, one in singles.items():
             assert one["tall_panel_rows"] == 0 and one["mid_panel_rows"] == 0
-            assert one["tallest_panel_rows"] == 0 and one["packings"] == 1
+            assert one["tallest_panel_rows"] == 0 and one["deep_panel_rows"] == 0
+            assert one["packings"] == 1
         assert singles[12]["rho"] == info["tall_rho"] and singles[8]["rho"] == info["mid_rho"]
-        assert singles[16]["rho"] == info["tallest_rho"]
+        assert singles[16]["rho"] == info["tallest_rho"] and singles[32]["rho"] == info["deep_rho"]
         assert info["packed_bytes"] == sum(one["packed_bytes"] for one in singles.values())
+        wide = sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K,
+                                  tile_cols=256)
+        assert wide["packings"] == 4 and wide["deep_panel_rows"] == 0
+    with pytest.raises(sd.SdnnError) as ei:  # 32-row panels need 128-column tiles
+        sd.plan_check_host(L.W.row_ptr, L.W.col_idx, L.W.values, L.W.M, L.W.K, panel_rows=32)
+    assert ei.value.code == 2
 
 
 def test_in_perm_relabels_columns():

@@ -465,18 +465,19 @@ def test_launch_shape_follows_density_and_grid():
     """The default plan's packing and tile width per call (sdnn_plan_launch_shape) on 256
     CUs: 4-row panels when they fill the device at 10 % (W0 at N = 4096), 8-row ones when
     4-row panels need more rounds (W0 at N = 16384), 12-row ones at 97 % where shorter panels
-    hold too few entries per chunk (C5's 768-row layers), 16-row ones where they need the
-    fewest rounds of workgroups (C5's 3072 x 768 layer, M = K = 2048 at 95 %), all on
-    256-column tiles; 128-column tiles where the 256-column launch gives its workgroups at
-    most 4 consumer waves (W0 and C2 at N = 1024, C5's 768 x 3072 layer at N = 1024, with
-    8-row panels there)."""
+    hold too few entries per chunk (C5's 768-row layer at N = 8192), 16-row ones where they
+    need the fewest rounds of workgroups (M = K = 2048 at 95 %), all on 256-column tiles;
+    128-column tiles where the 256-column launch gives its workgroups at most 4 consumer
+    waves (W0 and C2 at N = 1024, C5's 768 x 3072 layer at N = 1024, with 8-row panels
+    there), and 32-row panels on them at 97 % where their grid fills the CUs (C5's layers
+    at N = 16384)."""
     if torch.cuda.get_device_properties(0).multi_processor_count != 256:
         pytest.skip("the expected shapes are those of a 256-CU device")
     w0 = inputs.workload("w0", N=4).layers[0].W
     c2 = inputs.workload("c2", N=4).layers[0].W
     c5 = inputs.workload("c5", N=4, num_layers=1).layers
-    for W, N, want, tile in ((w0, 4096, 4, 256), (w0, 16384, 8, 256), (c5[0].W, 16384, 12, 256),
-                             (c5[4].W, 16384, 16, 256),
+    for W, N, want, tile in ((w0, 4096, 4, 256), (w0, 16384, 8, 256), (c5[0].W, 8192, 12, 256),
+                             (c5[0].W, 16384, 32, 128), (c5[4].W, 16384, 32, 128),
                              (inputs.s_layer(2048, 2048, 0.95).W, 4096, 16, 256),
                              (w0, 1024, 4, 128), (c2, 1024, 4, 128), (c5[5].W, 1024, 8, 128)):
         with sd.Plan.from_csr(W) as plan:

@@ -237,3 +237,68 @@ def test_tune_searches_both_widths():
         assert plan.launch_shape(N) == shape
         got = run(plan, B, None, "none", Bt=Bt)
     assert_parity(W, B, None, "none", got, f"tuned {shape}")
+
+
+@pytest.mark.parametrize("M,K,N,waves", [(200, 300, 132, None), (900, 768, 1000, 12),
+                                         (500, 640, 516, 3)])
+def test_deep_panels(M, K, N, waves):
+    """32-row panels (128-column tiles only, up to 14 consumer waves): parity with bias and
+    GELU, and bit for bit the 256-column result (ragged K and N, forced consumer counts)."""
+    W = inputs.pattern_uniform(M, K, 0.05, inputs.CFG_TEST, 5400 + M, 0.05)
+    B = inputs.dense_B(K, N, inputs.CFG_TEST, 5401)
+    bias = inputs.bias_normal(M, inputs.CFG_TEST, 5402, 0.02)
+    with Env(SDNN_FORCE_WAVES=waves):
+        with sd.Plan.from_csr(W, panel_rows=32, tile_cols=128) as plan:
+            assert plan.launch_shape(N)["panel_rows"] == 32
+            deep = run(plan, B, bias, "gelu")
+    with sd.Plan.from_csr(W, tile_cols=256) as plan:
+        wide = run(plan, B, bias, "gelu")
+    print(f"tiles: deep M {M} K {K} N {N}", flush=True)
+    assert_parity(W, B, bias, "gelu", deep, "deep panels")
+    assert np.array_equal(deep, wide)
+
+
+@pytest.mark.parametrize("splits", [2, 3])
+def test_deep_panels_k_split(splits):
+    M, K, N = 700, 1000, 260
+    W = inputs.pattern_uniform(M, K, 0.05, inputs.CFG_TEST, 5500, 0.05)
+    B = inputs.dense_B(K, N, inputs.CFG_TEST, 5501)
+    Bt = torch.from_numpy(B).to(DEV)
+    out = []
+    for kw in ({"panel_rows": 32, "tile_cols": 128}, {"tile_cols": 256}):
+        with sd.Plan.from_csr(W, split_chunks=3, **kw) as plan:
+            C = torch.full((M, N), float("nan"), device=DEV)
+            plan.spmm_split(Bt, C, None, "none", splits=splits)
+            torch.cuda.synchronize()
+            out.append(C.cpu().numpy())
+    assert_parity(W, B, None, "none", out[0], f"deep split {splits}")
+    assert np.array_equal(out[0], out[1])
+
+
+def test_deep_panels_need_128_column_calls():
+    """A plan of 32-row panels alone rejects calls that cannot run on 128-column tiles."""
+    W = inputs.pattern_uniform(64, 90, 0.1, inputs.CFG_TEST, 5600, 0.05)
+    with sd.Plan.from_csr(W, panel_rows=32, tile_cols=128) as plan:
+        with pytest.raises(sd.SdnnError) as ei:
+            plan.spmm(torch.zeros(90, 130, device=DEV), torch.zeros(64, 130, device=DEV))
+        assert ei.value.code == 2
+        with pytest.raises(sd.SdnnError) as ei:
+            plan.conv3x3(torch.zeros(10, 4, 4, 4, device=DEV), torch.zeros(64, 4, 4, 4, device=DEV))
+        assert ei.value.code == 2
+
+
+def test_default_plan_takes_deep_panels_at_97_percent():
+    """C5's 97 % layers at N = 16384 run on the default plan's 32-row packing with 12
+    consumer waves on 128-column tiles; at N = 8192 the 768-row layers' deep grid would
+    not fill the CUs and they keep the other packings."""
+    if torch.cuda.get_device_properties(0).multi_processor_count != 256:
+        pytest.skip("the expected shapes are those of a 256-CU device")
+    c5 = inputs.workload("c5", N=4, num_layers=1).layers
+    for li in (0, 4, 5):
+        with sd.Plan.from_csr(c5[li].W) as plan:
+            assert plan.launch_shape(16384) == {"panel_rows": 32, "waves": 12, "tile_cols": 128}
+            if c5[li].W.M == 768:
+                assert plan.launch_shape(8192)["panel_rows"] != 32
+    w0 = inputs.workload("w0", N=4).layers[0].W
+    with sd.Plan.from_csr(w0) as plan:  # 90 %: too dense for them
+        assert plan.launch_shape(16384)["panel_rows"] != 32
