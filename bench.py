@@ -246,25 +246,37 @@ def run_suite(out_path):
              f"{ALU_PEAK_TFLOPS:.1f} TFLOP/s (FP32 vector peak), % HBM of {HBM_PEAK_GBS:.0f} GB/s "
              "(algorithmic bytes 8 nnz + 4 KN + 4 MN + 4 M).", "",
              "## Every configuration", "",
-             "| layer | nnz | panel rows used | rho | cold median us (p10-p90) | cold mean us | "
-             "warm median us | GFLOP/s (cold mean) | % ALU | alg GB/s | % HBM |",
-             "|---|---|---|---|---|---|---|---|---|---|---|"]
+             "Launch: panel rows x consumer waves per workgroup, tile columns, as the default "
+             "plan picks them.  '256-col us': a plan fixed to 256-column tiles (tile_cols = "
+             "256, four packings), cold mean.  'tuned': after sdnn_plan_tune at this N, cold "
+             "mean and the shape it recorded.", "",
+             "| layer | nnz | launch | rho | cold median us (p10-p90) | cold mean us | "
+             "warm median us | GFLOP/s (cold mean) | % ALU | alg GB/s | % HBM | 256-col us | "
+             "tuned us (shape) |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
     timed = {}
     for label, L, N in _suite_layers():
         W = L.W
         with sd.Plan.from_csr(W) as plan:
             rw, rho = _packing_used(plan, N)
+            sh = plan.launch_shape(N)
             per, mean, nsets = _time_layer(plan, L, N)
             wper, _, _ = _time_layer(plan, L, N, cold=False)
+            tsh = plan.tune(N, torch.randn(W.K, N, device=dev), torch.empty(W.M, N, device=dev))
+            _, tmean, _ = _time_layer(plan, L, N)
+        with sd.Plan.from_csr(W, tile_cols=256) as plan:
+            _, mean256, _ = _time_layer(plan, L, N)
         flop = 2.0 * W.nnz * N
         ab = 8.0 * W.nnz + 4.0 * W.K * N + 4.0 * W.M * N + 4.0 * W.M
         t = mean * 1e-3
         timed[label] = mean
-        lines.append(f"| {label} | {W.nnz} | {rw} | {rho:.2f} | {_pct(per, .5)*1e3:.1f} "
+        lines.append(f"| {label} | {W.nnz} | {rw} x {sh['waves']}, {sh['tile_cols']} | {rho:.2f} | "
+                     f"{_pct(per, .5)*1e3:.1f} "
                      f"({_pct(per, .1)*1e3:.1f}-{_pct(per, .9)*1e3:.1f}) | {mean*1e3:.1f} | "
                      f"{_pct(wper, .5)*1e3:.1f} | {flop/t/1e9:.0f} | "
                      f"{100*flop/t/1e12/ALU_PEAK_TFLOPS:.1f} | {ab/t/1e9:.0f} | "
-                     f"{100*ab/t/1e9/HBM_PEAK_GBS:.1f} |")
+                     f"{100*ab/t/1e9/HBM_PEAK_GBS:.1f} | {mean256*1e3:.1f} | {tmean*1e3:.1f} "
+                     f"({tsh['panel_rows']} x {tsh['waves']}, {tsh['tile_cols']}) |")
         print(lines[-1], flush=True)
 
     lines += ["", "## Dense comparison: the library's FP32 GEMM kernel (same layouts and epilogue) "
@@ -365,7 +377,7 @@ def run_suite(out_path):
               f"order, the next plan built with in_perm): {pmean:.2f} ms per forward "
               f"= {flop/(pmean*1e-3)/1e12:.1f} TFLOP/s.",
               f"* Preparation of the {len(w.layers)} plans (validation, Algorithm 1, panel grouping, "
-              f"four packings, upload): {prep_s:.2f} s on the host."]
+              f"five packings and the 128-column stream, upload): {prep_s:.2f} s on the host."]
     print("\n".join(lines[-4:]), flush=True)
 
     # sparse 3x3 convolutions shaped like the paper's benchmark (Sec. 4.1): IC, OC in
@@ -423,11 +435,14 @@ def run_suite(out_path):
     lines += ["", "## K-split calls (sdnn_spmm_split / sdnn_conv3x3_split) on small grids", "",
               "Unsplit: the plain call on a plain plan.  Split: a plan with about 16-24 "
               "K-segments (split_chunks = S chunks of 32 rows each), called with the "
-              "library's choice of workgroups along K (auto) and with forced counts; "
-              "cold means of 50 launches, reduction included.", "",
+              "library's choice of workgroups along K (auto: the cost model) and with forced "
+              "counts, on the tile width the launch picks; 'tuned': after sdnn_plan_tune at "
+              "this N (products only), which also times every count on both tile widths "
+              "(workgroups along K, tile columns); cold means of 50 launches, reduction "
+              "included.", "",
               "| problem | column tiles x panels | unsplit us | S | auto us | " +
-              " | ".join(f"{k} along K us" for k in counts) + " | auto speedup |",
-              "|---|---|---|---|---|" + "---|" * len(counts) + "---|"]
+              " | ".join(f"{k} along K us" for k in counts) + " | auto speedup | tuned us |",
+              "|---|---|---|---|---|" + "---|" * len(counts) + "---|---|"]
     split_cases = [("W0 768x3072 90% N=1024", inputs.workload("w0", N=4).layers[0].W, 1024, None),
                    ("W0 768x3072 90% N=4096", inputs.workload("w0", N=4).layers[0].W, 4096, None),
                    ("C2 768x768 90% N=1024", inputs.workload("c2", N=4).layers[0].W, 1024, None),
@@ -461,14 +476,19 @@ def run_suite(out_path):
         with sd.Plan.from_csr(W) as plan:
             base = timed_mean(plan, None)
             rw, _ = _packing_used(plan, N)
-        grid = f"{-(-N // 256)} x {-(-W.M // rw)} ({rw}-row)"
+            tile = plan.launch_shape(N)["tile_cols"] if ch is None else 256
+        grid = f"{-(-N // tile)} x {-(-W.M // rw)} ({rw}-row, {tile}-col)"
         with sd.Plan.from_csr(W, split_chunks=S) as plan:
             ws = torch.empty(max(plan.workspace_floats(N), 1), device=dev)
             auto = timed_mean(plan, ws, 0)
             forced = [timed_mean(plan, ws, k) for k in counts]
             segs = plan.info["splits"]
+            tuned = "-"
+            if ch is None:
+                plan.tune(N, B, C)
+                tuned = f"{timed_mean(plan, ws, 0)*1e3:.1f} ({plan.split_runs(N)} along K)"
         lines.append(f"| {label} | {grid} | {base*1e3:.1f} | {S} ({segs} seg) | {auto*1e3:.1f} | " +
-                     " | ".join(f"{t_*1e3:.1f}" for t_ in forced) + f" | {base/auto:.2f}x |")
+                     " | ".join(f"{t_*1e3:.1f}" for t_ in forced) + f" | {base/auto:.2f}x | {tuned} |")
         print(lines[-1], flush=True)
         del C
 
