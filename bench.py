@@ -355,6 +355,26 @@ def run_suite(out_path):
     torch.cuda.synchronize()
     _, fmean = _launch_times(forward, 5)
     flop = sum(2.0 * L.W.nnz * w.N for L in w.layers)
+    # the same forward captured once as a HIP graph and replayed (the calls allocate nothing
+    # and never synchronise); each replay is checked against the eager result bit for bit
+    eager_out = acts[768][(sum(1 for L in w.layers if L.W.M != 3072) - 1) % 2].clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        forward(0)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        forward(0)
+    graph_ok = True
+    for _ in range(3):
+        graph.replay()
+        torch.cuda.synchronize()
+        last = acts[768][(sum(1 for L in w.layers if L.W.M != 3072) - 1) % 2]
+        graph_ok &= bool(torch.equal(last, eager_out))
+    _, gmean = _launch_times(lambda _i: graph.replay(), 5)
+    del graph
     for p_ in plans:
         p_.close()
     # the same chain in permuted space: every activation stays in its producer's row
@@ -373,6 +393,9 @@ def run_suite(out_path):
               f"* {len(w.layers)} products, {flop/1e9:.1f} GFLOP per forward; "
               f"{fmean:.2f} ms per forward = {flop/(fmean*1e-3)/1e12:.1f} TFLOP/s "
               f"(mean of 5 forwards after one warm-up, activations stay on the GPU).",
+              f"* Captured once as a HIP graph and replayed: {gmean:.2f} ms per forward = "
+              f"{flop/(gmean*1e-3)/1e12:.1f} TFLOP/s (every replay equal to the eager forward "
+              f"bit for bit: {'yes' if graph_ok else 'NO'}).",
               f"* In permuted space (each activation left in its producer's Algorithm 1 row "
               f"order, the next plan built with in_perm): {pmean:.2f} ms per forward "
               f"= {flop/(pmean*1e-3)/1e12:.1f} TFLOP/s.",
