@@ -302,3 +302,24 @@ def test_default_plan_takes_deep_panels_at_97_percent():
     w0 = inputs.workload("w0", N=4).layers[0].W
     with sd.Plan.from_csr(w0) as plan:  # 90 %: too dense for them
         assert plan.launch_shape(16384)["panel_rows"] != 32
+
+
+@pytest.mark.parametrize("kw", [{"tile_cols": 128}, {"tile_cols": 128, "panel_rows": 32}])
+def test_k_split_out_permuted(kw):
+    """K-split calls of out_permuted plans on 128-column tiles (4-row panels and 32-row ones):
+    the partials of each run are stored in the plan's row order and the reduction finds each
+    stored row's bias through the plan's permutation; C row i is output row perm[i]."""
+    M, K, N = 500, 900, 388
+    W = inputs.pattern_uniform(M, K, 0.06, inputs.CFG_TEST, 5700, 0.05)
+    B = inputs.dense_B(K, N, inputs.CFG_TEST, 5701)
+    bias = inputs.bias_normal(M, inputs.CFG_TEST, 5702, 0.02)
+    with sd.Plan.from_csr(W, out_permuted=True, split_chunks=2, **kw) as plan:
+        C = torch.full((M, N), float("nan"), device=DEV)
+        plan.spmm_split(torch.from_numpy(B).to(DEV), C, torch.from_numpy(bias).to(DEV), "gelu",
+                        splits=4)
+        torch.cuda.synchronize()
+        perm = plan.perm
+        assert plan.split_runs(N, 4) == 4
+    ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, K, B, bias, "gelu")
+    err = np.abs(C.cpu().numpy().astype(np.float64) - ref[perm])
+    assert (err <= tol_fp32(bound[perm], "gelu")).all()
