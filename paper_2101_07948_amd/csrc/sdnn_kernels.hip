@@ -504,10 +504,7 @@ struct LaunchCfg {
 // (65 KB of LDS each), but on the layers whose launch takes those tiles a grid of one per CU
 // with more consumer waves each was the faster (C2's 768 x 768 layer at N = 1024: 14.1 against
 // 15.4 us; the 768 x 3072 layer at N = 1024: 43.8 against 51.6 us).
-int slots_of(int num_cus, int tw) {
-  (void)tw;
-  return num_cus > 0 ? num_cus : 256;
-}
+int slots_of(int num_cus) { return num_cus > 0 ? num_cus : 256; }
 
 // Waves per SIMD the kernel for panel height RW and tile width tw allows (its VGPRs).
 int waves_per_simd(int RW, int tw) {
@@ -543,7 +540,7 @@ int64_t rounds_of(int64_t n_tiles, int npanels, int waves, int target) {
 // count allows, and within that many rounds the smallest workgroups (fewest panels
 // each, so the most workgroups share the work).  SDNN_FORCE_WAVES fixes the count.
 LaunchCfg choose_cfg(const DevPacking& pk, int num_cus, int N, int nseg = 1, int tw = kTileCols) {
-  const int target = slots_of(num_cus, tw);
+  const int target = slots_of(num_cus);
   int cap = max_consumers(pk.RW, tw);
   if (cap > pk.npanels) cap = pk.npanels;
   if (cap < 1) cap = 1;
@@ -600,7 +597,7 @@ const DevPacking& choose_packing(const sdnn_plan_s* p, int N, int nseg = 1, int 
   if (tw == kNarrowTileCols)
     if (const DevPacking* d = deep_packing(p, N, nseg)) return *d;
   const int64_t n_tiles = (int64_t)((N + tw - 1) / tw) * nseg;
-  const int cus = slots_of(p->num_cus, tw);
+  const int cus = slots_of(p->num_cus);
   const double density = (double)p->nnz / ((double)p->M * (double)p->K);
   auto per_chunk = [&](const DevPacking& pk) { return pk.RW * kChunk * density; };
   int64_t rounds[kMaxPackings];
@@ -801,6 +798,9 @@ hipError_t launch_panels(const sdnn_plan_s* p, const float* B, float* C, int32_t
   int tw = kTileCols;
   if (narrow_allowed(p, N, aligned, conv_hwn != nullptr))
     tw = shape ? shape->tile : tile ? tile : choose_tile(p, N, nk);
+  // a tuned shape on a packing that 256-column tiles cannot run (32-row panels), for a call
+  // that cannot use 128 columns: the rule decides instead
+  if (shape && p->pk[shape->pack].RW > kTallestPanel && tw != kNarrowTileCols) shape = nullptr;
   const DevPacking& pk =
       shape ? p->pk[shape->pack] : choose_packing(p, N, nk, tw);
   if (pk.RW > 16 && tw != kNarrowTileCols) return hipErrorInvalidValue;  // 128-column only

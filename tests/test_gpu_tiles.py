@@ -323,3 +323,26 @@ def test_k_split_out_permuted(kw):
     ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, K, B, bias, "gelu")
     err = np.abs(C.cpu().numpy().astype(np.float64) - ref[perm])
     assert (err <= tol_fp32(bound[perm], "gelu")).all()
+
+
+def test_tuned_deep_shape_with_a_call_that_cannot_use_it():
+    """After sdnn_plan_tune records a 32-row shape at some N, a call at that N that cannot run
+    on 128-column tiles (a B that is not 16-byte aligned) falls back to the rule's 256-column
+    launch and still agrees with the oracle."""
+    if torch.cuda.get_device_properties(0).multi_processor_count != 256:
+        pytest.skip("the deep launch is chosen for a 256-CU device")
+    L = inputs.workload("c5", N=4, num_layers=1).layers[5]
+    W, N = L.W, 16384
+    B = inputs.dense_B(W.K, N, inputs.CFG_TEST, 5800)
+    with sd.Plan.from_csr(W) as plan:
+        Bt = torch.from_numpy(B).to(DEV)
+        plan.tune(N, Bt, torch.empty(W.M, N, device=DEV))
+        flat = torch.empty(W.K * N + 1, device=DEV)
+        Bm = flat[1:].view(W.K, N)
+        Bm.copy_(Bt)
+        assert Bm.data_ptr() % 16 != 0
+        got = run(plan, B, None, "none", Bt=Bm)
+    cols = np.arange(0, N, 97)
+    ref, bound = oracle.spmm_f64(W.row_ptr, W.col_idx, W.values, W.K, B[:, cols], None, "none")
+    err = np.abs(got[:, cols].astype(np.float64) - ref)
+    assert (err <= tol_fp32(bound, "none")).all()
