@@ -1,6 +1,9 @@
 """Generates spmm_asm_gen.h: the inner loops of the gfx950 panel kernel as inline
-assembly.  One consumer routine per panel height RW and one producer routine per
-staging width.
+assembly.  One consumer routine per panel height RW and tile layout, and one producer
+routine per staging kind.  The description below is that of the 256-column layout
+(`WIDE`); the 128-column layout (`NARROW`, class Layout) differs only where stated there:
+2 columns per lane, 512-byte ring rows and their field at bit 9 of the address words,
+two producers that stage two rows per DMA, and 32-row panels beside the others.
 
 Why generated assembly: the consumer keeps a wavefront's RW x 4 output tile in fixed
 VGPRs and selects the row of each nonzero with VGPR index mode (s_set_gpr_idx_*), and
@@ -40,7 +43,9 @@ a7 bit 17 and the end-of-panel flag in a7 bit 9.  The ring row field is bits 10.
 so (a & 0x1fc00) | (16 * lane) is the LDS address of the lane's 4 B values; VGPR
 index mode uses only a's low 8 bits.
 
-Consumer register plan (pinned in the asm statement):
+Consumer register plan of the 256-column layout (pinned in the asm statement; the
+128-column one keeps v[32:47] / v[48:63] for B and v[64 + k*RW + r], k = 0..1, for the
+accumulators, and reads only the two ready words v[26:27]):
   v31 0x1fc00 (ring-row mask), v28 zero offset and v29 sink of the L2 touch loads,
   v[24:27] ready words, v30 temp, v[32:63] / v[64:95] B values of the group being multiplied /
   fetched, v[96 + k*RW + r] accumulator of row r, column 4*lane + k (k = 0..3);

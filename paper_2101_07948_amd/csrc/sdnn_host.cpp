@@ -386,7 +386,8 @@ struct Options {
   int32_t tile_cols = 0;         // 0: both tile widths; 256: 256-column tiles only; 128: 128 where the call allows
 };
 
-// Panel heights to pack: the explicit option, or the short and tall defaults.
+// Panel heights to pack: the explicit option, or the five defaults (the 32-row one only
+// for plans that hold the 128-column stream).
 static sdnn_status resolve_opts(const sdnn_plan_opts* opts, int32_t K, Options* o) {
   o->rws = {kShortPanel, kTallPanel, kMidPanel, kTallestPanel, kDeepPanel};
   if (!opts) return SDNN_OK;

@@ -7,7 +7,9 @@
 // into an output tile kept in registers; the register that a nonzero accumulates into
 // is fixed by generated code per matrix (Sec. 3.2.2, Fig. 3).  On CDNA4:
 //   * a consumer wavefront owns a panel of RW rows of the permuted W and a tile of 256
-//     columns of C; lane l holds columns 4l..4l+3 of all RW rows in VGPRs;
+//     columns of C; lane l holds columns 4l..4l+3 of all RW rows in VGPRs (or, on the
+//     128-column tiles that a call takes when they suit its grid, columns 2l and 2l+1,
+//     with half the LDS ring, so that two workgroups share a CU or 32-row panels fit);
 //   * the panel's nonzeros form one flat stream of (weight, ring row, row) entries
 //     read with scalar loads, so weights sit in SGPRs; the output row of each entry
 //     selects the accumulator through VGPR index mode instead of per-matrix generated
@@ -27,7 +29,7 @@
 //     (input channel x filter tap) straight from the input activations.
 // Plain FP32 FMA is used throughout (no MFMA: the work is not a dense contraction).
 //
-// Workgroups: one 256-column tile x one row-block of nc consecutive panels, plus the
+// Workgroups: one column tile x one row-block of nc consecutive panels, plus the
 // producer waves.  All panels of a row-block share the staged B rows.  The flat block
 // id is remapped so that all row-blocks of a tile land on one XCD (blocks are dealt
 // to the 8 XCDs round robin), letting them share that XCD's L2 copy of the B tile.
