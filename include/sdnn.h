@@ -301,7 +301,8 @@ sdnn_status sdnn_plan_launch_tile(sdnn_plan p, int32_t N, int32_t* tile_cols);
  * Must not run concurrently with any other call on the same plan.  Results of sdnn_spmm
  * do not depend on the shape.  On success *panel_rows and *waves (either may be NULL)
  * hold the chosen shape (sdnn_plan_launch_tile and sdnn_plan_split_runs report the rest).
- * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM (N <= 0, N >= 2^29, M = 0, B overlapping C),
+ * Errors: SDNN_ERR_NULL, SDNN_ERR_DIM (N <= 0, N >= 2^29, M = 0, B overlapping C, or a
+ * plan of 32-row panels alone with N % 4 != 0 or B or C not 16-byte aligned),
  * SDNN_ERR_DEVICE, SDNN_ERR_HIP. */
 sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, void* stream,
                            int32_t* panel_rows, int32_t* waves);

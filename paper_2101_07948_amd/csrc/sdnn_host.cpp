@@ -1177,6 +1177,10 @@ sdnn_status sdnn_plan_tune(sdnn_plan p, const float* B, float* C, int32_t N, voi
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess) return SDNN_ERR_HIP;
   if (cur != p->device) return SDNN_ERR_DEVICE;
+  // a plan of 32-row panels alone has no shape for a call that cannot use 128-column tiles
+  if (p->npack == 1 && p->pk[0].RW > kTallestPanel &&
+      (N % 4 != 0 || ((uintptr_t)B & 15) != 0 || ((uintptr_t)C & 15) != 0))
+    return SDNN_ERR_DIM;
   try {
     TunedShape chosen;
     if (tune_spmm(p, B, C, N, (hipStream_t)stream, &chosen) != hipSuccess) return SDNN_ERR_HIP;

@@ -947,6 +947,7 @@ hipError_t tune_spmm(sdnn_plan_s* p, const float* B, float* C, int32_t N, hipStr
         if (!dup) cands.push_back(TunedShape{N, k, w, tw});
       }
     }
+  if (cands.empty()) return hipErrorInvalidValue;  // no packing runs at this call's tile width
   hipEvent_t e0 = nullptr, e1 = nullptr;
   hipError_t err = hipEventCreate(&e0);
   if (err == hipSuccess) err = hipEventCreate(&e1);

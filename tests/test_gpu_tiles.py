@@ -285,6 +285,12 @@ def test_deep_panels_need_128_column_calls():
         with pytest.raises(sd.SdnnError) as ei:
             plan.conv3x3(torch.zeros(10, 4, 4, 4, device=DEV), torch.zeros(64, 4, 4, 4, device=DEV))
         assert ei.value.code == 2
+        # nor can it be tuned for such a call (no packing to time), and nothing is recorded
+        before = plan.launch_shape(130)
+        with pytest.raises(sd.SdnnError) as ei:
+            plan.tune(130, torch.zeros(90, 130, device=DEV), torch.zeros(64, 130, device=DEV))
+        assert ei.value.code == 2
+        assert plan.launch_shape(130) == before
 
 
 def test_default_plan_takes_deep_panels_at_97_percent():
